@@ -1,0 +1,163 @@
+"""Benchmark: ResidualAttention decode on one MI355X.
+
+Metric: decode attention tokens/s and achieved HBM GB/s (fraction of the 8 TB/s
+peak) for one Llama-3-8B-shaped attention layer with 16 agents that share a
+32768-token prefix (suffixes uniform in [256, 4096], rank 16, 32 q / 8 kv heads,
+head dim 128, bf16).  One step = one decode call (split kernel + combine kernel)
+over all 16 agents; tokens/s = agents x steps / time.
+
+Inputs are resident in HBM before timing starts.  Three independent copies of
+the caches are built and the steps rotate over them, so consecutive steps never
+read data the previous step left in the 256 MB last-level (MALL) cache.
+
+Roofline: the split kernel dominates.  Its algorithmic bytes per launch are the
+shared base pages counted once per segment, plus each agent's private base
+pages, rCache rows, adapter B matrices, queries, outputs, block tables and (RoPE
+on) the cos/sin rows read, and its duration is taken live from HIP events
+recorded around it on the launch stream.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2] [--rope 0|1]
+       [--pps N] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBS = 8000.0
+
+
+def algorithmic_bytes(wl, lw, agents, rope: bool) -> dict:
+    """Bytes one decode step must move at least once: each shared base page once, every agent's
+    private pages and rCache rows, adapters, queries, outputs, block tables, RoPE rows."""
+    ps, hkv, d, r = wl.page_size, wl.hkv, wl.d, wl.r
+    bb, rb, sl = lw._decode["host_bt"]
+    # distinct physical base pages and the most tokens any agent reads from each
+    pages = {}
+    for i in range(len(agents)):
+        n = int(sl[i])
+        for p in range((n + ps - 1) // ps):
+            valid = min(ps, n - p * ps)
+            pg = int(bb[i][p])
+            pages[pg] = max(pages.get(pg, 0), valid)
+    base_tokens = sum(pages.values())
+    base = base_tokens * hkv * d * 2 * 2
+    res_agents = [a for a in agents if wl.has_residual[a]]
+    resid = sum(int(wl.seq_len[a]) for a in res_agents) * r * 2 * 2
+    bmat = len(res_agents) * r * hkv * d * 2 * 2
+    qo = len(agents) * wl.hq * d * 2 * 2
+    tables = len(agents) * 2 * sum((int(x) + ps - 1) // ps for x in sl) // max(len(agents), 1) * 4
+    rope_b = (int(max(sl)) * (d // 2) * 2 * 4) if rope else 0
+    total = base + resid + bmat + qo + tables + rope_b
+    return {"total": total, "base": base, "rcache": resid, "b": bmat, "q_out": qo, "tables": tables,
+            "rope_table": rope_b, "base_tokens": base_tokens}
+
+
+def cpu_baseline(wl, agents, rope: bool, budget_s: float = 20.0) -> dict:
+    import oracle
+    from paper_2604_06370_amd import workloads as W
+    threads = oracle.default_threads()
+    done, t_used = [], 0.0
+    # evaluate agents one at a time until the time budget is spent (at least one)
+    for a in agents:
+        p = W.oracle_inputs(wl, agents=[a], rope=rope)
+        t0 = time.perf_counter()
+        oracle.residual_attention(p, n_threads=threads)
+        t_used += time.perf_counter() - t0
+        done.append(a)
+        if t_used >= budget_s:
+            break
+    return {"value": len(done) / t_used, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{len(done)} of {len(agents)} agents of the timed workload (all heads, fp64 C oracle, "
+                      f"{t_used:.1f} s)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--rope", type=int, default=1)
+    ap.add_argument("--pps", type=int, default=0, help="pages per split (0 = automatic)")
+    ap.add_argument("--copies", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (the kernel would shard by KV "
+              "head with no exchange; see DESIGN.md). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2604_06370_amd import workloads as W
+    from paper_2604_06370_amd.driver import LoadedWorkload
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = W.config(args.config)
+    rope = bool(args.rope) and wl.r > 0
+    print(f"# building {args.copies} cache copies of {wl.name} (rope={rope})", file=sys.stderr, flush=True)
+    lws = [LoadedWorkload(wl, device=dev, rope=rope, pages_per_split=args.pps) for _ in range(args.copies)]
+    agents = wl.decode_agents()
+    for lw in lws:
+        lw.decode_setup(agents)
+    info = lws[0]._decode["info"]
+    byts = algorithmic_bytes(wl, lws[0], agents, rope)
+    stream = torch.cuda.current_stream()
+
+    # live per-kernel timing: events recorded by the library around its two launches
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    for trio in ev:
+        for e in trio:
+            e.record(stream)  # materialise the HIP event
+    import ctypes
+    handles = [(ctypes.c_void_p * 3)(*[e.cuda_event for e in trio]) for trio in ev]
+
+    for i in range(args.warmup):
+        lws[i % len(lws)].decode()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        lw = lws[i % len(lws)]
+        lw._decode["args"].timing_events = ctypes.cast(handles[i], ctypes.c_void_p).value
+        lw.decode()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for lw in lws:
+        lw._decode["args"].timing_events = None
+    split_ms = np.array([ev[i][0].elapsed_time(ev[i][1]) for i in range(args.steps)])
+    comb_ms = np.array([ev[i][1].elapsed_time(ev[i][2]) for i in range(args.steps)])
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    value = len(agents) * args.steps / (t1 - t0)
+    split_avg = float(split_ms.mean())
+    achieved = byts["total"] / (split_avg * 1e-3) / 1e9
+    call_gbs = byts["total"] / (float((split_ms + comb_ms).mean()) * 1e-3) / 1e9
+
+    out = {
+        "metric": "decode attn tokens/s (+ achieved HBM GB/s), Llama-3-8B-shaped layer, 16 agents, 32K shared",
+        "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (seeded, shapes of config %d)" % args.config,
+        "config": {"workload": wl.name, "agents": len(agents), "hq": wl.hq, "hkv": wl.hkv, "head_dim": wl.d,
+                   "rank": wl.r, "page_size": wl.page_size, "rope": rope,
+                   "seq_len_mean": float(np.mean(wl.seq_len[agents])), "pages_per_split": info["pages_per_split"],
+                   "work_items": info["n_items"], "workgroups": info["n_blocks"], "cache_copies": args.copies},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None, "kernel": "decode_split_kernel",
+                     "algorithmic_bytes": byts["total"], "kernel_ms": split_avg,
+                     "combine_ms": float(comb_ms.mean()), "call_GBps": call_gbs},
+        "bytes": byts,
+    }
+    if not args.no_cpu_baseline:
+        print("# timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(wl, agents, rope)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

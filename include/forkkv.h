@@ -1,0 +1,274 @@
+/*
+ * forkkv.h -- C ABI of the MI355X (gfx950) ResidualAttention library.
+ *
+ * ForkKV (arXiv 2604.06370) splits the KV cache of many LoRA agents into a
+ * shared base cache (bCache = xW, RoPE'd keys, Section 5.1) and a small
+ * per-agent residual cache (rCache = xA_i, r values per token for K and for V,
+ * Section 2.2, Eq. 2).  This library provides
+ *   - the host-side DualRadixTree that hands out pages of both caches with fork
+ *     and copy-on-write semantics (Section 5.2), and
+ *   - ResidualAttention kernels for decode and chunked prefill (Section 5.3,
+ *     Algorithm 1) that rebuild each agent's keys as
+ *         K = K_base + RoPE(C_K . B_K)
+ *     on chip and fold the value residual in rank space,
+ *         O = (sum_p P_p V_base,p + (sum_p P_p C_V,p) . B_V) / l        (Eq. 4),
+ *     never writing a reconstructed K or V to memory.
+ *
+ * Conventions
+ *   - Every call returns fkv_status: 0 on success, a negative FKV_ERR_* code on
+ *     failure; fkv_last_error() then returns a message (thread-local, valid
+ *     until the next failing call on that thread).
+ *   - Host-side tree calls are single-threaded per tree (the scheduler owns the
+ *     tree).  A failing tree call leaves the tree unchanged.
+ *   - Device memory is owned by the caller: pools, queries, outputs, block
+ *     tables, plans and workspaces are caller allocations.  The library
+ *     allocates no device memory and never synchronises; kernels are enqueued on
+ *     the caller's stream (a hipStream_t passed as void*; NULL = null stream).
+ *   - Pointers documented as "device" must point to device memory of the
+ *     current HIP device; "host" pointers to ordinary host memory.
+ *   - bf16 means IEEE bfloat16 stored as 16-bit words.
+ *
+ * Data layout in HBM (d = head dim, ps = page size, r = rank, Hkv = KV heads):
+ *   base pool  [num_base_pages][2][Hkv][ps*d] bf16.  For page p, slot 0 holds
+ *              K as [ps][d] (token-major), slot 1 holds V as [d][ps]
+ *              (dimension-major).  One (page, K|V, head) block is contiguous.
+ *   res pool   [num_res_pages][2][ps*r] bf16.  Slot 0 holds C_K as [ps][r],
+ *              slot 1 holds C_V as [r][ps].
+ *   adapters   [n_adapters][2][r][Hkv*d] bf16: B_K then B_V, each the r x n
+ *              up-projection of Eq. 1 in row-major order (n = Hkv*d); KV head h
+ *              uses columns h*d .. h*d+d-1.  Any LoRA scaling is folded in by the
+ *              caller (Eq. 1 has none).
+ *   queries    [n_q][Hq][d] bf16, already RoPE'd.  Output has the same layout.
+ *   GQA        query head j reads KV head j / (Hq/Hkv).
+ */
+#ifndef FORKKV_H
+#define FORKKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t fkv_status;
+
+enum {
+    FKV_OK = 0,
+    FKV_ERR_INVALID = -1,     /* bad argument or inconsistent sizes */
+    FKV_ERR_OOM = -2,         /* a page pool cannot satisfy the request (nothing changed) */
+    FKV_ERR_NOT_FOUND = -3,   /* unknown sequence id */
+    FKV_ERR_EXISTS = -4,      /* sequence id already in use */
+    FKV_ERR_UNSUPPORTED = -5, /* a shape the kernels do not implement */
+    FKV_ERR_HIP = -6          /* a HIP runtime call failed (message has the HIP error) */
+};
+
+enum { FKV_POOL_BASE = 0, FKV_POOL_RES = 1 };
+
+/* Message of the last failing call on this thread ("" if none). */
+const char *fkv_last_error(void);
+/* Library version string. */
+const char *fkv_version(void);
+
+/* ------------------------------------------------------------------------ */
+/* DualRadixTree (host).  Section 5.2: a base radix tree keyed by token ids    */
+/* indexes bCache pages; a residual radix tree keyed by (agent id, token ids) */
+/* indexes rCache pages.  Both are radix trees with one page per edge.        */
+/* ------------------------------------------------------------------------ */
+
+typedef struct fkv_tree fkv_tree;
+
+typedef struct {
+    int32_t page_size;       /* tokens per page, both pools (1..1024) */
+    int32_t num_base_pages;  /* capacity of the base pool */
+    int32_t num_res_pages;   /* capacity of the residual pool */
+} fkv_tree_config;
+
+/* One device-side page copy the caller must perform (Section 5.2 copy-on-write):
+ * copy the first n_valid token slots of page src into page dst of pool `pool`.
+ * fkv_page_copy_launch performs a batch of them. */
+typedef struct {
+    int32_t pool, src, dst, n_valid;
+} fkv_page_copy;
+
+/* What the caller must do after fkv_fork / fkv_cow_append for one sequence:
+ * first perform `copies`, then write bCache for logical positions
+ * [base_valid, seq_len) and rCache for [res_valid, seq_len) into the slots
+ * given by the sequence's block tables (page = table[pos / ps], slot = pos % ps).
+ * Perform the copies before the next call on the tree. */
+typedef struct {
+    int64_t seq_len;
+    int64_t base_valid;
+    int64_t res_valid;
+    int32_t n_copies;
+    fkv_page_copy copies[2];
+} fkv_fill_plan;
+
+typedef struct {
+    int32_t base_pages_free, base_pages_referenced, base_pages_cached, base_pages_raw;
+    int32_t res_pages_free, res_pages_referenced, res_pages_cached, res_pages_raw;
+    int32_t n_sequences;
+    int64_t base_evictions, res_evictions;
+} fkv_pool_stats;
+
+/* Create / destroy a tree.  The tree owns host memory only. */
+fkv_status fkv_tree_create(const fkv_tree_config *cfg, fkv_tree **out);
+void fkv_tree_destroy(fkv_tree *tree);
+
+/* Allocate n pages of pool FKV_POOL_BASE or FKV_POOL_RES outside the trees
+ * (lowest free ids first, evicting unreferenced cached pages of that pool's
+ * tree when needed).  out_ids: host, n entries.  FKV_ERR_OOM if impossible. */
+fkv_status fkv_alloc_pages(fkv_tree *tree, int32_t pool, int32_t n, int32_t *out_ids);
+/* Return pages obtained from fkv_alloc_pages. */
+fkv_status fkv_free_pages(fkv_tree *tree, int32_t pool, int32_t n, const int32_t *ids);
+
+/* Fork (Section 5.2, "Fork Semantics with CoW"): create sequence seq_id for
+ * agent agent_id whose context is tokens[0..n) (host).  Step 1: longest-prefix
+ * match in the base tree; matched pages are inherited read-only and unmatched
+ * tokens get new base pages that extend the tree.  Step 2: the same in the
+ * residual tree under key (agent_id, tokens), so a new agent id gets exclusive
+ * rCache pages for its whole context.  A match that ends inside a page whose
+ * remaining slots the new sequence needs yields a copy of that page.
+ * Errors: FKV_ERR_EXISTS (seq_id in use), FKV_ERR_OOM, FKV_ERR_INVALID. */
+fkv_status fkv_fork(fkv_tree *tree, int32_t seq_id, int32_t agent_id, const int32_t *tokens, int64_t n,
+                    fkv_fill_plan *out);
+
+/* Append n tokens (host) to sequence seq_id (decode steps or a prefill chunk).
+ * A partially filled last page is written in place when the sequence is its only
+ * user and nothing beyond it is stored, and copied first otherwise
+ * (copy-on-write); further tokens go to new pages, which are inserted into the
+ * trees so later forks can share them. */
+fkv_status fkv_cow_append(fkv_tree *tree, int32_t seq_id, const int32_t *tokens, int64_t n,
+                          fkv_fill_plan *out);
+
+/* Drop a sequence.  Its pages stay cached in the trees until evicted (each tree
+ * has its own LRU order, Section 5.2 "Decoupled Eviction Policy"). */
+fkv_status fkv_release(fkv_tree *tree, int32_t seq_id);
+
+/* Length and page count of a sequence (host outputs). */
+fkv_status fkv_seq_info(const fkv_tree *tree, int32_t seq_id, int64_t *seq_len, int32_t *n_pages);
+
+/* Block tables for n sequences (all host buffers): base_bt and res_bt are
+ * [n][max_pages] int32 physical page ids, padded with 0 past each sequence's
+ * pages; seq_lens [n] int32.  FKV_ERR_INVALID if a sequence needs more than
+ * max_pages pages. */
+fkv_status fkv_get_block_tables(const fkv_tree *tree, const int32_t *seq_ids, int32_t n, int32_t max_pages,
+                                int32_t *base_bt, int32_t *res_bt, int32_t *seq_lens);
+
+fkv_status fkv_get_pool_stats(const fkv_tree *tree, fkv_pool_stats *out);
+
+/* ------------------------------------------------------------------------ */
+/* Decode plan (host).  Agents whose base block tables name the same physical */
+/* pages over a range of logical pages form a segment; each segment is split */
+/* into work items of at most 16 query rows (agents x query heads per KV head)*/
+/* and a bounded page range, so a base tile is streamed once per item and     */
+/* applied to all of its agents' query heads.                                 */
+/* ------------------------------------------------------------------------ */
+
+typedef struct fkv_plan fkv_plan;
+
+typedef struct {
+    int32_t n_agents;
+    int32_t hq, hkv;
+    int32_t page_size;
+    int32_t max_pages;        /* row stride of base_bt */
+    int32_t pages_per_split;  /* pages per work item; 0 = choose automatically */
+    int32_t num_cus;          /* compute units to fill; 0 = 256 */
+} fkv_decode_plan_params;
+
+typedef struct {
+    int64_t plan_words;       /* int32 words of the serialised plan */
+    int64_t workspace_bytes;  /* workspace fkv_residual_attention_decode needs for (d, r) given at query */
+    int32_t n_items;          /* work items */
+    int32_t n_blocks;         /* workgroups of the split kernel */
+    int32_t n_segments;       /* shared / private page ranges found */
+    int32_t pages_per_split;
+} fkv_plan_info;
+
+/* Build a plan from host block tables (base_bt [n_agents][max_pages], seq_lens [n_agents]). */
+fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *params, const int32_t *base_bt,
+                                  const int32_t *seq_lens, fkv_plan **out);
+void fkv_decode_plan_destroy(fkv_plan *plan);
+/* Sizes of the plan; workspace_bytes is computed for head dim d and rank r. */
+fkv_status fkv_decode_plan_info(const fkv_plan *plan, int32_t d, int32_t r, fkv_plan_info *out);
+/* Write the serialised plan (plan_words int32) to a host buffer; the caller copies
+ * it to device memory and passes that copy as fkv_attn_args.plan. */
+fkv_status fkv_decode_plan_serialize(const fkv_plan *plan, int32_t *out, int64_t capacity_words);
+/* Segment list (host outputs, n_segments entries each): first agent, agent count,
+ * first page, page count.  Agents of a segment are listed in seg_agents. */
+fkv_status fkv_decode_plan_segments(const fkv_plan *plan, int32_t *seg_first_page, int32_t *seg_n_pages,
+                                    int32_t *seg_n_agents, int32_t *seg_agents, int64_t seg_agents_capacity);
+
+/* ------------------------------------------------------------------------ */
+/* ResidualAttention (device).                                                */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    const void *q;              /* device bf16 [n_q][hq][d]; decode: n_q = n_agents, row a = agent a */
+    const void *base_kv;        /* device bf16 base pool (layout above) */
+    const void *res_kv;         /* device bf16 residual pool (layout above); unused when r == 0 */
+    const void *lora_b;         /* device bf16 adapters [n_adapters][2][r][hkv*d] */
+    const int32_t *adapter_idx; /* device [n_agents]; -1 = agent has no residual (base-only path) */
+    const int32_t *base_bt;     /* device [n_agents][max_pages] */
+    const int32_t *res_bt;      /* device [n_agents][max_pages] */
+    const int32_t *seq_lens;    /* device [n_agents], >= 1; keys 0..seq_len-1 */
+    const float *rope_cos;      /* device fp32 [rope_max_pos][d/2]; NULL = no RoPE on C_K.B_K */
+    const float *rope_sin;      /* device fp32 [rope_max_pos][d/2] */
+    const int32_t *plan;        /* device copy of a serialised decode plan (decode only) */
+    const int32_t *q_indptr;    /* device [n_agents+1] query rows per agent (prefill only) */
+    void *workspace;            /* device scratch of workspace_bytes (decode) */
+    size_t workspace_bytes;
+    void *out;                  /* device bf16 [n_q][hq][d] */
+    int32_t n_agents, hq, hkv, d, r, page_size, max_pages;
+    int32_t rope_max_pos;       /* rows of the RoPE tables; every key position must be below it */
+    int32_t n_q;                /* prefill: total query rows (= q_indptr[n_agents]) */
+    float scale;                /* softmax scale; typically 1/sqrt(d) */
+    void *const *timing_events; /* optional, host array of hipEvent_t: decode records [0] before its first
+                                   kernel, [1] between its two kernels and [2] after the second; prefill
+                                   records [0] and [1] around its kernel.  NULL = no events. */
+} fkv_attn_args;
+
+/* Decode: one query row per agent attends to all seq_len keys of its agent
+ * (the current token's K/V/C is already in the cache).  Section 5.3,
+ * Algorithm 1, split over the plan's work items with a log-sum-exp combine.
+ * `plan` is the host plan whose serialised copy args->plan points to (grid size
+ * and workspace size are taken from it); the block tables and sequence lengths
+ * in args must be the ones the plan was built from.
+ * Supported: d = 128, page_size = 16, r in {0, 8, 16, 32, 64}, hq/hkv in {4, 8}.
+ * Two kernels are enqueued (split, combine).  Errors: FKV_ERR_INVALID /
+ * FKV_ERR_UNSUPPORTED before any launch, FKV_ERR_HIP when a launch fails. */
+fkv_status fkv_residual_attention_decode(const fkv_attn_args *args, const fkv_plan *plan, void *stream);
+
+/* Chunked prefill: agent a's query rows q_indptr[a] .. q_indptr[a+1]-1 are the
+ * last n_a = q_indptr[a+1]-q_indptr[a] tokens of its sequence (already in the
+ * cache); row i sits at position seq_len[a] - n_a + i and attends causally to
+ * keys 0 .. that position.  Same shapes as decode; needs no plan or workspace. */
+fkv_status fkv_residual_attention_prefill(const fkv_attn_args *args, void *stream);
+
+/* Fill a RoPE table on the host (fp64 angles rounded to fp32): for position p
+ * and pair i < d/2, cos_out[p*d/2+i] = cos(p * base^(-2i/d)), likewise sin. */
+fkv_status fkv_rope_table(int32_t d, int32_t max_pos, double base, float *cos_out, float *sin_out);
+
+/* ------------------------------------------------------------------------ */
+/* Cache writes (device): copy-on-write page copies and token scatter.        */
+/* ------------------------------------------------------------------------ */
+
+/* Perform page copies (device array of n fkv_page_copy) in both pools.  base_kv
+ * and res_kv are the pools; hkv, d, r, page_size describe them. */
+fkv_status fkv_page_copy_launch(const fkv_page_copy *copies_dev, int32_t n, void *base_kv, void *res_kv,
+                                int32_t hkv, int32_t d, int32_t r, int32_t page_size, void *stream);
+
+/* Write logical rows into the pools through one sequence's block table.
+ * Positions pos0 .. pos0+n-1 of the sequence receive
+ *   base: k_src/v_src [n][hkv][d] bf16 (device; NULL skips the base pool)
+ *   res:  ck_src/cv_src [n][r] bf16 (device; NULL skips the residual pool)
+ * bt_base / bt_res: device block-table rows of that sequence. */
+fkv_status fkv_scatter_tokens(const int32_t *bt_base, const int32_t *bt_res, int64_t pos0, int64_t n,
+                              const void *k_src, const void *v_src, const void *ck_src, const void *cv_src,
+                              void *base_kv, void *res_kv, int32_t hkv, int32_t d, int32_t r,
+                              int32_t page_size, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FORKKV_H */

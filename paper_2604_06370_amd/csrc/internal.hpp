@@ -1,0 +1,40 @@
+// Internal declarations shared by the host-side sources of libforkkv.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/forkkv.h"
+
+namespace fkv {
+
+// Record a failure message for fkv_last_error() and return the status.
+fkv_status fail(fkv_status code, const std::string &msg);
+void clear_error();
+
+// Decode plan, host side.  Serialised layout (all int32):
+//   header[kHeaderWords]
+//   items   [n_items][kItemWords]  {page_begin, page_end, leader, n_ag, agent[16]}
+//   blocks  [n_blocks]             item * hkv + head, or -1 for an idle block
+//   agent_ptr [n_agents+1]         CSR over the partial slots of each agent
+//   agent_slot[...]                partial row base: (item*hkv) * 16 + slot*g  (add head*16 + jj)
+constexpr int kHeaderWords = 16;
+constexpr int kMaxRows = 16;       // query rows per work item (agents x query heads of a KV head)
+constexpr int kItemWords = 4 + kMaxRows;
+
+enum PlanHeader {
+    H_MAGIC = 0, H_N_ITEMS, H_N_BLOCKS, H_N_AGENTS, H_HKV, H_GROUP, H_AGENTS_PER_ITEM,
+    H_OFF_ITEMS, H_OFF_BLOCKS, H_OFF_AGENT_PTR, H_OFF_AGENT_SLOT, H_TOTAL_WORDS, H_PAGES_PER_SPLIT,
+    H_PAGE_SIZE, H_N_SEGMENTS
+};
+constexpr int32_t kPlanMagic = 0x464b5631;  // "FKV1"
+
+}  // namespace fkv
+
+struct fkv_plan {
+    std::vector<int32_t> words;
+    std::vector<int32_t> seg_first_page, seg_n_pages, seg_agent_off, seg_agents;
+    int32_t hkv = 0, g = 0, n_agents = 0;
+    int32_t max_pages_used = 0;  // longest sequence, in pages
+};

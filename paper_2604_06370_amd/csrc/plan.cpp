@@ -1,0 +1,245 @@
+// Decode plan: shared-base segments, work items and the workgroup order.
+//
+// A segment is a maximal run of logical pages over which a fixed set of agents
+// maps every page to the same physical base page (what the base tree's prefix
+// sharing produces, Section 5.2).  Each segment is cut into work items of at most
+// floor(16 / g) agents (16 query rows per KV head) and at most pages_per_split
+// pages.  The split kernel runs one workgroup per (work item, KV head); the base
+// tiles of a page range are therefore read once per item and applied to all of
+// its agents' query heads.
+//
+// Workgroup order: on MI355X consecutive workgroup ids are dealt round-robin to
+// the 8 XCDs, each with its own L2.  All workgroups that read the same base pages
+// (the agent groups of one segment split) or the same rCache rows (the KV heads of
+// one item) are placed on one XCD so those re-reads hit that XCD's L2.
+#include <algorithm>
+#include <cmath>
+#include <unordered_map>
+
+#include "internal.hpp"
+
+namespace {
+constexpr int kNumXcd = 8;
+}
+
+extern "C" {
+
+fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32_t *base_bt,
+                                  const int32_t *seq_lens, fkv_plan **out) {
+    fkv::clear_error();
+    if (!prm || !base_bt || !seq_lens || !out) return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: null argument");
+    const int32_t A = prm->n_agents, ps = prm->page_size, mp = prm->max_pages;
+    if (A < 1 || prm->hkv < 1 || prm->hq < 1 || ps < 1 || mp < 1 || prm->pages_per_split < 0)
+        return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: bad sizes");
+    if (prm->hq % prm->hkv) return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: hq % hkv != 0");
+    const int32_t g = prm->hq / prm->hkv;
+    if (g > fkv::kMaxRows) return fkv::fail(FKV_ERR_UNSUPPORTED, "fkv_decode_plan_create: more than 16 query heads per KV head");
+    const int32_t ag = fkv::kMaxRows / g;
+    std::vector<int32_t> npages(A);
+    int32_t P = 0;
+    for (int32_t a = 0; a < A; ++a) {
+        if (seq_lens[a] < 1) return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: seq_len < 1");
+        npages[a] = (seq_lens[a] + ps - 1) / ps;
+        if (npages[a] > mp) return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: seq_len exceeds max_pages * page_size");
+        P = std::max(P, npages[a]);
+    }
+
+    // 1. segments
+    struct Seg { int32_t first, n; std::vector<int32_t> agents; };
+    std::vector<Seg> segs;
+    std::vector<int32_t> open(A, -1);
+    std::unordered_map<int32_t, int32_t> group_of_page;
+    std::vector<std::vector<int32_t>> groups;
+    for (int32_t i = 0; i < P; ++i) {
+        group_of_page.clear();
+        groups.clear();
+        for (int32_t a = 0; a < A; ++a) {
+            if (i >= npages[a]) continue;
+            const int32_t pg = base_bt[(int64_t)a * mp + i];
+            auto it = group_of_page.find(pg);
+            if (it == group_of_page.end()) {
+                group_of_page.emplace(pg, (int32_t)groups.size());
+                groups.push_back({a});
+            } else {
+                groups[it->second].push_back(a);
+            }
+        }
+        for (auto &gr : groups) {
+            const int32_t s = open[gr[0]];
+            if (s >= 0 && segs[s].first + segs[s].n == i && segs[s].agents == gr) {
+                segs[s].n += 1;
+            } else {
+                segs.push_back({i, 1, gr});
+                for (int32_t a : gr) open[a] = (int32_t)segs.size() - 1;
+            }
+        }
+    }
+
+    // 2. pages per split
+    int64_t units = 0;  // page x agent-group units per KV head
+    for (auto &s : segs) units += (int64_t)s.n * ((int64_t)(s.agents.size() + ag - 1) / ag);
+    int32_t pps = prm->pages_per_split;
+    if (pps == 0) {
+        const int64_t cus = prm->num_cus > 0 ? prm->num_cus : 256;
+        const int64_t target_items = std::max<int64_t>(1, (4 * cus + prm->hkv - 1) / prm->hkv);
+        pps = (int32_t)std::max<int64_t>(4, (units + target_items - 1) / target_items);
+        pps = std::min(pps, 1024);
+        pps = (pps + 3) / 4 * 4;
+    }
+
+    // 3. work items, clustered by (segment, split)
+    struct Item { int32_t p0, p1; std::vector<int32_t> agents; };
+    std::vector<Item> items;
+    std::vector<std::pair<int32_t, int32_t>> clusters;  // [first item, item count)
+    std::vector<double> cluster_cost;
+    for (auto &s : segs) {
+        for (int32_t p0 = s.first; p0 < s.first + s.n; p0 += pps) {
+            const int32_t p1 = std::min(p0 + pps, s.first + s.n);
+            const int32_t first = (int32_t)items.size();
+            double cost = 0;
+            for (size_t k = 0; k < s.agents.size(); k += ag) {
+                Item it{p0, p1, {}};
+                for (size_t j = k; j < std::min(s.agents.size(), k + ag); ++j) it.agents.push_back(s.agents[j]);
+                cost += (double)(p1 - p0) * (2.0 + (double)it.agents.size());
+                items.push_back(std::move(it));
+            }
+            clusters.push_back({first, (int32_t)items.size() - first});
+            cluster_cost.push_back(cost);
+        }
+    }
+    const int32_t n_items = (int32_t)items.size();
+    const int32_t hkv = prm->hkv;
+
+    // 4. workgroup order: clusters dealt to XCDs by least accumulated cost
+    std::vector<std::vector<int32_t>> per_xcd(kNumXcd);
+    std::vector<double> load(kNumXcd, 0.0);
+    std::vector<int32_t> order(clusters.size());
+    for (size_t c = 0; c < clusters.size(); ++c) order[c] = (int32_t)c;
+    std::stable_sort(order.begin(), order.end(), [&](int32_t x, int32_t y) { return cluster_cost[x] > cluster_cost[y]; });
+    std::vector<int32_t> cluster_xcd(clusters.size());
+    for (int32_t c : order) {
+        const int32_t x = (int32_t)(std::min_element(load.begin(), load.end()) - load.begin());
+        load[x] += cluster_cost[c] * hkv;
+        cluster_xcd[c] = x;
+    }
+    for (size_t c = 0; c < clusters.size(); ++c) {
+        auto &lst = per_xcd[cluster_xcd[c]];
+        for (int32_t h = 0; h < hkv; ++h)
+            for (int32_t k = 0; k < clusters[c].second; ++k) lst.push_back((clusters[c].first + k) * hkv + h);
+    }
+    size_t depth = 0;
+    for (auto &l : per_xcd) depth = std::max(depth, l.size());
+    const int32_t n_blocks = (int32_t)(depth * kNumXcd);
+
+    // 5. partial slots per agent (CSR)
+    std::vector<std::vector<int32_t>> slots(A);
+    for (int32_t w = 0; w < n_items; ++w)
+        for (size_t j = 0; j < items[w].agents.size(); ++j)
+            slots[items[w].agents[j]].push_back((int32_t)(((int64_t)w * hkv) * fkv::kMaxRows + (int64_t)j * g));
+
+    // 6. serialise
+    auto *pl = new fkv_plan();
+    pl->hkv = hkv;
+    pl->g = g;
+    pl->n_agents = A;
+    pl->max_pages_used = P;
+    int64_t total_slots = 0;
+    for (auto &v : slots) total_slots += (int64_t)v.size();
+    const int64_t off_items = fkv::kHeaderWords;
+    const int64_t off_blocks = off_items + (int64_t)n_items * fkv::kItemWords;
+    const int64_t off_ptr = off_blocks + n_blocks;
+    const int64_t off_slot = off_ptr + A + 1;
+    const int64_t total = off_slot + total_slots;
+    if (total > INT32_MAX) {
+        delete pl;
+        return fkv::fail(FKV_ERR_UNSUPPORTED, "fkv_decode_plan_create: plan too large");
+    }
+    auto &w = pl->words;
+    w.assign(total, 0);
+    w[fkv::H_MAGIC] = fkv::kPlanMagic;
+    w[fkv::H_N_ITEMS] = n_items;
+    w[fkv::H_N_BLOCKS] = n_blocks;
+    w[fkv::H_N_AGENTS] = A;
+    w[fkv::H_HKV] = hkv;
+    w[fkv::H_GROUP] = g;
+    w[fkv::H_AGENTS_PER_ITEM] = ag;
+    w[fkv::H_OFF_ITEMS] = (int32_t)off_items;
+    w[fkv::H_OFF_BLOCKS] = (int32_t)off_blocks;
+    w[fkv::H_OFF_AGENT_PTR] = (int32_t)off_ptr;
+    w[fkv::H_OFF_AGENT_SLOT] = (int32_t)off_slot;
+    w[fkv::H_TOTAL_WORDS] = (int32_t)total;
+    w[fkv::H_PAGES_PER_SPLIT] = pps;
+    w[fkv::H_PAGE_SIZE] = ps;
+    w[fkv::H_N_SEGMENTS] = (int32_t)segs.size();
+    for (int32_t i = 0; i < n_items; ++i) {
+        int32_t *r = &w[off_items + (int64_t)i * fkv::kItemWords];
+        r[0] = items[i].p0;
+        r[1] = items[i].p1;
+        r[2] = items[i].agents[0];
+        r[3] = (int32_t)items[i].agents.size();
+        for (int32_t j = 0; j < fkv::kMaxRows; ++j) r[4 + j] = j < r[3] ? items[i].agents[j] : -1;
+    }
+    for (int32_t b = 0; b < n_blocks; ++b) {
+        const auto &lst = per_xcd[b % kNumXcd];
+        const size_t k = (size_t)(b / kNumXcd);
+        w[off_blocks + b] = k < lst.size() ? lst[k] : -1;
+    }
+    int64_t pos = off_slot;
+    for (int32_t a = 0; a < A; ++a) {
+        w[off_ptr + a] = (int32_t)(pos - off_slot);
+        for (int32_t s : slots[a]) w[pos++] = s;
+    }
+    w[off_ptr + A] = (int32_t)(pos - off_slot);
+    for (auto &s : segs) {
+        pl->seg_first_page.push_back(s.first);
+        pl->seg_n_pages.push_back(s.n);
+        pl->seg_agent_off.push_back((int32_t)pl->seg_agents.size());
+        pl->seg_agents.insert(pl->seg_agents.end(), s.agents.begin(), s.agents.end());
+    }
+    *out = pl;
+    return FKV_OK;
+}
+
+void fkv_decode_plan_destroy(fkv_plan *plan) { delete plan; }
+
+fkv_status fkv_decode_plan_info(const fkv_plan *plan, int32_t d, int32_t r, fkv_plan_info *out) {
+    fkv::clear_error();
+    if (!plan || !out || d < 1 || r < 0) return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_info: bad argument");
+    const auto &w = plan->words;
+    out->plan_words = (int64_t)w.size();
+    out->n_items = w[fkv::H_N_ITEMS];
+    out->n_blocks = w[fkv::H_N_BLOCKS];
+    out->n_segments = w[fkv::H_N_SEGMENTS];
+    out->pages_per_split = w[fkv::H_PAGES_PER_SPLIT];
+    const int64_t stride = (int64_t)(d + r + 2 + 3) / 4 * 4;
+    out->workspace_bytes = (int64_t)w[fkv::H_N_ITEMS] * plan->hkv * fkv::kMaxRows * stride * 4;
+    return FKV_OK;
+}
+
+fkv_status fkv_decode_plan_serialize(const fkv_plan *plan, int32_t *out, int64_t capacity_words) {
+    fkv::clear_error();
+    if (!plan || !out) return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_serialize: null argument");
+    if (capacity_words < (int64_t)plan->words.size())
+        return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_serialize: buffer too small");
+    std::copy(plan->words.begin(), plan->words.end(), out);
+    return FKV_OK;
+}
+
+fkv_status fkv_decode_plan_segments(const fkv_plan *plan, int32_t *first_page, int32_t *n_pages,
+                                    int32_t *n_agents, int32_t *agents, int64_t cap) {
+    fkv::clear_error();
+    if (!plan || !first_page || !n_pages || !n_agents || !agents)
+        return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_segments: null argument");
+    if (cap < (int64_t)plan->seg_agents.size()) return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_segments: buffer too small");
+    const size_t ns = plan->seg_first_page.size();
+    for (size_t s = 0; s < ns; ++s) {
+        first_page[s] = plan->seg_first_page[s];
+        n_pages[s] = plan->seg_n_pages[s];
+        const int32_t e = s + 1 < ns ? plan->seg_agent_off[s + 1] : (int32_t)plan->seg_agents.size();
+        n_agents[s] = e - plan->seg_agent_off[s];
+    }
+    std::copy(plan->seg_agents.begin(), plan->seg_agents.end(), agents);
+    return FKV_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,479 @@
+// ResidualAttention chunked prefill for gfx950 (Section 6 prefill kernel,
+// Algorithm 1 with a block of query rows).
+//
+// One workgroup = (agent a, KV head h, block of query tokens); its 128 rows are
+// (query token, query head of h).  Every row of the block belongs to the same
+// agent, so the agent's keys are rebuilt once per 64-key tile and shared by all
+// rows through LDS:
+//   wave w rebuilds page w of the tile:  U^T = B_K^T C_K^T  (MFMA),
+//                                        K_lora = RoPE_p(U) (rotate-half, fp32),
+//                                        K = K_base + K_lora -> bf16 -> LDS
+//   then every wave, for its 32 rows:    S^T = K Q^T        (16x16x32 MFMA)
+//                                        causal mask + online softmax
+//                                        O^T   += V^T P^T   (16x16x32 MFMA)
+//                                        acc_r^T += C_V^T P^T
+// and at the end O = (O + acc_r . B_V[h]) / l (Eq. 4) is written in bf16.
+//
+// The contraction index of the 16x16x32 products is permuted so that the
+// accumulator tiles of the 16x16x16 rebuild feed them without shuffles: in
+// k-step kk, slot j of lane group grp is head-dim index 32kk + 16(j/4) + 4grp +
+// j%4 for the key products, and key 16(j/4) + 4grp + j%4 of a 32-key half for the
+// value products.  Queries and values are loaded in the same order.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <string>
+
+#include "internal.hpp"
+#include "mfma.hpp"
+
+using namespace fkvk;
+
+namespace {
+
+constexpr int D = 128;
+constexpr int PS = 16;
+constexpr int WAVES = 4;
+constexpr int ROWS_PER_WAVE = 32;          // two 16-row tiles
+constexpr int ROWS_PER_WG = WAVES * ROWS_PER_WAVE;
+constexpr int TILE_KEYS = 64;              // four pages, one per wave
+constexpr float kNegInf = -INFINITY;
+
+struct PrefillArgs {
+    const uint16_t *q, *base_kv, *res_kv, *lora_b;
+    const int32_t *adapter_idx, *base_bt, *res_bt, *seq_lens, *q_indptr;
+    const float *rope_cos, *rope_sin;
+    uint16_t *out;
+    int32_t n_agents, hq, hkv, max_pages, blocks_per_agent_head;
+    float scale_log2;
+};
+
+template <int R, int G, bool ROPE>
+struct PrefillShape {
+    static constexpr int RT = R == 0 ? 0 : (R + 15) / 16;
+    static constexpr int TOK_PER_WG = ROWS_PER_WG / G;
+    static constexpr int SK_BYTES = 4 * 4 * 64 * 16;          // [page][kk][lane] 16 B
+    static constexpr int SV_BYTES = 4 * PS * D * 2;             // [page][d][16] bf16
+    static constexpr int SCV_BYTES = R > 0 ? 4 * R * PS * 2 : 16;  // [page][rho][16] bf16
+    static constexpr int SBK_BYTES = (R > 0 && ROPE) ? RT * 8 * 64 * 8 : 16;  // B_K^T fragments
+    static constexpr int SBV_BYTES = R > 0 ? R * D * 4 : 16;    // B_V[h] slice, fp32
+    static constexpr int SACC_BYTES = R > 0 ? ROWS_PER_WG * R * 4 : 16;  // acc_r rows for the epilogue
+    static constexpr int EPI_BYTES = SBV_BYTES + SACC_BYTES;
+    static constexpr int MAIN_BYTES = SK_BYTES + SV_BYTES + SCV_BYTES;
+    static constexpr int LDS_BYTES = (MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES) + SBK_BYTES;
+};
+
+template <int R, int G, bool ROPE>
+__global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
+    using S = PrefillShape<R, G, ROPE>;
+    constexpr int RT = S::RT;
+    constexpr int TPW = S::TOK_PER_WG;
+    __shared__ __attribute__((aligned(16))) unsigned char lds[S::LDS_BYTES];
+    u32x4 *sK = reinterpret_cast<u32x4 *>(lds);
+    uint16_t *sV = reinterpret_cast<uint16_t *>(lds + S::SK_BYTES);
+    uint16_t *sCV = reinterpret_cast<uint16_t *>(lds + S::SK_BYTES + S::SV_BYTES);
+    u32x2 *sBK = reinterpret_cast<u32x2 *>(lds + (S::MAIN_BYTES > S::EPI_BYTES ? S::MAIN_BYTES : S::EPI_BYTES));
+    float *sBV = reinterpret_cast<float *>(lds);
+    float *sAcc = reinterpret_cast<float *>(lds + S::SBV_BYTES);
+
+    const int hkv = p.hkv;
+    const int bpa = p.blocks_per_agent_head;
+    const int a = blockIdx.x / (hkv * bpa);
+    const int rem = blockIdx.x - a * hkv * bpa;
+    const int h = rem / bpa;
+    const int qb = rem - h * bpa;
+    const int q0 = p.q_indptr[a], nq = p.q_indptr[a + 1] - q0;
+    const int tok_begin = qb * TPW;
+    if (tok_begin >= nq) return;
+    const int L = p.seq_lens[a];
+    const int P0 = L - nq;  // position of the chunk's first query
+    const int ad = R > 0 ? p.adapter_idx[a] : -1;
+
+    const int lane = threadIdx.x & 63;
+    const int wave = uniform(threadIdx.x >> 6);
+    const int col = lane & 15, grp = lane >> 4;
+    const int64_t n = (int64_t)hkv * D;
+
+    // rows of this lane in the two 16-row tiles of the wave
+    int row_tok[2], row_pos[2];
+    bool row_ok[2];
+    u32x4 qf[2][4];
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+        const int r = wave * ROWS_PER_WAVE + nt * 16 + col;
+        const int t = tok_begin + r / G;
+        const int jj = r % G;
+        row_ok[nt] = t < nq;
+        row_tok[nt] = t;
+        row_pos[nt] = P0 + t;
+        const uint16_t *qr = p.q + ((int64_t)(q0 + (row_ok[nt] ? t : 0)) * p.hq + h * G + jj) * D;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+            u32x4 v = {0, 0, 0, 0};
+            if (row_ok[nt]) {
+                const u32x2 lo = ldg64(qr + 32 * kk + 4 * grp);
+                const u32x2 hi = ldg64(qr + 32 * kk + 16 + 4 * grp);
+                v = u32x4{lo.x, lo.y, hi.x, hi.y};
+            }
+            qf[nt][kk] = v;
+        }
+    }
+
+    // B_K^T fragments for the rebuild: lane holds B_K[16t + 4grp + i][h*D + 16mt + col]
+    if constexpr (R > 0 && ROPE) {
+        if (ad >= 0) {
+            const uint16_t *bk = p.lora_b + (int64_t)ad * 2 * R * n + (int64_t)h * D;
+            for (int idx = threadIdx.x; idx < RT * 8 * 64; idx += 256) {
+                const int ln = idx & 63, rest = idx >> 6;
+                const int mt = rest & 7, t = rest >> 3;
+                const int c = ln & 15, gg = ln >> 4;
+                uint32_t w[2];
+#pragma unroll
+                for (int j = 0; j < 2; ++j) {
+                    const int r0 = 16 * t + 4 * gg + 2 * j;
+                    const uint16_t lo = r0 < R ? bk[(int64_t)r0 * n + 16 * mt + c] : (uint16_t)0;
+                    const uint16_t hi = r0 + 1 < R ? bk[(int64_t)(r0 + 1) * n + 16 * mt + c] : (uint16_t)0;
+                    w[j] = (uint32_t)lo | ((uint32_t)hi << 16);
+                }
+                sBK[idx] = u32x2{w[0], w[1]};
+            }
+        }
+    }
+    // RoPE off: the residual key term of row j is (B_K q_j) . c_p; fold it as an extra
+    // contraction over the rank: S^T += C_K (B_K q)^T.
+    u32x2 wq[2][RT > 0 ? RT : 1];
+    if constexpr (R > 0 && !ROPE) {
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+            for (int t = 0; t < RT; ++t) {
+                f32x4 acc = {0, 0, 0, 0};
+                if (ad >= 0) {
+                    const int rho = 16 * t + col;
+                    const uint16_t *bk = p.lora_b + (int64_t)ad * 2 * R * n + (int64_t)rho * n + (int64_t)h * D;
+#pragma unroll
+                    for (int kk = 0; kk < 4; ++kk) {
+                        u32x4 av = {0, 0, 0, 0};
+                        if (rho < R) {
+                            const u32x2 lo = ldg64(bk + 32 * kk + 4 * grp);
+                            const u32x2 hi = ldg64(bk + 32 * kk + 16 + 4 * grp);
+                            av = u32x4{lo.x, lo.y, hi.x, hi.y};
+                        }
+                        acc = mfma32(av, qf[nt][kk], acc);  // W^T[rho][row]
+                    }
+                }
+                wq[nt][t] = pack4(acc);
+            }
+    }
+    __syncthreads();
+
+    f32x4 oacc[8][2];
+#pragma unroll
+    for (int mt = 0; mt < 8; ++mt) oacc[mt][0] = oacc[mt][1] = f32x4{0, 0, 0, 0};
+    f32x4 racc[RT > 0 ? RT : 1][2];
+#pragma unroll
+    for (int t = 0; t < (RT > 0 ? RT : 1); ++t) racc[t][0] = racc[t][1] = f32x4{0, 0, 0, 0};
+    float m_run[2] = {kNegInf, kNegInf}, l_run[2] = {0.f, 0.f};
+
+    const int n_pages = (L + PS - 1) / PS;
+    const int last_pos = P0 + (tok_begin + TPW < nq ? tok_begin + TPW : nq) - 1;
+    const int n_tiles = last_pos / TILE_KEYS + 1;
+    const int32_t *btb = p.base_bt + (int64_t)a * p.max_pages;
+    const int32_t *btr = R > 0 ? p.res_bt + (int64_t)a * p.max_pages : nullptr;
+    const int64_t kv_block = (int64_t)PS * D;
+
+    for (int tile = 0; tile < n_tiles; ++tile) {
+        // ---- stage: wave w rebuilds page w of the tile into LDS ----
+        {
+            const int pg = tile * 4 + wave;
+            const int tok0 = pg * PS;
+            const bool have = pg < n_pages;
+            const int bpage = have ? btb[pg] : 0;
+            const uint16_t *kblk = p.base_kv + ((int64_t)bpage * 2 * hkv + h) * kv_block;
+            const uint16_t *vblk = kblk + (int64_t)hkv * kv_block;
+            const int vis = L - tok0;  // valid keys in this page
+            // K_base in the permuted 16x16x32 A layout
+            f32x4 kacc[8];
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) {
+                u32x2 kb = have ? ldg64(kblk + col * D + 16 * mt + 4 * grp) : u32x2{0, 0};
+                kacc[mt] = f32x4{bf16_lo(kb.x), bf16_hi(kb.x), bf16_lo(kb.y), bf16_hi(kb.y)};
+            }
+            const uint16_t *rb = nullptr;
+            if constexpr (R > 0) {
+                if (ad >= 0 && have) rb = p.res_kv + (int64_t)btr[pg] * 2 * PS * R;
+            }
+            if constexpr (R > 0 && ROPE) {
+                if (rb) {
+                    f32x4 u[8];
+#pragma unroll
+                    for (int mt = 0; mt < 8; ++mt) u[mt] = f32x4{0, 0, 0, 0};
+#pragma unroll
+                    for (int t = 0; t < RT; ++t) {
+                        const u32x2 ck = (16 * t + 4 * grp < R) ? ldg64(rb + col * R + 16 * t + 4 * grp) : u32x2{0, 0};
+#pragma unroll
+                        for (int mt = 0; mt < 8; ++mt) u[mt] = mfma16(sBK[(t * 8 + mt) * 64 + lane], ck, u[mt]);
+                    }
+                    const float *cr = p.rope_cos + (int64_t)(tok0 + col) * (D / 2) + 4 * grp;
+                    const float *sr = p.rope_sin + (int64_t)(tok0 + col) * (D / 2) + 4 * grp;
+#pragma unroll
+                    for (int mt = 0; mt < 4; ++mt) {
+                        const f32x4 cs = *reinterpret_cast<const f32x4 *>(cr + 16 * mt);
+                        const f32x4 sn = *reinterpret_cast<const f32x4 *>(sr + 16 * mt);
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const float x = u[mt][i], y = u[mt + 4][i];
+                            kacc[mt][i] += x * cs[i] - y * sn[i];
+                            kacc[mt + 4][i] += y * cs[i] + x * sn[i];
+                        }
+                    }
+                }
+            }
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) {
+                const u32x2 lo = pack4(kacc[2 * kk]), hi = pack4(kacc[2 * kk + 1]);
+                sK[(wave * 4 + kk) * 64 + lane] = u32x4{lo.x, lo.y, hi.x, hi.y};
+            }
+            // V page as stored ([d][16 keys]); keys past the sequence end are zeroed
+            for (int e = lane; e < D * PS / 4; e += 64) {
+                u32x2 v = have ? ldg64(vblk + 4 * e) : u32x2{0, 0};
+                const int k0 = (4 * e) % PS;
+                if (k0 + 0 >= vis) v.x &= 0xffff0000u;
+                if (k0 + 1 >= vis) v.x &= 0x0000ffffu;
+                if (k0 + 2 >= vis) v.y &= 0xffff0000u;
+                if (k0 + 3 >= vis) v.y &= 0x0000ffffu;
+                *reinterpret_cast<u32x2 *>(sV + wave * D * PS + 4 * e) = v;
+            }
+            if constexpr (R > 0) {
+                for (int e = lane; e < R * PS / 4; e += 64) {
+                    u32x2 v = rb ? ldg64(rb + PS * R + 4 * e) : u32x2{0, 0};
+                    const int k0 = (4 * e) % PS;
+                    if (k0 + 0 >= vis) v.x &= 0xffff0000u;
+                    if (k0 + 1 >= vis) v.x &= 0x0000ffffu;
+                    if (k0 + 2 >= vis) v.y &= 0xffff0000u;
+                    if (k0 + 3 >= vis) v.y &= 0x0000ffffu;
+                    *reinterpret_cast<u32x2 *>(sCV + wave * R * PS + 4 * e) = v;
+                }
+            }
+        }
+        __syncthreads();
+
+        // ---- scores for the 64 keys of the tile, 2 row tiles ----
+        f32x4 sacc[4][2];
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt) {
+            sacc[kt][0] = sacc[kt][1] = f32x4{0, 0, 0, 0};
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) {
+                const u32x4 kf = sK[(kt * 4 + kk) * 64 + lane];
+                sacc[kt][0] = mfma32(kf, qf[0][kk], sacc[kt][0]);
+                sacc[kt][1] = mfma32(kf, qf[1][kk], sacc[kt][1]);
+            }
+        }
+        if constexpr (R > 0 && !ROPE) {
+            if (ad >= 0) {
+#pragma unroll
+                for (int kt = 0; kt < 4; ++kt) {
+                    const int pg = tile * 4 + kt;
+                    if (pg >= n_pages) continue;
+                    const uint16_t *rb = p.res_kv + (int64_t)btr[pg] * 2 * PS * R;
+#pragma unroll
+                    for (int t = 0; t < RT; ++t) {
+                        const u32x2 ck = (16 * t + 4 * grp < R) ? ldg64(rb + col * R + 16 * t + 4 * grp) : u32x2{0, 0};
+                        sacc[kt][0] = mfma16(ck, wq[0][t], sacc[kt][0]);
+                        sacc[kt][1] = mfma16(ck, wq[1][t], sacc[kt][1]);
+                    }
+                }
+            }
+        }
+
+        // ---- causal mask + online softmax (rows live in lanes) ----
+        u32x2 pf[4][2];
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+            float sv[4][4];
+            float mx = kNegInf;
+#pragma unroll
+            for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int key = tile * TILE_KEYS + kt * PS + 4 * grp + i;
+                    sv[kt][i] = (row_ok[nt] && key <= row_pos[nt]) ? sacc[kt][nt][i] * p.scale_log2 : kNegInf;
+                    mx = fmaxf(mx, sv[kt][i]);
+                }
+            mx = fmaxf(mx, __shfl_xor(mx, 16));
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const float m_new = fmaxf(m_run[nt], mx);
+            const float m_use = m_new == kNegInf ? 0.f : m_new;
+            const float alpha = fast_exp2(m_run[nt] - m_use);
+            float ps = 0.f;
+#pragma unroll
+            for (int kt = 0; kt < 4; ++kt) {
+                f32x4 pv;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    pv[i] = fast_exp2(sv[kt][i] - m_use);
+                    ps += pv[i];
+                }
+                pf[kt][nt] = pack4(pv);
+            }
+            l_run[nt] = l_run[nt] * alpha + ps;
+            m_run[nt] = m_new;
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) oacc[mt][nt] *= alpha;
+#pragma unroll
+            for (int t = 0; t < RT; ++t) racc[t][nt] *= alpha;
+        }
+
+        // ---- O^T += V^T P^T and acc_r^T += C_V^T P^T over two 32-key halves ----
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            const u32x4 pb0 = u32x4{pf[2 * half][0].x, pf[2 * half][0].y, pf[2 * half + 1][0].x, pf[2 * half + 1][0].y};
+            const u32x4 pb1 = u32x4{pf[2 * half][1].x, pf[2 * half][1].y, pf[2 * half + 1][1].x, pf[2 * half + 1][1].y};
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) {
+                const u32x2 lo = *reinterpret_cast<const u32x2 *>(sV + (2 * half) * D * PS + (16 * mt + col) * PS + 4 * grp);
+                const u32x2 hi = *reinterpret_cast<const u32x2 *>(sV + (2 * half + 1) * D * PS + (16 * mt + col) * PS + 4 * grp);
+                const u32x4 va = u32x4{lo.x, lo.y, hi.x, hi.y};
+                oacc[mt][0] = mfma32(va, pb0, oacc[mt][0]);
+                oacc[mt][1] = mfma32(va, pb1, oacc[mt][1]);
+            }
+            if constexpr (R > 0) {
+                if (ad >= 0) {
+#pragma unroll
+                    for (int t = 0; t < RT; ++t) {
+                        const int rho = 16 * t + col;
+                        u32x4 ca = {0, 0, 0, 0};
+                        if (rho < R) {
+                            const u32x2 lo = *reinterpret_cast<const u32x2 *>(sCV + (2 * half) * R * PS + rho * PS + 4 * grp);
+                            const u32x2 hi = *reinterpret_cast<const u32x2 *>(sCV + (2 * half + 1) * R * PS + rho * PS + 4 * grp);
+                            ca = u32x4{lo.x, lo.y, hi.x, hi.y};
+                        }
+                        racc[t][0] = mfma32(ca, pb0, racc[t][0]);
+                        racc[t][1] = mfma32(ca, pb1, racc[t][1]);
+                    }
+                }
+            }
+        }
+        __syncthreads();
+    }
+
+    // ---- epilogue: O = (acc + acc_r . B_V[h]) / l ----
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+        l_run[nt] += __shfl_xor(l_run[nt], 16);
+        l_run[nt] += __shfl_xor(l_run[nt], 32);
+    }
+    if constexpr (R > 0) {
+        if (ad >= 0) {
+            const uint16_t *bv = p.lora_b + ((int64_t)ad * 2 + 1) * R * n + (int64_t)h * D;
+            for (int e = threadIdx.x; e < R * D; e += 256) sBV[e] = bf16_to_f32(bv[(int64_t)(e / D) * n + (e % D)]);
+#pragma unroll
+            for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+                for (int t = 0; t < RT; ++t)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int rho = 16 * t + 4 * grp + i;
+                        if (rho < R) sAcc[(wave * ROWS_PER_WAVE + nt * 16 + col) * R + rho] = racc[t][nt][i];
+                    }
+            __syncthreads();
+#pragma unroll
+            for (int nt = 0; nt < 2; ++nt) {
+                const float *ar = sAcc + (wave * ROWS_PER_WAVE + nt * 16 + col) * R;
+                for (int rho = 0; rho < R; ++rho) {
+                    const float c = ar[rho];
+#pragma unroll
+                    for (int mt = 0; mt < 8; ++mt)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) oacc[mt][nt][i] += c * sBV[rho * D + 16 * mt + 4 * grp + i];
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+        if (!row_ok[nt]) continue;
+        const int r = wave * ROWS_PER_WAVE + nt * 16 + col;
+        const float inv = l_run[nt] > 0.f ? 1.f / l_run[nt] : 0.f;
+        uint16_t *orow = p.out + ((int64_t)(q0 + row_tok[nt]) * p.hq + h * G + r % G) * D;
+#pragma unroll
+        for (int mt = 0; mt < 8; ++mt) {
+            f32x4 o = oacc[mt][nt] * inv;
+            *reinterpret_cast<u32x2 *>(orow + 16 * mt + 4 * grp) = pack4(o);
+        }
+    }
+}
+
+template <int R, int G, bool ROPE>
+hipError_t launch_prefill(const PrefillArgs &pa, hipStream_t st, void *const *ev) {
+    using S = PrefillShape<R, G, ROPE>;
+    hipError_t e;
+    if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[0]), st)) != hipSuccess) return e;
+    const int grid = pa.n_agents * pa.hkv * pa.blocks_per_agent_head;
+    (void)sizeof(S);
+    hipLaunchKernelGGL((prefill_kernel<R, G, ROPE>), dim3(grid), dim3(256), 0, st, pa);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[1]), st)) != hipSuccess) return e;
+    return hipSuccess;
+}
+
+template <int G>
+hipError_t dispatch_prefill(int r, bool rope, const PrefillArgs &pa, hipStream_t st, void *const *ev) {
+    switch (r) {
+    case 0: return launch_prefill<0, G, false>(pa, st, ev);
+    case 8: return rope ? launch_prefill<8, G, true>(pa, st, ev) : launch_prefill<8, G, false>(pa, st, ev);
+    case 16: return rope ? launch_prefill<16, G, true>(pa, st, ev) : launch_prefill<16, G, false>(pa, st, ev);
+    case 32: return rope ? launch_prefill<32, G, true>(pa, st, ev) : launch_prefill<32, G, false>(pa, st, ev);
+    case 64: return rope ? launch_prefill<64, G, true>(pa, st, ev) : launch_prefill<64, G, false>(pa, st, ev);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+namespace fkv {
+fkv_status validate_attn_common(const fkv_attn_args *a, const char *who);
+}
+
+extern "C" fkv_status fkv_residual_attention_prefill(const fkv_attn_args *a, void *stream) {
+    fkv::clear_error();
+    fkv_status st = fkv::validate_attn_common(a, "fkv_residual_attention_prefill");
+    if (st != FKV_OK) return st;
+    if (!a->q_indptr || a->n_q < 1)
+        return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_prefill: q_indptr and n_q >= 1 are required");
+    const int g = a->hq / a->hkv;
+    if (g != 4 && g != 8)
+        return fkv::fail(FKV_ERR_UNSUPPORTED, "fkv_residual_attention_prefill: query heads per KV head must be 4 or 8");
+    if (a->rope_cos && (int64_t)a->rope_max_pos < (int64_t)a->max_pages * a->page_size)
+        return fkv::fail(FKV_ERR_INVALID,
+                         "fkv_residual_attention_prefill: RoPE table must cover max_pages * page_size positions");
+    PrefillArgs pa;
+    pa.q = static_cast<const uint16_t *>(a->q);
+    pa.base_kv = static_cast<const uint16_t *>(a->base_kv);
+    pa.res_kv = static_cast<const uint16_t *>(a->res_kv);
+    pa.lora_b = static_cast<const uint16_t *>(a->lora_b);
+    pa.adapter_idx = a->adapter_idx;
+    pa.base_bt = a->base_bt;
+    pa.res_bt = a->res_bt;
+    pa.seq_lens = a->seq_lens;
+    pa.q_indptr = a->q_indptr;
+    pa.rope_cos = a->rope_cos;
+    pa.rope_sin = a->rope_sin;
+    pa.out = static_cast<uint16_t *>(a->out);
+    pa.n_agents = a->n_agents;
+    pa.hq = a->hq;
+    pa.hkv = a->hkv;
+    pa.max_pages = a->max_pages;
+    // an agent's chunk can hold at most n_q rows; blocks past its own chunk exit at once
+    const int tok_per_wg = ROWS_PER_WG / g;
+    pa.blocks_per_agent_head = (a->n_q + tok_per_wg - 1) / tok_per_wg;
+    pa.scale_log2 = a->scale * 1.4426950408889634f;
+    const bool rope = a->rope_cos != nullptr && a->r > 0;
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    hipError_t e = g == 4 ? dispatch_prefill<4>(a->r, rope, pa, hs, a->timing_events)
+                          : dispatch_prefill<8>(a->r, rope, pa, hs, a->timing_events);
+    if (e != hipSuccess)
+        return fkv::fail(FKV_ERR_HIP, std::string("fkv_residual_attention_prefill: launch failed: ") + hipGetErrorString(e));
+    return FKV_OK;
+}

@@ -105,7 +105,7 @@ class Workload:
 
 def _build(name, seed, hq, hkv, d, r, ps, node_parent, node_len, agent_node, suffix_len,
            chunk_len, zero_residual, b_std, chunk_c_from_hidden=False, hidden=4096,
-           rope_theta=500000.0) -> Workload:
+           rope_theta=500000.0, q_std=1.0) -> Workload:
     """Assemble a workload.  Draw order: Q, base K/V per node in tree order, then
     per-agent suffix/chunk base K/V, then C per agent, then B per agent (the
     lengths are drawn by the caller before this, from the same generator)."""
@@ -128,7 +128,7 @@ def _build(name, seed, hq, hkv, d, r, ps, node_parent, node_len, agent_node, suf
     q_offset = np.zeros(A + 1, dtype=np.int64)
     q_offset[1:] = np.cumsum(nq)
     q_pos = np.concatenate([np.arange(seq_len[a] - nq[a], seq_len[a], dtype=np.int64) for a in range(A)])
-    q = _normal_bf16(rng, (int(q_offset[-1]), hq, d))
+    q = _normal_bf16(rng, (int(q_offset[-1]), hq, d), q_std)
     # base rows: tree nodes first (tree order), then each agent's suffix + chunk
     node_row0, rows = [], 0
     for v in range(len(node_len)):
@@ -205,7 +205,7 @@ def _build(name, seed, hq, hkv, d, r, ps, node_parent, node_len, agent_node, suf
 def fanout(name: str, seed: int, *, n_agents: int, prefix: int, suffix_lo: int, suffix_hi: int,
            hq: int, hkv: int, d: int = 128, r: int, ps: int = 16, b_std: float = 0.02,
            chunk: int = 0, zero_residual: Sequence[int] = (), chunk_c_from_hidden: bool = False,
-           fixed_suffix: Optional[int] = None) -> Workload:
+           fixed_suffix: Optional[int] = None, q_std: float = 1.0) -> Workload:
     """N agents forked from one shared prefix, each with a private suffix
     uniform in [suffix_lo, suffix_hi] (or ``fixed_suffix``) and an optional
     appended prefill chunk."""
@@ -215,7 +215,20 @@ def fanout(name: str, seed: int, *, n_agents: int, prefix: int, suffix_lo: int, 
     else:
         suffix = [int(x) for x in rng.integers(suffix_lo, suffix_hi + 1, size=n_agents)]
     return _build(name, rng, hq, hkv, d, r, ps, [-1], [prefix], [0] * n_agents, suffix,
-                  [chunk] * n_agents, set(zero_residual), b_std, chunk_c_from_hidden)
+                  [chunk] * n_agents, set(zero_residual), b_std, chunk_c_from_hidden, q_std=q_std)
+
+
+def tree(name: str, seed: int, *, node_parent: Sequence[int], node_len: Sequence[int],
+         agent_node: Sequence[int], suffix_lo: int, suffix_hi: int, hq: int, hkv: int, d: int = 128, r: int,
+         ps: int = 16, b_std: float = 0.02, chunk: Sequence[int] = (), zero_residual: Sequence[int] = (),
+         q_std: float = 1.0) -> Workload:
+    """Agents on a general fork tree (node_parent / node_len), each with a private suffix."""
+    rng = np.random.default_rng(seed)
+    A = len(agent_node)
+    suffix = [int(x) for x in rng.integers(suffix_lo, suffix_hi + 1, size=A)]
+    ch = list(chunk) if len(chunk) else [0] * A
+    return _build(name, rng, hq, hkv, d, r, ps, list(node_parent), list(node_len), list(agent_node), suffix,
+                  ch, set(zero_residual), b_std, q_std=q_std)
 
 
 def config(cfg: int, seed: Optional[int] = None) -> Workload:
