@@ -222,6 +222,8 @@ typedef struct {
     int32_t n_agents, hq, hkv, d, r, page_size, max_pages;
     int32_t rope_max_pos;       /* rows of the RoPE tables; every key position must be below it */
     int32_t n_q;                /* prefill: total query rows (= q_indptr[n_agents]) */
+    int32_t max_q_per_agent;    /* prefill: largest q_indptr[a+1] - q_indptr[a]; 0 = n_q.  Rows beyond
+                                   it are not computed, so it must not be understated. */
     float scale;                /* softmax scale; typically 1/sqrt(d) */
     void *const *timing_events; /* optional, host array of hipEvent_t: decode records [0] before its first
                                    kernel, [1] between its two kernels and [2] after the second; prefill

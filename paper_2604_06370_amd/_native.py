@@ -70,7 +70,7 @@ class fkv_attn_args(ctypes.Structure):
                 ("plan", c_vp), ("q_indptr", c_vp), ("workspace", c_vp), ("workspace_bytes", c_sz), ("out", c_vp),
                 ("n_agents", c_i32), ("hq", c_i32), ("hkv", c_i32), ("d", c_i32), ("r", c_i32),
                 ("page_size", c_i32), ("max_pages", c_i32), ("rope_max_pos", c_i32), ("n_q", c_i32),
-                ("scale", c_f32), ("timing_events", c_vp)]
+                ("max_q_per_agent", c_i32), ("scale", c_f32), ("timing_events", c_vp)]
 
 
 def _sig(name, restype, argtypes):

@@ -37,6 +37,7 @@ constexpr int WAVES = 4;
 constexpr int ROWS_PER_WAVE = 32;          // two 16-row tiles
 constexpr int ROWS_PER_WG = WAVES * ROWS_PER_WAVE;
 constexpr int TILE_KEYS = 64;              // four pages, one per wave
+constexpr int kXcds = 8;
 constexpr float kNegInf = -INFINITY;
 
 struct PrefillArgs {
@@ -76,12 +77,16 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
     float *sBV = reinterpret_cast<float *>(lds);
     float *sAcc = reinterpret_cast<float *>(lds + S::SBV_BYTES);
 
+    // Consecutive workgroup ids go round-robin to the 8 XCDs: keep all query blocks of one
+    // (agent, KV head) on one XCD so the key/value tiles they all stream hit that XCD's L2.
     const int hkv = p.hkv;
     const int bpa = p.blocks_per_agent_head;
-    const int a = blockIdx.x / (hkv * bpa);
-    const int rem = blockIdx.x - a * hkv * bpa;
-    const int h = rem / bpa;
-    const int qb = rem - h * bpa;
+    const int xcd = blockIdx.x % kXcds, local = blockIdx.x / kXcds;
+    const int pair = (local / bpa) * kXcds + xcd;
+    const int qb = local - (local / bpa) * bpa;
+    if (pair >= p.n_agents * hkv) return;
+    const int a = pair / hkv;
+    const int h = pair - a * hkv;
     const int q0 = p.q_indptr[a], nq = p.q_indptr[a + 1] - q0;
     const int tok_begin = qb * TPW;
     if (tok_begin >= nq) return;
@@ -410,7 +415,8 @@ hipError_t launch_prefill(const PrefillArgs &pa, hipStream_t st, void *const *ev
     using S = PrefillShape<R, G, ROPE>;
     hipError_t e;
     if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[0]), st)) != hipSuccess) return e;
-    const int grid = pa.n_agents * pa.hkv * pa.blocks_per_agent_head;
+    const int pairs = (pa.n_agents * pa.hkv + kXcds - 1) / kXcds * kXcds;
+    const int grid = pairs * pa.blocks_per_agent_head;
     (void)sizeof(S);
     hipLaunchKernelGGL((prefill_kernel<R, G, ROPE>), dim3(grid), dim3(256), 0, st, pa);
     if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -465,9 +471,11 @@ extern "C" fkv_status fkv_residual_attention_prefill(const fkv_attn_args *a, voi
     pa.hq = a->hq;
     pa.hkv = a->hkv;
     pa.max_pages = a->max_pages;
-    // an agent's chunk can hold at most n_q rows; blocks past its own chunk exit at once
+    // query blocks per (agent, KV head); blocks past an agent's own chunk exit at once
     const int tok_per_wg = ROWS_PER_WG / g;
-    pa.blocks_per_agent_head = (a->n_q + tok_per_wg - 1) / tok_per_wg;
+    const int maxq = a->max_q_per_agent > 0 ? a->max_q_per_agent : a->n_q;
+    if (maxq > a->n_q) return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_prefill: max_q_per_agent > n_q");
+    pa.blocks_per_agent_head = (maxq + tok_per_wg - 1) / tok_per_wg;
     pa.scale_log2 = a->scale * 1.4426950408889634f;
     const bool rope = a->rope_cos != nullptr && a->r > 0;
     hipStream_t hs = static_cast<hipStream_t>(stream);

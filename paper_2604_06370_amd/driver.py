@@ -82,6 +82,7 @@ class LoadedWorkload:
                                   hkv, d, r, ps)
 
         self.fill_plans = []
+        self.append_plans = []
         for a in range(A):
             L0 = len(wl.fork_tokens[a])
             release_some(0, (L0 + ps - 1) // ps + 1)
@@ -98,6 +99,7 @@ class LoadedWorkload:
                 fp = self.tree.cow_append(a, wl.chunk_tokens[a])
                 rt.page_copy(fp.copies, self.base_kv, self.res_kv, hkv, d, r, ps)
                 fill(a, L0, fp.seq_len, fp.base_valid, fp.res_valid)
+                self.append_plans.append(fp)
         del base_k_dev, base_v_dev
         torch.cuda.synchronize(self.device)
         self.q_all = _bf16(wl.q, self.device)
@@ -166,7 +168,7 @@ class LoadedWorkload:
                                   base_bt=st["base_bt"], res_bt=st["res_bt"] if wl.r > 0 else None,
                                   seq_lens=st["seq_lens"], out=st["out"], hq=wl.hq, hkv=wl.hkv, d=wl.d, r=wl.r,
                                   page_size=wl.page_size, rope=self.rope_tab, q_indptr=st["q_indptr"],
-                                  n_q=int(indptr[-1]))
+                                  n_q=int(indptr[-1]), max_q_per_agent=int(max(counts)))
         self._prefill = st
         return st
 

@@ -207,7 +207,7 @@ def scatter_tokens(bt_base_row: Optional[torch.Tensor], bt_res_row: Optional[tor
 
 
 def make_args(*, q, base_kv, res_kv, lora_b, adapter_idx, base_bt, res_bt, seq_lens, out, hq, hkv, d, r,
-              page_size, rope=None, plan_dev=None, q_indptr=None, workspace=None, n_q=0,
+              page_size, rope=None, plan_dev=None, q_indptr=None, workspace=None, n_q=0, max_q_per_agent=0,
               scale: Optional[float] = None) -> N.fkv_attn_args:
     p = lambda t: t.data_ptr() if t is not None else None
     a = N.fkv_attn_args()
@@ -223,6 +223,7 @@ def make_args(*, q, base_kv, res_kv, lora_b, adapter_idx, base_bt, res_bt, seq_l
     a.max_pages = base_bt.shape[1]
     a.rope_max_pos = rope[0].shape[0] if rope is not None else 0
     a.n_q = n_q
+    a.max_q_per_agent = max_q_per_agent
     a.scale = scale if scale is not None else 1.0 / float(np.sqrt(d))
     return a
 
