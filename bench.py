@@ -87,6 +87,9 @@ def main():
     ap.add_argument("--pps", type=int, default=0, help="pages per split (0 = automatic)")
     ap.add_argument("--copies", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mb", type=int, default=0,
+                    help="also run one plain device copy of this many MiB (reference kernel of known size "
+                         "for calibrating HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (the kernel would shard by KV "
@@ -117,6 +120,21 @@ def main():
             e.record(stream)  # materialise the HIP event
     import ctypes
     handles = [(ctypes.c_void_p * 3)(*[e.cuda_event for e in trio]) for trio in ev]
+
+    copy_probe = None
+    if args.copy_probe_mb > 0:
+        nbytes = args.copy_probe_mb << 20
+        src = torch.ones(nbytes // 2, dtype=torch.bfloat16, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        dst.copy_(src)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        copy_probe = {"bytes_read": nbytes, "bytes_written": nbytes, "ms": ms, "GBps_read_plus_write": 2 * nbytes / ms / 1e6}
+        del src, dst
 
     for i in range(args.warmup):
         lws[i % len(lws)].decode()
@@ -153,6 +171,8 @@ def main():
                      "combine_ms": float(comb_ms.mean()), "call_GBps": call_gbs},
         "bytes": byts,
     }
+    if copy_probe is not None:
+        out["copy_probe"] = copy_probe
     if not args.no_cpu_baseline:
         print("# timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wl, agents, rope)

@@ -29,9 +29,13 @@
  *   - bf16 means IEEE bfloat16 stored as 16-bit words.
  *
  * Data layout in HBM (d = head dim, ps = page size, r = rank, Hkv = KV heads):
- *   base pool  [num_base_pages][2][Hkv][ps*d] bf16.  For page p, slot 0 holds
- *              K as [ps][d] (token-major), slot 1 holds V as [d][ps]
- *              (dimension-major).  One (page, K|V, head) block is contiguous.
+ *   base pool  [num_base_pages][2][Hkv][ps*d] bf16: slot 0 holds K, slot 1 holds V;
+ *              one (page, K|V, head) block of ps*d values is contiguous.  For the
+ *              supported ps = 16, d = 128 a block is stored in the order the
+ *              kernels' matrix-core fragments read it (one 16-byte load per lane):
+ *                K (token t, dim i): (i/32)*512 + (t + 16*((i%16)/4))*8 + 4*((i%32)/16) + i%4
+ *                V (token t, dim i): (i/32)*512 + (i%16 + 16*(t/4))*8 + 4*((i/16)%2) + t%4
+ *              fkv_scatter_tokens writes this order; other shapes use K [ps][d], V [d][ps].
  *   res pool   [num_res_pages][2][ps*r] bf16.  Slot 0 holds C_K as [ps][r],
  *              slot 1 holds C_V as [r][ps].
  *   adapters   [n_adapters][2][r][Hkv*d] bf16: B_K then B_V, each the r x n
@@ -212,8 +216,9 @@ typedef struct {
     const int32_t *base_bt;     /* device [n_agents][max_pages] */
     const int32_t *res_bt;      /* device [n_agents][max_pages] */
     const int32_t *seq_lens;    /* device [n_agents], >= 1; keys 0..seq_len-1 */
-    const float *rope_cos;      /* device fp32 [rope_max_pos][d/2]; NULL = no RoPE on C_K.B_K */
-    const float *rope_sin;      /* device fp32 [rope_max_pos][d/2] */
+    const float *rope_cos;      /* device fp32 table from fkv_rope_table (rope_max_pos*d/2 values);
+                                   NULL = no RoPE on C_K.B_K */
+    const float *rope_sin;      /* device fp32 table from fkv_rope_table */
     const int32_t *plan;        /* device copy of a serialised decode plan (decode only) */
     const int32_t *q_indptr;    /* device [n_agents+1] query rows per agent (prefill only) */
     void *workspace;            /* device scratch of workspace_bytes (decode) */
@@ -247,8 +252,11 @@ fkv_status fkv_residual_attention_decode(const fkv_attn_args *args, const fkv_pl
  * keys 0 .. that position.  Same shapes as decode; needs no plan or workspace. */
 fkv_status fkv_residual_attention_prefill(const fkv_attn_args *args, void *stream);
 
-/* Fill a RoPE table on the host (fp64 angles rounded to fp32): for position p
- * and pair i < d/2, cos_out[p*d/2+i] = cos(p * base^(-2i/d)), likewise sin. */
+/* Fill the RoPE tables on the host (fp64 angles rounded to fp32): for position p
+ * and pair i < d/2 the entry is cos(p * base^(-2i/d)) (sin likewise), stored at
+ * (p/16)*1024 + (i/16)*256 + (p%16 + 16*((i%16)/4))*4 + i%4, the order in which the
+ * kernels' fragments read them.  Needs d = 128 and max_pos a multiple of 16;
+ * each table holds max_pos*d/2 floats. */
 fkv_status fkv_rope_table(int32_t d, int32_t max_pos, double base, float *cos_out, float *sin_out);
 
 /* ------------------------------------------------------------------------ */

@@ -52,15 +52,18 @@ const char *fkv_version(void) { return "forkkv-mi355x 0.1 (gfx950)"; }
 
 fkv_status fkv_rope_table(int32_t d, int32_t max_pos, double base, float *cos_out, float *sin_out) {
     fkv::clear_error();
-    if (d < 2 || d % 2 || max_pos < 1 || !(base > 0.0) || !cos_out || !sin_out)
-        return fkv::fail(FKV_ERR_INVALID, "fkv_rope_table: bad argument");
+    if (d != 128 || max_pos < 16 || max_pos % 16 || !(base > 0.0) || !cos_out || !sin_out)
+        return fkv::fail(FKV_ERR_INVALID, "fkv_rope_table: needs d = 128 and max_pos a positive multiple of 16");
     const int32_t half = d / 2;
     for (int32_t i = 0; i < half; ++i) {
         const double inv_freq = std::pow(base, -2.0 * (double)i / (double)d);
+        // pair i = 16*mt + 4*grp + k of position 16*page + t sits at [page][mt][t + 16*grp][k]
+        const int32_t mt = i / 16, grp = (i % 16) / 4, k = i % 4;
         for (int32_t p = 0; p < max_pos; ++p) {
             const double ang = (double)p * inv_freq;
-            cos_out[(int64_t)p * half + i] = (float)std::cos(ang);
-            sin_out[(int64_t)p * half + i] = (float)std::sin(ang);
+            const int64_t off = (int64_t)(p / 16) * 1024 + mt * 256 + (p % 16 + 16 * grp) * 4 + k;
+            cos_out[off] = (float)std::cos(ang);
+            sin_out[off] = (float)std::sin(ang);
         }
     }
     return FKV_OK;

@@ -37,6 +37,7 @@ constexpr int PS = 16;
 constexpr int ROWS = 16;
 constexpr int WAVES = 4;
 constexpr float kNegInf = -INFINITY;
+constexpr int kMaxPagesPerItem = fkv::kMaxPagesPerItem;
 
 struct DecodeArgs {
     const uint16_t *q, *base_kv, *res_kv, *lora_b;
@@ -48,6 +49,8 @@ struct DecodeArgs {
     int32_t hq, hkv, max_pages, ws_stride;
     float scale_log2;  // softmax scale * log2(e)
 };
+
+__device__ __forceinline__ int hkv_of(const DecodeArgs &p) { return p.hkv; }
 
 template <int R>
 struct RankTiles {
@@ -62,11 +65,12 @@ struct SplitShape {
     static constexpr int STAGE_HALFS = ROPE ? AG * R * D : 0;         // B_K slices, row-major
     static constexpr int BKT_WORDS = ROPE ? AG * RT * 8 * 64 * 2 : 0;  // B_K^T fragments (u32)
     static constexpr int UNION_BYTES = (MERGE_FLOATS * 4 > STAGE_HALFS * 2) ? MERGE_FLOATS * 4 : STAGE_HALFS * 2;
-    static constexpr int LDS_BYTES = UNION_BYTES + BKT_WORDS * 4;
+    static constexpr int TABLE_WORDS = (1 + (R > 0 ? AG : 0)) * kMaxPagesPerItem;  // block-table entries
+    static constexpr int LDS_BYTES = UNION_BYTES + BKT_WORDS * 4 + TABLE_WORDS * 4;
 };
 
 template <int R, int G, bool ROPE>
-__global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
+__global__ __launch_bounds__(256, ROPE ? 1 : 2) void decode_split_kernel(DecodeArgs p) {
     using S = SplitShape<R, G, ROPE>;
     constexpr int AG = S::AG;
     constexpr int RT = S::RT;
@@ -102,17 +106,27 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
         max_len = max_len > slot_len[s] ? max_len : slot_len[s];
     }
 
-    // Q^T as the B operand of the 16x16x32 product: lane holds q[row=col][8*grp + 32*kk + 0..7].
+    // Q^T as the B operand of the 16x16x32 products.  The head-dim index of slot j in
+    // k-step kk is 32kk + 16(j/4) + 4grp + j%4 for this lane group: the same order in
+    // which a rebuilt key tile leaves the 16x16x16 accumulators, so base keys, rebuilt
+    // keys and queries all use one permuted order.
     const uint16_t *qrow = p.q + ((int64_t)my_agent * p.hq + qh) * D;
     u32x4 qf[4];
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) qf[kk] = row_active ? ldg128(qrow + 8 * grp + 32 * kk) : u32x4{0, 0, 0, 0};
+    for (int kk = 0; kk < 4; ++kk) {
+        u32x4 v = {0, 0, 0, 0};
+        if (row_active) {
+            const u32x2 lo = ldg64(qrow + 32 * kk + 4 * grp);
+            const u32x2 hi = ldg64(qrow + 32 * kk + 16 + 4 * grp);
+            v = u32x4{lo.x, lo.y, hi.x, hi.y};
+        }
+        qf[kk] = v;
+    }
 
     const int64_t n = (int64_t)hkv * D;
     const int64_t res_page_halfs = 2 * PS * R;
     // ---- prologue: per-agent residual key operands ----
     u32x2 wf[RT > 0 ? RT : 1];   // RoPE off: (B_K q) for this lane's row, bf16, B operand of 16x16x16
-    u32x2 q16[ROPE ? 8 : 1];     // RoPE on: q[row=col][16*mt + 4*grp + 0..3]
     if constexpr (R > 0 && !ROPE) {
         f32x4 wacc[RT];
 #pragma unroll
@@ -127,7 +141,12 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
                 f32x4 acc = {0, 0, 0, 0};
 #pragma unroll
                 for (int kk = 0; kk < 4; ++kk) {
-                    const u32x4 a = rho < R ? ldg128(bk + (int64_t)rho * n + 8 * grp + 32 * kk) : u32x4{0, 0, 0, 0};
+                    u32x4 a = {0, 0, 0, 0};
+                    if (rho < R) {
+                        const u32x2 lo = ldg64(bk + (int64_t)rho * n + 32 * kk + 4 * grp);
+                        const u32x2 hi = ldg64(bk + (int64_t)rho * n + 32 * kk + 16 + 4 * grp);
+                        a = u32x4{lo.x, lo.y, hi.x, hi.y};
+                    }
                     acc = mfma32(a, qf[kk], acc);
                 }
                 if (my_slot == s) wacc[t] = acc;
@@ -167,12 +186,21 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
             lds_bkt[idx * 2 + 0] = w[0];
             lds_bkt[idx * 2 + 1] = w[1];
         }
-#pragma unroll
-        for (int mt = 0; mt < 8; ++mt) q16[mt] = row_active ? ldg64(qrow + 16 * mt + 4 * grp) : u32x2{0, 0};
-        __syncthreads();
     }
+    // block-table entries of the item's pages: one round trip for the whole item
+    int32_t *s_tab = reinterpret_cast<int32_t *>(lds + S::UNION_BYTES + S::BKT_WORDS * 4);
+    const int npg = pg1 - pg0;
+    for (int i = threadIdx.x; i < npg; i += 256) s_tab[i] = p.base_bt[(int64_t)leader * p.max_pages + pg0 + i];
+    if constexpr (R > 0) {
+#pragma unroll
+        for (int s = 0; s < AG; ++s)
+            for (int i = threadIdx.x; i < npg; i += 256)
+                s_tab[(1 + s) * kMaxPagesPerItem + i] =
+                    slot_ad[s] >= 0 ? p.res_bt[(int64_t)slot_agent[s] * p.max_pages + pg0 + i] : 0;
+    }
+    __syncthreads();
 
-    // ---- main loop over this wave's pages ----
+    // ---- main loop: this wave's pages, next page's loads in flight during compute ----
     f32x4 oacc[8];
 #pragma unroll
     for (int mt = 0; mt < 8; ++mt) oacc[mt] = f32x4{0, 0, 0, 0};
@@ -181,80 +209,96 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
     for (int t = 0; t < (RT > 0 ? RT : 1); ++t) racc[t] = f32x4{0, 0, 0, 0};
     float m_run = kNegInf, l_run = 0.f;
 
-    const int32_t *bt_leader = p.base_bt + (int64_t)leader * p.max_pages;
     const int64_t kv_block = (int64_t)PS * D;   // halfs per (page, K|V, head) block
-    for (int pg = pg0 + wave; pg < pg1; pg += WAVES) {
-        const int bpage = bt_leader[pg];
-        const uint16_t *kblk = p.base_kv + ((int64_t)bpage * 2 * hkv + h) * kv_block;
-        const uint16_t *vblk = kblk + (int64_t)hkv * kv_block;
+    struct Frag {
+        f32x4 cs[ROPE ? 4 : 1], sn[ROPE ? 4 : 1];
         u32x4 kf[4];
         u32x2 vf[8];
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk) kf[kk] = ldg128(kblk + col * D + 8 * grp + 32 * kk);
-#pragma unroll
-        for (int mt = 0; mt < 8; ++mt) vf[mt] = ldg64(vblk + (16 * mt + col) * PS + 4 * grp);
+        u32x2 ck[AG][RT > 0 ? RT : 1];
+        u32x2 cv[AG][RT > 0 ? RT : 1];
+    };
+    // Every load below is issued unconditionally and in a fixed order, so the compiler
+    // can count them: a prefetch of the next page then stays in flight while the
+    // current page computes.  Lanes or slots that have no data read a valid address
+    // and their values are zeroed or ignored.
+    auto load = [&](int pg, Frag &f) {
+        const int li = pg - pg0;
         const int tok0 = pg * PS;
-        // tokens of this page past every agent's end are zeroed in V (they may hold any bits)
+        if constexpr (ROPE) {  // issued first: they are consumed first
+            const float *cr = p.rope_cos + (int64_t)pg * (PS * D / 2) + lane * 4;
+            const float *sr = p.rope_sin + (int64_t)pg * (PS * D / 2) + lane * 4;
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt) {
+                f.cs[mt] = *reinterpret_cast<const f32x4 *>(cr + 256 * mt);
+                f.sn[mt] = *reinterpret_cast<const f32x4 *>(sr + 256 * mt);
+            }
+        }
+        // K and V blocks are stored in fragment order: one 16-byte load per lane each
+        const int bpage = uniform(s_tab[li]);
+        const uint16_t *kblk = p.base_kv + ((int64_t)bpage * 2 * hkv + h) * kv_block;
+        const uint16_t *vblk = kblk + (int64_t)hkv * kv_block;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) f.kf[kk] = ldg128(kblk + kk * 512 + lane * 8);
+#pragma unroll
+        for (int q2 = 0; q2 < 4; ++q2) {
+            const u32x4 v = ldg128(vblk + q2 * 512 + lane * 8);
+            f.vf[2 * q2] = u32x2{v.x, v.y};
+            f.vf[2 * q2 + 1] = u32x2{v.z, v.w};
+        }
+        if constexpr (R > 0) {
+#pragma unroll
+            for (int s = 0; s < AG; ++s) {
+                const int rpage = uniform(s_tab[(1 + s) * kMaxPagesPerItem + li]);
+                const uint16_t *rb = p.res_kv + (int64_t)rpage * res_page_halfs;
+#pragma unroll
+                for (int t = 0; t < RT; ++t) {
+                    const int rho = 16 * t + col;
+                    const int rk = 16 * t + 4 * grp;
+                    const u32x2 cv = ldg64(rb + PS * R + (rho < R ? rho : R - 1) * PS + 4 * grp);
+                    const u32x2 ck = ldg64(rb + col * R + (rk < R ? rk : R - 4));
+                    f.cv[s][t] = rho < R ? cv : u32x2{0, 0};
+                    f.ck[s][t] = rk < R ? ck : u32x2{0, 0};
+                }
+            }
+        }
+    };
+    auto mask4 = [&](u32x2 v, int vis) {  // zero tokens 4grp+i >= vis of a [.][tok] fragment
+        if (4 * grp + 0 >= vis) v.x &= 0xffff0000u;
+        if (4 * grp + 1 >= vis) v.x &= 0x0000ffffu;
+        if (4 * grp + 2 >= vis) v.y &= 0xffff0000u;
+        if (4 * grp + 3 >= vis) v.y &= 0x0000ffffu;
+        return v;
+    };
+    auto compute = [&](Frag &f, int pg) {
+        const int tok0 = pg * PS;
+        // tokens past every agent's end are zeroed in V (they may hold any bits)
         const int vis = max_len - tok0;
         if (vis < PS) {
 #pragma unroll
-            for (int mt = 0; mt < 8; ++mt) {
-                if (4 * grp + 0 >= vis) vf[mt].x &= 0xffff0000u;
-                if (4 * grp + 1 >= vis) vf[mt].x &= 0x0000ffffu;
-                if (4 * grp + 2 >= vis) vf[mt].y &= 0xffff0000u;
-                if (4 * grp + 3 >= vis) vf[mt].y &= 0x0000ffffu;
-            }
+            for (int mt = 0; mt < 8; ++mt) f.vf[mt] = mask4(f.vf[mt], vis);
         }
-        f32x4 cs[ROPE ? 4 : 1], sn[ROPE ? 4 : 1];
-        if constexpr (ROPE) {
-            const float *cr = p.rope_cos + (int64_t)(tok0 + col) * (D / 2) + 4 * grp;
-            const float *sr = p.rope_sin + (int64_t)(tok0 + col) * (D / 2) + 4 * grp;
-#pragma unroll
-            for (int mt = 0; mt < 4; ++mt) {
-                cs[mt] = *reinterpret_cast<const f32x4 *>(cr + 16 * mt);
-                sn[mt] = *reinterpret_cast<const f32x4 *>(sr + 16 * mt);
-            }
-        }
-
         // S^T = K_base Q^T
         f32x4 sacc = {0, 0, 0, 0};
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) sacc = mfma32(kf[kk], qf[kk], sacc);
-
-        u32x2 cvf[AG][RT > 0 ? RT : 1];
+        for (int kk = 0; kk < 4; ++kk) sacc = mfma32(f.kf[kk], qf[kk], sacc);
         if constexpr (R > 0) {
 #pragma unroll
             for (int s = 0; s < AG; ++s) {
                 if (slot_ad[s] < 0) continue;
-                const int rpage = p.res_bt[(int64_t)slot_agent[s] * p.max_pages + pg];
-                const uint16_t *rb = p.res_kv + (int64_t)rpage * res_page_halfs;
                 const int svis = slot_len[s] - tok0;
+                if (svis < PS) {
 #pragma unroll
-                for (int t = 0; t < RT; ++t) {
-                    // C_V^T fragment: lane holds C_V[tok = 4grp + 0..3][rho = 16t + col]
-                    const int rho = 16 * t + col;
-                    u32x2 v = rho < R ? ldg64(rb + PS * R + rho * PS + 4 * grp) : u32x2{0, 0};
-                    if (svis < PS) {
-                        if (4 * grp + 0 >= svis) v.x &= 0xffff0000u;
-                        if (4 * grp + 1 >= svis) v.x &= 0x0000ffffu;
-                        if (4 * grp + 2 >= svis) v.y &= 0xffff0000u;
-                        if (4 * grp + 3 >= svis) v.y &= 0x0000ffffu;
-                    }
-                    cvf[s][t] = v;
+                    for (int t = 0; t < RT; ++t) f.cv[s][t] = mask4(f.cv[s][t], svis);
                 }
-                // C_K fragment: lane holds C_K[tok = col][rho = 16t + 4grp + 0..3]
-                u32x2 ckf[RT];
-#pragma unroll
-                for (int t = 0; t < RT; ++t)
-                    ckf[t] = (16 * t + 4 * grp < R) ? ldg64(rb + col * R + 16 * t + 4 * grp) : u32x2{0, 0};
                 if constexpr (!ROPE) {
 #pragma unroll
                     for (int t = 0; t < RT; ++t) {
                         const u32x2 b = my_slot == s ? wf[t] : u32x2{0, 0};
-                        sacc = mfma16(ckf[t], b, sacc);
+                        sacc = mfma16(f.ck[s][t], b, sacc);
                     }
                 } else {
-                    // Stage 1: U^T = B_K^T C_K^T (rows d, columns tokens), then deferred RoPE
+                    // Stage 1: U^T = B_K^T C_K^T (rows d, columns tokens), deferred RoPE, then
+                    // S^T += K_lora Q_s^T with the rebuilt tile as the 16x16x32 A operand.
                     f32x4 u[8];
 #pragma unroll
                     for (int mt = 0; mt < 8; ++mt) {
@@ -263,7 +307,7 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
                         for (int t = 0; t < RT; ++t) {
                             const u32x2 a = *reinterpret_cast<const u32x2 *>(
                                 lds_bkt + ((((s * RT + t) * 8 + mt) * 64) + lane) * 2);
-                            u[mt] = mfma16(a, ckf[t], u[mt]);
+                            u[mt] = mfma16(a, f.ck[s][t], u[mt]);
                         }
                     }
 #pragma unroll
@@ -271,14 +315,15 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
 #pragma unroll
                         for (int i = 0; i < 4; ++i) {
                             const float x = u[mt][i], y = u[mt + 4][i];
-                            u[mt][i] = x * cs[mt][i] - y * sn[mt][i];
-                            u[mt + 4][i] = y * cs[mt][i] + x * sn[mt][i];
+                            u[mt][i] = x * f.cs[mt][i] - y * f.sn[mt][i];
+                            u[mt + 4][i] = y * f.cs[mt][i] + x * f.sn[mt][i];
                         }
                     }
 #pragma unroll
-                    for (int mt = 0; mt < 8; ++mt) {
-                        const u32x2 b = my_slot == s ? q16[mt] : u32x2{0, 0};
-                        sacc = mfma16(pack4(u[mt]), b, sacc);
+                    for (int kk = 0; kk < 4; ++kk) {
+                        const u32x2 lo = pack4(u[2 * kk]), hi = pack4(u[2 * kk + 1]);
+                        const u32x4 b = my_slot == s ? qf[kk] : u32x4{0, 0, 0, 0};
+                        sacc = mfma32(u32x4{lo.x, lo.y, hi.x, hi.y}, b, sacc);
                     }
                 }
             }
@@ -311,7 +356,7 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
 #pragma unroll
         for (int mt = 0; mt < 8; ++mt) {
             oacc[mt] *= alpha;
-            oacc[mt] = mfma16(vf[mt], pf, oacc[mt]);
+            oacc[mt] = mfma16(f.vf[mt], pf, oacc[mt]);
         }
         if constexpr (R > 0) {
 #pragma unroll
@@ -321,8 +366,28 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
                 if (slot_ad[s] < 0) continue;
                 const u32x2 pm = my_slot == s ? pf : u32x2{0, 0};
 #pragma unroll
-                for (int t = 0; t < RT; ++t) racc[t] = mfma16(cvf[s][t], pm, racc[t]);
+                for (int t = 0; t < RT; ++t) racc[t] = mfma16(f.cv[s][t], pm, racc[t]);
             }
+        }
+    };
+
+    // Two register buffers: the next page (clamped to this wave's last page, so the
+    // final prefetch re-reads a page that is already in cache) loads while the
+    // current one computes.
+    Frag fa, fb;
+    int pg = pg0 + wave;
+    if (pg < pg1) {
+        const int last = pg + (pg1 - 1 - pg) / WAVES * WAVES;
+        load(pg, fa);
+        for (;;) {
+            load(pg + WAVES <= last ? pg + WAVES : last, fb);
+            compute(fa, pg);
+            pg += WAVES;
+            if (pg > last) break;
+            load(pg + WAVES <= last ? pg + WAVES : last, fa);
+            compute(fb, pg);
+            pg += WAVES;
+            if (pg > last) break;
         }
     }
     l_run += __shfl_xor(l_run, 16);
@@ -384,65 +449,91 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
     }
 }
 
-// Log-sum-exp merge of one agent's partials and Stage 3 of Algorithm 1:
-// O = (acc + acc_r . B_V[h]) / l for the g query heads of KV head h.
+// Log-sum-exp merge of one agent's partials and Stage 3 of Algorithm 1 for one query
+// head j (KV head h = j / G): O = (sum_k w_k acc_k + (sum_k w_k acc_r,k) . B_V[h]) / L
+// with w_k = 2^(m_k - M), M = max_k m_k, L = sum_k w_k l_k.
+constexpr int kCombineThreads = 128;
+constexpr int kMaxItemsPerAgent = fkv::kMaxItemsPerAgent;
+
 template <int R, int G>
-__global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs p) {
-    const int hkv = p.hkv;
-    const int a = blockIdx.x / hkv, h = blockIdx.x - (blockIdx.x / hkv) * hkv;
+__global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(DecodeArgs p) {
+    const int hq = p.hq;
+    const int a = blockIdx.x / hq;
+    const int j = blockIdx.x - a * hq;
+    const int h = j / G, jj = j - h * G;
     const int32_t *plan = p.plan;
-    const int32_t *ptr = plan + plan[fkv::H_OFF_AGENT_PTR];
     const int32_t *slots = plan + plan[fkv::H_OFF_AGENT_SLOT];
-    const int k0 = ptr[a], k1 = ptr[a + 1];
+    const int k0 = plan[plan[fkv::H_OFF_AGENT_PTR] + a];
+    const int K = plan[plan[fkv::H_OFF_AGENT_PTR] + a + 1] - k0;
     const int ad = R > 0 ? p.adapter_idx[a] : -1;
-    __shared__ float sM[G], sL[G];
-    __shared__ float sR[G][R > 0 ? R : 1];
     const int stride = p.ws_stride;
     const int tid = threadIdx.x;
-    if (tid < G) {
-        float M = kNegInf;
-        for (int k = k0; k < k1; ++k) M = fmaxf(M, p.ws[(int64_t)(slots[k] + h * ROWS + tid) * stride]);
-        const float Mu = M == kNegInf ? 0.f : M;
-        float L = 0.f;
-        for (int k = k0; k < k1; ++k) {
-            const float *rec = p.ws + (int64_t)(slots[k] + h * ROWS + tid) * stride;
-            L += fast_exp2(rec[0] - Mu) * rec[1];
-        }
-        sM[tid] = Mu;
-        sL[tid] = L;
+    __shared__ float sW[kMaxItemsPerAgent];
+    __shared__ int sRow[kMaxItemsPerAgent];
+    __shared__ float sRed[2];
+    __shared__ float sAccR[R > 0 ? R : 1];
+
+    // M = max_k m_k
+    float mloc = kNegInf;
+    for (int k = tid; k < K; k += kCombineThreads) {
+        const int row = slots[k0 + k] + h * ROWS + jj;
+        sRow[k] = row;
+        const float m = p.ws[(int64_t)row * stride];
+        sW[k] = m;
+        mloc = fmaxf(mloc, m);
     }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) mloc = fmaxf(mloc, __shfl_xor(mloc, o));
+    if ((tid & 63) == 0) sRed[tid >> 6] = mloc;
     __syncthreads();
+    const float M = fmaxf(sRed[0], sRed[1]);
+    const float Mu = M == kNegInf ? 0.f : M;
+    __syncthreads();
+    // w_k and L = sum_k w_k l_k
+    float lloc = 0.f;
+    for (int k = tid; k < K; k += kCombineThreads) {
+        const float w = fast_exp2(sW[k] - Mu);
+        sW[k] = w;
+        lloc += w * p.ws[(int64_t)sRow[k] * stride + 1];
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) lloc += __shfl_xor(lloc, o);
+    if ((tid & 63) == 0) sRed[tid >> 6] = lloc;
+    __syncthreads();
+    const float L = sRed[0] + sRed[1];
+    // acc_r = sum_k w_k acc_r,k
     if constexpr (R > 0) {
-        for (int idx = tid; idx < G * R; idx += 256) {
-            const int jj = idx / R, rho = idx - jj * R;
+        if (ad >= 0 && tid < R) {
             float v = 0.f;
-            for (int k = k0; k < k1; ++k) {
-                const float *rec = p.ws + (int64_t)(slots[k] + h * ROWS + jj) * stride;
-                v += fast_exp2(rec[0] - sM[jj]) * rec[2 + D + rho];
-            }
-            sR[jj][rho] = v;
+            for (int k = 0; k < K; ++k) v += sW[k] * p.ws[(int64_t)sRow[k] * stride + 2 + D + tid];
+            sAccR[tid] = v;
         }
+    }
+    // acc[d] = sum_k w_k acc_k[d]
+    float acc = 0.f;
+    {
+        const int dd = tid;
+        int k = 0;
+        for (; k + 4 <= K; k += 4) {
+            const float a0 = p.ws[(int64_t)sRow[k] * stride + 2 + dd];
+            const float a1 = p.ws[(int64_t)sRow[k + 1] * stride + 2 + dd];
+            const float a2 = p.ws[(int64_t)sRow[k + 2] * stride + 2 + dd];
+            const float a3 = p.ws[(int64_t)sRow[k + 3] * stride + 2 + dd];
+            acc += sW[k] * a0 + sW[k + 1] * a1 + sW[k + 2] * a2 + sW[k + 3] * a3;
+        }
+        for (; k < K; ++k) acc += sW[k] * p.ws[(int64_t)sRow[k] * stride + 2 + dd];
+    }
+    if constexpr (R > 0) {
         __syncthreads();
-    }
-    for (int idx = tid; idx < G * D; idx += 256) {
-        const int jj = idx / D, dd = idx - jj * D;
-        float v = 0.f;
-        for (int k = k0; k < k1; ++k) {
-            const float *rec = p.ws + (int64_t)(slots[k] + h * ROWS + jj) * stride;
-            v += fast_exp2(rec[0] - sM[jj]) * rec[2 + dd];
-        }
-        if constexpr (R > 0) {
-            if (ad >= 0) {
-                const uint16_t *bv = p.lora_b + ((int64_t)ad * 2 + 1) * R * hkv * D + (int64_t)h * D + dd;
+        if (ad >= 0) {
+            const uint16_t *bv = p.lora_b + ((int64_t)ad * 2 + 1) * R * hkv_of(p) * D + (int64_t)h * D + tid;
 #pragma unroll 8
-                for (int rho = 0; rho < R; ++rho) v += sR[jj][rho] * bf16_to_f32(bv[(int64_t)rho * hkv * D]);
-            }
+            for (int rho = 0; rho < R; ++rho) acc += sAccR[rho] * bf16_to_f32(bv[(int64_t)rho * hkv_of(p) * D]);
         }
-        const float L = sL[jj];
-        const float o = L > 0.f ? v / L : 0.f;
-        typedef __bf16 bf1;
-        p.out[((int64_t)a * p.hq + h * G + jj) * D + dd] = __builtin_bit_cast(uint16_t, (bf1)o);
     }
+    const float o = L > 0.f ? acc / L : 0.f;
+    typedef __bf16 bf1;
+    p.out[((int64_t)a * hq + j) * D + tid] = __builtin_bit_cast(uint16_t, (bf1)o);
 }
 
 template <int R, int G, bool ROPE>
@@ -452,7 +543,7 @@ hipError_t launch_decode(const DecodeArgs &da, int n_blocks, int n_agents, hipSt
     hipLaunchKernelGGL((decode_split_kernel<R, G, ROPE>), dim3(n_blocks), dim3(256), 0, st, da);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[1]), st)) != hipSuccess) return e;
-    hipLaunchKernelGGL((decode_combine_kernel<R, G>), dim3(n_agents * da.hkv), dim3(256), 0, st, da);
+    hipLaunchKernelGGL((decode_combine_kernel<R, G>), dim3(n_agents * da.hq), dim3(kCombineThreads), 0, st, da);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[2]), st)) != hipSuccess) return e;
     return hipSuccess;

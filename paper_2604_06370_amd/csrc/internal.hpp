@@ -22,6 +22,8 @@ void clear_error();
 constexpr int kHeaderWords = 16;
 constexpr int kMaxRows = 16;       // query rows per work item (agents x query heads of a KV head)
 constexpr int kItemWords = 4 + kMaxRows;
+constexpr int kMaxPagesPerItem = 512;  // upper bound of pages_per_split (block tables are staged in LDS)
+constexpr int kMaxItemsPerAgent = 1024;  // work items one agent may span (the combine stages them in LDS)
 
 enum PlanHeader {
     H_MAGIC = 0, H_N_ITEMS, H_N_BLOCKS, H_N_AGENTS, H_HKV, H_GROUP, H_AGENTS_PER_ITEM,

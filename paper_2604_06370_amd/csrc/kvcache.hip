@@ -1,8 +1,13 @@
 // Cache writes: copy-on-write page copies (Section 5.2) and scattering new tokens'
 // bCache K/V and rCache C_K/C_V into their page slots.
 //
-// Page layouts (bf16): base page [2][Hkv][ps*d] with K as [ps][d] and V as [d][ps];
-// residual page [2][ps*r] with C_K as [ps][r] and C_V as [r][ps].
+// Page layouts (bf16): base page [2][Hkv][ps*d]; residual page [2][ps*r] with C_K as
+// [ps][r] and C_V as [r][ps].  With ps = 16 and d = 128 the K and V blocks of one
+// (page, head) are stored in the order in which the attention kernels' matrix-core
+// fragments read them (one 16-byte load per lane, 1 KB per wave instruction):
+//   K element (token t, dim d) at  (d/32)*512 + (t + 16*((d%16)/4))*8 + 4*((d%32)/16) + d%4
+//   V element (token t, dim d) at  (d/32)*512 + (d%16 + 16*(t/4))*8 + 4*((d/16)%2) + t%4
+// Other shapes use plain [ps][d] (K) and [d][ps] (V).
 #include <hip/hip_runtime.h>
 
 #include <string>
@@ -10,6 +15,25 @@
 #include "internal.hpp"
 
 namespace {
+
+// Offsets of (token t, dim dd) inside a K or V block (see the layout note above).
+__device__ __forceinline__ int64_t k_off(int t, int dd, int ps, int d) {
+    if (ps == 16 && d == 128) return (dd >> 5) * 512 + (t + 16 * ((dd & 15) >> 2)) * 8 + 4 * ((dd & 31) >> 4) + (dd & 3);
+    return (int64_t)t * d + dd;
+}
+__device__ __forceinline__ int64_t v_off(int t, int dd, int ps, int d) {
+    if (ps == 16 && d == 128) return (dd >> 5) * 512 + ((dd & 15) + 16 * (t >> 2)) * 8 + 4 * ((dd >> 4) & 1) + (t & 3);
+    return (int64_t)dd * ps + t;
+}
+// Token slot of element e of a K or V block.
+__device__ __forceinline__ int k_slot(int64_t e, int ps, int d) {
+    if (ps == 16 && d == 128) return (int)(((e & 511) >> 3) & 15);
+    return (int)(e / d);
+}
+__device__ __forceinline__ int v_slot(int64_t e, int ps, int d) {
+    if (ps == 16 && d == 128) return (int)(4 * (((e & 511) >> 3) >> 4) + (e & 3));
+    return (int)(e % ps);
+}
 
 struct CopyArgs {
     const fkv_page_copy *copies;
@@ -30,7 +54,7 @@ __global__ __launch_bounds__(256) void page_copy_kernel(CopyArgs a) {
         for (int64_t e = threadIdx.x; e < page; e += blockDim.x) {
             const int64_t within = e % blk;
             const bool is_v = (e / blk) >= a.hkv;
-            const int slot = is_v ? (int)(within % a.ps) : (int)(within / a.d);
+            const int slot = is_v ? v_slot(within, a.ps, a.d) : k_slot(within, a.ps, a.d);
             if (slot < n_valid) dst[e] = src[e];
         }
     } else {
@@ -68,8 +92,8 @@ __global__ __launch_bounds__(256) void scatter_kernel(ScatterArgs a) {
         uint16_t *pg = a.base_kv + (int64_t)page * 2 * a.hkv * blk;
         for (int e = threadIdx.x; e < a.hkv * a.d; e += blockDim.x) {
             const int hh = e / a.d, dd = e - hh * a.d;
-            pg[hh * blk + (int64_t)slot * a.d + dd] = a.k_src[j * a.hkv * a.d + e];
-            pg[(a.hkv + hh) * blk + (int64_t)dd * a.ps + slot] = a.v_src[j * a.hkv * a.d + e];
+            pg[hh * blk + k_off(slot, dd, a.ps, a.d)] = a.k_src[j * a.hkv * a.d + e];
+            pg[(a.hkv + hh) * blk + v_off(slot, dd, a.ps, a.d)] = a.v_src[j * a.hkv * a.d + e];
         }
     }
     if (a.ck_src && a.r > 0) {

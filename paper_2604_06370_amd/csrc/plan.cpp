@@ -83,9 +83,11 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
         const int64_t cus = prm->num_cus > 0 ? prm->num_cus : 256;
         const int64_t target_items = std::max<int64_t>(1, (4 * cus + prm->hkv - 1) / prm->hkv);
         pps = (int32_t)std::max<int64_t>(4, (units + target_items - 1) / target_items);
-        pps = std::min(pps, 1024);
+        pps = std::min(pps, fkv::kMaxPagesPerItem);
         pps = (pps + 3) / 4 * 4;
     }
+    if (pps > fkv::kMaxPagesPerItem)
+        return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: pages_per_split above 512");
 
     // 3. work items, clustered by (segment, split)
     struct Item { int32_t p0, p1; std::vector<int32_t> agents; };
@@ -136,6 +138,12 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     for (int32_t w = 0; w < n_items; ++w)
         for (size_t j = 0; j < items[w].agents.size(); ++j)
             slots[items[w].agents[j]].push_back((int32_t)(((int64_t)w * hkv) * fkv::kMaxRows + (int64_t)j * g));
+
+    for (auto &v : slots)
+        if (v.size() > (size_t)fkv::kMaxItemsPerAgent) {
+            return fkv::fail(FKV_ERR_UNSUPPORTED,
+                             "fkv_decode_plan_create: more than 1024 work items for one agent; raise pages_per_split");
+        }
 
     // 6. serialise
     auto *pl = new fkv_plan();

@@ -197,12 +197,13 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
             const uint16_t *kblk = p.base_kv + ((int64_t)bpage * 2 * hkv + h) * kv_block;
             const uint16_t *vblk = kblk + (int64_t)hkv * kv_block;
             const int vis = L - tok0;  // valid keys in this page
-            // K_base in the permuted 16x16x32 A layout
+            // K_base, stored in the permuted 16x16x32 A layout: one 16-byte load per k-step
             f32x4 kacc[8];
 #pragma unroll
-            for (int mt = 0; mt < 8; ++mt) {
-                u32x2 kb = have ? ldg64(kblk + col * D + 16 * mt + 4 * grp) : u32x2{0, 0};
-                kacc[mt] = f32x4{bf16_lo(kb.x), bf16_hi(kb.x), bf16_lo(kb.y), bf16_hi(kb.y)};
+            for (int kk = 0; kk < 4; ++kk) {
+                const u32x4 kb = have ? ldg128(kblk + kk * 512 + lane * 8) : u32x4{0, 0, 0, 0};
+                kacc[2 * kk] = f32x4{bf16_lo(kb.x), bf16_hi(kb.x), bf16_lo(kb.y), bf16_hi(kb.y)};
+                kacc[2 * kk + 1] = f32x4{bf16_lo(kb.z), bf16_hi(kb.z), bf16_lo(kb.w), bf16_hi(kb.w)};
             }
             const uint16_t *rb = nullptr;
             if constexpr (R > 0) {
@@ -219,12 +220,12 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
 #pragma unroll
                         for (int mt = 0; mt < 8; ++mt) u[mt] = mfma16(sBK[(t * 8 + mt) * 64 + lane], ck, u[mt]);
                     }
-                    const float *cr = p.rope_cos + (int64_t)(tok0 + col) * (D / 2) + 4 * grp;
-                    const float *sr = p.rope_sin + (int64_t)(tok0 + col) * (D / 2) + 4 * grp;
+                    const float *cr = p.rope_cos + (int64_t)pg * (PS * D / 2) + lane * 4;
+                    const float *sr = p.rope_sin + (int64_t)pg * (PS * D / 2) + lane * 4;
 #pragma unroll
                     for (int mt = 0; mt < 4; ++mt) {
-                        const f32x4 cs = *reinterpret_cast<const f32x4 *>(cr + 16 * mt);
-                        const f32x4 sn = *reinterpret_cast<const f32x4 *>(sr + 16 * mt);
+                        const f32x4 cs = *reinterpret_cast<const f32x4 *>(cr + 256 * mt);
+                        const f32x4 sn = *reinterpret_cast<const f32x4 *>(sr + 256 * mt);
 #pragma unroll
                         for (int i = 0; i < 4; ++i) {
                             const float x = u[mt][i], y = u[mt + 4][i];
@@ -242,7 +243,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
             // V page as stored ([d][16 keys]); keys past the sequence end are zeroed
             for (int e = lane; e < D * PS / 4; e += 64) {
                 u32x2 v = have ? ldg64(vblk + 4 * e) : u32x2{0, 0};
-                const int k0 = (4 * e) % PS;
+                const int k0 = 4 * ((((4 * e) & 511) >> 3) >> 4);  // tokens k0..k0+3 (fragment order)
                 if (k0 + 0 >= vis) v.x &= 0xffff0000u;
                 if (k0 + 1 >= vis) v.x &= 0x0000ffffu;
                 if (k0 + 2 >= vis) v.y &= 0xffff0000u;
@@ -337,8 +338,9 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
             const u32x4 pb1 = u32x4{pf[2 * half][1].x, pf[2 * half][1].y, pf[2 * half + 1][1].x, pf[2 * half + 1][1].y};
 #pragma unroll
             for (int mt = 0; mt < 8; ++mt) {
-                const u32x2 lo = *reinterpret_cast<const u32x2 *>(sV + (2 * half) * D * PS + (16 * mt + col) * PS + 4 * grp);
-                const u32x2 hi = *reinterpret_cast<const u32x2 *>(sV + (2 * half + 1) * D * PS + (16 * mt + col) * PS + 4 * grp);
+                const int voff = (mt >> 1) * 512 + lane * 8 + 4 * (mt & 1);
+                const u32x2 lo = *reinterpret_cast<const u32x2 *>(sV + (2 * half) * D * PS + voff);
+                const u32x2 hi = *reinterpret_cast<const u32x2 *>(sV + (2 * half + 1) * D * PS + voff);
                 const u32x4 va = u32x4{lo.x, lo.y, hi.x, hi.y};
                 oacc[mt][0] = mfma32(va, pb0, oacc[mt][0]);
                 oacc[mt][1] = mfma32(va, pb1, oacc[mt][1]);

@@ -173,6 +173,7 @@ class DecodePlan:
 
 def rope_tables(d: int, max_pos: int, base: float, device) -> Tuple[torch.Tensor, torch.Tensor]:
     """fkv_rope_table on the host, copied to the device."""
+    max_pos = (max_pos + 15) // 16 * 16
     cos = np.zeros((max_pos, d // 2), dtype=np.float32)
     sin = np.zeros((max_pos, d // 2), dtype=np.float32)
     check(N.fkv_rope_table(d, max_pos, base, _ptr(cos), _ptr(sin)), "fkv_rope_table")

@@ -179,14 +179,20 @@ def test_decode_plan_segments_follow_the_fork_tree():
 
 
 def test_rope_table_matches_fp64_definition():
-    d, P, base = 128, 300, 500000.0
-    cos = np.zeros((P, d // 2), np.float32)
-    sin = np.zeros((P, d // 2), np.float32)
+    d, P, base = 128, 304, 500000.0
+    cos = np.zeros(P * d // 2, np.float32)
+    sin = np.zeros(P * d // 2, np.float32)
     rt.check(N.fkv_rope_table(d, P, base, cos.ctypes.data, sin.ctypes.data))
+    # undo the fragment order: [page][mt][t + 16*grp][k] -> [position][pair]
+    c5 = cos.reshape(P // 16, 4, 4, 16, 4)      # page, mt, grp, t, k
+    s5 = sin.reshape(P // 16, 4, 4, 16, 4)
+    c = c5.transpose(0, 3, 1, 2, 4).reshape(P, d // 2)
+    s = s5.transpose(0, 3, 1, 2, 4).reshape(P, d // 2)
     p = np.arange(P)[:, None]
     ang = p * base ** (-2.0 * np.arange(d // 2)[None, :] / d)
-    np.testing.assert_array_equal(cos, np.cos(ang).astype(np.float32))
-    np.testing.assert_array_equal(sin, np.sin(ang).astype(np.float32))
+    np.testing.assert_array_equal(c, np.cos(ang).astype(np.float32))
+    np.testing.assert_array_equal(s, np.sin(ang).astype(np.float32))
+    assert N.fkv_rope_table(d, 300, base, cos.ctypes.data, sin.ctypes.data) == N.FKV_ERR_INVALID
 
 
 def test_attention_entry_points_reject_bad_arguments_before_launching():
