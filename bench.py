@@ -85,6 +85,7 @@ def main():
     ap.add_argument("--config", type=int, default=2)
     ap.add_argument("--rope", type=int, default=1)
     ap.add_argument("--pps", type=int, default=0, help="pages per split (0 = automatic)")
+    ap.add_argument("--item-agents", type=int, default=0, help="agents per decode work item (0 = automatic)")
     ap.add_argument("--copies", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
@@ -105,7 +106,8 @@ def main():
     wl = W.config(args.config)
     rope = bool(args.rope) and wl.r > 0
     print(f"# building {args.copies} cache copies of {wl.name} (rope={rope})", file=sys.stderr, flush=True)
-    lws = [LoadedWorkload(wl, device=dev, rope=rope, pages_per_split=args.pps) for _ in range(args.copies)]
+    lws = [LoadedWorkload(wl, device=dev, rope=rope, pages_per_split=args.pps,
+                          item_agents=args.item_agents) for _ in range(args.copies)]
     agents = wl.decode_agents()
     for lw in lws:
         lw.decode_setup(agents)

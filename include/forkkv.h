@@ -176,8 +176,11 @@ typedef struct {
     int32_t hq, hkv;
     int32_t page_size;
     int32_t max_pages;        /* row stride of base_bt */
-    int32_t pages_per_split;  /* pages per work item; 0 = choose automatically */
+    int32_t pages_per_split;  /* pages per work item (<= 256); 0 = choose automatically */
     int32_t num_cus;          /* compute units to fill; 0 = 256 */
+    int32_t max_item_agents;  /* agents sharing one work item; 0 = 4 groups of floor(16/g).  The RoPE
+                                 decode kernels need it <= 256 / r (their B_K fragments live in LDS);
+                                 fkv_decode_plan_default_agents gives the right value. */
 } fkv_decode_plan_params;
 
 typedef struct {
@@ -188,6 +191,9 @@ typedef struct {
     int32_t n_segments;       /* shared / private page ranges found */
     int32_t pages_per_split;
 } fkv_plan_info;
+
+/* Agents per work item that the decode kernel for (hq, hkv, r, rope) accepts. */
+int32_t fkv_decode_plan_default_agents(int32_t hq, int32_t hkv, int32_t r, int32_t rope);
 
 /* Build a plan from host block tables (base_bt [n_agents][max_pages], seq_lens [n_agents]). */
 fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *params, const int32_t *base_bt,
@@ -241,7 +247,8 @@ typedef struct {
  * `plan` is the host plan whose serialised copy args->plan points to (grid size
  * and workspace size are taken from it); the block tables and sequence lengths
  * in args must be the ones the plan was built from.
- * Supported: d = 128, page_size = 16, r in {0, 8, 16, 32, 64}, hq/hkv in {4, 8}.
+ * Supported: d = 128, page_size = 16, r in {0, 8, 16, 32, 64}, hq/hkv in {4, 8}; with RoPE the
+ * plan's max_item_agents must not exceed 256 / r.
  * Two kernels are enqueued (split, combine).  Errors: FKV_ERR_INVALID /
  * FKV_ERR_UNSUPPORTED before any launch, FKV_ERR_HIP when a launch fails. */
 fkv_status fkv_residual_attention_decode(const fkv_attn_args *args, const fkv_plan *plan, void *stream);

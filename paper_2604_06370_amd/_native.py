@@ -56,7 +56,7 @@ class fkv_pool_stats(ctypes.Structure):
 
 class fkv_decode_plan_params(ctypes.Structure):
     _fields_ = [("n_agents", c_i32), ("hq", c_i32), ("hkv", c_i32), ("page_size", c_i32), ("max_pages", c_i32),
-                ("pages_per_split", c_i32), ("num_cus", c_i32)]
+                ("pages_per_split", c_i32), ("num_cus", c_i32), ("max_item_agents", c_i32)]
 
 
 class fkv_plan_info(ctypes.Structure):
@@ -94,6 +94,7 @@ fkv_get_block_tables = _sig("fkv_get_block_tables", c_i32, [c_vp, c_vp, c_i32, c
 fkv_get_pool_stats = _sig("fkv_get_pool_stats", c_i32, [c_vp, ctypes.POINTER(fkv_pool_stats)])
 fkv_decode_plan_create = _sig("fkv_decode_plan_create", c_i32,
                               [ctypes.POINTER(fkv_decode_plan_params), c_vp, c_vp, ctypes.POINTER(c_vp)])
+fkv_decode_plan_default_agents = _sig("fkv_decode_plan_default_agents", c_i32, [c_i32, c_i32, c_i32, c_i32])
 fkv_decode_plan_destroy = _sig("fkv_decode_plan_destroy", None, [c_vp])
 fkv_decode_plan_info = _sig("fkv_decode_plan_info", c_i32, [c_vp, c_i32, c_i32, ctypes.POINTER(fkv_plan_info)])
 fkv_decode_plan_serialize = _sig("fkv_decode_plan_serialize", c_i32, [c_vp, c_vp, c_i64])

@@ -15,21 +15,26 @@ void clear_error();
 
 // Decode plan, host side.  Serialised layout (all int32):
 //   header[kHeaderWords]
-//   items   [n_items][kItemWords]  {page_begin, page_end, leader, n_ag, agent[16]}
+//   items   [n_items][kItemWords]  {page_begin, page_end, leader, n_ag, row_base, agent[16]}
 //   blocks  [n_blocks]             item * hkv + head, or -1 for an idle block
-//   agent_ptr [n_agents+1]         CSR over the partial slots of each agent
-//   agent_slot[...]                partial row base: (item*hkv) * 16 + slot*g  (add head*16 + jj)
-constexpr int kHeaderWords = 16;
-constexpr int kMaxRows = 16;       // query rows per work item (agents x query heads of a KV head)
-constexpr int kItemWords = 4 + kMaxRows;
-constexpr int kMaxPagesPerItem = 512;  // upper bound of pages_per_split (block tables are staged in LDS)
+//   agent_ptr [n_agents+1]         CSR over the partial rows of each agent
+//   agent_slot[...]                (row_base + slot*g) * hkv  (add jj*hkv + head for query head jj)
+// An item holds up to four agent groups; a group is the floor(16/g) agents whose
+// query heads of one KV head fill the 16 rows of one matrix-core tile.
+constexpr int kHeaderWords = 24;
+constexpr int kMaxRows = 16;        // query rows of one agent group (one wave's row tile)
+constexpr int kMaxGroups = 4;       // agent groups per item (one wave each)
+constexpr int kMaxItemAgents = 16;  // agents per item
+constexpr int kItemWords = 5 + kMaxItemAgents;
+constexpr int kMaxPagesPerItem = 256;  // upper bound of pages_per_split (block tables are staged in LDS)
 constexpr int kMaxItemsPerAgent = 1024;  // work items one agent may span (the combine stages them in LDS)
 
 enum PlanHeader {
     H_MAGIC = 0, H_N_ITEMS, H_N_BLOCKS, H_N_AGENTS, H_HKV, H_GROUP, H_AGENTS_PER_ITEM,
     H_OFF_ITEMS, H_OFF_BLOCKS, H_OFF_AGENT_PTR, H_OFF_AGENT_SLOT, H_TOTAL_WORDS, H_PAGES_PER_SPLIT,
-    H_PAGE_SIZE, H_N_SEGMENTS
+    H_PAGE_SIZE, H_N_SEGMENTS, H_TOTAL_ROWS, H_MAX_ITEM_AGENTS, H_FIELDS
 };
+static_assert(H_FIELDS <= kHeaderWords, "plan header fields overflow the header");
 constexpr int32_t kPlanMagic = 0x464b5631;  // "FKV1"
 
 }  // namespace fkv

@@ -34,7 +34,10 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     if (prm->hq % prm->hkv) return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: hq % hkv != 0");
     const int32_t g = prm->hq / prm->hkv;
     if (g > fkv::kMaxRows) return fkv::fail(FKV_ERR_UNSUPPORTED, "fkv_decode_plan_create: more than 16 query heads per KV head");
-    const int32_t ag = fkv::kMaxRows / g;
+    const int32_t ag = fkv::kMaxRows / g;  // agents per group
+    int32_t item_agents = prm->max_item_agents > 0 ? prm->max_item_agents : fkv::kMaxGroups * ag;
+    item_agents = std::min(item_agents, std::min(fkv::kMaxGroups * ag, fkv::kMaxItemAgents));
+    if (item_agents < 1) return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: bad max_item_agents");
     std::vector<int32_t> npages(A);
     int32_t P = 0;
     for (int32_t a = 0; a < A; ++a) {
@@ -75,44 +78,64 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
         }
     }
 
-    // 2. pages per split
-    int64_t units = 0;  // page x agent-group units per KV head
-    for (auto &s : segs) units += (int64_t)s.n * ((int64_t)(s.agents.size() + ag - 1) / ag);
+    // 2. agent chunks per segment: up to item_agents agents, in whole groups of ag where
+    //    possible; chunks of 3 groups are split 2 + 1 so each item has 1, 2 or 4 groups
+    auto chunk_sizes = [&](size_t na) {
+        std::vector<size_t> out;
+        const size_t full = (size_t)item_agents;
+        while (na > 0) {
+            size_t c = std::min(na, full);
+            const size_t groups = (c + ag - 1) / ag;
+            if (groups == 3) c = std::min(c, (size_t)(2 * ag));
+            out.push_back(c);
+            na -= c;
+        }
+        return out;
+    };
+    // 3. pages per split: enough workgroups for every CU to hold a few
+    int64_t units = 0;  // (page x item) units per KV head
+    for (auto &s : segs) units += (int64_t)s.n * (int64_t)chunk_sizes(s.agents.size()).size();
     int32_t pps = prm->pages_per_split;
     if (pps == 0) {
         const int64_t cus = prm->num_cus > 0 ? prm->num_cus : 256;
-        const int64_t target_items = std::max<int64_t>(1, (4 * cus + prm->hkv - 1) / prm->hkv);
-        pps = (int32_t)std::max<int64_t>(4, (units + target_items - 1) / target_items);
+        const int64_t target_items = std::max<int64_t>(1, (3 * cus + prm->hkv - 1) / prm->hkv);
+        pps = (int32_t)std::max<int64_t>(8, (units + target_items - 1) / target_items);
         pps = std::min(pps, fkv::kMaxPagesPerItem);
-        pps = (pps + 3) / 4 * 4;
+        pps = (pps + 1) / 2 * 2;
     }
     if (pps > fkv::kMaxPagesPerItem)
-        return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: pages_per_split above 512");
+        return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: pages_per_split above 256");
 
-    // 3. work items, clustered by (segment, split)
-    struct Item { int32_t p0, p1; std::vector<int32_t> agents; };
+    // 4. work items, clustered by (segment, split)
+    struct Item { int32_t p0, p1, row_base; std::vector<int32_t> agents; };
     std::vector<Item> items;
     std::vector<std::pair<int32_t, int32_t>> clusters;  // [first item, item count)
     std::vector<double> cluster_cost;
+    int64_t total_rows = 0;
     for (auto &s : segs) {
+        const std::vector<size_t> chunks = chunk_sizes(s.agents.size());
         for (int32_t p0 = s.first; p0 < s.first + s.n; p0 += pps) {
             const int32_t p1 = std::min(p0 + pps, s.first + s.n);
             const int32_t first = (int32_t)items.size();
             double cost = 0;
-            for (size_t k = 0; k < s.agents.size(); k += ag) {
-                Item it{p0, p1, {}};
-                for (size_t j = k; j < std::min(s.agents.size(), k + ag); ++j) it.agents.push_back(s.agents[j]);
-                cost += (double)(p1 - p0) * (2.0 + (double)it.agents.size());
+            size_t k = 0;
+            for (size_t c : chunks) {
+                Item it{p0, p1, (int32_t)total_rows, {}};
+                for (size_t j = k; j < k + c; ++j) it.agents.push_back(s.agents[j]);
+                k += c;
+                total_rows += (int64_t)c * g;
+                cost += (double)(p1 - p0) * (8.0 + (double)it.agents.size());
                 items.push_back(std::move(it));
             }
             clusters.push_back({first, (int32_t)items.size() - first});
             cluster_cost.push_back(cost);
         }
     }
+    if (total_rows * prm->hkv > INT32_MAX) return fkv::fail(FKV_ERR_UNSUPPORTED, "fkv_decode_plan_create: too many rows");
     const int32_t n_items = (int32_t)items.size();
     const int32_t hkv = prm->hkv;
 
-    // 4. workgroup order: clusters dealt to XCDs by least accumulated cost
+    // 5. workgroup order: clusters dealt to XCDs by least accumulated cost
     std::vector<std::vector<int32_t>> per_xcd(kNumXcd);
     std::vector<double> load(kNumXcd, 0.0);
     std::vector<int32_t> order(clusters.size());
@@ -133,11 +156,12 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     for (auto &l : per_xcd) depth = std::max(depth, l.size());
     const int32_t n_blocks = (int32_t)(depth * kNumXcd);
 
-    // 5. partial slots per agent (CSR)
+    // 6. partial rows per agent (CSR): row (row_base + slot*g + jj) of head h lives at
+    //    partial index (row_base + slot*g + jj) * hkv + h
     std::vector<std::vector<int32_t>> slots(A);
     for (int32_t w = 0; w < n_items; ++w)
         for (size_t j = 0; j < items[w].agents.size(); ++j)
-            slots[items[w].agents[j]].push_back((int32_t)(((int64_t)w * hkv) * fkv::kMaxRows + (int64_t)j * g));
+            slots[items[w].agents[j]].push_back((int32_t)(((int64_t)items[w].row_base + (int64_t)j * g) * hkv));
 
     for (auto &v : slots)
         if (v.size() > (size_t)fkv::kMaxItemsPerAgent) {
@@ -145,7 +169,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
                              "fkv_decode_plan_create: more than 1024 work items for one agent; raise pages_per_split");
         }
 
-    // 6. serialise
+    // 7. serialise
     auto *pl = new fkv_plan();
     pl->hkv = hkv;
     pl->g = g;
@@ -179,13 +203,16 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     w[fkv::H_PAGES_PER_SPLIT] = pps;
     w[fkv::H_PAGE_SIZE] = ps;
     w[fkv::H_N_SEGMENTS] = (int32_t)segs.size();
+    w[fkv::H_TOTAL_ROWS] = (int32_t)total_rows;
+    w[fkv::H_MAX_ITEM_AGENTS] = item_agents;
     for (int32_t i = 0; i < n_items; ++i) {
         int32_t *r = &w[off_items + (int64_t)i * fkv::kItemWords];
         r[0] = items[i].p0;
         r[1] = items[i].p1;
         r[2] = items[i].agents[0];
         r[3] = (int32_t)items[i].agents.size();
-        for (int32_t j = 0; j < fkv::kMaxRows; ++j) r[4 + j] = j < r[3] ? items[i].agents[j] : -1;
+        r[4] = items[i].row_base;
+        for (int32_t j = 0; j < fkv::kMaxItemAgents; ++j) r[5 + j] = j < r[3] ? items[i].agents[j] : -1;
     }
     for (int32_t b = 0; b < n_blocks; ++b) {
         const auto &lst = per_xcd[b % kNumXcd];
@@ -220,8 +247,17 @@ fkv_status fkv_decode_plan_info(const fkv_plan *plan, int32_t d, int32_t r, fkv_
     out->n_segments = w[fkv::H_N_SEGMENTS];
     out->pages_per_split = w[fkv::H_PAGES_PER_SPLIT];
     const int64_t stride = (int64_t)(d + r + 2 + 3) / 4 * 4;
-    out->workspace_bytes = (int64_t)w[fkv::H_N_ITEMS] * plan->hkv * fkv::kMaxRows * stride * 4;
+    out->workspace_bytes = (int64_t)w[fkv::H_TOTAL_ROWS] * plan->hkv * stride * 4;
     return FKV_OK;
+}
+
+int32_t fkv_decode_plan_default_agents(int32_t hq, int32_t hkv, int32_t r, int32_t rope) {
+    if (hq < 1 || hkv < 1 || hq % hkv) return 0;
+    const int32_t g = hq / hkv;
+    if (g > fkv::kMaxRows) return 0;
+    int32_t n = std::min(fkv::kMaxGroups * (fkv::kMaxRows / g), fkv::kMaxItemAgents);
+    if (rope && r > 0) n = std::min(n, 256 / r);
+    return n;
 }
 
 fkv_status fkv_decode_plan_serialize(const fkv_plan *plan, int32_t *out, int64_t capacity_words) {

@@ -26,7 +26,7 @@ def _bf16(a: np.ndarray, device) -> torch.Tensor:
 
 class LoadedWorkload:
     def __init__(self, wl: Workload, device="cuda", rope: bool = True, placement_seed: Optional[int] = None,
-                 no_residual: bool = False, pages_per_split: int = 0, base_pages: Optional[int] = None,
+                 no_residual: bool = False, pages_per_split: int = 0, item_agents: int = 0, base_pages: Optional[int] = None,
                  res_pages: Optional[int] = None):
         self.wl = wl
         self.device = torch.device(device)
@@ -105,6 +105,7 @@ class LoadedWorkload:
         self.q_all = _bf16(wl.q, self.device)
         self.rope_tab = rt.rope_tables(d, max_pages * ps, wl.rope_theta, self.device) if self.rope else None
         self.pages_per_split = pages_per_split
+        self.item_agents = item_agents
         self._decode = None
         self._prefill = None
 
@@ -113,7 +114,9 @@ class LoadedWorkload:
         wl = self.wl
         agents = list(wl.decode_agents() if agents is None else agents)
         bb, rb, sl = self.tree.block_tables(agents, self.max_pages)
-        plan = rt.DecodePlan(bb, sl, wl.hq, wl.hkv, wl.page_size, self.pages_per_split)
+        plan = rt.DecodePlan(bb, sl, wl.hq, wl.hkv, wl.page_size, self.pages_per_split,
+                             max_item_agents=self.item_agents or rt.decode_plan_default_agents(
+                                 wl.hq, wl.hkv, wl.r, self.rope))
         info = plan.info(wl.d, wl.r)
         dev = self.device
         q_rows = torch.tensor([int(wl.q_offset[a]) for a in agents], device=dev)

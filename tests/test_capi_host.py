@@ -209,3 +209,83 @@ def test_attention_entry_points_reject_bad_arguments_before_launching():
     a.r = 16   # residual pointers missing
     assert N.fkv_residual_attention_decode(ctypes.byref(a), None, None) == N.FKV_ERR_INVALID
     assert "res_kv" in N.fkv_last_error().decode()
+
+
+def _parse_plan(words):
+    """Decode the serialised plan (layout of internal.hpp) into items, blocks and the CSR."""
+    H = dict(n_items=1, n_blocks=2, n_agents=3, hkv=4, g=5, off_items=7, off_blocks=8, off_ptr=9, off_slot=10,
+             total_rows=15, max_item_agents=16)
+    h = {k: int(words[v]) for k, v in H.items()}
+    items = []
+    for i in range(h["n_items"]):
+        r = words[h["off_items"] + 21 * i: h["off_items"] + 21 * (i + 1)]
+        items.append(dict(p0=int(r[0]), p1=int(r[1]), leader=int(r[2]), nag=int(r[3]), row_base=int(r[4]),
+                          agents=[int(x) for x in r[5:5 + int(r[3])]], pad=[int(x) for x in r[5 + int(r[3]):]]))
+    blocks = words[h["off_blocks"]: h["off_blocks"] + h["n_blocks"]]
+    ptr = words[h["off_ptr"]: h["off_ptr"] + h["n_agents"] + 1]
+    slots = words[h["off_slot"]: h["off_slot"] + int(ptr[-1])]
+    return h, items, blocks, ptr, slots
+
+
+def _synthetic_tables(rng, n_agents, groups, prefix_pages, mid_pages, max_suffix_pages, ps=16):
+    """Block tables of a fork tree: one shared root, `groups` mid-level branches, private tails."""
+    nxt = [0]
+
+    def fresh(n):
+        ids = list(range(nxt[0], nxt[0] + n))
+        nxt[0] += n
+        return ids
+    root = fresh(prefix_pages)
+    mids = [fresh(mid_pages) for _ in range(groups)]
+    rows, lens = [], []
+    for a in range(n_agents):
+        tail = int(rng.integers(1, max_suffix_pages + 1))
+        pages = root + mids[a % groups] + fresh(tail)
+        rows.append(pages)
+        lens.append((len(pages) - 1) * ps + int(rng.integers(1, ps + 1)))
+    mp = max(len(r) for r in rows)
+    bb = np.full((n_agents, mp), -1, np.int32)
+    for a, r in enumerate(rows):
+        bb[a, :len(r)] = r
+    return bb, np.array(lens, np.int32)
+
+
+@pytest.mark.parametrize("hq,hkv,r,rope", [(32, 8, 16, True), (32, 8, 16, False), (64, 8, 64, True),
+                                           (64, 8, 32, False), (8, 2, 8, True), (32, 8, 64, True)])
+@pytest.mark.parametrize("pps", [0, 4, 64])
+def test_decode_plan_items_cover_every_agent_page_once(hq, hkv, r, rope, pps):
+    """Host-side invariants the decode kernels rely on for in-bounds access: every (agent,
+    page) in exactly one item, items within the page and agent limits, disjoint partial rows
+    and a CSR that points each agent's query heads at exactly its rows."""
+    rng = np.random.default_rng(hq + r + pps)
+    g = hq // hkv
+    for n_agents, groups, pre, mid, suf in [(16, 1, 300, 0, 40), (37, 3, 64, 9, 5), (5, 5, 0, 3, 2)]:
+        bb, sl = _synthetic_tables(rng, n_agents, groups, pre, mid, suf)
+        n_item = rt.decode_plan_default_agents(hq, hkv, r, rope)
+        plan = rt.DecodePlan(bb, sl, hq, hkv, 16, pps, max_item_agents=n_item)
+        h, items, blocks, ptr, slots = _parse_plan(plan.serialize())
+        assert h["max_item_agents"] <= (256 // r if rope else 16) and h["max_item_agents"] <= 4 * (16 // g)
+        seen = np.zeros(bb.shape, np.int32)
+        rows = np.zeros(h["total_rows"], np.int32)
+        for it in items:
+            assert 0 <= it["p0"] < it["p1"] and it["p1"] - it["p0"] <= 256
+            assert 1 <= it["nag"] <= h["max_item_agents"] and it["leader"] == it["agents"][0]
+            assert all(x == -1 for x in it["pad"])
+            for a in it["agents"]:
+                assert it["p1"] <= (sl[a] + 15) // 16
+                assert (bb[a, it["p0"]:it["p1"]] == bb[it["leader"], it["p0"]:it["p1"]]).all()
+                seen[a, it["p0"]:it["p1"]] += 1
+            rows[it["row_base"]: it["row_base"] + it["nag"] * g] += 1
+        for a in range(n_agents):
+            npg = (sl[a] + 15) // 16
+            assert (seen[a, :npg] == 1).all() and (seen[a, npg:] == 0).all()
+        assert (rows == 1).all()
+        ids = [b for b in blocks if b >= 0]
+        assert sorted(ids) == list(range(len(items) * hkv)) and len(blocks) % 8 == 0
+        for a in range(n_agents):
+            mine = sorted(int(s) // hkv for s in slots[ptr[a]:ptr[a + 1]])
+            want = sorted(it["row_base"] + it["agents"].index(a) * g for it in items if a in it["agents"])
+            assert mine == want and all(int(s) % hkv == 0 for s in slots[ptr[a]:ptr[a + 1]])
+        info = plan.info(128, r)
+        assert info["workspace_bytes"] == h["total_rows"] * hkv * ((128 + r + 2 + 3) // 4 * 4) * 4
+        plan.close()
