@@ -176,11 +176,12 @@ typedef struct {
     int32_t hq, hkv;
     int32_t page_size;
     int32_t max_pages;        /* row stride of base_bt */
-    int32_t pages_per_split;  /* pages per work item (<= 256); 0 = choose automatically */
+    int32_t pages_per_split;  /* pages per work item (<= 64); 0 = choose automatically */
     int32_t num_cus;          /* compute units to fill; 0 = 256 */
-    int32_t max_item_agents;  /* agents sharing one work item; 0 = 4 groups of floor(16/g).  The RoPE
-                                 decode kernels need it <= 256 / r (their B_K fragments live in LDS);
-                                 fkv_decode_plan_default_agents gives the right value. */
+    int32_t max_item_agents;  /* agents sharing one work item; 0 = as many as the kernel takes
+                                 (fkv_decode_plan_default_agents); larger values are clamped */
+    int32_t r;                /* residual rank the plan will be run with (0, 8, 16, 32, 64) */
+    int32_t rope;             /* nonzero: the plan will be run with RoPE tables */
 } fkv_decode_plan_params;
 
 typedef struct {
@@ -192,7 +193,10 @@ typedef struct {
     int32_t pages_per_split;
 } fkv_plan_info;
 
-/* Agents per work item that the decode kernel for (hq, hkv, r, rope) accepts. */
+/* Most agents one decode work item can hold for (hq, hkv, r, rope): with RoPE one group
+ * of floor(16/g) agents; without RoPE up to four groups, as many as fit one LDS stage
+ * together with a page of four KV heads' base blocks.  Returns 0 for an unsupported
+ * head layout. */
 int32_t fkv_decode_plan_default_agents(int32_t hq, int32_t hkv, int32_t r, int32_t rope);
 
 /* Build a plan from host block tables (base_bt [n_agents][max_pages], seq_lens [n_agents]). */

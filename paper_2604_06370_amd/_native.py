@@ -17,6 +17,12 @@ if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2604_06370_amd.build` "
                       "(or __graft_entry__.build())")
 
+# The library and PyTorch must share one HIP runtime: torch ships its own
+# libamdhip64 (same soname as the one the library links), so torch is loaded first and
+# the library's dependency then resolves to it.  Loaded the other way round, the
+# process would hold two runtimes and one of them would see no device.
+import torch  # noqa: E402,F401  (load order only)
+
 lib = ctypes.CDLL(LIB_PATH)
 
 c_i32, c_i64, c_f32, c_f64, c_vp, c_sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double, \
@@ -56,7 +62,8 @@ class fkv_pool_stats(ctypes.Structure):
 
 class fkv_decode_plan_params(ctypes.Structure):
     _fields_ = [("n_agents", c_i32), ("hq", c_i32), ("hkv", c_i32), ("page_size", c_i32), ("max_pages", c_i32),
-                ("pages_per_split", c_i32), ("num_cus", c_i32), ("max_item_agents", c_i32)]
+                ("pages_per_split", c_i32), ("num_cus", c_i32), ("max_item_agents", c_i32), ("r", c_i32),
+                ("rope", c_i32)]
 
 
 class fkv_plan_info(ctypes.Structure):

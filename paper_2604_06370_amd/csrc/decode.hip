@@ -1,17 +1,18 @@
 // ResidualAttention decode for gfx950 (Section 5.3, Algorithm 1).
 //
-// One workgroup = one (work item, KV head h).  A work item is a page range of a
-// segment together with up to four groups of agents that read the same base
-// pages there; a group is the floor(16/g) agents whose g query heads of KV head h
-// fill the 16 rows of one matrix-core tile.
-//  - single-group items (typically private suffixes): the four waves stride over
-//    the pages with a register-double-buffered pipeline and are merged through LDS
-//    at the end;
-//  - multi-group items (shared prefixes): each base page is loaded once into LDS
-//    and every wave applies it to its own group's 16 rows, so a shared page crosses
-//    the memory hierarchy once per workgroup instead of once per group.
-// Each row leaves one partial (m, l, acc, acc_r) in the workspace; a second kernel
-// merges an agent's partials (log-sum-exp combine) and applies Stage 3.
+// One workgroup = one (work item, KV head h), four waves.  A work item is a page range
+// of a segment together with the agents that read the same base pages there, in groups
+// of floor(16/g) agents whose g query heads of KV head h fill the 16 rows of one
+// matrix-core tile.  An item of ng groups runs on the four waves as ng groups x 4/ngp
+// copies (ngp = ng rounded up to 1, 2 or 4); each copy covers its share of the pages
+// and writes its own partial rows (acc, acc_r, m, l) straight from registers.  A second
+// kernel merges an agent's partials (log-sum-exp combine) and applies Stage 3.
+//  - single-group items (private suffixes; every item with RoPE or rank >= 32): the
+//    waves stride over the pages with a register-double-buffered pipeline;
+//  - multi-group items (shared prefixes): stages of two pages; each base K/V block is
+//    loaded once into LDS (two stages ahead, through registers) and every wave applies
+//    it to its own group's 16 rows, so a shared page crosses the memory hierarchy once
+//    per workgroup instead of once per group.
 //
 // Per page and wave (all products on the matrix cores, fp32 accumulate):
 //   S^T  = K_base . Q^T                               16x16x32, all rows of the wave
@@ -45,6 +46,7 @@ constexpr int WAVES = 4;
 constexpr float kNegInf = -INFINITY;
 constexpr int kMaxPagesPerItem = fkv::kMaxPagesPerItem;
 constexpr int kBlockHalfs = PS * D;  // bf16 values in one (page, K|V, head) block
+constexpr int kBlockBytes = kBlockHalfs * 2;
 
 struct DecodeArgs {
     const uint16_t *q, *base_kv, *res_kv, *lora_b;
@@ -60,17 +62,172 @@ struct DecodeArgs {
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
 constexpr int cmin(int a, int b) { return a < b ? a : b; }
 
+// Partial row record in the workspace (floats): acc[D], acc_r[R], m, l; stride
+// rounded up to a multiple of 4 so every record is 16-byte aligned.
+__host__ __device__ constexpr int ws_stride_of(int r) { return (D + r + 2 + 3) / 4 * 4; }
+
+// ---------------------------------------------------------------------------
+// Per-wave row state and the page update shared by both kernels.
+template <int R>
+struct Rows {
+    static constexpr int RT = R == 0 ? 0 : (R + 15) / 16;  // 16-wide rank tiles
+    static constexpr int RTX = RT > 0 ? RT : 1;
+    f32x4 oacc[8];     // O^T[16mt + 4grp + i][row col]
+    f32x4 racc[RTX];   // acc_r^T[16t + 4grp + i][row col]
+    float m, l;
+    __device__ __forceinline__ void init() {
+#pragma unroll
+        for (int mt = 0; mt < 8; ++mt) oacc[mt] = f32x4{0, 0, 0, 0};
+#pragma unroll
+        for (int t = 0; t < RTX; ++t) racc[t] = f32x4{0, 0, 0, 0};
+        m = kNegInf;
+        l = 0.f;
+    }
+};
+
+// Zero tokens 4grp+i >= vis of a [.][token] fragment (bf16 pairs).
+__device__ __forceinline__ u32x2 mask4(u32x2 v, int vis, int grp) {
+    if (4 * grp + 0 >= vis) v.x &= 0xffff0000u;
+    if (4 * grp + 1 >= vis) v.x &= 0x0000ffffu;
+    if (4 * grp + 2 >= vis) v.y &= 0xffff0000u;
+    if (4 * grp + 3 >= vis) v.y &= 0x0000ffffu;
+    return v;
+}
+
+// Maximum over the four lane groups (lanes l, l^16, l^32, l^48) with the gfx950 lane
+// swaps (plain VALU, no LDS round trip).
+__device__ __forceinline__ float max_over_groups(float x) {
+    const uint32_t u = __float_as_uint(x);
+    const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    const float y = fmaxf(x, __uint_as_float((threadIdx.x & 32) ? a[0] : a[1]));
+    const uint32_t v = __float_as_uint(y);
+    const auto b = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+    return fmaxf(y, __uint_as_float((threadIdx.x & 16) ? b[0] : b[1]));
+}
+
+// Stage 2 on one page's S^T tile plus the value products.  Tokens tok0+4grp+i at or
+// past `len` (this lane's row's sequence length) or on an invalid page get zero weight;
+// vf must already be zero for tokens past every row's length, cv for tokens past its
+// slot's residual length.
+//
+// The running maximum m is only moved (and acc, acc_r, l rescaled) when some row's new
+// scores exceed it by more than 2^kLazyRescale; otherwise the weights 2^(s - m) of this
+// page stay below 2^kLazyRescale.  acc, acc_r and l always refer to the same m, so the
+// partial is exact whichever m it ends with.
+constexpr float kLazyRescale = 8.f;
+
+template <int R, int NS>
+__device__ __forceinline__ void softmax_pv(Rows<R> &st, f32x4 sacc, bool valid, int tok0, int len, float scale_log2,
+                                           const u32x2 *vf, const u32x2 (*cv)[Rows<R>::RTX], int my_slot_l,
+                                           int grp) {
+    float sv[4];
+    float mx = kNegInf;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int tok = tok0 + 4 * grp + i;
+        sv[i] = (valid && tok < len) ? sacc[i] * scale_log2 : kNegInf;
+        mx = fmaxf(mx, sv[i]);
+    }
+    mx = max_over_groups(mx);
+    if (__builtin_amdgcn_ballot_w64(mx > st.m + kLazyRescale) != 0) {
+        const float m_new = fmaxf(st.m, mx);
+        const float alpha = fast_exp2(st.m - (m_new == kNegInf ? 0.f : m_new));
+        st.l *= alpha;
+#pragma unroll
+        for (int mt = 0; mt < 8; ++mt) st.oacc[mt] *= alpha;
+#pragma unroll
+        for (int t = 0; t < Rows<R>::RT; ++t) st.racc[t] *= alpha;
+        st.m = m_new;
+    }
+    const float m_use = st.m == kNegInf ? 0.f : st.m;
+    f32x4 pv;
+    float psum = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        pv[i] = fast_exp2(sv[i] - m_use);
+        psum += pv[i];
+    }
+    st.l += psum;
+    const u32x2 pf = pack4(pv);
+#pragma unroll
+    for (int mt = 0; mt < 8; ++mt) st.oacc[mt] = mfma16(vf[mt], pf, st.oacc[mt]);
+    if constexpr (R > 0) {
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+            const u32x2 pm = my_slot_l == s ? pf : u32x2{0, 0};
+#pragma unroll
+            for (int t = 0; t < Rows<R>::RT; ++t) st.racc[t] = mfma16(cv[s][t], pm, st.racc[t]);
+        }
+    }
+}
+
+// This wave's partial rows, straight from the accumulators (l summed over lane groups).
+template <int R>
+__device__ __forceinline__ void write_partial(const DecodeArgs &p, Rows<R> &st, bool row_active, int64_t prow,
+                                              int grp) {
+    st.l += __shfl_xor(st.l, 16);
+    st.l += __shfl_xor(st.l, 32);
+    if (!row_active) return;
+    float *dst = p.ws + prow * p.ws_stride;
+#pragma unroll
+    for (int mt = 0; mt < 8; ++mt) *reinterpret_cast<f32x4 *>(dst + 16 * mt + 4 * grp) = st.oacc[mt];
+#pragma unroll
+    for (int t = 0; t < Rows<R>::RT; ++t)
+        if (16 * t + 4 * grp < R) *reinterpret_cast<f32x4 *>(dst + D + 16 * t + 4 * grp) = st.racc[t];
+    if (grp == 0) {
+        dst[D + R] = st.m;
+        dst[D + R + 1] = st.l;
+    }
+}
+
+// Q^T as the B operand of the 16x16x32 products.  The head-dim index of slot j in
+// k-step kk is 32kk + 16(j/4) + 4grp + j%4 for this lane group: the order in which
+// a rebuilt key tile leaves the 16x16x16 accumulators and in which K blocks are
+// stored, so base keys, rebuilt keys and queries all share it.
+__device__ __forceinline__ void load_q(const uint16_t *qrow, bool active, int grp, u32x4 *qf) {
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+        u32x4 v = {0, 0, 0, 0};
+        if (active) {
+            const u32x2 lo = ldg64(qrow + 32 * kk + 4 * grp);
+            const u32x2 hi = ldg64(qrow + 32 * kk + 16 + 4 * grp);
+            v = u32x4{lo.x, lo.y, hi.x, hi.y};
+        }
+        qf[kk] = v;
+    }
+}
+
+// Lane-constant element offsets (within one agent's rCache page: C_K [16][R] then
+// C_V^T [R][16]) of the fragments this lane reads, and whether they are inside R.
+template <int R>
+struct ResOffsets {
+    static constexpr int RTX = Rows<R>::RTX;
+    int ck[RTX], cv[RTX];
+    bool ck_ok[RTX], cv_ok[RTX];
+    __device__ __forceinline__ ResOffsets(int col, int grp) {
+#pragma unroll
+        for (int t = 0; t < RTX; ++t) {
+            const int rho = 16 * t + col, rk = 16 * t + 4 * grp;
+            cv_ok[t] = rho < R;
+            ck_ok[t] = rk < R;
+            cv[t] = PS * R + (rho < R ? rho : (R > 0 ? R - 1 : 0)) * PS + 4 * grp;  // C_V^T[rho][tok 4grp..]
+            ck[t] = col * R + (rk < R ? rk : (R >= 4 ? R - 4 : 0));                 // C_K[tok col][rho 4grp..]
+        }
+    }
+};
+
+// ---------------------------------------------------------------------------
+// RoPE off: one workgroup per (work item, KV head), four waves.
 template <int R, int G, bool ROPE>
 struct SplitShape {
-    static constexpr int AG = ROWS / G;                                        // agents per group
-    static constexpr int RT = R == 0 ? 0 : (R + 15) / 16;                      // 16-wide rank tiles
-    static constexpr int MAX_SLOTS = cmin(fkv::kMaxGroups * AG, fkv::kMaxItemAgents);
-    static constexpr int BKT_SLOTS = ROPE ? cmin(MAX_SLOTS, 256 / (R > 0 ? R : 1)) : 0;
-    static constexpr int MERGE_BYTES = WAVES * ((8 + RT) * 256 + 2 * ROWS) * 4;
-    static constexpr int STAGE_BYTES = 2 * 2 * 2 * kBlockHalfs * 2;           // [buf][page][K|V] blocks
-    static constexpr int BSTAGE_BYTES = ROPE ? 4 * R * D * 2 : 0;             // B_K rows of 4 slots
-    static constexpr int UNION_BYTES = cmax(MERGE_BYTES, cmax(STAGE_BYTES, BSTAGE_BYTES));
-    static constexpr int BKT_BYTES = BKT_SLOTS * RT * 8 * 64 * 8;             // B_K^T fragments
+    static constexpr int AG = ROWS / G;                                         // agents per group
+    static constexpr int RT = R == 0 ? 0 : (R + 15) / 16;                       // 16-wide rank tiles
+    static constexpr bool MULTI = !ROPE && R < 32;                             // several groups per item
+    static constexpr int MAX_SLOTS = MULTI ? cmin(fkv::kMaxGroups * AG, fkv::kMaxItemAgents) : AG;
+    static constexpr int STAGE_BYTES = MULTI ? 2 * 2 * 2 * kBlockHalfs * 2 : 0;  // [buf][page][K|V] blocks
+    static constexpr int BSTAGE_BYTES = ROPE ? AG * R * D * 2 : 0;              // row-major B_K slices
+    static constexpr int UNION_BYTES = cmax(16, cmax(STAGE_BYTES, BSTAGE_BYTES));
+    static constexpr int BKT_BYTES = ROPE ? AG * RT * 8 * 64 * 8 : 0;           // B_K^T fragments
     static constexpr int TABLE_WORDS = (1 + (R > 0 ? MAX_SLOTS : 0)) * kMaxPagesPerItem;
     static constexpr int LDS_BYTES = UNION_BYTES + BKT_BYTES + TABLE_WORDS * 4;
 };
@@ -82,7 +239,6 @@ __global__ __launch_bounds__(256, ROPE ? 1 : 2) void decode_split_kernel(DecodeA
     constexpr int RT = S::RT;
     constexpr int RTX = RT > 0 ? RT : 1;
     __shared__ __attribute__((aligned(16))) unsigned char lds[S::LDS_BYTES];
-    float *lds_f = reinterpret_cast<float *>(lds);
     uint16_t *lds_h = reinterpret_cast<uint16_t *>(lds);
     uint32_t *lds_bkt = reinterpret_cast<uint32_t *>(lds + S::UNION_BYTES);
     int32_t *s_tab = reinterpret_cast<int32_t *>(lds + S::UNION_BYTES + S::BKT_BYTES);
@@ -96,6 +252,7 @@ __global__ __launch_bounds__(256, ROPE ? 1 : 2) void decode_split_kernel(DecodeA
     const int32_t *rec = plan + plan[fkv::H_OFF_ITEMS] + item * fkv::kItemWords;
     const int pg0 = rec[0], pg1 = rec[1], leader = rec[2], nag = rec[3], row_base = rec[4];
     const int32_t *item_agents = rec + 5;
+    if (ROPE && nag > AG) return;  // rejected on the host: RoPE items hold one group
     const int ng = (nag + AG - 1) / AG;                 // agent groups in the item (1..4)
     const int ngp = ng == 1 ? 1 : (ng == 2 ? 2 : 4);   // groups rounded to a divisor of 4
 
@@ -103,23 +260,42 @@ __global__ __launch_bounds__(256, ROPE ? 1 : 2) void decode_split_kernel(DecodeA
     const int wave = uniform(threadIdx.x >> 6);
     const int col = lane & 15, grp = lane >> 4;
     const int my_group = wave % ngp;
+    const int copy = wave / ngp;                        // which of the 4/ngp waves of the group
     const int sb = my_group * AG;                       // first item slot of this wave's group
     const int my_slot_l = col / G;                      // this lane's row: slot within the group
-    const bool row_active = my_slot_l < AG && sb + my_slot_l < nag;
+    const bool row_active = sb + my_slot_l < nag;
     const int my_agent = row_active ? item_agents[sb + my_slot_l] : 0;
-    const int my_len = row_active ? p.seq_lens[my_agent] : 0;
     const int qh = h * G + (col % G);
 
-    int slot_ad[AG], slot_len[AG];
+    // block-table entries of the item's pages, for the base pool and every slot's
+    // residual pool, staged in LDS with one parallel pass
+    const int npg = pg1 - pg0;
+    const int n_tab = R > 0 ? 1 + ngp * AG : 1;
+    for (int idx = threadIdx.x; idx < n_tab * npg; idx += 256) {
+        const int t = idx / npg, i = idx - t * npg;
+        int32_t v = 0;
+        if (t == 0) {
+            v = p.base_bt[(int64_t)leader * p.max_pages + pg0 + i];
+        } else if (t - 1 < nag) {
+            v = p.res_bt[(int64_t)item_agents[t - 1] * p.max_pages + pg0 + i];
+        }
+        s_tab[t * kMaxPagesPerItem + i] = v;
+    }
+
+    // per slot of the wave's group: adapter, and the tokens whose rCache rows are used
+    // (the sequence length, or 0 for an empty slot or an agent without adapter)
+    int slot_ad[AG], res_len[AG];
     int max_len = 0;  // longest sequence of the wave's group (V tokens past it are zeroed)
 #pragma unroll
     for (int s = 0; s < AG; ++s) {
         const bool ok = sb + s < nag;
         const int ag_id = ok ? item_agents[sb + s] : 0;
+        const int len = ok ? p.seq_lens[ag_id] : 0;
         slot_ad[s] = (ok && R > 0) ? p.adapter_idx[ag_id] : -1;
-        slot_len[s] = ok ? p.seq_lens[ag_id] : 0;
-        max_len = max_len > slot_len[s] ? max_len : slot_len[s];
+        res_len[s] = slot_ad[s] >= 0 ? len : 0;
+        max_len = max_len > len ? max_len : len;
     }
+    const int my_len = row_active ? p.seq_lens[my_agent] : 0;
 
     // Q^T as the B operand of the 16x16x32 products.  The head-dim index of slot j in
     // k-step kk is 32kk + 16(j/4) + 4grp + j%4 for this lane group: the order in which
@@ -140,95 +316,78 @@ __global__ __launch_bounds__(256, ROPE ? 1 : 2) void decode_split_kernel(DecodeA
 
     const int64_t n = (int64_t)hkv * D;
     const int64_t res_page_halfs = 2 * PS * R;
-    // ---- prologue: per-agent residual key operands ----
-    u32x2 wf[RTX];   // RoPE off: (B_K q) for this lane's row, bf16, B operand of 16x16x16
-    if constexpr (R > 0 && !ROPE) {
-        f32x4 wacc[RTX];
+    // RoPE off: W = B_K q per row (bf16, B operand of the 16x16x16 residual products);
+    // computed after the first pages' loads are issued so its latency overlaps theirs
+    u32x2 wf[RTX];
 #pragma unroll
-        for (int t = 0; t < RT; ++t) wacc[t] = f32x4{0, 0, 0, 0};
+    for (int t = 0; t < RTX; ++t) wf[t] = u32x2{0, 0};
+    auto prep_w = [&]() {
+        if constexpr (R > 0 && !ROPE) {
+            f32x4 wacc[RTX];
 #pragma unroll
-        for (int s = 0; s < AG; ++s) {
-            if (slot_ad[s] < 0) continue;
-            const uint16_t *bk = p.lora_b + (int64_t)slot_ad[s] * 2 * R * n + (int64_t)h * D;
+            for (int t = 0; t < RT; ++t) wacc[t] = f32x4{0, 0, 0, 0};
 #pragma unroll
-            for (int t = 0; t < RT; ++t) {
-                const int rho = 16 * t + col;
-                f32x4 acc = {0, 0, 0, 0};
+            for (int s = 0; s < AG; ++s) {
+                const int ad = slot_ad[s] >= 0 ? slot_ad[s] : 0;  // slots without adapter: result unused
+                const uint16_t *bk = p.lora_b + (int64_t)ad * 2 * R * n + (int64_t)h * D;
 #pragma unroll
-                for (int kk = 0; kk < 4; ++kk) {
-                    u32x4 a = {0, 0, 0, 0};
-                    if (rho < R) {
-                        const u32x2 lo = ldg64(bk + (int64_t)rho * n + 32 * kk + 4 * grp);
-                        const u32x2 hi = ldg64(bk + (int64_t)rho * n + 32 * kk + 16 + 4 * grp);
-                        a = u32x4{lo.x, lo.y, hi.x, hi.y};
+                for (int t = 0; t < RT; ++t) {
+                    const int rho = 16 * t + col;
+                    f32x4 acc = {0, 0, 0, 0};
+#pragma unroll
+                    for (int kk = 0; kk < 4; ++kk) {
+                        const int64_t ro = (int64_t)(rho < R ? rho : 0) * n;
+                        const u32x2 lo = ldg64(bk + ro + 32 * kk + 4 * grp);
+                        const u32x2 hi = ldg64(bk + ro + 32 * kk + 16 + 4 * grp);
+                        const u32x4 a = rho < R ? u32x4{lo.x, lo.y, hi.x, hi.y} : u32x4{0, 0, 0, 0};
+                        acc = mfma32(a, qf[kk], acc);
                     }
-                    acc = mfma32(a, qf[kk], acc);
+                    if (my_slot_l == s && slot_ad[s] >= 0) wacc[t] = acc;
                 }
-                if (my_slot_l == s) wacc[t] = acc;
             }
-        }
 #pragma unroll
-        for (int t = 0; t < RT; ++t) wf[t] = pack4(wacc[t]);
-    }
+            for (int t = 0; t < RT; ++t) wf[t] = pack4(wacc[t]);
+        }
+    };
+    __syncthreads();  // tables staged
+
     if constexpr (ROPE) {
-        // B_K^T fragments of every item slot (lane holds B_K[16t + 4grp + i][16mt + col]),
-        // built from row-major B_K slices staged four slots at a time.
-        const int nstage = ngp * AG;  // unused slots of the last group get zero fragments
-        for (int s0 = 0; s0 < nstage; s0 += 4) {
-            const int ns = nstage - s0 < 4 ? nstage - s0 : 4;
-            for (int idx = threadIdx.x; idx < ns * R * (D / 8); idx += 256) {
-                const int sl = idx / (R * (D / 8));
-                const int rem = idx - sl * (R * (D / 8));
-                const int rho = rem / (D / 8), c8 = rem - rho * (D / 8);
-                const int ad = s0 + sl < nag ? p.adapter_idx[item_agents[s0 + sl]] : -1;
-                u32x4 v = {0, 0, 0, 0};
-                if (ad >= 0) v = ldg128(p.lora_b + (int64_t)ad * 2 * R * n + (int64_t)rho * n + (int64_t)h * D + 8 * c8);
-                *reinterpret_cast<u32x4 *>(lds_h + (sl * R + rho) * D + 8 * c8) = v;
-            }
-            __syncthreads();
-            for (int idx = threadIdx.x; idx < ns * RT * 8 * 64; idx += 256) {
-                const int ln = idx & 63;
-                const int rest = idx >> 6;  // (sl*RT + t)*8 + mt
-                const int mt = rest & 7, st = rest >> 3;
-                const int sl = st / RTX, t = st - sl * RTX;
-                const int c = ln & 15, gg = ln >> 4;
-                uint32_t w[2];
+        // B_K^T fragments of the group's slots (lane holds B_K[16t + 4grp + i][16mt + col]),
+        // built from row-major B_K slices staged in LDS
+        for (int idx = threadIdx.x; idx < AG * R * (D / 8); idx += 256) {
+            const int sl = idx / (R * (D / 8));
+            const int rem = idx - sl * (R * (D / 8));
+            const int rho = rem / (D / 8), c8 = rem - rho * (D / 8);
+            const int ad = sl < nag ? p.adapter_idx[item_agents[sl]] : -1;
+            u32x4 v = {0, 0, 0, 0};
+            if (ad >= 0) v = ldg128(p.lora_b + (int64_t)ad * 2 * R * n + (int64_t)rho * n + (int64_t)h * D + 8 * c8);
+            *reinterpret_cast<u32x4 *>(lds_h + (sl * R + rho) * D + 8 * c8) = v;
+        }
+        __syncthreads();
+        for (int idx = threadIdx.x; idx < AG * RT * 8 * 64; idx += 256) {
+            const int ln = idx & 63;
+            const int rest = idx >> 6;  // (sl*RT + t)*8 + mt
+            const int mt = rest & 7, st = rest >> 3;
+            const int sl = st / RTX, t = st - sl * RTX;
+            const int c = ln & 15, gg = ln >> 4;
+            uint32_t w[2];
 #pragma unroll
-                for (int j = 0; j < 2; ++j) {
-                    const int r0 = 16 * t + 4 * gg + 2 * j;
-                    const uint16_t lo = r0 < R ? lds_h[(sl * R + r0) * D + 16 * mt + c] : (uint16_t)0;
-                    const uint16_t hi = r0 + 1 < R ? lds_h[(sl * R + r0 + 1) * D + 16 * mt + c] : (uint16_t)0;
-                    w[j] = (uint32_t)lo | ((uint32_t)hi << 16);
-                }
-                const int o = ((((s0 + sl) * RTX + t) * 8 + mt) * 64 + ln) * 2;
-                lds_bkt[o] = w[0];
-                lds_bkt[o + 1] = w[1];
+            for (int j = 0; j < 2; ++j) {
+                const int r0 = 16 * t + 4 * gg + 2 * j;
+                const uint16_t lo = r0 < R ? lds_h[(sl * R + r0) * D + 16 * mt + c] : (uint16_t)0;
+                const uint16_t hi = r0 + 1 < R ? lds_h[(sl * R + r0 + 1) * D + 16 * mt + c] : (uint16_t)0;
+                w[j] = (uint32_t)lo | ((uint32_t)hi << 16);
             }
-            __syncthreads();
+            const int o = (((sl * RTX + t) * 8 + mt) * 64 + ln) * 2;
+            lds_bkt[o] = w[0];
+            lds_bkt[o + 1] = w[1];
         }
+        __syncthreads();
     }
-    // block-table entries of the item's pages: one round trip for the whole item
-    const int npg = pg1 - pg0;
-    for (int i = threadIdx.x; i < npg; i += 256) s_tab[i] = p.base_bt[(int64_t)leader * p.max_pages + pg0 + i];
-    if constexpr (R > 0) {
-        // slots past nag (the unused tail of the last group) read residual page 0, masked
-        for (int s = 0; s < ngp * AG; ++s) {
-            const int ag_id = s < nag ? item_agents[s] : 0;
-            const bool has = s < nag && p.adapter_idx[ag_id] >= 0;
-            for (int i = threadIdx.x; i < npg; i += 256)
-                s_tab[(1 + s) * kMaxPagesPerItem + i] = has ? p.res_bt[(int64_t)ag_id * p.max_pages + pg0 + i] : 0;
-        }
-    }
-    __syncthreads();
 
     // ---- state of this wave's 16 rows ----
-    f32x4 oacc[8];
-#pragma unroll
-    for (int mt = 0; mt < 8; ++mt) oacc[mt] = f32x4{0, 0, 0, 0};
-    f32x4 racc[RTX];
-#pragma unroll
-    for (int t = 0; t < RTX; ++t) racc[t] = f32x4{0, 0, 0, 0};
-    float m_run = kNegInf, l_run = 0.f;
+    Rows<R> st;
+    st.init();
 
     // lane-constant element offsets of the rCache fragment loads
     int ck_off[RTX], cv_off[RTX];
@@ -241,17 +400,19 @@ __global__ __launch_bounds__(256, ROPE ? 1 : 2) void decode_split_kernel(DecodeA
         cv_off[t] = PS * R + (rho < R ? rho : (R > 0 ? R - 1 : 0)) * PS + 4 * grp;   // C_V^T[rho][tok 4grp..]
         ck_off[t] = col * R + (rk < R ? rk : (R >= 4 ? R - 4 : 0));                  // C_K[tok col][rho 4grp..]
     }
-    auto mask4 = [&](u32x2 v, int vis) {  // zero tokens 4grp+i >= vis of a [.][tok] fragment
+    auto mask4g = [&](u32x2 v, int vis) {  // zero tokens 4grp+i >= vis of a [.][tok] fragment
         if (4 * grp + 0 >= vis) v.x &= 0xffff0000u;
         if (4 * grp + 1 >= vis) v.x &= 0x0000ffffu;
         if (4 * grp + 2 >= vis) v.y &= 0xffff0000u;
         if (4 * grp + 3 >= vis) v.y &= 0x0000ffffu;
         return v;
     };
-    // rCache fragments of slot sb+s for logical page pg
+    // rCache fragments of slot sb+s for logical page pg.  Slots without an adapter (or
+    // past the item's agents) read residual page 0; compute_page zeroes them (their
+    // residual length is 0), whatever that page holds.
     auto load_res = [&](int pg, int s, u32x2 *ck, u32x2 *cv) {
-        const int rpage = uniform(s_tab[(1 + sb + s) * kMaxPagesPerItem + (pg - pg0)]);
-        const uint16_t *rb = p.res_kv + (int64_t)rpage * res_page_halfs;
+        const int tab = uniform(s_tab[(1 + sb + s) * kMaxPagesPerItem + (pg - pg0)]);
+        const uint16_t *rb = p.res_kv + (int64_t)(slot_ad[s] >= 0 ? tab : 0) * res_page_halfs;
 #pragma unroll
         for (int t = 0; t < RT; ++t) {
             const u32x2 v = ldg64(rb + cv_off[t]);
@@ -280,7 +441,7 @@ __global__ __launch_bounds__(256, ROPE ? 1 : 2) void decode_split_kernel(DecodeA
         const int vis = max_len - tok0;   // tokens past every agent's end may hold any bits
         if (vis < PS) {
 #pragma unroll
-            for (int mt = 0; mt < 8; ++mt) vf[mt] = mask4(vf[mt], vis);
+            for (int mt = 0; mt < 8; ++mt) vf[mt] = mask4g(vf[mt], vis);
         }
         f32x4 sacc = {0, 0, 0, 0};
 #pragma unroll
@@ -288,14 +449,13 @@ __global__ __launch_bounds__(256, ROPE ? 1 : 2) void decode_split_kernel(DecodeA
         if constexpr (R > 0) {
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
-                // slots without an adapter contribute zeros (zero W or zero B_K^T)
                 // rCache tokens past the slot's own length are unwritten: zero them (a NaN
                 // there would reach every row through the zero entries of the other slots)
-                const int svis = slot_len[s] - tok0;
+                const int svis = res_len[s] - tok0;
                 if (svis < PS) {
 #pragma unroll
                     for (int t = 0; t < RT; ++t) {
-                        cv[s][t] = mask4(cv[s][t], svis);
+                        cv[s][t] = mask4g(cv[s][t], svis);
                         ck[s][t] = col < svis ? ck[s][t] : u32x2{0, 0};
                     }
                 }
@@ -314,7 +474,7 @@ __global__ __launch_bounds__(256, ROPE ? 1 : 2) void decode_split_kernel(DecodeA
 #pragma unroll
                         for (int t = 0; t < RT; ++t) {
                             const u32x2 a = *reinterpret_cast<const u32x2 *>(
-                                lds_bkt + (((((sb + s) * RTX + t) * 8 + mt) * 64) + lane) * 2);
+                                lds_bkt + ((((sb + s) * RTX + t) * 8 + mt) * 64 + lane) * 2);
                             u[mt] = mfma16(a, ck[s][t], u[mt]);
                         }
                     }
@@ -336,45 +496,8 @@ __global__ __launch_bounds__(256, ROPE ? 1 : 2) void decode_split_kernel(DecodeA
                 }
             }
         }
-        // Stage 2: online softmax over this page's 16 tokens (rows live in lanes)
-        float sv[4];
-        float mx = kNegInf;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int tok = tok0 + 4 * grp + i;
-            sv[i] = (valid && row_active && tok < my_len) ? sacc[i] * p.scale_log2 : kNegInf;
-            mx = fmaxf(mx, sv[i]);
-        }
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m_run, mx);
-        const float m_use = m_new == kNegInf ? 0.f : m_new;
-        const float alpha = fast_exp2(m_run - m_use);
-        f32x4 pv;
-        float psum = 0.f;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            pv[i] = fast_exp2(sv[i] - m_use);
-            psum += pv[i];
-        }
-        l_run = l_run * alpha + psum;
-        m_run = m_new;
-        const u32x2 pf = pack4(pv);
-#pragma unroll
-        for (int mt = 0; mt < 8; ++mt) {
-            oacc[mt] *= alpha;
-            oacc[mt] = mfma16(vf[mt], pf, oacc[mt]);
-        }
-        if constexpr (R > 0) {
-#pragma unroll
-            for (int t = 0; t < RT; ++t) racc[t] *= alpha;
-#pragma unroll
-            for (int s = 0; s < NS; ++s) {
-                const u32x2 pm = my_slot_l == s ? pf : u32x2{0, 0};
-#pragma unroll
-                for (int t = 0; t < RT; ++t) racc[t] = mfma16(cv[s][t], pm, racc[t]);
-            }
-        }
+        // Stage 2 and the value products
+        softmax_pv<R, NS>(st, sacc, valid && row_active, tok0, my_len, p.scale_log2, vf, cv, my_slot_l, grp);
     };
 
     if (ng == 1) {
@@ -412,9 +535,11 @@ __global__ __launch_bounds__(256, ROPE ? 1 : 2) void decode_split_kernel(DecodeA
             };
             Frag fa, fb;
             int pg = pg0 + wave;
-            if (pg < pg1) {
-                const int last = pg + (pg1 - 1 - pg) / WAVES * WAVES;
-                load(pg, fa);
+            const bool busy = pg < pg1;
+            const int last = busy ? pg + (pg1 - 1 - pg) / WAVES * WAVES : pg0;
+            load(busy ? pg : pg0, fa);
+            prep_w();
+            if (busy) {
                 for (;;) {
                     load(pg + WAVES <= last ? pg + WAVES : last, fb);
                     compute_page(ns_tag, pg, true, fa.kf, fa.vf, fa.ck, fa.cv, fa.cs, fa.sn);
@@ -435,48 +560,47 @@ __global__ __launch_bounds__(256, ROPE ? 1 : 2) void decode_split_kernel(DecodeA
         else if (nag == 2 || AG == 2) run_pages(I2{});
         else if (nag == 3) run_pages(I3{});
         else run_pages(I4{});
-    } else {
-        // ---- several groups: stages of two pages, base K/V loaded once into LDS ----
-        // Wave w loads block (K if w even, V if odd) of stage page w/2 for everyone and
-        // computes its own group: both stage pages (4 groups) or stage page w/2 (2 groups).
-        constexpr int NSR = R > 0 ? AG : 1;
-        struct Stage {
-            u32x4 kv[4];                                 // this wave's share of the stage's base blocks
-            u32x2 ck[2][NSR][RTX], cv[2][NSR][RTX];      // rCache of the wave's pages
-            f32x4 cs[2][ROPE ? 4 : 1], sn[2][ROPE ? 4 : 1];
-        };
-        const int last = pg1 - 1;
-        const int lpage = wave >> 1, lkv = wave & 1;     // what this wave loads
-        const int npages_w = ngp == 4 ? 2 : 1;           // stage pages this wave computes
-        const int wpage0 = ngp == 4 ? 0 : (wave >> 1);
-        auto load_stage = [&](int sp, Stage &st) {
-            const int pl = sp + lpage <= last ? sp + lpage : last;
-            const int bpage = uniform(s_tab[pl - pg0]);
-            const uint16_t *blkp = p.base_kv + (((int64_t)bpage * 2 + lkv) * hkv + h) * kBlockHalfs;
+    } else if constexpr (S::MULTI) {
+        // ---- several groups: stages of two pages, base K/V shared through LDS ----
+        // Wave w loads block (K if w even, V if odd) of stage page w/2 for everyone, two
+        // stages ahead (registers, then LDS one stage before use), and computes its own
+        // group: both stage pages (4 groups) or stage page w/2 (2 groups).  The rCache
+        // rows of its group are loaded one stage ahead.  All loads are unconditional
+        // (past the item's end they re-read its last page), so the compiler can keep the
+        // later stages in flight while it waits for the one it needs.
+        auto run_groups = [&](auto npw_tag) {
+            constexpr int NPW = decltype(npw_tag)::value;  // stage pages this wave computes
+            constexpr int NSR = R > 0 ? AG : 1;
+            struct Cres { u32x2 ck[NPW][NSR][RTX], cv[NPW][NSR][RTX]; };
+            using IA = std::integral_constant<int, (R > 0 ? AG : 1)>;
+            const int last = pg1 - 1;
+            const int lpage = wave >> 1, lkv = wave & 1;   // what this wave loads for everyone
+            const int wpage0 = NPW == 2 ? 0 : (wave >> 1);  // first stage page it computes
+            auto load_base = [&](int sp, u32x4 *kv) {
+                const int pl = sp + lpage <= last ? sp + lpage : last;
+                const int bpage = uniform(s_tab[pl - pg0]);
+                const uint16_t *blkp = p.base_kv + (((int64_t)bpage * 2 + lkv) * hkv + h) * kBlockHalfs;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) st.kv[i] = ldg128(blkp + i * 512 + lane * 8);
+                for (int i = 0; i < 4; ++i) kv[i] = ldg128(blkp + i * 512 + lane * 8);
+            };
+            auto store_base = [&](int buf, const u32x4 *kv) {
+                uint16_t *dst = lds_h + ((buf * 2 + lpage) * 2 + lkv) * kBlockHalfs;
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                if (j < npages_w) {
-                    const int pj = sp + wpage0 + j <= last ? sp + wpage0 + j : last;
-                    if constexpr (ROPE) load_rope(pj, st.cs[j], st.sn[j]);
-                    if constexpr (R > 0) {
+                for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4 *>(dst + i * 512 + lane * 8) = kv[i];
+            };
+            auto load_c = [&](int sp, Cres &c) {
+                if constexpr (R > 0) {
 #pragma unroll
-                        for (int s = 0; s < AG; ++s) load_res(pj, s, st.ck[j][s], st.cv[j][s]);
+                    for (int j = 0; j < NPW; ++j) {
+                        const int pj = sp + wpage0 + j <= last ? sp + wpage0 + j : last;
+#pragma unroll
+                        for (int s = 0; s < AG; ++s) load_res(pj, s, c.ck[j][s], c.cv[j][s]);
                     }
                 }
-            }
-        };
-        auto store_stage = [&](int buf, const Stage &st) {
-            uint16_t *dst = lds_h + ((buf * 2 + lpage) * 2 + lkv) * kBlockHalfs;
+            };
+            auto compute_stage = [&](int buf, int sp, Cres &c) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4 *>(dst + i * 512 + lane * 8) = st.kv[i];
-        };
-        auto compute_stage = [&](int buf, int sp, Stage &st) {
-            using IA = std::integral_constant<int, (R > 0 ? AG : 1)>;
-#pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                if (j < npages_w) {
+                for (int j = 0; j < NPW; ++j) {
                     const int pj = sp + wpage0 + j;
                     const uint16_t *kb = lds_h + ((buf * 2 + wpage0 + j) * 2 + 0) * kBlockHalfs;
                     const uint16_t *vb = kb + kBlockHalfs;
@@ -490,103 +614,292 @@ __global__ __launch_bounds__(256, ROPE ? 1 : 2) void decode_split_kernel(DecodeA
                         vf[2 * q2] = u32x2{v.x, v.y};
                         vf[2 * q2 + 1] = u32x2{v.z, v.w};
                     }
-                    compute_page(IA{}, pj <= last ? pj : last, pj <= last, kf, vf, st.ck[j], st.cv[j], st.cs[j],
-                                 st.sn[j]);
+                    compute_page(IA{}, pj <= last ? pj : last, pj <= last, kf, vf, c.ck[j], c.cv[j], nullptr,
+                                 nullptr);
+                }
+            };
+            u32x4 bx[4], by[4];
+            Cres ca, cb;
+            int sp = pg0;
+            load_c(sp, ca);
+            load_base(sp, bx);
+            store_base(0, bx);
+            load_base(sp + 2, by);
+            prep_w();
+            __syncthreads();
+            int buf = 0;
+            for (;;) {
+                // LDS buf holds stage sp; by holds stage sp+2 (in flight); ca holds C(sp)
+                load_c(sp + 2, cb);
+                load_base(sp + 4, bx);
+                compute_stage(buf, sp, ca);
+                store_base(buf ^ 1, by);
+                __syncthreads();
+                sp += 2;
+                buf ^= 1;
+                if (sp >= pg1) break;
+                load_c(sp + 2, ca);
+                load_base(sp + 4, by);
+                compute_stage(buf, sp, cb);
+                store_base(buf ^ 1, bx);
+                __syncthreads();
+                sp += 2;
+                buf ^= 1;
+                if (sp >= pg1) break;
+            }
+        };
+        if (ngp == 4) run_groups(std::integral_constant<int, 2>{});
+        else run_groups(std::integral_constant<int, 1>{});
+    }
+
+    write_partial<R>(p, st, row_active, (int64_t)(row_base + copy * nag * G + my_group * ROWS + col) * hkv + h,
+                     grp);
+}
+
+
+// ---------------------------------------------------------------------------
+// RoPE on: one agent group per item; waves stride over the pages, registers
+// double-buffered.  The loop is specialised on the number NS of agent slots so that
+// every load it issues is consumed; all loads are unconditional and in a fixed order,
+// so the compiler can count them and the prefetched page stays in flight.
+template <int R, int G>
+struct RopeShape {
+    static constexpr int AG = ROWS / G;
+    static constexpr int RT = (R + 15) / 16;
+    static constexpr int BSTAGE_BYTES = AG * R * D * 2;     // row-major B_K slices
+    static constexpr int BKT_BYTES = AG * RT * 8 * 64 * 8;  // B_K^T fragments
+    static constexpr int TABLE_WORDS = (1 + AG) * kMaxPagesPerItem;
+};
+
+template <int R, int G>
+__global__ __launch_bounds__(256, 1) void decode_rope_kernel(DecodeArgs p) {
+    static_assert(R > 0, "RoPE decode needs a residual");
+    using S = RopeShape<R, G>;
+    using RowsT = Rows<R>;
+    constexpr int AG = S::AG;
+    constexpr int RT = S::RT;
+    constexpr int RTX = RT;
+    __shared__ __attribute__((aligned(16))) uint16_t b_stage[S::BSTAGE_BYTES / 2];
+    __shared__ __attribute__((aligned(16))) uint32_t lds_bkt[S::BKT_BYTES / 4];
+    __shared__ int32_t s_tab[S::TABLE_WORDS];
+
+    const int32_t *plan = p.plan;
+    const int blk = plan[plan[fkv::H_OFF_BLOCKS] + blockIdx.x];
+    if (blk < 0) return;
+    const int hkv = p.hkv;
+    const int item = blk / hkv;
+    const int h = blk - item * hkv;
+    const int32_t *rec = plan + plan[fkv::H_OFF_ITEMS] + item * fkv::kItemWords;
+    const int pg0 = rec[0], pg1 = rec[1], leader = rec[2], nag = rec[3], row_base = rec[4];
+    const int32_t *item_agents = rec + 5;
+    if (nag > AG || pg1 - pg0 > kMaxPagesPerItem) return;  // rejected on the host
+
+    const int lane = threadIdx.x & 63;
+    const int wave = uniform(threadIdx.x >> 6);
+    const int col = lane & 15, grp = lane >> 4;
+    const int my_slot_l = col / G;
+    const bool row_active = my_slot_l < nag;
+    const int my_agent = row_active ? item_agents[my_slot_l] : 0;
+    const int qh = h * G + (col % G);
+
+    const int npg = pg1 - pg0;
+    for (int idx = threadIdx.x; idx < (1 + nag) * npg; idx += 256) {
+        const int t = idx / npg, i = idx - t * npg;
+        int32_t v;
+        if (t == 0) {
+            v = p.base_bt[(int64_t)leader * p.max_pages + pg0 + i];
+        } else {
+            const int ag_id = item_agents[t - 1];
+            const int32_t rp = p.res_bt[(int64_t)ag_id * p.max_pages + pg0 + i];
+            v = p.adapter_idx[ag_id] >= 0 ? rp : 0;
+        }
+        s_tab[t * kMaxPagesPerItem + i] = v;
+    }
+    int res_len[AG];
+    int max_len = 0;
+#pragma unroll
+    for (int s = 0; s < AG; ++s) {
+        const bool ok = s < nag;
+        const int ag_id = ok ? item_agents[s] : 0;
+        const int len = ok ? p.seq_lens[ag_id] : 0;
+        res_len[s] = (ok && p.adapter_idx[ag_id] >= 0) ? len : 0;
+        max_len = max(max_len, len);
+    }
+    const int my_len = row_active ? p.seq_lens[my_agent] : 0;
+    u32x4 qf[4];
+    load_q(p.q + ((int64_t)my_agent * p.hq + qh) * D, row_active, grp, qf);
+
+    // B_K^T fragments of the group's slots (lane holds B_K[16t + 4grp + i][16mt + col]),
+    // built from row-major B_K slices staged in LDS; zero for empty slots / no adapter
+    const int64_t n = (int64_t)hkv * D;
+    for (int idx = threadIdx.x; idx < AG * R * (D / 8); idx += 256) {
+        const int sl = idx / (R * (D / 8));
+        const int rem = idx - sl * (R * (D / 8));
+        const int rho = rem / (D / 8), c8 = rem - rho * (D / 8);
+        const int ad = sl < nag ? p.adapter_idx[item_agents[sl]] : -1;
+        u32x4 v = {0, 0, 0, 0};
+        if (ad >= 0) v = ldg128(p.lora_b + (int64_t)ad * 2 * R * n + (int64_t)rho * n + (int64_t)h * D + 8 * c8);
+        *reinterpret_cast<u32x4 *>(b_stage + (sl * R + rho) * D + 8 * c8) = v;
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < AG * RT * 8 * 64; idx += 256) {
+        const int ln = idx & 63;
+        const int rest = idx >> 6;  // (sl*RT + t)*8 + mt
+        const int mt = rest & 7, sti = rest >> 3;
+        const int sl = sti / RTX, t = sti - sl * RTX;
+        const int c = ln & 15, gg = ln >> 4;
+        uint32_t w[2];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int r0 = 16 * t + 4 * gg + 2 * j;
+            const uint16_t lo = r0 < R ? b_stage[(sl * R + r0) * D + 16 * mt + c] : (uint16_t)0;
+            const uint16_t hi = r0 + 1 < R ? b_stage[(sl * R + r0 + 1) * D + 16 * mt + c] : (uint16_t)0;
+            w[j] = (uint32_t)lo | ((uint32_t)hi << 16);
+        }
+        const int o = (((sl * RTX + t) * 8 + mt) * 64 + ln) * 2;
+        lds_bkt[o] = w[0];
+        lds_bkt[o + 1] = w[1];
+    }
+    __syncthreads();  // tables and B_K^T fragments ready
+
+    const ResOffsets<R> ro(col, grp);
+    RowsT st;
+    st.init();
+    const int64_t res_page_halfs = 2 * PS * R;
+
+    auto run_pages = [&](auto ns_tag) {
+        constexpr int NS = decltype(ns_tag)::value;
+        struct Frag {
+            f32x4 cs[4], sn[4];
+            u32x4 kf[4];
+            u32x2 vf[8];
+            u32x2 ck[NS][RTX];
+            u32x2 cv[NS][RTX];
+        };
+        auto load = [&](int pg, Frag &f) {
+            // RoPE rows first: they are consumed first
+            const float *cr = p.rope_cos + (int64_t)pg * (PS * D / 2);
+            const float *sr = p.rope_sin + (int64_t)pg * (PS * D / 2);
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt) {
+                f.cs[mt] = *reinterpret_cast<const f32x4 *>(cr + 256 * mt + lane * 4);
+                f.sn[mt] = *reinterpret_cast<const f32x4 *>(sr + 256 * mt + lane * 4);
+            }
+            const int bpage = uniform(s_tab[pg - pg0]);
+            const uint16_t *kblk = p.base_kv + ((int64_t)bpage * 2 * hkv + h) * kBlockHalfs;
+            const uint16_t *vblk = kblk + (int64_t)hkv * kBlockHalfs;
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) f.kf[kk] = ldg128(kblk + kk * 512 + lane * 8);
+#pragma unroll
+            for (int q2 = 0; q2 < 4; ++q2) {
+                const u32x4 v = ldg128(vblk + q2 * 512 + lane * 8);
+                f.vf[2 * q2] = u32x2{v.x, v.y};
+                f.vf[2 * q2 + 1] = u32x2{v.z, v.w};
+            }
+#pragma unroll
+            for (int s = 0; s < NS; ++s) {
+                const int rpage = uniform(s_tab[(1 + s) * kMaxPagesPerItem + (pg - pg0)]);
+                const uint16_t *rb = p.res_kv + (int64_t)rpage * res_page_halfs;
+#pragma unroll
+                for (int t = 0; t < RT; ++t) {
+                    const u32x2 v = ldg64(rb + ro.cv[t]);
+                    const u32x2 k = ldg64(rb + ro.ck[t]);
+                    f.cv[s][t] = ro.cv_ok[t] ? v : u32x2{0, 0};
+                    f.ck[s][t] = ro.ck_ok[t] ? k : u32x2{0, 0};
                 }
             }
         };
-        Stage sa, sb2;
-        int sp = pg0;
-        load_stage(sp, sa);
-        store_stage(0, sa);
-        __syncthreads();
-        int buf = 0;
-        for (;;) {
-            load_stage(sp + 2, sb2);     // past the item end this re-reads the last page (unused)
-            compute_stage(buf, sp, sa);
-            store_stage(buf ^ 1, sb2);
-            __syncthreads();
-            sp += 2;
-            buf ^= 1;
-            if (sp >= pg1) break;
-            load_stage(sp + 2, sa);
-            compute_stage(buf, sp, sb2);
-            store_stage(buf ^ 1, sa);
-            __syncthreads();
-            sp += 2;
-            buf ^= 1;
-            if (sp >= pg1) break;
-        }
-    }
-    l_run += __shfl_xor(l_run, 16);
-    l_run += __shfl_xor(l_run, 32);
-
-    // ---- merge the waves that hold the same group and write one partial per row ----
-    __syncthreads();  // LDS stages of the main loop are dead from here on
-    constexpr int TILES = 8 + RT;
-    float *lds_m = lds_f + WAVES * TILES * 256;
-    float *lds_l = lds_m + WAVES * ROWS;
-    {
-        float *mine = lds_f + wave * TILES * 256;
+        auto compute = [&](int pg, Frag &f) {
+            const int tok0 = pg * PS;
+            const int vis = max_len - tok0;
+            if (vis < PS) {
 #pragma unroll
-        for (int mt = 0; mt < 8; ++mt) *reinterpret_cast<f32x4 *>(mine + (mt * 64 + lane) * 4) = oacc[mt];
-#pragma unroll
-        for (int t = 0; t < RT; ++t) *reinterpret_cast<f32x4 *>(mine + ((8 + t) * 64 + lane) * 4) = racc[t];
-        if (grp == 0) {
-            lds_m[wave * ROWS + col] = m_run;
-            lds_l[wave * ROWS + col] = l_run;
-        }
-    }
-    __syncthreads();
-    const int rows_used = nag * G;
-    const int rec_len = 2 + D + R;
-    const int nw = WAVES / ngp;  // waves holding each group
-    for (int idx = threadIdx.x; idx < rows_used * rec_len; idx += 256) {
-        const int r = idx / rec_len, k = idx - r * rec_len;
-        const int gr = r / ROWS, rr = r - gr * ROWS;   // group and row within its tile
-        float mw[WAVES], M = kNegInf;
-#pragma unroll
-        for (int i = 0; i < WAVES; ++i) {
-            mw[i] = i < nw ? lds_m[(gr + i * ngp) * ROWS + rr] : kNegInf;
-            M = fmaxf(M, mw[i]);
-        }
-        const float Mu = M == kNegInf ? 0.f : M;
-        float v = 0.f;
-        if (k == 0) {
-            v = M;
-        } else if (k == 1) {
-#pragma unroll
-            for (int i = 0; i < WAVES; ++i)
-                if (i < nw) v += fast_exp2(mw[i] - Mu) * lds_l[(gr + i * ngp) * ROWS + rr];
-        } else {
-            const int e = k - 2;
-            int tile, ln, ii;
-            if (e < D) {
-                tile = e >> 4;
-                ln = rr + 16 * ((e & 15) >> 2);
-                ii = e & 3;
-            } else {
-                const int rho = e - D;
-                tile = 8 + (rho >> 4);
-                ln = rr + 16 * ((rho & 15) >> 2);
-                ii = rho & 3;
+                for (int mt = 0; mt < 8; ++mt) f.vf[mt] = mask4(f.vf[mt], vis, grp);
             }
+            f32x4 sacc = {0, 0, 0, 0};
 #pragma unroll
-            for (int i = 0; i < WAVES; ++i)
-                if (i < nw) v += fast_exp2(mw[i] - Mu) * lds_f[(gr + i * ngp) * TILES * 256 + (tile * 64 + ln) * 4 + ii];
+            for (int kk = 0; kk < 4; ++kk) sacc = mfma32(f.kf[kk], qf[kk], sacc);
+#pragma unroll
+            for (int s = 0; s < NS; ++s) {
+                const int svis = res_len[s] - tok0;
+                if (svis < PS) {
+#pragma unroll
+                    for (int t = 0; t < RT; ++t) {
+                        f.cv[s][t] = mask4(f.cv[s][t], svis, grp);
+                        f.ck[s][t] = col < svis ? f.ck[s][t] : u32x2{0, 0};
+                    }
+                }
+                // Stage 1: U^T = B_K^T C_K^T, deferred RoPE, then S^T += K_lora Q_s^T
+                f32x4 u[8];
+#pragma unroll
+                for (int mt = 0; mt < 8; ++mt) {
+                    u[mt] = f32x4{0, 0, 0, 0};
+#pragma unroll
+                    for (int t = 0; t < RT; ++t) {
+                        const u32x2 a =
+                            *reinterpret_cast<const u32x2 *>(lds_bkt + (((s * RTX + t) * 8 + mt) * 64 + lane) * 2);
+                        u[mt] = mfma16(a, f.ck[s][t], u[mt]);
+                    }
+                }
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float x = u[mt][i], y = u[mt + 4][i];
+                        u[mt][i] = x * f.cs[mt][i] - y * f.sn[mt][i];
+                        u[mt + 4][i] = y * f.cs[mt][i] + x * f.sn[mt][i];
+                    }
+                }
+#pragma unroll
+                for (int kk = 0; kk < 4; ++kk) {
+                    const u32x2 lo = pack4(u[2 * kk]), hi = pack4(u[2 * kk + 1]);
+                    const u32x4 b = my_slot_l == s ? qf[kk] : u32x4{0, 0, 0, 0};
+                    sacc = mfma32(u32x4{lo.x, lo.y, hi.x, hi.y}, b, sacc);
+                }
+            }
+            softmax_pv<R, NS>(st, sacc, row_active, tok0, my_len, p.scale_log2, f.vf, f.cv, my_slot_l, grp);
+        };
+        Frag fa, fb;
+        int pg = pg0 + wave;
+        if (pg < pg1) {
+            const int last = pg + (pg1 - 1 - pg) / WAVES * WAVES;
+            load(pg, fa);
+            for (;;) {
+                load(pg + WAVES <= last ? pg + WAVES : last, fb);
+                compute(pg, fa);
+                pg += WAVES;
+                if (pg > last) break;
+                load(pg + WAVES <= last ? pg + WAVES : last, fa);
+                compute(pg, fb);
+                pg += WAVES;
+                if (pg > last) break;
+            }
         }
-        p.ws[((int64_t)(row_base + r) * hkv + h) * p.ws_stride + k] = v;
-    }
+    };
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, cmin(2, AG)>;
+    using I3 = std::integral_constant<int, cmin(3, AG)>;
+    using I4 = std::integral_constant<int, cmin(4, AG)>;
+    if (nag == 1) run_pages(I1{});
+    else if (nag == 2 || AG == 2) run_pages(I2{});
+    else if (nag == 3) run_pages(I3{});
+    else run_pages(I4{});
+
+    write_partial<R>(p, st, row_active, (int64_t)(row_base + wave * nag * G + col) * hkv + h, grp);
 }
+
 
 // Log-sum-exp merge of one agent's partials and Stage 3 of Algorithm 1 for one query
 // head j (KV head h = j / G): O = (sum_k w_k acc_k + (sum_k w_k acc_r,k) . B_V[h]) / L
-// with w_k = 2^(m_k - M), M = max_k m_k, L = sum_k w_k l_k.
-constexpr int kCombineThreads = 128;
-constexpr int kMaxItemsPerAgent = fkv::kMaxItemsPerAgent;
+// with w_k = 2^(m_k - M), M = max_k m_k, L = sum_k w_k l_k.  Wave w folds partials
+// k = w, w+4, ... with a running maximum (lane c holds columns c, c+64, c+128 of the
+// record), the four waves are merged through LDS, then B_V is applied once.
+constexpr int kCombineThreads = 256;
 
 template <int R, int G>
 __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(DecodeArgs p) {
+    constexpr int NCOL = D + R;
+    constexpr int NC = (NCOL + 63) / 64;
     const int hq = p.hq;
     const int a = blockIdx.x / hq;
     const int j = blockIdx.x - a * hq;
@@ -597,80 +910,91 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(DecodeA
     const int K = plan[plan[fkv::H_OFF_AGENT_PTR] + a + 1] - k0;
     const int ad = R > 0 ? p.adapter_idx[a] : -1;
     const int stride = p.ws_stride;
-    const int tid = threadIdx.x;
-    __shared__ float sW[kMaxItemsPerAgent];
-    __shared__ int sRow[kMaxItemsPerAgent];
-    __shared__ float sRed[2];
-    __shared__ float sAccR[R > 0 ? R : 1];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int add = jj * p.hkv + h;
+    __shared__ float sM[4], sL[4];
+    __shared__ float sAcc[4][NCOL];
+    __shared__ float sFin[NCOL];
+    __shared__ float sOut[D];
 
-    // M = max_k m_k
-    float mloc = kNegInf;
-    for (int k = tid; k < K; k += kCombineThreads) {
-        const int row = slots[k0 + k] + jj * p.hkv + h;
-        sRow[k] = row;
-        const float m = p.ws[(int64_t)row * stride];
-        sW[k] = m;
-        mloc = fmaxf(mloc, m);
-    }
+    float M = kNegInf, L = 0.f, acc[NC];
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) mloc = fmaxf(mloc, __shfl_xor(mloc, o));
-    if ((tid & 63) == 0) sRed[tid >> 6] = mloc;
-    __syncthreads();
-    const float M = fmaxf(sRed[0], sRed[1]);
-    const float Mu = M == kNegInf ? 0.f : M;
-    __syncthreads();
-    // w_k and L = sum_k w_k l_k
-    float lloc = 0.f;
-    for (int k = tid; k < K; k += kCombineThreads) {
-        const float w = fast_exp2(sW[k] - Mu);
-        sW[k] = w;
-        lloc += w * p.ws[(int64_t)sRow[k] * stride + 1];
-    }
+    for (int c = 0; c < NC; ++c) acc[c] = 0.f;
+    constexpr int U = 4;
+    for (int kb = wave; kb < K; kb += 4 * U) {
+        float mv[U], lv[U], v[U][NC];
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) lloc += __shfl_xor(lloc, o);
-    if ((tid & 63) == 0) sRed[tid >> 6] = lloc;
-    __syncthreads();
-    const float L = sRed[0] + sRed[1];
-    // acc_r = sum_k w_k acc_r,k
-    if constexpr (R > 0) {
-        if (ad >= 0 && tid < R) {
-            float v = 0.f;
-            for (int k = 0; k < K; ++k) v += sW[k] * p.ws[(int64_t)sRow[k] * stride + 2 + D + tid];
-            sAccR[tid] = v;
+        for (int u = 0; u < U; ++u) {
+            const int k = kb + 4 * u;
+            const int kc = k < K ? k : kb;
+            const float *src = p.ws + (int64_t)(slots[k0 + kc] + add) * stride;
+            mv[u] = k < K ? src[NCOL] : kNegInf;
+            lv[u] = src[NCOL + 1];
+#pragma unroll
+            for (int c = 0; c < NC; ++c) v[u][c] = lane + 64 * c < NCOL ? src[lane + 64 * c] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const float Mn = fmaxf(M, mv[u]);
+            const float Mu = Mn == kNegInf ? 0.f : Mn;
+            const float e0 = fast_exp2(M - Mu), e1 = fast_exp2(mv[u] - Mu);
+            L = L * e0 + lv[u] * e1;
+#pragma unroll
+            for (int c = 0; c < NC; ++c) acc[c] = acc[c] * e0 + v[u][c] * e1;
+            M = Mn;
         }
     }
-    // acc[d] = sum_k w_k acc_k[d]
-    float acc = 0.f;
-    {
-        const int dd = tid;
-        int k = 0;
-        for (; k + 4 <= K; k += 4) {
-            const float a0 = p.ws[(int64_t)sRow[k] * stride + 2 + dd];
-            const float a1 = p.ws[(int64_t)sRow[k + 1] * stride + 2 + dd];
-            const float a2 = p.ws[(int64_t)sRow[k + 2] * stride + 2 + dd];
-            const float a3 = p.ws[(int64_t)sRow[k + 3] * stride + 2 + dd];
-            acc += sW[k] * a0 + sW[k + 1] * a1 + sW[k + 2] * a2 + sW[k + 3] * a3;
-        }
-        for (; k < K; ++k) acc += sW[k] * p.ws[(int64_t)sRow[k] * stride + 2 + dd];
+    if (lane == 0) {
+        sM[wave] = M;
+        sL[wave] = L;
     }
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+        if (lane + 64 * c < NCOL) sAcc[wave][lane + 64 * c] = acc[c];
+    __syncthreads();
+    float Mt = kNegInf;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) Mt = fmaxf(Mt, sM[w]);
+    const float Mtu = Mt == kNegInf ? 0.f : Mt;
+    float ew[4], Lt = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        ew[w] = fast_exp2(sM[w] - Mtu);
+        Lt += ew[w] * sL[w];
+    }
+    if (tid < NCOL) sFin[tid] = ew[0] * sAcc[0][tid] + ew[1] * sAcc[1][tid] + ew[2] * sAcc[2][tid] + ew[3] * sAcc[3][tid];
+    __syncthreads();
+    // Stage 3: O = (acc + acc_r . B_V) / L; the rank sum is split over the two halves of
+    // the workgroup
+    const int d = tid & (D - 1), half = tid >> 7;
+    float o = half == 0 ? sFin[d] : 0.f;
     if constexpr (R > 0) {
-        __syncthreads();
         if (ad >= 0) {
-            const uint16_t *bv = p.lora_b + ((int64_t)ad * 2 + 1) * R * p.hkv * D + (int64_t)h * D + tid;
-#pragma unroll 8
-            for (int rho = 0; rho < R; ++rho) acc += sAccR[rho] * bf16_to_f32(bv[(int64_t)rho * p.hkv * D]);
+            constexpr int RH = (R + 1) / 2;
+            const uint16_t *bv = p.lora_b + ((int64_t)ad * 2 + 1) * R * p.hkv * D + (int64_t)h * D + d;
+#pragma unroll
+            for (int i = 0; i < RH; ++i) {
+                const int rho = half * RH + i;
+                if (rho < R) o += sFin[D + rho] * bf16_to_f32(bv[(int64_t)rho * p.hkv * D]);
+            }
         }
     }
-    const float o = L > 0.f ? acc / L : 0.f;
-    typedef __bf16 bf1;
-    p.out[((int64_t)a * hq + j) * D + tid] = __builtin_bit_cast(uint16_t, (bf1)o);
+    if (half == 1) sOut[d] = o;
+    __syncthreads();
+    if (half == 0) {
+        o += sOut[d];
+        const float res = Lt > 0.f ? o / Lt : 0.f;
+        typedef __bf16 bf1;
+        p.out[((int64_t)a * hq + j) * D + d] = __builtin_bit_cast(uint16_t, (bf1)res);
+    }
 }
 
 template <int R, int G, bool ROPE>
-hipError_t launch_decode(const DecodeArgs &da, int n_blocks, int n_agents, hipStream_t st, void *const *ev) {
+hipError_t launch_decode(const DecodeArgs &da, int n_blocks, int n_agents, int hpb, hipStream_t st, void *const *ev) {
     hipError_t e;
     if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[0]), st)) != hipSuccess) return e;
-    hipLaunchKernelGGL((decode_split_kernel<R, G, ROPE>), dim3(n_blocks), dim3(256), 0, st, da);
+    if constexpr (ROPE) hipLaunchKernelGGL((decode_rope_kernel<R, G>), dim3(n_blocks), dim3(256), 0, st, da);
+    else hipLaunchKernelGGL((decode_split_kernel<R, G, false>), dim3(n_blocks), dim3(256), 0, st, da);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[1]), st)) != hipSuccess) return e;
     hipLaunchKernelGGL((decode_combine_kernel<R, G>), dim3(n_agents * da.hq), dim3(kCombineThreads), 0, st, da);
@@ -680,22 +1004,24 @@ hipError_t launch_decode(const DecodeArgs &da, int n_blocks, int n_agents, hipSt
 }
 
 template <int R, int G>
-hipError_t dispatch_rope(bool rope, const DecodeArgs &da, int nb, int na, hipStream_t st, void *const *ev) {
+hipError_t dispatch_rope(bool rope, const DecodeArgs &da, int nb, int na, int hpb, hipStream_t st, void *const *ev) {
     if constexpr (R == 0) {
-        return launch_decode<0, G, false>(da, nb, na, st, ev);
+        return launch_decode<0, G, false>(da, nb, na, hpb, st, ev);
     } else {
-        return rope ? launch_decode<R, G, true>(da, nb, na, st, ev) : launch_decode<R, G, false>(da, nb, na, st, ev);
+        return rope ? launch_decode<R, G, true>(da, nb, na, hpb, st, ev)
+                    : launch_decode<R, G, false>(da, nb, na, hpb, st, ev);
     }
 }
 
 template <int G>
-hipError_t dispatch_rank(int r, bool rope, const DecodeArgs &da, int nb, int na, hipStream_t st, void *const *ev) {
+hipError_t dispatch_rank(int r, bool rope, const DecodeArgs &da, int nb, int na, int hpb, hipStream_t st,
+                         void *const *ev) {
     switch (r) {
-    case 0: return dispatch_rope<0, G>(rope, da, nb, na, st, ev);
-    case 8: return dispatch_rope<8, G>(rope, da, nb, na, st, ev);
-    case 16: return dispatch_rope<16, G>(rope, da, nb, na, st, ev);
-    case 32: return dispatch_rope<32, G>(rope, da, nb, na, st, ev);
-    case 64: return dispatch_rope<64, G>(rope, da, nb, na, st, ev);
+    case 0: return dispatch_rope<0, G>(rope, da, nb, na, hpb, st, ev);
+    case 8: return dispatch_rope<8, G>(rope, da, nb, na, hpb, st, ev);
+    case 16: return dispatch_rope<16, G>(rope, da, nb, na, hpb, st, ev);
+    case 32: return dispatch_rope<32, G>(rope, da, nb, na, hpb, st, ev);
+    case 64: return dispatch_rope<64, G>(rope, da, nb, na, hpb, st, ev);
     default: return hipErrorInvalidValue;
     }
 }
@@ -725,9 +1051,18 @@ extern "C" fkv_status fkv_residual_attention_decode(const fkv_attn_args *a, cons
         return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: RoPE table shorter than the longest sequence");
     if (g != 4 && g != 8)
         return fkv::fail(FKV_ERR_UNSUPPORTED, "fkv_residual_attention_decode: query heads per KV head must be 4 or 8");
-    if (a->rope_cos && a->r > 0 && w[fkv::H_MAX_ITEM_AGENTS] > 256 / a->r)
-        return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: with RoPE the plan may hold at most 256 / r "
-                                          "agents per work item (fkv_decode_plan_default_agents)");
+    const bool rope_on = a->rope_cos != nullptr && a->r > 0;
+    if (w[fkv::H_RANK] != a->r || w[fkv::H_ROPE] != (rope_on ? 1 : 0))
+        return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: the plan was built for another rank or "
+                                          "RoPE setting");
+    const int hpb = w[fkv::H_HEADS_PER_BLOCK];
+    if (hpb != fkv::decode_heads_per_block(a->hkv, rope_on))
+        return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: plan built for another head blocking");
+    if (w[fkv::H_MAX_ITEM_AGENTS] > fkv::decode_item_agent_cap(g, a->hkv, a->r, rope_on))
+        return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: the plan puts more agents in a work item "
+                                          "than this kernel takes");
+    if (w[fkv::H_PAGES_PER_SPLIT] > fkv::kMaxPagesPerItem)
+        return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: plan items longer than 64 pages");
     DecodeArgs da;
     da.q = static_cast<const uint16_t *>(a->q);
     da.base_kv = static_cast<const uint16_t *>(a->base_kv);
@@ -745,13 +1080,13 @@ extern "C" fkv_status fkv_residual_attention_decode(const fkv_attn_args *a, cons
     da.hq = a->hq;
     da.hkv = a->hkv;
     da.max_pages = a->max_pages;
-    da.ws_stride = (a->d + a->r + 2 + 3) / 4 * 4;
+    da.ws_stride = ws_stride_of(a->r);
     da.scale_log2 = a->scale * 1.4426950408889634f;
     const int nb = w[fkv::H_N_BLOCKS];
     hipStream_t hs = static_cast<hipStream_t>(stream);
     const bool rope = a->rope_cos != nullptr && a->r > 0;
-    hipError_t e = g == 4 ? dispatch_rank<4>(a->r, rope, da, nb, a->n_agents, hs, a->timing_events)
-                          : dispatch_rank<8>(a->r, rope, da, nb, a->n_agents, hs, a->timing_events);
+    hipError_t e = g == 4 ? dispatch_rank<4>(a->r, rope, da, nb, a->n_agents, hpb, hs, a->timing_events)
+                          : dispatch_rank<8>(a->r, rope, da, nb, a->n_agents, hpb, hs, a->timing_events);
     if (e != hipSuccess)
         return fkv::fail(FKV_ERR_HIP, std::string("fkv_residual_attention_decode: launch failed: ") + hipGetErrorString(e));
     return FKV_OK;

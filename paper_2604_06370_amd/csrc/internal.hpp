@@ -16,23 +16,38 @@ void clear_error();
 // Decode plan, host side.  Serialised layout (all int32):
 //   header[kHeaderWords]
 //   items   [n_items][kItemWords]  {page_begin, page_end, leader, n_ag, row_base, agent[16]}
-//   blocks  [n_blocks]             item * hkv + head, or -1 for an idle block
+//   blocks  [n_blocks]             item * (hkv / H) + head block, or -1 for an idle block
+//                                  (H = heads per block, header word H_HEADS_PER_BLOCK)
 //   agent_ptr [n_agents+1]         CSR over the partial rows of each agent
-//   agent_slot[...]                (row_base + slot*g) * hkv  (add jj*hkv + head for query head jj)
+//   agent_slot[...]                (row_base + (copy*n_ag + slot)*g) * hkv  (add jj*hkv + head
+//                                  for query head jj)
 // An item holds up to four agent groups; a group is the floor(16/g) agents whose
-// query heads of one KV head fill the 16 rows of one matrix-core tile.
+// query heads of one KV head fill the 16 rows of one matrix-core tile.  An item of
+// ng groups runs on 4 / ngp wave copies (ngp = 1, 2, 4 for ng = 1, 2, 3..4); every
+// copy writes its own partial rows, so the item owns copies * n_ag * g rows.
 constexpr int kHeaderWords = 24;
 constexpr int kMaxRows = 16;        // query rows of one agent group (one wave's row tile)
 constexpr int kMaxGroups = 4;       // agent groups per item (one wave each)
 constexpr int kMaxItemAgents = 16;  // agents per item
 constexpr int kItemWords = 5 + kMaxItemAgents;
-constexpr int kMaxPagesPerItem = 256;  // upper bound of pages_per_split (block tables are staged in LDS)
-constexpr int kMaxItemsPerAgent = 1024;  // work items one agent may span (the combine stages them in LDS)
+constexpr int kMaxPagesPerItem = 64;  // upper bound of pages_per_split (block tables are staged in LDS)
+
+// Decode: one workgroup per (work item, KV head).  An item holds up to four agent
+// groups without RoPE and rank below 32 (their base pages are shared through LDS and
+// each group keeps its rCache fragments of two pages in registers); with RoPE, or with
+// a rank of 32 or more, it holds one group.  Largest number of agents per work item:
+constexpr int decode_heads_per_block(int, bool) { return 1; }
+constexpr int decode_item_agent_cap(int g, int hkv, int r, bool rope) {
+    (void)hkv;
+    const int ag = kMaxRows / g;
+    if ((rope && r > 0) || r >= 32) return ag;
+    return kMaxGroups * ag < kMaxItemAgents ? kMaxGroups * ag : kMaxItemAgents;
+}
 
 enum PlanHeader {
     H_MAGIC = 0, H_N_ITEMS, H_N_BLOCKS, H_N_AGENTS, H_HKV, H_GROUP, H_AGENTS_PER_ITEM,
     H_OFF_ITEMS, H_OFF_BLOCKS, H_OFF_AGENT_PTR, H_OFF_AGENT_SLOT, H_TOTAL_WORDS, H_PAGES_PER_SPLIT,
-    H_PAGE_SIZE, H_N_SEGMENTS, H_TOTAL_ROWS, H_MAX_ITEM_AGENTS, H_FIELDS
+    H_PAGE_SIZE, H_N_SEGMENTS, H_TOTAL_ROWS, H_MAX_ITEM_AGENTS, H_HEADS_PER_BLOCK, H_RANK, H_ROPE, H_FIELDS
 };
 static_assert(H_FIELDS <= kHeaderWords, "plan header fields overflow the header");
 constexpr int32_t kPlanMagic = 0x464b5631;  // "FKV1"

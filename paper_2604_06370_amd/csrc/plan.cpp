@@ -2,11 +2,11 @@
 //
 // A segment is a maximal run of logical pages over which a fixed set of agents
 // maps every page to the same physical base page (what the base tree's prefix
-// sharing produces, Section 5.2).  Each segment is cut into work items of at most
-// floor(16 / g) agents (16 query rows per KV head) and at most pages_per_split
-// pages.  The split kernel runs one workgroup per (work item, KV head); the base
-// tiles of a page range are therefore read once per item and applied to all of
-// its agents' query heads.
+// sharing produces, Section 5.2).  Each segment is cut into work items of up to
+// four agent groups (a group is floor(16 / g) agents: 16 query rows per KV head)
+// and a page range.  The split kernel runs one workgroup per (work item, KV head);
+// the base tiles of a page range are therefore read once per item and applied to
+// all of its agents' query heads.
 //
 // Workgroup order: on MI355X consecutive workgroup ids are dealt round-robin to
 // the 8 XCDs, each with its own L2.  All workgroups that read the same base pages
@@ -35,9 +35,12 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     const int32_t g = prm->hq / prm->hkv;
     if (g > fkv::kMaxRows) return fkv::fail(FKV_ERR_UNSUPPORTED, "fkv_decode_plan_create: more than 16 query heads per KV head");
     const int32_t ag = fkv::kMaxRows / g;  // agents per group
-    int32_t item_agents = prm->max_item_agents > 0 ? prm->max_item_agents : fkv::kMaxGroups * ag;
-    item_agents = std::min(item_agents, std::min(fkv::kMaxGroups * ag, fkv::kMaxItemAgents));
-    if (item_agents < 1) return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: bad max_item_agents");
+    if (prm->r < 0 || prm->max_item_agents < 0) return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: bad r / max_item_agents");
+    const bool rope = prm->rope != 0 && prm->r > 0;
+    const int32_t hpb = fkv::decode_heads_per_block(prm->hkv, rope);
+    const int32_t cap = fkv::decode_item_agent_cap(g, prm->hkv, prm->r, rope);
+    if (cap < 1) return fkv::fail(FKV_ERR_UNSUPPORTED, "fkv_decode_plan_create: rank too large for the decode kernels");
+    const int32_t item_agents = prm->max_item_agents > 0 ? std::min(prm->max_item_agents, cap) : cap;
     std::vector<int32_t> npages(A);
     int32_t P = 0;
     for (int32_t a = 0; a < A; ++a) {
@@ -92,27 +95,48 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
         }
         return out;
     };
-    // 3. pages per split: enough workgroups for every CU to hold a few
-    int64_t units = 0;  // (page x item) units per KV head
-    for (auto &s : segs) units += (int64_t)s.n * (int64_t)chunk_sizes(s.agents.size()).size();
-    int32_t pps = prm->pages_per_split;
-    if (pps == 0) {
-        const int64_t cus = prm->num_cus > 0 ? prm->num_cus : 256;
-        const int64_t target_items = std::max<int64_t>(1, (3 * cus + prm->hkv - 1) / prm->hkv);
-        pps = (int32_t)std::max<int64_t>(8, (units + target_items - 1) / target_items);
-        pps = std::min(pps, fkv::kMaxPagesPerItem);
-        pps = (pps + 1) / 2 * 2;
+    // 3. pages per item: one split size for every segment, chosen so that there are
+    //    about three (item, head block) workgroups per compute unit (with two resident
+    //    workgroups per unit and items of up to four agent groups this measured best:
+    //    longer units pay the per-unit prologue less often, shorter ones balance the
+    //    tail better).  Splits of a segment are made equal instead of a full-size run
+    //    plus a short remainder.
+    const int64_t cus = prm->num_cus > 0 ? prm->num_cus : 256;
+    const int32_t nhb_units = prm->hkv / hpb;
+    std::vector<int32_t> seg_pps(segs.size());
+    {
+        int64_t units = 0;  // (page x agent chunk) units per head block
+        for (auto &s : segs) units += (int64_t)s.n * (int64_t)chunk_sizes(s.agents.size()).size();
+        // about three (item, head block) workgroups per compute unit
+        const int32_t auto_pps = (int32_t)std::max<int64_t>(
+            4, std::min<int64_t>(fkv::kMaxPagesPerItem, (units * nhb_units + 3 * cus - 1) / (3 * cus)));
+        for (size_t i = 0; i < segs.size(); ++i) {
+            int32_t pps = prm->pages_per_split > 0 ? prm->pages_per_split : auto_pps;
+            if (pps > fkv::kMaxPagesPerItem)
+                return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: pages_per_split above 64");
+            if (prm->pages_per_split == 0) {
+                const int32_t n_split = (segs[i].n + pps - 1) / pps;
+                pps = (segs[i].n + n_split - 1) / n_split;
+            }
+            seg_pps[i] = pps;
+        }
     }
-    if (pps > fkv::kMaxPagesPerItem)
-        return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: pages_per_split above 256");
+    const double per_page_base = 8.0 * hpb;
+    const double unit_overhead = 12.0 * per_page_base;
 
-    // 4. work items, clustered by (segment, split)
-    struct Item { int32_t p0, p1, row_base; std::vector<int32_t> agents; };
+    // 4. work items, clustered by (segment, split).  An item of ng agent groups runs its
+    //    groups on 4 / ngp wave copies (ngp = ng rounded up to 1, 2 or 4), each writing its
+    //    own partial rows: rows = copies * agents * g.
+    struct Item { int32_t p0, p1, row_base, copies; double cost; std::vector<int32_t> agents; };
     std::vector<Item> items;
     std::vector<std::pair<int32_t, int32_t>> clusters;  // [first item, item count)
     std::vector<double> cluster_cost;
     int64_t total_rows = 0;
-    for (auto &s : segs) {
+    int32_t pps_max = 0;
+    for (size_t si = 0; si < segs.size(); ++si) {
+        const auto &s = segs[si];
+        const int32_t pps = seg_pps[si];
+        pps_max = std::max(pps_max, pps);
         const std::vector<size_t> chunks = chunk_sizes(s.agents.size());
         for (int32_t p0 = s.first; p0 < s.first + s.n; p0 += pps) {
             const int32_t p1 = std::min(p0 + pps, s.first + s.n);
@@ -120,11 +144,14 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
             double cost = 0;
             size_t k = 0;
             for (size_t c : chunks) {
-                Item it{p0, p1, (int32_t)total_rows, {}};
+                const int32_t ng = (int32_t)((c + ag - 1) / ag);
+                const int32_t ngp = ng == 1 ? 1 : (ng == 2 ? 2 : 4);
+                Item it{p0, p1, (int32_t)total_rows, fkv::kMaxGroups / ngp, 0.0, {}};
                 for (size_t j = k; j < k + c; ++j) it.agents.push_back(s.agents[j]);
                 k += c;
-                total_rows += (int64_t)c * g;
-                cost += (double)(p1 - p0) * (8.0 + (double)it.agents.size());
+                total_rows += (int64_t)it.copies * (int64_t)c * g;
+                it.cost = unit_overhead + (double)(p1 - p0) * (per_page_base + (double)c);
+                cost += it.cost;
                 items.push_back(std::move(it));
             }
             clusters.push_back({first, (int32_t)items.size() - first});
@@ -135,39 +162,39 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     const int32_t n_items = (int32_t)items.size();
     const int32_t hkv = prm->hkv;
 
-    // 5. workgroup order: clusters dealt to XCDs by least accumulated cost
+    // 5. workgroup order: clusters dealt to XCDs by least accumulated cost (all heads of a
+    //    cluster on one XCD), then each XCD's units longest-first so the dispatcher's greedy
+    //    fill is a longest-processing-time schedule
     std::vector<std::vector<int32_t>> per_xcd(kNumXcd);
     std::vector<double> load(kNumXcd, 0.0);
     std::vector<int32_t> order(clusters.size());
     for (size_t c = 0; c < clusters.size(); ++c) order[c] = (int32_t)c;
     std::stable_sort(order.begin(), order.end(), [&](int32_t x, int32_t y) { return cluster_cost[x] > cluster_cost[y]; });
-    std::vector<int32_t> cluster_xcd(clusters.size());
+    const int32_t nhb = hkv / hpb;  // head blocks per item
     for (int32_t c : order) {
         const int32_t x = (int32_t)(std::min_element(load.begin(), load.end()) - load.begin());
         load[x] += cluster_cost[c] * hkv;
-        cluster_xcd[c] = x;
+        auto &lst = per_xcd[x];
+        for (int32_t hb = 0; hb < nhb; ++hb)
+            for (int32_t k = 0; k < clusters[c].second; ++k) lst.push_back((clusters[c].first + k) * nhb + hb);
     }
-    for (size_t c = 0; c < clusters.size(); ++c) {
-        auto &lst = per_xcd[cluster_xcd[c]];
-        for (int32_t h = 0; h < hkv; ++h)
-            for (int32_t k = 0; k < clusters[c].second; ++k) lst.push_back((clusters[c].first + k) * hkv + h);
-    }
+    for (auto &lst : per_xcd)
+        std::stable_sort(lst.begin(), lst.end(),
+                         [&](int32_t x, int32_t y) { return items[x / nhb].cost > items[y / nhb].cost; });
     size_t depth = 0;
     for (auto &l : per_xcd) depth = std::max(depth, l.size());
     const int32_t n_blocks = (int32_t)(depth * kNumXcd);
 
-    // 6. partial rows per agent (CSR): row (row_base + slot*g + jj) of head h lives at
-    //    partial index (row_base + slot*g + jj) * hkv + h
+    // 6. partial rows per agent (CSR): copy c of agent slot j, query head jj of head h lives
+    //    at partial index (row_base + (c * n_agents_in_item + j) * g + jj) * hkv + h
     std::vector<std::vector<int32_t>> slots(A);
-    for (int32_t w = 0; w < n_items; ++w)
-        for (size_t j = 0; j < items[w].agents.size(); ++j)
-            slots[items[w].agents[j]].push_back((int32_t)(((int64_t)items[w].row_base + (int64_t)j * g) * hkv));
-
-    for (auto &v : slots)
-        if (v.size() > (size_t)fkv::kMaxItemsPerAgent) {
-            return fkv::fail(FKV_ERR_UNSUPPORTED,
-                             "fkv_decode_plan_create: more than 1024 work items for one agent; raise pages_per_split");
-        }
+    for (int32_t w = 0; w < n_items; ++w) {
+        const int64_t nag = (int64_t)items[w].agents.size();
+        for (int32_t c = 0; c < items[w].copies; ++c)
+            for (int64_t j = 0; j < nag; ++j)
+                slots[items[w].agents[j]].push_back(
+                    (int32_t)(((int64_t)items[w].row_base + ((int64_t)c * nag + j) * g) * hkv));
+    }
 
     // 7. serialise
     auto *pl = new fkv_plan();
@@ -200,11 +227,14 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     w[fkv::H_OFF_AGENT_PTR] = (int32_t)off_ptr;
     w[fkv::H_OFF_AGENT_SLOT] = (int32_t)off_slot;
     w[fkv::H_TOTAL_WORDS] = (int32_t)total;
-    w[fkv::H_PAGES_PER_SPLIT] = pps;
+    w[fkv::H_PAGES_PER_SPLIT] = pps_max;
     w[fkv::H_PAGE_SIZE] = ps;
     w[fkv::H_N_SEGMENTS] = (int32_t)segs.size();
     w[fkv::H_TOTAL_ROWS] = (int32_t)total_rows;
     w[fkv::H_MAX_ITEM_AGENTS] = item_agents;
+    w[fkv::H_HEADS_PER_BLOCK] = hpb;
+    w[fkv::H_RANK] = prm->r;
+    w[fkv::H_ROPE] = rope ? 1 : 0;
     for (int32_t i = 0; i < n_items; ++i) {
         int32_t *r = &w[off_items + (int64_t)i * fkv::kItemWords];
         r[0] = items[i].p0;
@@ -255,9 +285,12 @@ int32_t fkv_decode_plan_default_agents(int32_t hq, int32_t hkv, int32_t r, int32
     if (hq < 1 || hkv < 1 || hq % hkv) return 0;
     const int32_t g = hq / hkv;
     if (g > fkv::kMaxRows) return 0;
-    int32_t n = std::min(fkv::kMaxGroups * (fkv::kMaxRows / g), fkv::kMaxItemAgents);
-    if (rope && r > 0) n = std::min(n, 256 / r);
-    return n;
+    // Without RoPE the residual key term is one small product per page and agent, so a
+    // workgroup serves up to four groups from each staged base page (as many agents as
+    // fit one LDS stage).  With RoPE the per-page rebuild (Stage 1 plus the rotation)
+    // dominates; one group per workgroup keeps the four waves independent.
+    if (r < 0) return 0;
+    return fkv::decode_item_agent_cap(g, hkv, r, rope != 0 && r > 0);
 }
 
 fkv_status fkv_decode_plan_serialize(const fkv_plan *plan, int32_t *out, int64_t capacity_words) {

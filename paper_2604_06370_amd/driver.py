@@ -115,8 +115,7 @@ class LoadedWorkload:
         agents = list(wl.decode_agents() if agents is None else agents)
         bb, rb, sl = self.tree.block_tables(agents, self.max_pages)
         plan = rt.DecodePlan(bb, sl, wl.hq, wl.hkv, wl.page_size, self.pages_per_split,
-                             max_item_agents=self.item_agents or rt.decode_plan_default_agents(
-                                 wl.hq, wl.hkv, wl.r, self.rope))
+                             max_item_agents=self.item_agents, r=wl.r, rope=self.rope)
         info = plan.info(wl.d, wl.r)
         dev = self.device
         q_rows = torch.tensor([int(wl.q_offset[a]) for a in agents], device=dev)

@@ -120,14 +120,16 @@ def decode_plan_default_agents(hq: int, hkv: int, r: int, rope: bool) -> int:
 
 
 class DecodePlan:
-    """fkv_decode_plan_create over host block tables; keeps the host handle and a device copy."""
+    """fkv_decode_plan_create over host block tables; keeps the host handle and a device copy.
+    A plan is built for one rank r and RoPE setting and must be run with them."""
 
     def __init__(self, base_bt: np.ndarray, seq_lens: np.ndarray, hq: int, hkv: int, page_size: int,
-                 pages_per_split: int = 0, num_cus: int = 0, max_item_agents: int = 0):
+                 pages_per_split: int = 0, num_cus: int = 0, max_item_agents: int = 0, r: int = 0,
+                 rope: bool = False):
         bb = np.ascontiguousarray(base_bt, dtype=np.int32)
         sl = np.ascontiguousarray(seq_lens, dtype=np.int32)
         prm = N.fkv_decode_plan_params(bb.shape[0], hq, hkv, page_size, bb.shape[1], pages_per_split, num_cus,
-                                       max_item_agents)
+                                       max_item_agents, r, int(bool(rope)))
         h = N.c_vp()
         check(N.fkv_decode_plan_create(ctypes.byref(prm), _ptr(bb), _ptr(sl), ctypes.byref(h)),
               "fkv_decode_plan_create")

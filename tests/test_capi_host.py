@@ -159,7 +159,7 @@ def test_decode_plan_segments_follow_the_fork_tree():
         t.fork(a, a, toks)
         agents.append(a)
     bb, rb, sl = t.block_tables(agents, 64)
-    plan = rt.DecodePlan(bb, sl, hq=8, hkv=2, page_size=ps, pages_per_split=8)
+    plan = rt.DecodePlan(bb, sl, hq=8, hkv=2, page_size=ps, pages_per_split=8, r=16)
     segs = plan.segments()
     assert segs[0] == (0, 32, [0, 1, 2, 3, 4, 5])
     assert (32, 4, [0, 2]) in segs and (32, 4, [1, 3]) in segs
@@ -214,7 +214,7 @@ def test_attention_entry_points_reject_bad_arguments_before_launching():
 def _parse_plan(words):
     """Decode the serialised plan (layout of internal.hpp) into items, blocks and the CSR."""
     H = dict(n_items=1, n_blocks=2, n_agents=3, hkv=4, g=5, off_items=7, off_blocks=8, off_ptr=9, off_slot=10,
-             total_rows=15, max_item_agents=16)
+             total_rows=15, max_item_agents=16, heads_per_block=17, rank=18, rope=19)
     h = {k: int(words[v]) for k, v in H.items()}
     items = []
     for i in range(h["n_items"]):
@@ -256,15 +256,21 @@ def _synthetic_tables(rng, n_agents, groups, prefix_pages, mid_pages, max_suffix
 def test_decode_plan_items_cover_every_agent_page_once(hq, hkv, r, rope, pps):
     """Host-side invariants the decode kernels rely on for in-bounds access: every (agent,
     page) in exactly one item, items within the page and agent limits, disjoint partial rows
-    and a CSR that points each agent's query heads at exactly its rows."""
+    (one set per wave copy of a group) and a CSR that points each agent's query heads at
+    exactly its rows."""
     rng = np.random.default_rng(hq + r + pps)
     g = hq // hkv
     for n_agents, groups, pre, mid, suf in [(16, 1, 300, 0, 40), (37, 3, 64, 9, 5), (5, 5, 0, 3, 2)]:
         bb, sl = _synthetic_tables(rng, n_agents, groups, pre, mid, suf)
         n_item = rt.decode_plan_default_agents(hq, hkv, r, rope)
-        plan = rt.DecodePlan(bb, sl, hq, hkv, 16, pps, max_item_agents=n_item)
+        plan = rt.DecodePlan(bb, sl, hq, hkv, 16, pps, r=r, rope=rope)
         h, items, blocks, ptr, slots = _parse_plan(plan.serialize())
-        assert h["max_item_agents"] <= (256 // r if rope else 16) and h["max_item_agents"] <= 4 * (16 // g)
+        assert h["max_item_agents"] == n_item and (h["rank"], h["rope"]) == (r, int(rope))
+        assert n_item <= (16 // g if rope else 16) and n_item <= 4 * (16 // g)
+        hpb = h["heads_per_block"]
+        assert hpb in (1, 2, 4) and hkv % hpb == 0 and (hpb == 1 or not rope)
+        # with head blocks (the LDS-staged kernel) one page of an item fits its 48 KB stage
+        assert hpb == 1 or 8192 * hpb + n_item * 64 * r <= 48 * 1024
         seen = np.zeros(bb.shape, np.int32)
         rows = np.zeros(h["total_rows"], np.int32)
         for it in items:
@@ -275,16 +281,19 @@ def test_decode_plan_items_cover_every_agent_page_once(hq, hkv, r, rope, pps):
                 assert it["p1"] <= (sl[a] + 15) // 16
                 assert (bb[a, it["p0"]:it["p1"]] == bb[it["leader"], it["p0"]:it["p1"]]).all()
                 seen[a, it["p0"]:it["p1"]] += 1
-            rows[it["row_base"]: it["row_base"] + it["nag"] * g] += 1
+            ng = -(-it["nag"] // (16 // g))
+            it["copies"] = 4 // (1 if ng == 1 else 2 if ng == 2 else 4)
+            rows[it["row_base"]: it["row_base"] + it["copies"] * it["nag"] * g] += 1
         for a in range(n_agents):
             npg = (sl[a] + 15) // 16
             assert (seen[a, :npg] == 1).all() and (seen[a, npg:] == 0).all()
         assert (rows == 1).all()
         ids = [b for b in blocks if b >= 0]
-        assert sorted(ids) == list(range(len(items) * hkv)) and len(blocks) % 8 == 0
+        assert sorted(ids) == list(range(len(items) * (hkv // hpb))) and len(blocks) % 8 == 0
         for a in range(n_agents):
             mine = sorted(int(s) // hkv for s in slots[ptr[a]:ptr[a + 1]])
-            want = sorted(it["row_base"] + it["agents"].index(a) * g for it in items if a in it["agents"])
+            want = sorted(it["row_base"] + (c * it["nag"] + it["agents"].index(a)) * g
+                          for it in items if a in it["agents"] for c in range(it["copies"]))
             assert mine == want and all(int(s) % hkv == 0 for s in slots[ptr[a]:ptr[a + 1]])
         info = plan.info(128, r)
         assert info["workspace_bytes"] == h["total_rows"] * hkv * ((128 + r + 2 + 3) // 4 * 4) * 4

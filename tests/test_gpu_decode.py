@@ -153,14 +153,27 @@ def test_repeated_calls_are_deterministic():
     assert torch.equal(a, b)
 
 
-@pytest.mark.parametrize("pps", [4, 8, 64, 256])
-def test_split_sizes_agree(pps):
+@pytest.mark.parametrize("rope", [False, True])
+@pytest.mark.parametrize("pps", [4, 7, 64])
+def test_split_sizes_agree(pps, rope):
     # the split count changes only the (exactly merged) partition of the keys
     wl = W.fanout("splits", 42, n_agents=8, prefix=1024, suffix_lo=3, suffix_hi=300, hq=32, hkv=8, r=16)
-    lw = LoadedWorkload(wl, rope=True, pages_per_split=pps)
+    lw = LoadedWorkload(wl, rope=rope, pages_per_split=pps)
     out = lw.decode().clone()
     torch.cuda.synchronize()
-    check_close(f"pps={pps}", out, oracle_decode(wl, wl.decode_agents(), True))
+    check_close(f"pps={pps} rope={rope}", out, oracle_decode(wl, wl.decode_agents(), rope))
+    lw.close()
+
+
+@pytest.mark.parametrize("item_agents", [1, 3, 4, 6, 8, 13, 16])
+def test_agents_per_item_agree(item_agents):
+    # 1..4 agent groups per work item (the last one partly filled), 1, 2 or 4 wave copies
+    wl = W.fanout("groups", 43, n_agents=16, prefix=700, suffix_lo=1, suffix_hi=120, hq=32, hkv=8, r=16)
+    lw = LoadedWorkload(wl, rope=False, item_agents=item_agents)
+    out = lw.decode().clone()
+    torch.cuda.synchronize()
+    check_close(f"item_agents={item_agents}", out, oracle_decode(wl, wl.decode_agents(), False))
+    lw.close()
 
 
 @pytest.mark.parametrize("rope", [False, True])
