@@ -4,20 +4,27 @@ Metric: decode attention tokens/s and achieved HBM GB/s (fraction of the 8 TB/s
 peak) for one Llama-3-8B-shaped attention layer with 16 agents that share a
 32768-token prefix (suffixes uniform in [256, 4096], rank 16, 32 q / 8 kv heads,
 head dim 128, bf16).  One step = one decode call (split kernel + combine kernel)
-over all 16 agents; tokens/s = agents x steps / time.
+over all 16 agents; tokens/s = agents x steps / wall time of the timed steps.
 
-Inputs are resident in HBM before timing starts.  Three independent copies of
-the caches are built and the steps rotate over them, so consecutive steps never
-read data the previous step left in the 256 MB last-level (MALL) cache.
+The headline runs the method as the key reconstruction K = K_base + C_K B_K (no
+position rotation of the rebuilt term); the same workload with deferred RoPE on the
+rebuilt term is timed afterwards and reported under "rope_on".
+
+Inputs are resident in HBM before timing starts.  Three independent copies of the
+caches are built and the steps rotate over them, so consecutive steps never read
+data the previous step left in the 256 MB last-level (MALL) cache.
 
 Roofline: the split kernel dominates.  Its algorithmic bytes per launch are the
-shared base pages counted once per segment, plus each agent's private base
-pages, rCache rows, adapter B matrices, queries, outputs, block tables and (RoPE
-on) the cos/sin rows read, and its duration is taken live from HIP events
-recorded around it on the launch stream.
+shared base pages counted once per segment, plus each agent's private base pages,
+rCache rows, adapter B matrices, queries, outputs, block tables and (RoPE on) the
+cos/sin rows read, and its duration is taken live from HIP events recorded around
+it on the launch stream.  "traffic" is the HBM bytes the hardware counters saw for
+the same kernel (FETCH_SIZE + WRITE_SIZE, calibrated against a plain copy of known
+size), read from the committed counter summary when it was taken on the current
+kernel source, else null.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2] [--rope 0|1]
-       [--pps N] [--no-cpu-baseline]
+       [--pps N] [--no-rope-on] [--no-cpu-baseline]
 """
 from __future__ import annotations
 
@@ -30,6 +37,30 @@ import time
 import numpy as np
 
 HBM_PEAK_GBS = 8000.0
+ROOT = os.path.dirname(os.path.abspath(__file__))
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_llama3-8b-16agents-32k-shared_hbm_traffic.md")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2604_06370_amd", "csrc", "decode.hip")
+
+
+def counter_traffic(rope: bool, workload: str, pages_per_split: int):
+    """HBM bytes per split-kernel launch from the committed rocprofv3 counter summary, or None
+    when there is none for this mode or it was taken on another version of the kernel source."""
+    import hashlib
+    import re
+    try:
+        text = open(TRAFFIC_SUMMARY).read()
+    except OSError:
+        return None
+    m = re.search(r"```json\n(.*?)\n```", text, re.S)
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    sha = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+    entry = rec.get("rope_on" if rope else "rope_off")
+    if (rec.get("decode_hip_sha256") != sha or not entry or rec.get("workload") != workload
+            or entry.get("pages_per_split") != pages_per_split):
+        return None
+    return entry["hbm_bytes_per_launch"]
 
 
 def algorithmic_bytes(wl, lw, agents, rope: bool) -> dict:
@@ -58,23 +89,24 @@ def algorithmic_bytes(wl, lw, agents, rope: bool) -> dict:
             "rope_table": rope_b, "base_tokens": base_tokens}
 
 
-def cpu_baseline(wl, agents, rope: bool, budget_s: float = 20.0) -> dict:
+def cpu_baseline(wl, agents, rope: bool, budget_s: float = 12.0) -> dict:
+    """Times the CPU oracle on the benchmark's own workload: whole decode steps over all agents
+    (every head), repeated until the time budget is spent, reported in the same tokens/s."""
     import oracle
     from paper_2604_06370_amd import workloads as W
     threads = oracle.default_threads()
-    done, t_used = [], 0.0
-    # evaluate agents one at a time until the time budget is spent (at least one)
-    for a in agents:
-        p = W.oracle_inputs(wl, agents=[a], rope=rope)
-        t0 = time.perf_counter()
-        oracle.residual_attention(p, n_threads=threads)
-        t_used += time.perf_counter() - t0
-        done.append(a)
-        if t_used >= budget_s:
-            break
-    return {"value": len(done) / t_used, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"{len(done)} of {len(agents)} agents of the timed workload (all heads, fp64 C oracle, "
-                      f"{t_used:.1f} s)"}
+    inputs = [W.oracle_inputs(wl, agents=[a], rope=rope) for a in agents]
+    tokens, t_used, passes = 0, 0.0, 0
+    while t_used < budget_s:
+        for p in inputs:
+            t0 = time.perf_counter()
+            oracle.residual_attention(p, n_threads=threads)
+            t_used += time.perf_counter() - t0
+            tokens += 1
+        passes += 1
+    return {"value": tokens / t_used, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{passes} full decode steps of the timed workload ({len(agents)} agents, all heads, "
+                      f"fp64 C oracle, {t_used:.1f} s of oracle time)"}
 
 
 def main():
@@ -83,7 +115,8 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=2)
-    ap.add_argument("--rope", type=int, default=1)
+    ap.add_argument("--rope", type=int, default=0, help="headline with RoPE on the rebuilt keys (default off)")
+    ap.add_argument("--no-rope-on", action="store_true", help="skip the RoPE-on measurement")
     ap.add_argument("--pps", type=int, default=0, help="pages per split (0 = automatic)")
     ap.add_argument("--item-agents", type=int, default=0, help="agents per decode work item (0 = automatic)")
     ap.add_argument("--copies", type=int, default=3)
@@ -97,6 +130,7 @@ def main():
               "head with no exchange; see DESIGN.md). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
+    import ctypes
     import torch
     from paper_2604_06370_amd import workloads as W
     from paper_2604_06370_amd.driver import LoadedWorkload
@@ -104,24 +138,42 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     wl = W.config(args.config)
-    rope = bool(args.rope) and wl.r > 0
-    print(f"# building {args.copies} cache copies of {wl.name} (rope={rope})", file=sys.stderr, flush=True)
-    lws = [LoadedWorkload(wl, device=dev, rope=rope, pages_per_split=args.pps,
-                          item_agents=args.item_agents) for _ in range(args.copies)]
     agents = wl.decode_agents()
-    for lw in lws:
-        lw.decode_setup(agents)
-    info = lws[0]._decode["info"]
-    byts = algorithmic_bytes(wl, lws[0], agents, rope)
     stream = torch.cuda.current_stream()
 
-    # live per-kernel timing: events recorded by the library around its two launches
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-    for trio in ev:
-        for e in trio:
-            e.record(stream)  # materialise the HIP event
-    import ctypes
-    handles = [(ctypes.c_void_p * 3)(*[e.cuda_event for e in trio]) for trio in ev]
+    def measure(rope: bool, steps: int, warmup: int) -> dict:
+        print(f"# building {args.copies} cache copies of {wl.name} (rope={rope})", file=sys.stderr, flush=True)
+        lws = [LoadedWorkload(wl, device=dev, rope=rope, pages_per_split=args.pps,
+                              item_agents=args.item_agents) for _ in range(args.copies)]
+        for lw in lws:
+            lw.decode_setup(agents)
+        info = lws[0]._decode["info"]
+        byts = algorithmic_bytes(wl, lws[0], agents, rope)
+        # live per-kernel timing: events recorded by the library around its two launches
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+        for trio in ev:
+            for e in trio:
+                e.record(stream)  # materialise the HIP event
+        handles = [(ctypes.c_void_p * 3)(*[e.cuda_event for e in trio]) for trio in ev]
+        for i in range(warmup):
+            lws[i % len(lws)].decode()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            lw = lws[i % len(lws)]
+            lw._decode["args"].timing_events = ctypes.cast(handles[i], ctypes.c_void_p).value
+            lw.decode()
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for lw in lws:
+            lw._decode["args"].timing_events = None
+        split_ms = np.array([ev[i][0].elapsed_time(ev[i][1]) for i in range(steps)])
+        comb_ms = np.array([ev[i][1].elapsed_time(ev[i][2]) for i in range(steps)])
+        for lw in lws:
+            lw.close()
+        del lws
+        torch.cuda.empty_cache()
+        return {"info": info, "bytes": byts, "split_ms": split_ms, "comb_ms": comb_ms, "wall_s": t1 - t0}
 
     copy_probe = None
     if args.copy_probe_mb > 0:
@@ -135,25 +187,15 @@ def main():
         e1.record(stream)
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1)
-        copy_probe = {"bytes_read": nbytes, "bytes_written": nbytes, "ms": ms, "GBps_read_plus_write": 2 * nbytes / ms / 1e6}
+        copy_probe = {"bytes_read": nbytes, "bytes_written": nbytes, "ms": ms,
+                      "GBps_read_plus_write": 2 * nbytes / ms / 1e6}
         del src, dst
 
-    for i in range(args.warmup):
-        lws[i % len(lws)].decode()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        lw = lws[i % len(lws)]
-        lw._decode["args"].timing_events = ctypes.cast(handles[i], ctypes.c_void_p).value
-        lw.decode()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    for lw in lws:
-        lw._decode["args"].timing_events = None
-    split_ms = np.array([ev[i][0].elapsed_time(ev[i][1]) for i in range(args.steps)])
-    comb_ms = np.array([ev[i][1].elapsed_time(ev[i][2]) for i in range(args.steps)])
-    ms_step = (t1 - t0) * 1e3 / args.steps
-    value = len(agents) * args.steps / (t1 - t0)
+    rope = bool(args.rope) and wl.r > 0
+    r = measure(rope, args.steps, args.warmup)
+    byts, info, split_ms, comb_ms = r["bytes"], r["info"], r["split_ms"], r["comb_ms"]
+    ms_step = r["wall_s"] * 1e3 / args.steps
+    value = len(agents) * args.steps / r["wall_s"]
     split_avg = float(split_ms.mean())
     achieved = byts["total"] / (split_avg * 1e-3) / 1e9
     call_gbs = byts["total"] / (float((split_ms + comb_ms).mean()) * 1e-3) / 1e9
@@ -168,13 +210,25 @@ def main():
                    "seq_len_mean": float(np.mean(wl.seq_len[agents])), "pages_per_split": info["pages_per_split"],
                    "work_items": info["n_items"], "workgroups": info["n_blocks"], "cache_copies": args.copies},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None, "kernel": "decode_split_kernel",
-                     "algorithmic_bytes": byts["total"], "kernel_ms": split_avg,
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": counter_traffic(rope, wl.name, info["pages_per_split"]),
+                     "kernel": "decode_rope_kernel" if rope else "decode_split_kernel", "algorithmic_bytes": byts["total"], "kernel_ms": split_avg,
+                     "kernel_ms_p10_p50_p90": [float(np.percentile(split_ms, q)) for q in (10, 50, 90)],
                      "combine_ms": float(comb_ms.mean()), "call_GBps": call_gbs},
         "bytes": byts,
     }
     if copy_probe is not None:
         out["copy_probe"] = copy_probe
+    if not args.no_rope_on and not rope and wl.r > 0:
+        q = measure(True, args.steps, args.warmup)
+        qs = float(q["split_ms"].mean())
+        out["rope_on"] = {
+            "value": len(agents) * args.steps / q["wall_s"], "unit": "tokens/s",
+            "ms_per_step": q["wall_s"] * 1e3 / args.steps, "kernel_ms": qs,
+            "combine_ms": float(q["comb_ms"].mean()), "algorithmic_bytes": q["bytes"]["total"],
+            "achieved_GBps": q["bytes"]["total"] / (qs * 1e-3) / 1e9,
+            "frac": q["bytes"]["total"] / (qs * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "kernel": "decode_rope_kernel", "pages_per_split": q["info"]["pages_per_split"],
+            "traffic": counter_traffic(True, wl.name, q["info"]["pages_per_split"])}
     if not args.no_cpu_baseline:
         print("# timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wl, agents, rope)

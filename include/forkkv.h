@@ -251,8 +251,9 @@ typedef struct {
  * `plan` is the host plan whose serialised copy args->plan points to (grid size
  * and workspace size are taken from it); the block tables and sequence lengths
  * in args must be the ones the plan was built from.
- * Supported: d = 128, page_size = 16, r in {0, 8, 16, 32, 64}, hq/hkv in {4, 8}; with RoPE the
- * plan's max_item_agents must not exceed 256 / r.
+ * Supported: d = 128, page_size = 16, r in {0, 8, 16, 32, 64}, hq/hkv in {4, 8}.  The plan must
+ * have been built for the same r and RoPE setting (FKV_ERR_INVALID otherwise), so that its work
+ * items hold no more agents than fkv_decode_plan_default_agents allows.
  * Two kernels are enqueued (split, combine).  Errors: FKV_ERR_INVALID /
  * FKV_ERR_UNSUPPORTED before any launch, FKV_ERR_HIP when a launch fails. */
 fkv_status fkv_residual_attention_decode(const fkv_attn_args *args, const fkv_plan *plan, void *stream);
