@@ -37,6 +37,7 @@ import time
 import numpy as np
 
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 matrix-core peak of MI355X
 ROOT = os.path.dirname(os.path.abspath(__file__))
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_llama3-8b-16agents-32k-shared_hbm_traffic.md")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2604_06370_amd", "csrc", "decode.hip")
@@ -89,6 +90,26 @@ def algorithmic_bytes(wl, lw, agents, rope: bool) -> dict:
             "rope_table": rope_b, "base_tokens": base_tokens}
 
 
+def prefill_flops(wl, agents) -> dict:
+    """Algorithmic flops of one chunked-prefill call: every query row attends to the keys it can
+    see (QK^T and P V_base over all query heads, P C_V in rank space), each agent's keys are
+    rebuilt once (C_K B_K for every KV head) and every row applies B_V once."""
+    hq, hkv, d, r = wl.hq, wl.hkv, wl.d, wl.r
+    attn = rebuild = bv = 0
+    rows = 0
+    for a in agents:
+        n = wl.n_queries(a)
+        L = int(wl.seq_len[a])
+        p0 = L - n
+        visible = n * p0 + n * (n + 1) // 2  # sum over rows of (p0 + i + 1)
+        res = r if wl.has_residual[a] else 0
+        attn += visible * (4 * hq * d + 2 * hq * res)
+        rebuild += L * 2 * res * d * hkv
+        bv += n * 2 * hq * res * d
+        rows += n
+    return {"total": attn + rebuild + bv, "attention": attn, "rebuild": rebuild, "b_v": bv, "rows": rows}
+
+
 def cpu_baseline(wl, agents, rope: bool, budget_s: float = 12.0) -> dict:
     """Times the CPU oracle on the benchmark's own workload: whole decode steps over all agents
     (every head), repeated until the time budget is spent, reported in the same tokens/s."""
@@ -109,6 +130,51 @@ def cpu_baseline(wl, agents, rope: bool, budget_s: float = 12.0) -> dict:
                       f"fp64 C oracle, {t_used:.1f} s of oracle time)"}
 
 
+def measure_prefill(args, dev, stream) -> dict:
+    """Chunked prefill on one workload (default: 16 agents append 2048-token chunks after a
+    32768-token shared prefix), RoPE off and on; bound by the matrix cores."""
+    import ctypes
+    import torch
+    from paper_2604_06370_amd import workloads as W
+    from paper_2604_06370_amd.driver import LoadedWorkload
+
+    print(f"# generating prefill workload {args.prefill_config}", file=sys.stderr, flush=True)
+    wl = W.config(args.prefill_config)
+    agents = wl.prefill_agents()
+    fl = prefill_flops(wl, agents)
+    res = {"workload": wl.name, "agents": len(agents), "query_rows": fl["rows"], "kernel": "prefill_kernel",
+           "flops": fl["total"], "flops_split": fl, "bound": "mfma", "peak": MFMA_BF16_PEAK_TFLOPS,
+           "unit": "TFLOP/s"}
+    for rope in (False, True):
+        lw = LoadedWorkload(wl, device=dev, rope=rope)
+        lw.prefill_setup(agents)
+        n = args.prefill_steps
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(n)]
+        for pair in ev:
+            for e in pair:
+                e.record(stream)
+        handles = [(ctypes.c_void_p * 2)(*[e.cuda_event for e in pair]) for pair in ev]
+        lw.prefill()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(n):
+            lw._prefill["args"].timing_events = ctypes.cast(handles[i], ctypes.c_void_p).value
+            lw.prefill()
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        lw._prefill["args"].timing_events = None
+        ms = np.array([e[0].elapsed_time(e[1]) for e in ev])
+        k_ms = float(ms.mean())
+        tflops = fl["total"] / (k_ms * 1e-3) / 1e12
+        res["rope_on" if rope else "rope_off"] = {
+            "kernel_ms": k_ms, "kernel_ms_p10_p50_p90": [float(np.percentile(ms, q)) for q in (10, 50, 90)],
+            "tokens_per_s": fl["rows"] * n / (t1 - t0), "achieved": tflops, "frac": tflops / MFMA_BF16_PEAK_TFLOPS}
+        lw.close()
+        del lw
+        torch.cuda.empty_cache()
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -121,6 +187,9 @@ def main():
     ap.add_argument("--item-agents", type=int, default=0, help="agents per decode work item (0 = automatic)")
     ap.add_argument("--copies", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-prefill", action="store_true", help="skip the chunked-prefill measurement")
+    ap.add_argument("--prefill-config", type=int, default=3)
+    ap.add_argument("--prefill-steps", type=int, default=10)
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="also run one plain device copy of this many MiB (reference kernel of known size "
                          "for calibrating HBM byte counters)")
@@ -229,6 +298,8 @@ def main():
             "frac": q["bytes"]["total"] / (qs * 1e-3) / 1e9 / HBM_PEAK_GBS,
             "kernel": "decode_rope_kernel", "pages_per_split": q["info"]["pages_per_split"],
             "traffic": counter_traffic(True, wl.name, q["info"]["pages_per_split"])}
+    if not args.no_prefill:
+        out["prefill"] = measure_prefill(args, dev, stream)
     if not args.no_cpu_baseline:
         print("# timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wl, agents, rope)

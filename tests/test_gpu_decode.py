@@ -188,3 +188,25 @@ def test_config2_full_size_sampled(rope):
     ref = oracle_decode(wl, sample, rope)
     check_close(f"cfg2-full rope={rope}", out[sample], ref)
     lw.close()
+
+
+@pytest.fixture(scope="module")
+def config4():
+    return W.config(4)
+
+
+@pytest.mark.parametrize("rope", [False, True])
+def test_config4_full_size_sampled(config4, rope):
+    """Config 4 at full size: 64 agents over a 131072-token root, four sub-groups of 16 that
+    share 8192 more tokens, private suffixes U[128, 2048], rank 32.  The oracle evaluates one
+    agent of every sub-group (all heads)."""
+    wl = config4
+    print(f"case cfg4-full rope={rope}: agents={wl.n_agents} L={list(wl.seq_len[:4])}...", flush=True)
+    lw = LoadedWorkload(wl, rope=rope)
+    agents = wl.decode_agents()
+    out = lw.decode().clone()
+    torch.cuda.synchronize()
+    sample = [0, 21, 42, 63]
+    ref = oracle_decode(wl, sample, rope)
+    check_close(f"cfg4-full rope={rope}", out[[agents.index(a) for a in sample]], ref)
+    lw.close()

@@ -117,3 +117,31 @@ def test_config3_full_size_sampled(rope):
     pos = {int(x): i for i, x in enumerate(st["rows"])}
     check_close(f"cfg3-full rope={rope}", out[[pos[int(x)] for x in p["q_index"]]], ref)
     lw.close()
+
+
+@pytest.mark.parametrize("rope", [False, True])
+def test_config5_mixed_full_size_sampled(rope):
+    """Config 5 at full size: 32 agents of a 70B-shaped layer (64 q / 8 kv heads, rank 64) over
+    three trees (8K / 32K / 64K prefixes), agents i mod 10 == 9 without residual; 8 agents
+    prefill a 1024-token chunk and 24 decode, both calls on one stream.  Sampled decode agents
+    cover every tree and a zero-residual agent; sampled prefill rows cover three agents."""
+    wl = W.config(5)
+    print(f"case cfg5-full rope={rope}: agents={wl.n_agents} L={list(wl.seq_len[:6])}...", flush=True)
+    lw = LoadedWorkload(wl, rope=rope)
+    dec_agents = wl.decode_agents()
+    st = lw.prefill_setup()
+    out_d = lw.decode().clone()
+    out_p = lw.prefill().clone()
+    torch.cuda.synchronize()
+    dsample = [0, 1, 2, 9, 29]
+    p = W.oracle_inputs(wl, agents=dsample, rope=rope)
+    ref = oracle.residual_attention(p)
+    check_close(f"cfg5-decode rope={rope}", out_d[[dec_agents.index(a) for a in dsample]], ref)
+    rng = np.random.default_rng(11)
+    pagents = [3, 19, 23]
+    q_rows = {a: np.unique(np.concatenate([[0, 1, 15, 16, 1023], rng.integers(0, 1024, 5)])) for a in pagents}
+    p = W.oracle_inputs(wl, agents=pagents, q_rows=q_rows, rope=rope)
+    ref = oracle.residual_attention(p)
+    pos = {int(x): i for i, x in enumerate(st["rows"])}
+    check_close(f"cfg5-prefill rope={rope}", out_p[[pos[int(x)] for x in p["q_index"]]], ref)
+    lw.close()
