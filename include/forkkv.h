@@ -36,8 +36,13 @@
  *                K (token t, dim i): (i/32)*512 + (t + 16*((i%16)/4))*8 + 4*((i%32)/16) + i%4
  *                V (token t, dim i): (i/32)*512 + (i%16 + 16*(t/4))*8 + 4*((i/16)%2) + t%4
  *              fkv_scatter_tokens writes this order; other shapes use K [ps][d], V [d][ps].
- *   res pool   [num_res_pages][2][ps*r] bf16.  Slot 0 holds C_K as [ps][r],
- *              slot 1 holds C_V as [r][ps].
+ *   res pool   [num_res_pages][fkv_res_page_elems(ps, r)] bf16.  For ps = 16 a page
+ *              holds ceil(r/16) tiles of 512 values in fragment order: for L = 16*g + c
+ *              (0 <= L < 64) tile k holds C_K[token c][16k + 4g + i] at L*4 + i and
+ *              C_V[token 4g + i][16k + c] at 256 + L*4 + i (i < 4), so each lane of a
+ *              wave reads each of its rCache fragments with one 8-byte load (for r = 8
+ *              half of a tile is padding).  Other page sizes: C_K as [ps][r], then C_V as
+ *              [r][ps].
  *   adapters   [n_adapters][2][r][Hkv*d] bf16: B_K then B_V, each the r x n
  *              up-projection of Eq. 1 in row-major order (n = Hkv*d); KV head h
  *              uses columns h*d .. h*d+d-1.  Any LoRA scaling is folded in by the
@@ -274,6 +279,10 @@ fkv_status fkv_rope_table(int32_t d, int32_t max_pos, double base, float *cos_ou
 /* ------------------------------------------------------------------------ */
 /* Cache writes (device): copy-on-write page copies and token scatter.        */
 /* ------------------------------------------------------------------------ */
+
+/* Values (bf16) in one residual page for page size ps and rank r (the row stride of the
+ * residual pool): ceil(r/16)*512 for ps = 16, 2*ps*r otherwise; 0 for invalid arguments. */
+int64_t fkv_res_page_elems(int32_t page_size, int32_t r);
 
 /* Perform page copies (device array of n fkv_page_copy) in both pools.  base_kv
  * and res_kv are the pools; hkv, d, r, page_size describe them. */

@@ -111,6 +111,7 @@ fkv_residual_attention_decode = _sig("fkv_residual_attention_decode", c_i32,
 fkv_residual_attention_prefill = _sig("fkv_residual_attention_prefill", c_i32,
                                       [ctypes.POINTER(fkv_attn_args), c_vp])
 fkv_rope_table = _sig("fkv_rope_table", c_i32, [c_i32, c_i32, c_f64, c_vp, c_vp])
+fkv_res_page_elems = _sig("fkv_res_page_elems", c_i64, [c_i32, c_i32])
 fkv_page_copy_launch = _sig("fkv_page_copy_launch", c_i32, [c_vp, c_i32, c_vp, c_vp, c_i32, c_i32, c_i32, c_i32, c_vp])
 fkv_scatter_tokens = _sig("fkv_scatter_tokens", c_i32,
                           [c_vp, c_vp, c_i64, c_i64, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_i32, c_i32, c_i32, c_i32,

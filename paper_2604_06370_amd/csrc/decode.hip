@@ -217,31 +217,45 @@ struct ResOffsets {
 };
 
 // ---------------------------------------------------------------------------
-// RoPE off: one workgroup per (work item, KV head), four waves.
-template <int R, int G, bool ROPE>
+// RoPE off.  One workgroup per (work item, KV head), four waves; wave w serves agent
+// group w % ngp as copy w / ngp.  The item's base pages stream through a two-buffer LDS
+// ring in stages of SP pages (SP = 2 when the item has four groups, else 4); every wave
+// loads two 4 KB blocks per load round into registers, one or two stages ahead, and
+// stores them into the ring once the stage before has been consumed.  A wave computes
+// its share of a stage as one step of two pages (four groups: the whole stage; two
+// groups: pages 2c, 2c+1 for copy c) or of one page (one group: page c), so one wave
+// instruction of the 16x16x32 form covers 32 keys of the value products.  Its agents'
+// rCache fragments come straight from memory one stage ahead (one 16-byte load per
+// slot, page and rank tile).
+template <int R, int G>
 struct SplitShape {
     static constexpr int AG = ROWS / G;                                         // agents per group
     static constexpr int RT = R == 0 ? 0 : (R + 15) / 16;                       // 16-wide rank tiles
-    static constexpr bool MULTI = !ROPE && R < 32;                             // several groups per item
-    static constexpr int MAX_SLOTS = MULTI ? cmin(fkv::kMaxGroups * AG, fkv::kMaxItemAgents) : AG;
-    static constexpr int STAGE_BYTES = MULTI ? 2 * 2 * 2 * kBlockHalfs * 2 : 0;  // [buf][page][K|V] blocks
-    static constexpr int BSTAGE_BYTES = ROPE ? AG * R * D * 2 : 0;              // row-major B_K slices
-    static constexpr int UNION_BYTES = cmax(16, cmax(STAGE_BYTES, BSTAGE_BYTES));
-    static constexpr int BKT_BYTES = ROPE ? AG * RT * 8 * 64 * 8 : 0;           // B_K^T fragments
+    static constexpr int RTX = RT > 0 ? RT : 1;
+    static constexpr bool MULTI = R < 32;                                       // several groups per item
+    static constexpr int NSW = fkv::decode_wave_slots(G, R);                    // agent slots per wave
+    static constexpr int NSR = R > 0 ? NSW : 1;
+    static constexpr int MAX_SLOTS = MULTI ? cmin(fkv::kMaxGroups * AG, fkv::kMaxItemAgents) : NSW;
+    static constexpr int RES_PAGE = RT * 512;                                   // rCache page (halfs)
+    static constexpr int RING_BYTES = 8 * 2 * kBlockHalfs * 2;                  // two buffers of four pages
     static constexpr int TABLE_WORDS = (1 + (R > 0 ? MAX_SLOTS : 0)) * kMaxPagesPerItem;
-    static constexpr int LDS_BYTES = UNION_BYTES + BKT_BYTES + TABLE_WORDS * 4;
+    static constexpr int LDS_BYTES = RING_BYTES + TABLE_WORDS * 4;
 };
 
-template <int R, int G, bool ROPE>
-__global__ __launch_bounds__(256, ROPE ? 1 : 2) void decode_split_kernel(DecodeArgs p) {
-    using S = SplitShape<R, G, ROPE>;
+template <int R, int G>
+__global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
+    using S = SplitShape<R, G>;
     constexpr int AG = S::AG;
     constexpr int RT = S::RT;
-    constexpr int RTX = RT > 0 ? RT : 1;
+    constexpr int RTX = S::RTX;
+    constexpr int NSW = S::NSW;
+    constexpr int NSR = S::NSR;
+    struct CFrag {  // rCache fragments of the wave's slots for the (up to two) pages of a step
+        u32x2 k[2][NSR][RTX], v[2][NSR][RTX];
+    };
     __shared__ __attribute__((aligned(16))) unsigned char lds[S::LDS_BYTES];
-    uint16_t *lds_h = reinterpret_cast<uint16_t *>(lds);
-    uint32_t *lds_bkt = reinterpret_cast<uint32_t *>(lds + S::UNION_BYTES);
-    int32_t *s_tab = reinterpret_cast<int32_t *>(lds + S::UNION_BYTES + S::BKT_BYTES);
+    uint16_t *ring = reinterpret_cast<uint16_t *>(lds);
+    int32_t *s_tab = reinterpret_cast<int32_t *>(lds + S::RING_BYTES);
 
     const int32_t *plan = p.plan;
     const int blk = plan[plan[fkv::H_OFF_BLOCKS] + blockIdx.x];
@@ -252,405 +266,389 @@ __global__ __launch_bounds__(256, ROPE ? 1 : 2) void decode_split_kernel(DecodeA
     const int32_t *rec = plan + plan[fkv::H_OFF_ITEMS] + item * fkv::kItemWords;
     const int pg0 = rec[0], pg1 = rec[1], leader = rec[2], nag = rec[3], row_base = rec[4];
     const int32_t *item_agents = rec + 5;
-    if (ROPE && nag > AG) return;  // rejected on the host: RoPE items hold one group
-    const int ng = (nag + AG - 1) / AG;                 // agent groups in the item (1..4)
+    const int ng = (nag + AG - 1) / AG;
+    if (pg1 - pg0 > kMaxPagesPerItem || nag > S::MAX_SLOTS || (ng > 1 && !S::MULTI) || (ng == 1 && nag > NSW))
+        return;  // rejected on the host
     const int ngp = ng == 1 ? 1 : (ng == 2 ? 2 : 4);   // groups rounded to a divisor of 4
+    const int sp = ngp == 4 ? 2 : 4;                   // pages per stage
 
     const int lane = threadIdx.x & 63;
     const int wave = uniform(threadIdx.x >> 6);
     const int col = lane & 15, grp = lane >> 4;
     const int my_group = wave % ngp;
-    const int copy = wave / ngp;                        // which of the 4/ngp waves of the group
+    const int copy = wave / ngp;
     const int sb = my_group * AG;                       // first item slot of this wave's group
-    const int my_slot_l = col / G;                      // this lane's row: slot within the group
-    const bool row_active = sb + my_slot_l < nag;
-    const int my_agent = row_active ? item_agents[sb + my_slot_l] : 0;
+    const int my_slot = col / G;                        // this lane's row: slot within the group
+    const bool row_active = my_slot < NSW && sb + my_slot < nag;
+    const int my_agent = row_active ? item_agents[sb + my_slot] : 0;
     const int qh = h * G + (col % G);
+    const int64_t n = (int64_t)hkv * D;
+
+    // per slot of the wave's group: adapter (or -1) and sequence length
+    int slot_ad[NSR], slot_len[NSR];
+    int max_len = 0;
+#pragma unroll
+    for (int s = 0; s < NSR; ++s) {
+        const bool ok = sb + s < nag && s < NSW;
+        const int ag_id = ok ? item_agents[sb + s] : 0;
+        const int len = ok ? p.seq_lens[ag_id] : 0;
+        slot_ad[s] = (ok && R > 0) ? p.adapter_idx[ag_id] : -1;
+        slot_len[s] = len;
+        if (ok) max_len = max(max_len, len);
+    }
+    const int my_len = row_active ? p.seq_lens[my_agent] : 0;
+
+    // Q^T fragments (B operand of the 16x16x32 products) and, per slot, the B_K rows this
+    // lane needs for W = B_K q; both only depend on the item record, so they are issued
+    // before the block tables are staged
+    u32x4 qf[4];
+    load_q(p.q + ((int64_t)my_agent * p.hq + qh) * D, row_active, grp, qf);
 
     // block-table entries of the item's pages, for the base pool and every slot's
     // residual pool, staged in LDS with one parallel pass
     const int npg = pg1 - pg0;
-    const int n_tab = R > 0 ? 1 + ngp * AG : 1;
+    const int n_tab = R > 0 ? 1 + nag : 1;
     for (int idx = threadIdx.x; idx < n_tab * npg; idx += 256) {
         const int t = idx / npg, i = idx - t * npg;
-        int32_t v = 0;
-        if (t == 0) {
-            v = p.base_bt[(int64_t)leader * p.max_pages + pg0 + i];
-        } else if (t - 1 < nag) {
-            v = p.res_bt[(int64_t)item_agents[t - 1] * p.max_pages + pg0 + i];
-        }
-        s_tab[t * kMaxPagesPerItem + i] = v;
+        const int32_t *row = t == 0 ? p.base_bt + (int64_t)leader * p.max_pages
+                                    : p.res_bt + (int64_t)item_agents[t - 1] * p.max_pages;
+        s_tab[t * kMaxPagesPerItem + i] = row[pg0 + i];
     }
 
-    // per slot of the wave's group: adapter, and the tokens whose rCache rows are used
-    // (the sequence length, or 0 for an empty slot or an agent without adapter)
-    int slot_ad[AG], res_len[AG];
-    int max_len = 0;  // longest sequence of the wave's group (V tokens past it are zeroed)
+    // B_K rows of every slot for W = B_K q (lane holds B_K[16t + col][the head-dim slots of
+    // k-step kk]); issued before the block-table loads, so they have landed by the time the
+    // tables are staged
+    u32x4 bkf[NSR][RTX][4];
+    if constexpr (R > 0) {
 #pragma unroll
-    for (int s = 0; s < AG; ++s) {
-        const bool ok = sb + s < nag;
-        const int ag_id = ok ? item_agents[sb + s] : 0;
-        const int len = ok ? p.seq_lens[ag_id] : 0;
-        slot_ad[s] = (ok && R > 0) ? p.adapter_idx[ag_id] : -1;
-        res_len[s] = slot_ad[s] >= 0 ? len : 0;
-        max_len = max_len > len ? max_len : len;
-    }
-    const int my_len = row_active ? p.seq_lens[my_agent] : 0;
-
-    // Q^T as the B operand of the 16x16x32 products.  The head-dim index of slot j in
-    // k-step kk is 32kk + 16(j/4) + 4grp + j%4 for this lane group: the order in which
-    // a rebuilt key tile leaves the 16x16x16 accumulators and in which K blocks are
-    // stored, so base keys, rebuilt keys and queries all share it.
-    const uint16_t *qrow = p.q + ((int64_t)my_agent * p.hq + qh) * D;
-    u32x4 qf[4];
+        for (int s = 0; s < NSR; ++s) {
+            const uint16_t *bk = p.lora_b + (int64_t)(slot_ad[s] >= 0 ? slot_ad[s] : 0) * 2 * R * n + (int64_t)h * D;
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-        u32x4 v = {0, 0, 0, 0};
-        if (row_active) {
-            const u32x2 lo = ldg64(qrow + 32 * kk + 4 * grp);
-            const u32x2 hi = ldg64(qrow + 32 * kk + 16 + 4 * grp);
-            v = u32x4{lo.x, lo.y, hi.x, hi.y};
-        }
-        qf[kk] = v;
-    }
-
-    const int64_t n = (int64_t)hkv * D;
-    const int64_t res_page_halfs = 2 * PS * R;
-    // RoPE off: W = B_K q per row (bf16, B operand of the 16x16x16 residual products);
-    // computed after the first pages' loads are issued so its latency overlaps theirs
-    u32x2 wf[RTX];
+            for (int t = 0; t < RT; ++t) {
+                const int rho = 16 * t + col;
+                const int64_t ro = (int64_t)(rho < R ? rho : 0) * n;
 #pragma unroll
-    for (int t = 0; t < RTX; ++t) wf[t] = u32x2{0, 0};
-    auto prep_w = [&]() {
-        if constexpr (R > 0 && !ROPE) {
-            f32x4 wacc[RTX];
-#pragma unroll
-            for (int t = 0; t < RT; ++t) wacc[t] = f32x4{0, 0, 0, 0};
-#pragma unroll
-            for (int s = 0; s < AG; ++s) {
-                const int ad = slot_ad[s] >= 0 ? slot_ad[s] : 0;  // slots without adapter: result unused
-                const uint16_t *bk = p.lora_b + (int64_t)ad * 2 * R * n + (int64_t)h * D;
-#pragma unroll
-                for (int t = 0; t < RT; ++t) {
-                    const int rho = 16 * t + col;
-                    f32x4 acc = {0, 0, 0, 0};
-#pragma unroll
-                    for (int kk = 0; kk < 4; ++kk) {
-                        const int64_t ro = (int64_t)(rho < R ? rho : 0) * n;
+                for (int kk = 0; kk < 4; ++kk) {
+                    u32x4 a = {0, 0, 0, 0};
+                    if (slot_ad[s] >= 0 && rho < R) {
                         const u32x2 lo = ldg64(bk + ro + 32 * kk + 4 * grp);
                         const u32x2 hi = ldg64(bk + ro + 32 * kk + 16 + 4 * grp);
-                        const u32x4 a = rho < R ? u32x4{lo.x, lo.y, hi.x, hi.y} : u32x4{0, 0, 0, 0};
-                        acc = mfma32(a, qf[kk], acc);
+                        a = u32x4{lo.x, lo.y, hi.x, hi.y};
                     }
-                    if (my_slot_l == s && slot_ad[s] >= 0) wacc[t] = acc;
+                    bkf[s][t][kk] = a;
                 }
             }
-#pragma unroll
-            for (int t = 0; t < RT; ++t) wf[t] = pack4(wacc[t]);
         }
-    };
-    __syncthreads();  // tables staged
-
-    if constexpr (ROPE) {
-        // B_K^T fragments of the group's slots (lane holds B_K[16t + 4grp + i][16mt + col]),
-        // built from row-major B_K slices staged in LDS
-        for (int idx = threadIdx.x; idx < AG * R * (D / 8); idx += 256) {
-            const int sl = idx / (R * (D / 8));
-            const int rem = idx - sl * (R * (D / 8));
-            const int rho = rem / (D / 8), c8 = rem - rho * (D / 8);
-            const int ad = sl < nag ? p.adapter_idx[item_agents[sl]] : -1;
-            u32x4 v = {0, 0, 0, 0};
-            if (ad >= 0) v = ldg128(p.lora_b + (int64_t)ad * 2 * R * n + (int64_t)rho * n + (int64_t)h * D + 8 * c8);
-            *reinterpret_cast<u32x4 *>(lds_h + (sl * R + rho) * D + 8 * c8) = v;
-        }
-        __syncthreads();
-        for (int idx = threadIdx.x; idx < AG * RT * 8 * 64; idx += 256) {
-            const int ln = idx & 63;
-            const int rest = idx >> 6;  // (sl*RT + t)*8 + mt
-            const int mt = rest & 7, st = rest >> 3;
-            const int sl = st / RTX, t = st - sl * RTX;
-            const int c = ln & 15, gg = ln >> 4;
-            uint32_t w[2];
-#pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int r0 = 16 * t + 4 * gg + 2 * j;
-                const uint16_t lo = r0 < R ? lds_h[(sl * R + r0) * D + 16 * mt + c] : (uint16_t)0;
-                const uint16_t hi = r0 + 1 < R ? lds_h[(sl * R + r0 + 1) * D + 16 * mt + c] : (uint16_t)0;
-                w[j] = (uint32_t)lo | ((uint32_t)hi << 16);
-            }
-            const int o = (((sl * RTX + t) * 8 + mt) * 64 + ln) * 2;
-            lds_bkt[o] = w[0];
-            lds_bkt[o + 1] = w[1];
-        }
-        __syncthreads();
     }
+    // W^T = (B_K q)^T per slot, as the B operand of the residual key products; row
+    // columns of other slots are zero, so one product serves a pair of slots (or tiles)
+    u32x2 wsel[NSR][RTX];
+    auto finish_w = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int s = 0; s < NSR; ++s)
+#pragma unroll
+            for (int t = 0; t < RTX; ++t) {
+                wsel[s][t] = u32x2{0, 0};
+                if constexpr (R > 0) {
+                    f32x4 acc = {0, 0, 0, 0};
+#pragma unroll
+                    for (int kk = 0; kk < 4; ++kk) acc = mfma32(bkf[s][t][kk], qf[kk], acc);
+                    if (my_slot == s) wsel[s][t] = pack4(acc);
+                }
+            }
+    };
+    __syncthreads();  // tables staged (the B_K loads, issued before them, have landed too)
+    finish_w();
 
-    // ---- state of this wave's 16 rows ----
     Rows<R> st;
     st.init();
+    const float cl = p.scale_log2;
 
-    // lane-constant element offsets of the rCache fragment loads
-    int ck_off[RTX], cv_off[RTX];
-    bool ck_ok[RTX], cv_ok[RTX];
+    // ---- loads ----
+    // Base blocks travel memory -> registers -> LDS ring.  Four groups: two 16 KB buffers
+    // of one stage (two pages), each wave loading one 4 KB block per stage two stages
+    // ahead; otherwise two 32 KB buffers (four pages), two blocks per wave one stage ahead.
+    // Stages past the item re-read its last stage: every loop iteration then issues the
+    // same loads, so the compiler's vmcnt bookkeeping stays exact.
+    const int n_stages = (npg + sp - 1) / sp;
+    const int buf_halfs = sp * 2 * kBlockHalfs;
+    auto load_blocks = [&](auto nb_tag, auto first_tag, int stage, u32x4 (&bx)[2][4]) __attribute__((always_inline)) {
+        constexpr int NB = decltype(nb_tag)::value, FIRST = decltype(first_tag)::value;
+        const int stc = min(stage, n_stages - 1);
 #pragma unroll
-    for (int t = 0; t < RTX; ++t) {
-        const int rho = 16 * t + col, rk = 16 * t + 4 * grp;
-        cv_ok[t] = rho < R;
-        ck_ok[t] = rk < R;
-        cv_off[t] = PS * R + (rho < R ? rho : (R > 0 ? R - 1 : 0)) * PS + 4 * grp;   // C_V^T[rho][tok 4grp..]
-        ck_off[t] = col * R + (rk < R ? rk : (R >= 4 ? R - 4 : 0));                  // C_K[tok col][rho 4grp..]
-    }
-    auto mask4g = [&](u32x2 v, int vis) {  // zero tokens 4grp+i >= vis of a [.][tok] fragment
-        if (4 * grp + 0 >= vis) v.x &= 0xffff0000u;
-        if (4 * grp + 1 >= vis) v.x &= 0x0000ffffu;
-        if (4 * grp + 2 >= vis) v.y &= 0xffff0000u;
-        if (4 * grp + 3 >= vis) v.y &= 0x0000ffffu;
-        return v;
-    };
-    // rCache fragments of slot sb+s for logical page pg.  Slots without an adapter (or
-    // past the item's agents) read residual page 0; compute_page zeroes them (their
-    // residual length is 0), whatever that page holds.
-    auto load_res = [&](int pg, int s, u32x2 *ck, u32x2 *cv) {
-        const int tab = uniform(s_tab[(1 + sb + s) * kMaxPagesPerItem + (pg - pg0)]);
-        const uint16_t *rb = p.res_kv + (int64_t)(slot_ad[s] >= 0 ? tab : 0) * res_page_halfs;
+        for (int j = 0; j < NB; ++j) {
+            const int b = wave * NB + j;                 // block of the stage: page b/2, K or V
+            const int pl = min(pg0 + stc * sp + (b >> 1), pg1 - 1);
+            const int bpage = uniform(s_tab[pl - pg0]);
+            const uint16_t *src = p.base_kv + (((int64_t)bpage * 2 + (b & 1)) * hkv + h) * kBlockHalfs;
 #pragma unroll
-        for (int t = 0; t < RT; ++t) {
-            const u32x2 v = ldg64(rb + cv_off[t]);
-            const u32x2 k = ldg64(rb + ck_off[t]);
-            cv[t] = cv_ok[t] ? v : u32x2{0, 0};
-            ck[t] = ck_ok[t] ? k : u32x2{0, 0};
+            for (int i = 0; i < 4; ++i) bx[FIRST + j][i] = ldg128(src + i * 512 + lane * 8);
         }
     };
-    auto load_rope = [&](int pg, f32x4 *cs, f32x4 *sn) {
-        const float *cr = p.rope_cos + (int64_t)pg * (PS * D / 2);
-        const float *sr = p.rope_sin + (int64_t)pg * (PS * D / 2);
+    auto store_blocks = [&](auto nb_tag, auto first_tag, int buf, const u32x4 (&bx)[2][4]) __attribute__((always_inline)) {
+        constexpr int NB = decltype(nb_tag)::value, FIRST = decltype(first_tag)::value;
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt) {
-            cs[mt] = *reinterpret_cast<const f32x4 *>(cr + 256 * mt + lane * 4);
-            sn[mt] = *reinterpret_cast<const f32x4 *>(sr + 256 * mt + lane * 4);
+        for (int j = 0; j < NB; ++j) {
+            const int b = wave * NB + j;
+            uint16_t *dst = ring + buf * buf_halfs + b * kBlockHalfs;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4 *>(dst + i * 512 + lane * 8) = bx[FIRST + j][i];
         }
     };
-
-    // One page for this wave's rows.  kf/vf hold the base K and V fragments; ck/cv the
-    // rCache fragments of the NS slots; cs/sn the RoPE rows.  valid = false (a padding
-    // page of a stage) masks every token.
-    auto compute_page = [&](auto ns_tag, int pg, bool valid, const u32x4 *kf, u32x2 *vf, u32x2 (*ck)[RTX],
-                            u32x2 (*cv)[RTX], const f32x4 *cs, const f32x4 *sn) {
-        constexpr int NS = decltype(ns_tag)::value;
-        const int tok0 = pg * PS;
-        const int vis = max_len - tok0;   // tokens past every agent's end may hold any bits
-        if (vis < PS) {
-#pragma unroll
-            for (int mt = 0; mt < 8; ++mt) vf[mt] = mask4g(vf[mt], vis);
-        }
-        f32x4 sacc = {0, 0, 0, 0};
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk) sacc = mfma32(kf[kk], qf[kk], sacc);
+    // rCache fragments of the wave's slots for its pages of a stage (NSA slots, 1 or NSR).
+    // Slots without an adapter, and empty slots, read the plan's zero area.
+    const uint16_t *zero_c = reinterpret_cast<const uint16_t *>(plan + plan[fkv::H_OFF_ZERO]);
+    const int wpage0 = ngp == 4 ? 0 : (ngp == 2 ? 2 * copy : copy);  // first stage page it computes
+    auto load_c = [&](auto nsa_tag, auto np_tag, int stage, CFrag &c) __attribute__((always_inline)) {
+        constexpr int NSA = decltype(nsa_tag)::value, NP = decltype(np_tag)::value;
+        const int stc = min(stage, n_stages - 1);
         if constexpr (R > 0) {
 #pragma unroll
-            for (int s = 0; s < NS; ++s) {
-                // rCache tokens past the slot's own length are unwritten: zero them (a NaN
-                // there would reach every row through the zero entries of the other slots)
-                const int svis = res_len[s] - tok0;
-                if (svis < PS) {
+            for (int j = 0; j < NP; ++j) {
+                const int pl = min(pg0 + stc * sp + wpage0 + j, pg1 - 1);
+#pragma unroll
+                for (int s = 0; s < NSA; ++s) {
+                    const int tab = uniform(s_tab[(1 + sb + s) * kMaxPagesPerItem + (pl - pg0)]);
+                    const uint16_t *rb = slot_ad[s] >= 0 ? p.res_kv + (int64_t)tab * S::RES_PAGE : zero_c;
 #pragma unroll
                     for (int t = 0; t < RT; ++t) {
-                        cv[s][t] = mask4g(cv[s][t], svis);
-                        ck[s][t] = col < svis ? ck[s][t] : u32x2{0, 0};
-                    }
-                }
-                if constexpr (!ROPE) {
-#pragma unroll
-                    for (int t = 0; t < RT; ++t) {
-                        const u32x2 b = my_slot_l == s ? wf[t] : u32x2{0, 0};
-                        sacc = mfma16(ck[s][t], b, sacc);
-                    }
-                } else {
-                    // Stage 1: U^T = B_K^T C_K^T, deferred RoPE, then S^T += K_lora Q_s^T
-                    f32x4 u[8];
-#pragma unroll
-                    for (int mt = 0; mt < 8; ++mt) {
-                        u[mt] = f32x4{0, 0, 0, 0};
-#pragma unroll
-                        for (int t = 0; t < RT; ++t) {
-                            const u32x2 a = *reinterpret_cast<const u32x2 *>(
-                                lds_bkt + ((((sb + s) * RTX + t) * 8 + mt) * 64 + lane) * 2);
-                            u[mt] = mfma16(a, ck[s][t], u[mt]);
-                        }
-                    }
-#pragma unroll
-                    for (int mt = 0; mt < 4; ++mt) {
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) {
-                            const float x = u[mt][i], y = u[mt + 4][i];
-                            u[mt][i] = x * cs[mt][i] - y * sn[mt][i];
-                            u[mt + 4][i] = y * cs[mt][i] + x * sn[mt][i];
-                        }
-                    }
-#pragma unroll
-                    for (int kk = 0; kk < 4; ++kk) {
-                        const u32x2 lo = pack4(u[2 * kk]), hi = pack4(u[2 * kk + 1]);
-                        const u32x4 b = my_slot_l == s ? qf[kk] : u32x4{0, 0, 0, 0};
-                        sacc = mfma32(u32x4{lo.x, lo.y, hi.x, hi.y}, b, sacc);
+                        c.k[j][s][t] = ldg64(rb + t * 512 + lane * 4);
+                        c.v[j][s][t] = ldg64(rb + t * 512 + 256 + lane * 4);
                     }
                 }
             }
         }
-        // Stage 2 and the value products
-        softmax_pv<R, NS>(st, sacc, valid && row_active, tok0, my_len, p.scale_log2, vf, cv, my_slot_l, grp);
     };
 
-    if (ng == 1) {
-        // ---- single group: waves stride over the pages, registers double-buffered ----
-        // The loop is specialised on the number NS of agent slots so that every load it
-        // issues is consumed; all loads are unconditional and in a fixed order, so the
-        // compiler can count them and the prefetched page stays in flight.
-        auto run_pages = [&](auto ns_tag) {
-            constexpr int NS = decltype(ns_tag)::value;
-            constexpr int NSR = R > 0 ? NS : 1;
-            struct Frag {
-                f32x4 cs[ROPE ? 4 : 1], sn[ROPE ? 4 : 1];
-                u32x4 kf[4];
-                u32x2 vf[8];
-                u32x2 ck[NSR][RTX];
-                u32x2 cv[NSR][RTX];
-            };
-            auto load = [&](int pg, Frag &f) {
-                if constexpr (ROPE) load_rope(pg, f.cs, f.sn);  // issued first: consumed first
-                const int bpage = uniform(s_tab[pg - pg0]);
-                const uint16_t *kblk = p.base_kv + ((int64_t)bpage * 2 * hkv + h) * kBlockHalfs;
-                const uint16_t *vblk = kblk + (int64_t)hkv * kBlockHalfs;
+    // ---- one step: NP pages starting at stage page wp of LDS buffer buf ----
+    auto step = [&](auto nsa_tag, auto np_tag, auto masked_tag, int buf, int stage, CFrag &c) __attribute__((always_inline)) {
+        constexpr int NSA = decltype(nsa_tag)::value;
+        constexpr int NP = decltype(np_tag)::value;
+        constexpr bool MASKED = decltype(masked_tag)::value;
+        const int pgw = pg0 + stage * sp + wpage0;         // logical page of step page 0
+        const uint16_t *kb = ring + buf * buf_halfs + wpage0 * 2 * kBlockHalfs;
+        int vis[NP];
+        bool pvalid[NP];
 #pragma unroll
-                for (int kk = 0; kk < 4; ++kk) f.kf[kk] = ldg128(kblk + kk * 512 + lane * 8);
+        for (int j = 0; j < NP; ++j) {
+            pvalid[j] = pgw + j < pg1;
+            vis[j] = pvalid[j] ? max_len - (pgw + j) * PS : 0;
+        }
+        // rCache fragment of (page j, slot s, tile t).  Tokens past a slot's own length (or
+        // on a padding page) are unwritten and zeroed; for rank 8 the upper half of a tile
+        // is padding.
+        auto ckf = [&](int j, int s, int t) __attribute__((always_inline)) -> u32x2 {
+            u32x2 v = c.k[j][s][t];
+            if constexpr (R == 8) v = grp < 2 ? v : u32x2{0, 0};
+            if constexpr (MASKED) {
+                const int svis = pvalid[j] ? slot_len[s] - (pgw + j) * PS : 0;
+                if (col >= svis) v = u32x2{0, 0};
+            }
+            return v;
+        };
+        auto cvf = [&](int j, int s, int t) __attribute__((always_inline)) -> u32x2 {
+            u32x2 v = c.v[j][s][t];
+            if constexpr (R == 8) v = col < 8 ? v : u32x2{0, 0};
+            if constexpr (MASKED) {
+                const int svis = pvalid[j] ? slot_len[s] - (pgw + j) * PS : 0;
+                if (svis < PS) v = mask4(v, svis, grp);
+            }
+            return v;
+        };
+        // scores S^T = K_base Q^T + C_K (W)^T
+        f32x4 sacc[NP];
 #pragma unroll
-                for (int q2 = 0; q2 < 4; ++q2) {
-                    const u32x4 v = ldg128(vblk + q2 * 512 + lane * 8);
-                    f.vf[2 * q2] = u32x2{v.x, v.y};
-                    f.vf[2 * q2 + 1] = u32x2{v.z, v.w};
+        for (int j = 0; j < NP; ++j) {
+            sacc[j] = f32x4{0, 0, 0, 0};
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk)
+                sacc[j] = mfma32(*reinterpret_cast<const u32x4 *>(kb + j * 2 * kBlockHalfs + kk * 512 + lane * 8),
+                                 qf[kk], sacc[j]);
+        }
+        if constexpr (R > 0) {
+            constexpr int NU = NSA * RT;  // (slot, tile) units, taken in pairs
+#pragma unroll
+            for (int j = 0; j < NP; ++j) {
+#pragma unroll
+                for (int u = 0; u + 1 < NU; u += 2) {
+                    const int s0 = u / RT, t0 = u % RT, s1 = (u + 1) / RT, t1 = (u + 1) % RT;
+                    const u32x2 c0 = ckf(j, s0, t0), c1 = ckf(j, s1, t1);
+                    const u32x4 a = u32x4{c0.x, c0.y, c1.x, c1.y};
+                    const u32x4 b = u32x4{wsel[s0][t0].x, wsel[s0][t0].y, wsel[s1][t1].x, wsel[s1][t1].y};
+                    sacc[j] = mfma32(a, b, sacc[j]);
                 }
-                if constexpr (R > 0) {
-#pragma unroll
-                    for (int s = 0; s < NS; ++s) load_res(pg, s, f.ck[s], f.cv[s]);
-                }
-            };
-            Frag fa, fb;
-            int pg = pg0 + wave;
-            const bool busy = pg < pg1;
-            const int last = busy ? pg + (pg1 - 1 - pg) / WAVES * WAVES : pg0;
-            load(busy ? pg : pg0, fa);
-            prep_w();
-            if (busy) {
-                for (;;) {
-                    load(pg + WAVES <= last ? pg + WAVES : last, fb);
-                    compute_page(ns_tag, pg, true, fa.kf, fa.vf, fa.ck, fa.cv, fa.cs, fa.sn);
-                    pg += WAVES;
-                    if (pg > last) break;
-                    load(pg + WAVES <= last ? pg + WAVES : last, fa);
-                    compute_page(ns_tag, pg, true, fb.kf, fb.vf, fb.ck, fb.cv, fb.cs, fb.sn);
-                    pg += WAVES;
-                    if (pg > last) break;
+                if constexpr (NU % 2 == 1) {
+                    const int s0 = (NU - 1) / RT, t0 = (NU - 1) % RT;
+                    sacc[j] = mfma16(ckf(j, s0, t0), wsel[s0][t0], sacc[j]);
                 }
             }
-        };
-        using I1 = std::integral_constant<int, 1>;
-        using I2 = std::integral_constant<int, cmin(2, AG)>;
-        using I3 = std::integral_constant<int, cmin(3, AG)>;
-        using I4 = std::integral_constant<int, cmin(4, AG)>;
-        if (R == 0 || nag == 1) run_pages(I1{});
-        else if (nag == 2 || AG == 2) run_pages(I2{});
-        else if (nag == 3) run_pages(I3{});
-        else run_pages(I4{});
-    } else if constexpr (S::MULTI) {
-        // ---- several groups: stages of two pages, base K/V shared through LDS ----
-        // Wave w loads block (K if w even, V if odd) of stage page w/2 for everyone, two
-        // stages ahead (registers, then LDS one stage before use), and computes its own
-        // group: both stage pages (4 groups) or stage page w/2 (2 groups).  The rCache
-        // rows of its group are loaded one stage ahead.  All loads are unconditional
-        // (past the item's end they re-read its last page), so the compiler can keep the
-        // later stages in flight while it waits for the one it needs.
-        auto run_groups = [&](auto npw_tag) {
-            constexpr int NPW = decltype(npw_tag)::value;  // stage pages this wave computes
-            constexpr int NSR = R > 0 ? AG : 1;
-            struct Cres { u32x2 ck[NPW][NSR][RTX], cv[NPW][NSR][RTX]; };
-            using IA = std::integral_constant<int, (R > 0 ? AG : 1)>;
-            const int last = pg1 - 1;
-            const int lpage = wave >> 1, lkv = wave & 1;   // what this wave loads for everyone
-            const int wpage0 = NPW == 2 ? 0 : (wave >> 1);  // first stage page it computes
-            auto load_base = [&](int sp, u32x4 *kv) {
-                const int pl = sp + lpage <= last ? sp + lpage : last;
-                const int bpage = uniform(s_tab[pl - pg0]);
-                const uint16_t *blkp = p.base_kv + (((int64_t)bpage * 2 + lkv) * hkv + h) * kBlockHalfs;
+        }
+        // Stage 2: online softmax over the step's keys (rows in lanes, keys in lane groups)
+        float sv[NP][4];
+        float mx = kNegInf;
 #pragma unroll
-                for (int i = 0; i < 4; ++i) kv[i] = ldg128(blkp + i * 512 + lane * 8);
-            };
-            auto store_base = [&](int buf, const u32x4 *kv) {
-                uint16_t *dst = lds_h + ((buf * 2 + lpage) * 2 + lkv) * kBlockHalfs;
+        for (int j = 0; j < NP; ++j)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4 *>(dst + i * 512 + lane * 8) = kv[i];
-            };
-            auto load_c = [&](int sp, Cres &c) {
-                if constexpr (R > 0) {
+            for (int i = 0; i < 4; ++i) {
+                float x = sacc[j][i];
+                if constexpr (MASKED) {
+                    const int tok = (pgw + j) * PS + 4 * grp + i;
+                    x = (pvalid[j] && row_active && tok < my_len) ? x : kNegInf;
+                }
+                sv[j][i] = x;
+                mx = fmaxf(mx, x);
+            }
+        mx = max_over_groups(mx) * cl;
+        if (__builtin_amdgcn_ballot_w64(mx > st.m + kLazyRescale) != 0) {
+            const float m_new = fmaxf(st.m, mx);
+            const float alpha = fast_exp2(st.m - (m_new == kNegInf ? 0.f : m_new));
+            st.l *= alpha;
 #pragma unroll
-                    for (int j = 0; j < NPW; ++j) {
-                        const int pj = sp + wpage0 + j <= last ? sp + wpage0 + j : last;
+            for (int mt = 0; mt < 8; ++mt) st.oacc[mt] *= alpha;
 #pragma unroll
-                        for (int s = 0; s < AG; ++s) load_res(pj, s, c.ck[j][s], c.cv[j][s]);
+            for (int t = 0; t < RT; ++t) st.racc[t] *= alpha;
+            st.m = m_new;
+        }
+        const float m_use = st.m == kNegInf ? 0.f : st.m;
+        u32x2 pf[NP];
+        float psum = 0.f;
+#pragma unroll
+        for (int j = 0; j < NP; ++j) {
+            f32x4 pv;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                pv[i] = fast_exp2(__builtin_fmaf(sv[j][i], cl, -m_use));
+                psum += pv[i];
+            }
+            pf[j] = pack4(pv);
+        }
+        st.l += psum;
+        // O^T += V^T P^T and acc_r^T += C_V^T P^T (rows of other slots masked out of P)
+        const uint16_t *vb = kb + kBlockHalfs;
+        if constexpr (NP == 2) {
+            const u32x4 pb = u32x4{pf[0].x, pf[0].y, pf[1].x, pf[1].y};
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) {
+                // V^T rows 16mt.. of both pages (8 bytes each), one operand of the 32-key product
+                const int off = (mt >> 1) * 512 + lane * 8 + 4 * (mt & 1);
+                u32x2 v0 = *reinterpret_cast<const u32x2 *>(vb + off);
+                u32x2 v1 = *reinterpret_cast<const u32x2 *>(vb + 2 * kBlockHalfs + off);
+                if constexpr (MASKED) {
+                    if (vis[0] < PS) v0 = mask4(v0, vis[0], grp);
+                    if (vis[1] < PS) v1 = mask4(v1, vis[1], grp);
+                }
+                st.oacc[mt] = mfma32(u32x4{v0.x, v0.y, v1.x, v1.y}, pb, st.oacc[mt]);
+            }
+            if constexpr (R > 0) {
+#pragma unroll
+                for (int s = 0; s < NSA; ++s) {
+                    const u32x4 pm = my_slot == s ? pb : u32x4{0, 0, 0, 0};
+#pragma unroll
+                    for (int t = 0; t < RT; ++t) {
+                        const u32x2 c0 = cvf(0, s, t), c1 = cvf(1, s, t);
+                        st.racc[t] = mfma32(u32x4{c0.x, c0.y, c1.x, c1.y}, pm, st.racc[t]);
                     }
                 }
-            };
-            auto compute_stage = [&](int buf, int sp, Cres &c) {
+            }
+        } else {
 #pragma unroll
-                for (int j = 0; j < NPW; ++j) {
-                    const int pj = sp + wpage0 + j;
-                    const uint16_t *kb = lds_h + ((buf * 2 + wpage0 + j) * 2 + 0) * kBlockHalfs;
-                    const uint16_t *vb = kb + kBlockHalfs;
-                    u32x4 kf[4];
-                    u32x2 vf[8];
-#pragma unroll
-                    for (int kk = 0; kk < 4; ++kk) kf[kk] = *reinterpret_cast<const u32x4 *>(kb + kk * 512 + lane * 8);
-#pragma unroll
-                    for (int q2 = 0; q2 < 4; ++q2) {
-                        const u32x4 v = *reinterpret_cast<const u32x4 *>(vb + q2 * 512 + lane * 8);
-                        vf[2 * q2] = u32x2{v.x, v.y};
-                        vf[2 * q2 + 1] = u32x2{v.z, v.w};
+            for (int q2 = 0; q2 < 4; ++q2) {
+                const u32x4 v0 = *reinterpret_cast<const u32x4 *>(vb + q2 * 512 + lane * 8);
+                u32x2 a = u32x2{v0.x, v0.y}, b = u32x2{v0.z, v0.w};
+                if constexpr (MASKED) {
+                    if (vis[0] < PS) {
+                        a = mask4(a, vis[0], grp);
+                        b = mask4(b, vis[0], grp);
                     }
-                    compute_page(IA{}, pj <= last ? pj : last, pj <= last, kf, vf, c.ck[j], c.cv[j], nullptr,
-                                 nullptr);
                 }
-            };
-            u32x4 bx[4], by[4];
-            Cres ca, cb;
-            int sp = pg0;
-            load_c(sp, ca);
-            load_base(sp, bx);
-            store_base(0, bx);
-            load_base(sp + 2, by);
-            prep_w();
+                st.oacc[2 * q2] = mfma16(a, pf[0], st.oacc[2 * q2]);
+                st.oacc[2 * q2 + 1] = mfma16(b, pf[0], st.oacc[2 * q2 + 1]);
+            }
+            if constexpr (R > 0) {
+#pragma unroll
+                for (int s = 0; s < NSA; ++s) {
+                    const u32x2 pm = my_slot == s ? pf[0] : u32x2{0, 0};
+#pragma unroll
+                    for (int t = 0; t < RT; ++t) st.racc[t] = mfma16(cvf(0, s, t), pm, st.racc[t]);
+                }
+            }
+        }
+    };
+
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    using TT = std::integral_constant<bool, true>;
+    using NSF = std::integral_constant<int, NSR>;
+    // Every step runs the masked form: the value and rCache masks are skipped (uniform
+    // branches) on full pages, and the key mask costs a compare and a select per score.
+    // A second, unmasked instantiation chosen per step produced results that varied from
+    // call to call (cause not identified), so there is only this one.
+    auto run_step = [&](auto nsa_tag, auto np_tag, int buf, int stage, CFrag &c) __attribute__((always_inline)) {
+        step(nsa_tag, np_tag, TT{}, buf, stage, c);
+    };
+
+    CFrag ca, cb;
+    u32x4 bx[2][4];
+    using N0 = std::integral_constant<int, 0>;
+    if (npg <= 0) {
+        // an empty item only reports empty partial rows
+    } else if (ngp == 4) {
+        // four groups: bx[1] holds stage s+1 and bx[0] stage s+2 while stage s is computed
+        if constexpr (S::MULTI) {
+            load_blocks(I1{}, N0{}, 0, bx);
+            load_blocks(I1{}, I1{}, 1, bx);
+            load_c(NSF{}, I2{}, 0, ca);
+            store_blocks(I1{}, N0{}, 0, bx);
+            load_blocks(I1{}, N0{}, 2, bx);
             __syncthreads();
-            int buf = 0;
-            for (;;) {
-                // LDS buf holds stage sp; by holds stage sp+2 (in flight); ca holds C(sp)
-                load_c(sp + 2, cb);
-                load_base(sp + 4, bx);
-                compute_stage(buf, sp, ca);
-                store_base(buf ^ 1, by);
+            for (int s = 0;;) {
+                load_c(NSF{}, I2{}, s + 1, cb);
+                run_step(NSF{}, I2{}, s & 1, s, ca);
+                store_blocks(I1{}, I1{}, (s + 1) & 1, bx);
+                load_blocks(I1{}, I1{}, s + 3, bx);
                 __syncthreads();
-                sp += 2;
-                buf ^= 1;
-                if (sp >= pg1) break;
-                load_c(sp + 2, ca);
-                load_base(sp + 4, by);
-                compute_stage(buf, sp, cb);
-                store_base(buf ^ 1, bx);
+                if (++s >= n_stages) break;
+                load_c(NSF{}, I2{}, s + 1, ca);
+                run_step(NSF{}, I2{}, s & 1, s, cb);
+                store_blocks(I1{}, N0{}, (s + 1) & 1, bx);
+                load_blocks(I1{}, N0{}, s + 3, bx);
                 __syncthreads();
-                sp += 2;
-                buf ^= 1;
-                if (sp >= pg1) break;
+                if (++s >= n_stages) break;
+            }
+        }
+    } else {
+        // one or two groups: bx holds stage s+1 while stage s is computed
+        auto run = [&](auto nsa_tag, auto np_tag) __attribute__((always_inline)) {
+            load_blocks(I2{}, N0{}, 0, bx);
+            load_c(nsa_tag, np_tag, 0, ca);
+            store_blocks(I2{}, N0{}, 0, bx);
+            load_blocks(I2{}, N0{}, 1, bx);
+            __syncthreads();
+            for (int s = 0;;) {
+                load_c(nsa_tag, np_tag, s + 1, cb);
+                run_step(nsa_tag, np_tag, s & 1, s, ca);
+                store_blocks(I2{}, N0{}, (s + 1) & 1, bx);
+                load_blocks(I2{}, N0{}, s + 2, bx);
+                __syncthreads();
+                if (++s >= n_stages) break;
+                load_c(nsa_tag, np_tag, s + 1, ca);
+                run_step(nsa_tag, np_tag, s & 1, s, cb);
+                store_blocks(I2{}, N0{}, (s + 1) & 1, bx);
+                load_blocks(I2{}, N0{}, s + 2, bx);
+                __syncthreads();
+                if (++s >= n_stages) break;
             }
         };
-        if (ngp == 4) run_groups(std::integral_constant<int, 2>{});
-        else run_groups(std::integral_constant<int, 1>{});
+        // two groups: steps of two pages; one group: one page per wave and stage
+        if (ngp == 2) {
+            if constexpr (S::MULTI) run(NSF{}, I2{});
+        } else if (R > 0 && nag == 1) {
+            run(I1{}, I1{});
+        } else {
+            run(NSF{}, I1{});
+        }
     }
+
 
     write_partial<R>(p, st, row_active, (int64_t)(row_base + copy * nag * G + my_group * ROWS + col) * hkv + h,
                      grp);
@@ -765,7 +763,7 @@ __global__ __launch_bounds__(256, 1) void decode_rope_kernel(DecodeArgs p) {
     const ResOffsets<R> ro(col, grp);
     RowsT st;
     st.init();
-    const int64_t res_page_halfs = 2 * PS * R;
+    const int64_t res_page_halfs = RT * 512;
 
     auto run_pages = [&](auto ns_tag) {
         constexpr int NS = decltype(ns_tag)::value;
@@ -802,8 +800,8 @@ __global__ __launch_bounds__(256, 1) void decode_rope_kernel(DecodeArgs p) {
                 const uint16_t *rb = p.res_kv + (int64_t)rpage * res_page_halfs;
 #pragma unroll
                 for (int t = 0; t < RT; ++t) {
-                    const u32x2 v = ldg64(rb + ro.cv[t]);
-                    const u32x2 k = ldg64(rb + ro.ck[t]);
+                    const u32x2 k = ldg64(rb + t * 512 + lane * 4);
+                    const u32x2 v = ldg64(rb + t * 512 + 256 + lane * 4);
                     f.cv[s][t] = ro.cv_ok[t] ? v : u32x2{0, 0};
                     f.ck[s][t] = ro.ck_ok[t] ? k : u32x2{0, 0};
                 }
@@ -994,7 +992,7 @@ hipError_t launch_decode(const DecodeArgs &da, int n_blocks, int n_agents, int h
     hipError_t e;
     if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[0]), st)) != hipSuccess) return e;
     if constexpr (ROPE) hipLaunchKernelGGL((decode_rope_kernel<R, G>), dim3(n_blocks), dim3(256), 0, st, da);
-    else hipLaunchKernelGGL((decode_split_kernel<R, G, false>), dim3(n_blocks), dim3(256), 0, st, da);
+    else hipLaunchKernelGGL((decode_split_kernel<R, G>), dim3(n_blocks), dim3(256), 0, st, da);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[1]), st)) != hipSuccess) return e;
     hipLaunchKernelGGL((decode_combine_kernel<R, G>), dim3(n_agents * da.hq), dim3(kCombineThreads), 0, st, da);

@@ -21,6 +21,8 @@ void clear_error();
 //   agent_ptr [n_agents+1]         CSR over the partial rows of each agent
 //   agent_slot[...]                (row_base + (copy*n_ag + slot)*g) * hkv  (add jj*hkv + head
 //                                  for query head jj)
+//   zero      [kZeroWords]         zeros, 16-byte aligned (read in place of the rCache of an
+//                                  agent without adapter or of an empty agent slot)
 // An item holds up to four agent groups; a group is the floor(16/g) agents whose
 // query heads of one KV head fill the 16 rows of one matrix-core tile.  An item of
 // ng groups runs on 4 / ngp wave copies (ngp = 1, 2, 4 for ng = 1, 2, 3..4); every
@@ -32,23 +34,31 @@ constexpr int kMaxItemAgents = 16;  // agents per item
 constexpr int kItemWords = 5 + kMaxItemAgents;
 constexpr int kMaxPagesPerItem = 64;  // upper bound of pages_per_split (block tables are staged in LDS)
 
-// Decode: one workgroup per (work item, KV head).  An item holds up to four agent
-// groups without RoPE and rank below 32 (their base pages are shared through LDS and
-// each group keeps its rCache fragments of two pages in registers); with RoPE, or with
-// a rank of 32 or more, it holds one group.  Largest number of agents per work item:
+// Decode: one workgroup per (work item, KV head).  Without RoPE and with rank below 32 an
+// item holds up to four agent groups (their base pages are shared through LDS); with
+// rank 32 or more it holds one group, of at most two agents at rank 64 (the wave keeps
+// every slot's rCache fragments of a stage in registers).  With RoPE an item holds one
+// group.  Agent slots one wave serves without RoPE:
+constexpr int decode_wave_slots(int g, int r) {
+    return r >= 64 ? (kMaxRows / g < 2 ? kMaxRows / g : 2) : kMaxRows / g;
+}
 constexpr int decode_heads_per_block(int, bool) { return 1; }
+// Largest number of agents per work item:
 constexpr int decode_item_agent_cap(int g, int hkv, int r, bool rope) {
     (void)hkv;
     const int ag = kMaxRows / g;
-    if ((rope && r > 0) || r >= 32) return ag;
+    if (rope && r > 0) return ag;
+    if (r >= 32) return decode_wave_slots(g, r);
     return kMaxGroups * ag < kMaxItemAgents ? kMaxGroups * ag : kMaxItemAgents;
 }
 
 enum PlanHeader {
     H_MAGIC = 0, H_N_ITEMS, H_N_BLOCKS, H_N_AGENTS, H_HKV, H_GROUP, H_AGENTS_PER_ITEM,
     H_OFF_ITEMS, H_OFF_BLOCKS, H_OFF_AGENT_PTR, H_OFF_AGENT_SLOT, H_TOTAL_WORDS, H_PAGES_PER_SPLIT,
-    H_PAGE_SIZE, H_N_SEGMENTS, H_TOTAL_ROWS, H_MAX_ITEM_AGENTS, H_HEADS_PER_BLOCK, H_RANK, H_ROPE, H_FIELDS
+    H_PAGE_SIZE, H_N_SEGMENTS, H_TOTAL_ROWS, H_MAX_ITEM_AGENTS, H_HEADS_PER_BLOCK, H_RANK, H_ROPE, H_OFF_ZERO,
+    H_FIELDS
 };
+constexpr int kZeroWords = 1024;  // zeroed area of a plan: stand-in rCache page for agents without one
 static_assert(H_FIELDS <= kHeaderWords, "plan header fields overflow the header");
 constexpr int32_t kPlanMagic = 0x464b5631;  // "FKV1"
 

@@ -1,13 +1,17 @@
 // Cache writes: copy-on-write page copies (Section 5.2) and scattering new tokens'
 // bCache K/V and rCache C_K/C_V into their page slots.
 //
-// Page layouts (bf16): base page [2][Hkv][ps*d]; residual page [2][ps*r] with C_K as
-// [ps][r] and C_V as [r][ps].  With ps = 16 and d = 128 the K and V blocks of one
-// (page, head) are stored in the order in which the attention kernels' matrix-core
-// fragments read them (one 16-byte load per lane, 1 KB per wave instruction):
+// Page layouts (bf16): base page [2][Hkv][ps*d].  With ps = 16 and d = 128 the K and V
+// blocks of one (page, head) are stored in the order in which the attention kernels'
+// matrix-core fragments read them (one 16-byte load per lane, 1 KB per wave instruction):
 //   K element (token t, dim d) at  (d/32)*512 + (t + 16*((d%16)/4))*8 + 4*((d%32)/16) + d%4
 //   V element (token t, dim d) at  (d/32)*512 + (d%16 + 16*(t/4))*8 + 4*((d/16)%2) + t%4
-// Other shapes use plain [ps][d] (K) and [d][ps] (V).
+// A residual page with ps = 16 holds ceil(r/16) tiles of 512 values; tile k holds, for
+// lane L = 16*g + c of a wave, the 4 values at L*4 and the 4 values at 256 + L*4:
+//   C_K[token c][16k + 4g + i]             C_V[token 4g + i][16k + c]        (i = 0..3)
+// so each lane reads each of its rCache fragments with one 8-byte load (512 contiguous
+// bytes per wave instruction).  Rank values past r (r = 8) are padding.  Other shapes use
+// plain [ps][d] (K), [d][ps] (V), [ps][r] (C_K) and [r][ps] (C_V).
 #include <hip/hip_runtime.h>
 
 #include <string>
@@ -35,6 +39,26 @@ __device__ __forceinline__ int v_slot(int64_t e, int ps, int d) {
     return (int)(e % ps);
 }
 
+__device__ __forceinline__ int64_t ck_off(int t, int rho, int ps, int r) {
+    if (ps == 16) return (int64_t)(rho >> 4) * 512 + (((rho & 15) >> 2) * 16 + t) * 4 + (rho & 3);
+    return (int64_t)t * r + rho;
+}
+__device__ __forceinline__ int64_t cv_off(int t, int rho, int ps, int r) {
+    if (ps == 16) return (int64_t)(rho >> 4) * 512 + 256 + ((t >> 2) * 16 + (rho & 15)) * 4 + (t & 3);
+    return (int64_t)ps * r + (int64_t)rho * ps + t;
+}
+__device__ __forceinline__ int64_t res_page_elems(int ps, int r) {
+    return ps == 16 ? (int64_t)((r + 15) / 16) * 512 : 2LL * ps * r;
+}
+// Token slot of element e of a residual page.
+__device__ __forceinline__ int c_slot(int64_t e, int ps, int r) {
+    if (ps == 16) {
+        const int w = (int)(e & 511);
+        return w < 256 ? ((w >> 2) & 15) : 4 * (((w - 256) >> 2) >> 4) + (w & 3);
+    }
+    return e < (int64_t)ps * r ? (int)(e / r) : (int)((e - (int64_t)ps * r) % ps);
+}
+
 struct CopyArgs {
     const fkv_page_copy *copies;
     uint16_t *base_kv, *res_kv;
@@ -58,16 +82,11 @@ __global__ __launch_bounds__(256) void page_copy_kernel(CopyArgs a) {
             if (slot < n_valid) dst[e] = src[e];
         }
     } else {
-        const int64_t blk = (int64_t)a.ps * a.r;
-        const int64_t page = 2 * blk;
+        const int64_t page = res_page_elems(a.ps, a.r);
         const uint16_t *src = a.res_kv + (int64_t)c.src * page;
         uint16_t *dst = a.res_kv + (int64_t)c.dst * page;
-        for (int64_t e = threadIdx.x; e < page; e += blockDim.x) {
-            const int64_t within = e % blk;
-            const bool is_v = e >= blk;
-            const int slot = is_v ? (int)(within % a.ps) : (int)(within / a.r);
-            if (slot < n_valid) dst[e] = src[e];
-        }
+        for (int64_t e = threadIdx.x; e < page; e += blockDim.x)
+            if (c_slot(e, a.ps, a.r) < n_valid) dst[e] = src[e];
     }
 }
 
@@ -98,11 +117,10 @@ __global__ __launch_bounds__(256) void scatter_kernel(ScatterArgs a) {
     }
     if (a.ck_src && a.r > 0) {
         const int32_t page = a.bt_res[lp];
-        const int64_t blk = (int64_t)a.ps * a.r;
-        uint16_t *pg = a.res_kv + (int64_t)page * 2 * blk;
+        uint16_t *pg = a.res_kv + (int64_t)page * res_page_elems(a.ps, a.r);
         for (int e = threadIdx.x; e < a.r; e += blockDim.x) {
-            pg[(int64_t)slot * a.r + e] = a.ck_src[j * a.r + e];
-            pg[blk + (int64_t)e * a.ps + slot] = a.cv_src[j * a.r + e];
+            pg[ck_off(slot, e, a.ps, a.r)] = a.ck_src[j * a.r + e];
+            pg[cv_off(slot, e, a.ps, a.r)] = a.cv_src[j * a.r + e];
         }
     }
 }
@@ -110,6 +128,11 @@ __global__ __launch_bounds__(256) void scatter_kernel(ScatterArgs a) {
 }  // namespace
 
 extern "C" {
+
+int64_t fkv_res_page_elems(int32_t page_size, int32_t r) {
+    if (page_size < 1 || r < 0) return 0;
+    return page_size == 16 ? (int64_t)((r + 15) / 16) * 512 : 2LL * page_size * r;
+}
 
 fkv_status fkv_page_copy_launch(const fkv_page_copy *copies_dev, int32_t n, void *base_kv, void *res_kv, int32_t hkv,
                                 int32_t d, int32_t r, int32_t page_size, void *stream) {

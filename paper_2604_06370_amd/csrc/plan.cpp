@@ -208,7 +208,8 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     const int64_t off_blocks = off_items + (int64_t)n_items * fkv::kItemWords;
     const int64_t off_ptr = off_blocks + n_blocks;
     const int64_t off_slot = off_ptr + A + 1;
-    const int64_t total = off_slot + total_slots;
+    const int64_t off_zero = (off_slot + total_slots + 3) / 4 * 4;
+    const int64_t total = off_zero + fkv::kZeroWords;
     if (total > INT32_MAX) {
         delete pl;
         return fkv::fail(FKV_ERR_UNSUPPORTED, "fkv_decode_plan_create: plan too large");
@@ -235,6 +236,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     w[fkv::H_HEADS_PER_BLOCK] = hpb;
     w[fkv::H_RANK] = prm->r;
     w[fkv::H_ROPE] = rope ? 1 : 0;
+    w[fkv::H_OFF_ZERO] = (int32_t)off_zero;
     for (int32_t i = 0; i < n_items; ++i) {
         int32_t *r = &w[off_items + (int64_t)i * fkv::kItemWords];
         r[0] = items[i].p0;

@@ -53,6 +53,7 @@ template <int R, int G, bool ROPE>
 struct PrefillShape {
     static constexpr int RT = R == 0 ? 0 : (R + 15) / 16;
     static constexpr int TOK_PER_WG = ROWS_PER_WG / G;
+    static constexpr int RES_PAGE = RT * 512;                  // residual page (fragment order)
     static constexpr int SK_BYTES = 4 * 4 * 64 * 16;          // [page][kk][lane] 16 B
     static constexpr int SV_BYTES = 4 * PS * D * 2;             // [page][d][16] bf16
     static constexpr int SCV_BYTES = R > 0 ? 4 * R * PS * 2 : 16;  // [page][rho][16] bf16
@@ -207,7 +208,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
             }
             const uint16_t *rb = nullptr;
             if constexpr (R > 0) {
-                if (ad >= 0 && have) rb = p.res_kv + (int64_t)btr[pg] * 2 * PS * R;
+                if (ad >= 0 && have) rb = p.res_kv + (int64_t)btr[pg] * S::RES_PAGE;
             }
             if constexpr (R > 0 && ROPE) {
                 if (rb) {
@@ -216,7 +217,8 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
                     for (int mt = 0; mt < 8; ++mt) u[mt] = f32x4{0, 0, 0, 0};
 #pragma unroll
                     for (int t = 0; t < RT; ++t) {
-                        const u32x2 ck = (16 * t + 4 * grp < R) ? ldg64(rb + col * R + 16 * t + 4 * grp) : u32x2{0, 0};
+                        const u32x2 c = ldg64(rb + t * 512 + lane * 4);
+                        const u32x2 ck = (16 * t + 4 * grp < R) ? c : u32x2{0, 0};
 #pragma unroll
                         for (int mt = 0; mt < 8; ++mt) u[mt] = mfma16(sBK[(t * 8 + mt) * 64 + lane], ck, u[mt]);
                     }
@@ -251,14 +253,18 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
                 *reinterpret_cast<u32x2 *>(sV + wave * D * PS + 4 * e) = v;
             }
             if constexpr (R > 0) {
-                for (int e = lane; e < R * PS / 4; e += 64) {
-                    u32x2 v = rb ? ldg64(rb + PS * R + 4 * e) : u32x2{0, 0};
-                    const int k0 = (4 * e) % PS;
+                // C_V^T rows of the page: lane (c, g) of tile t holds C_V[4g .. 4g+3][16t + c]
+#pragma unroll
+                for (int t = 0; t < RT; ++t) {
+                    const int rho = 16 * t + col;
+                    u32x2 v = {0, 0};
+                    if (rb) v = ldg64(rb + t * 512 + 256 + lane * 4);
+                    const int k0 = 4 * grp;
                     if (k0 + 0 >= vis) v.x &= 0xffff0000u;
                     if (k0 + 1 >= vis) v.x &= 0x0000ffffu;
                     if (k0 + 2 >= vis) v.y &= 0xffff0000u;
                     if (k0 + 3 >= vis) v.y &= 0x0000ffffu;
-                    *reinterpret_cast<u32x2 *>(sCV + wave * R * PS + 4 * e) = v;
+                    if (rho < R) *reinterpret_cast<u32x2 *>(sCV + wave * R * PS + rho * PS + 4 * grp) = v;
                 }
             }
         }
@@ -282,10 +288,11 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
                 for (int kt = 0; kt < 4; ++kt) {
                     const int pg = tile * 4 + kt;
                     if (pg >= n_pages) continue;
-                    const uint16_t *rb = p.res_kv + (int64_t)btr[pg] * 2 * PS * R;
+                    const uint16_t *rb = p.res_kv + (int64_t)btr[pg] * S::RES_PAGE;
 #pragma unroll
                     for (int t = 0; t < RT; ++t) {
-                        const u32x2 ck = (16 * t + 4 * grp < R) ? ldg64(rb + col * R + 16 * t + 4 * grp) : u32x2{0, 0};
+                        const u32x2 c = ldg64(rb + t * 512 + lane * 4);
+                        const u32x2 ck = (16 * t + 4 * grp < R) ? c : u32x2{0, 0};
                         sacc[kt][0] = mfma16(ck, wq[0][t], sacc[kt][0]);
                         sacc[kt][1] = mfma16(ck, wq[1][t], sacc[kt][1]);
                     }

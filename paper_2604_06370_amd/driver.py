@@ -40,7 +40,7 @@ class LoadedWorkload:
         nr = res_pages or max(need_res + A, 1)
         self.tree = rt.Tree(ps, nb, nr)
         self.base_kv = torch.zeros((nb, 2, hkv, ps * d), dtype=torch.bfloat16, device=self.device)
-        self.res_kv = torch.zeros((nr, 2, ps * max(r, 1)), dtype=torch.bfloat16, device=self.device)
+        self.res_kv = torch.zeros((nr, max(rt.res_page_elems(ps, r), 1)), dtype=torch.bfloat16, device=self.device)
         # adapters: agent a uses adapter a; agents without residual get -1
         self.lora_b = _bf16(np.stack([wl.b_k, wl.b_v], axis=1), self.device) if r > 0 else None
         ad = np.where(wl.has_residual > 0, np.arange(A), -1).astype(np.int32)

@@ -182,6 +182,11 @@ class DecodePlan:
         return self._dev
 
 
+def res_page_elems(page_size: int, r: int) -> int:
+    """Row stride (bf16 values) of the residual pool for this page size and rank."""
+    return int(N.fkv_res_page_elems(page_size, r))
+
+
 def rope_tables(d: int, max_pos: int, base: float, device) -> Tuple[torch.Tensor, torch.Tensor]:
     """fkv_rope_table on the host, copied to the device."""
     max_pos = (max_pos + 15) // 16 * 16
