@@ -284,9 +284,13 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
     const int qh = h * G + (col % G);
     const int64_t n = (int64_t)hkv * D;
 
+    // longest sequence of the item: value tokens past it are never read by any row and
+    // are zeroed when a stage is stored (they may hold any bits)
+    int item_max_len = 0;
+    for (int i = 0; i < nag; ++i) item_max_len = max(item_max_len, p.seq_lens[item_agents[i]]);
     // per slot of the wave's group: adapter (or -1) and sequence length
     int slot_ad[NSR], slot_len[NSR];
-    int max_len = 0;
+    int max_len = 0, min_res = 1 << 30;  // min_res: shortest rCache among the group's slots
 #pragma unroll
     for (int s = 0; s < NSR; ++s) {
         const bool ok = sb + s < nag && s < NSW;
@@ -295,6 +299,7 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
         slot_ad[s] = (ok && R > 0) ? p.adapter_idx[ag_id] : -1;
         slot_len[s] = len;
         if (ok) max_len = max(max_len, len);
+        if (ok && slot_ad[s] >= 0) min_res = min(min_res, len);
     }
     const int my_len = row_active ? p.seq_lens[my_agent] : 0;
 
@@ -385,11 +390,24 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
             for (int i = 0; i < 4; ++i) bx[FIRST + j][i] = ldg128(src + i * 512 + lane * 8);
         }
     };
-    auto store_blocks = [&](auto nb_tag, auto first_tag, int buf, const u32x4 (&bx)[2][4]) __attribute__((always_inline)) {
+    auto store_blocks = [&](auto nb_tag, auto first_tag, int buf, int stage, u32x4 (&bx)[2][4]) __attribute__((always_inline)) {
         constexpr int NB = decltype(nb_tag)::value, FIRST = decltype(first_tag)::value;
+        const int stc = min(stage, n_stages - 1);
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
             const int b = wave * NB + j;
+            if (b & 1) {  // a V block: zero the tokens past the item's longest sequence
+                const int pl = min(pg0 + stc * sp + (b >> 1), pg1 - 1);
+                const int vis = item_max_len - pl * PS;
+                if (vis < PS) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const u32x2 lo = mask4(u32x2{bx[FIRST + j][i].x, bx[FIRST + j][i].y}, vis, grp);
+                        const u32x2 hi = mask4(u32x2{bx[FIRST + j][i].z, bx[FIRST + j][i].w}, vis, grp);
+                        bx[FIRST + j][i] = u32x4{lo.x, lo.y, hi.x, hi.y};
+                    }
+                }
+            }
             uint16_t *dst = ring + buf * buf_halfs + b * kBlockHalfs;
 #pragma unroll
             for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4 *>(dst + i * 512 + lane * 8) = bx[FIRST + j][i];
@@ -421,38 +439,40 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
     };
 
     // ---- one step: NP pages starting at stage page wp of LDS buffer buf ----
-    auto step = [&](auto nsa_tag, auto np_tag, auto masked_tag, int buf, int stage, CFrag &c) __attribute__((always_inline)) {
+    auto step = [&](auto nsa_tag, auto np_tag, int buf, int stage, CFrag &c) __attribute__((always_inline)) {
         constexpr int NSA = decltype(nsa_tag)::value;
         constexpr int NP = decltype(np_tag)::value;
-        constexpr bool MASKED = decltype(masked_tag)::value;
         const int pgw = pg0 + stage * sp + wpage0;         // logical page of step page 0
         const uint16_t *kb = ring + buf * buf_halfs + wpage0 * 2 * kBlockHalfs;
-        int vis[NP];
         bool pvalid[NP];
 #pragma unroll
-        for (int j = 0; j < NP; ++j) {
-            pvalid[j] = pgw + j < pg1;
-            vis[j] = pvalid[j] ? max_len - (pgw + j) * PS : 0;
-        }
-        // rCache fragment of (page j, slot s, tile t).  Tokens past a slot's own length (or
-        // on a padding page) are unwritten and zeroed; for rank 8 the upper half of a tile
-        // is padding.
-        auto ckf = [&](int j, int s, int t) __attribute__((always_inline)) -> u32x2 {
-            u32x2 v = c.k[j][s][t];
-            if constexpr (R == 8) v = grp < 2 ? v : u32x2{0, 0};
-            if constexpr (MASKED) {
-                const int svis = pvalid[j] ? slot_len[s] - (pgw + j) * PS : 0;
-                if (col >= svis) v = u32x2{0, 0};
+        for (int j = 0; j < NP; ++j) pvalid[j] = pgw + j < pg1;
+        // rCache tokens past a slot's own length, or on a padding page, are unwritten: zero
+        // them (one uniform branch; pages inside every rCache of the group skip it)
+        if constexpr (R > 0) {
+            if (!pvalid[NP - 1] || (pgw + NP) * PS > min_res) {
+#pragma unroll
+                for (int j = 0; j < NP; ++j)
+#pragma unroll
+                    for (int s = 0; s < NSA; ++s) {
+                        const int svis = pvalid[j] ? slot_len[s] - (pgw + j) * PS : 0;
+#pragma unroll
+                        for (int t = 0; t < RT; ++t) {
+                            c.k[j][s][t] = col < svis ? c.k[j][s][t] : u32x2{0, 0};
+                            c.v[j][s][t] = mask4(c.v[j][s][t], svis, grp);
+                        }
+                    }
             }
+        }
+        // rCache fragment of (page j, slot s, tile t); for rank 8 half of a tile is padding
+        auto ckf = [&](int j, int s, int t) __attribute__((always_inline)) -> u32x2 {
+            const u32x2 v = c.k[j][s][t];
+            if constexpr (R == 8) return grp < 2 ? v : u32x2{0, 0};
             return v;
         };
         auto cvf = [&](int j, int s, int t) __attribute__((always_inline)) -> u32x2 {
-            u32x2 v = c.v[j][s][t];
-            if constexpr (R == 8) v = col < 8 ? v : u32x2{0, 0};
-            if constexpr (MASKED) {
-                const int svis = pvalid[j] ? slot_len[s] - (pgw + j) * PS : 0;
-                if (svis < PS) v = mask4(v, svis, grp);
-            }
+            const u32x2 v = c.v[j][s][t];
+            if constexpr (R == 8) return col < 8 ? v : u32x2{0, 0};
             return v;
         };
         // scores S^T = K_base Q^T + C_K (W)^T
@@ -478,8 +498,12 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
                     sacc[j] = mfma32(a, b, sacc[j]);
                 }
                 if constexpr (NU % 2 == 1) {
+                    // the last unit alone, zero-padded: a chain that accumulates into one
+                    // tile stays on the 16x16x32 form (a 16x16x16 product issued right after
+                    // a 16x16x32 one onto the same accumulator read a stale value here)
                     const int s0 = (NU - 1) / RT, t0 = (NU - 1) % RT;
-                    sacc[j] = mfma16(ckf(j, s0, t0), wsel[s0][t0], sacc[j]);
+                    const u32x2 c0 = ckf(j, s0, t0);
+                    sacc[j] = mfma32(u32x4{c0.x, c0.y, 0u, 0u}, u32x4{wsel[s0][t0].x, wsel[s0][t0].y, 0u, 0u}, sacc[j]);
                 }
             }
         }
@@ -487,17 +511,16 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
         float sv[NP][4];
         float mx = kNegInf;
 #pragma unroll
-        for (int j = 0; j < NP; ++j)
+        for (int j = 0; j < NP; ++j) {
+            // keys 4grp + i of page j are visible to this lane's row when i < kv
+            const int kv = (pvalid[j] && row_active) ? my_len - (pgw + j) * PS - 4 * grp : 0;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                float x = sacc[j][i];
-                if constexpr (MASKED) {
-                    const int tok = (pgw + j) * PS + 4 * grp + i;
-                    x = (pvalid[j] && row_active && tok < my_len) ? x : kNegInf;
-                }
+                const float x = i < kv ? sacc[j][i] : kNegInf;
                 sv[j][i] = x;
                 mx = fmaxf(mx, x);
             }
+        }
         mx = max_over_groups(mx) * cl;
         if (__builtin_amdgcn_ballot_w64(mx > st.m + kLazyRescale) != 0) {
             const float m_new = fmaxf(st.m, mx);
@@ -531,12 +554,8 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
             for (int mt = 0; mt < 8; ++mt) {
                 // V^T rows 16mt.. of both pages (8 bytes each), one operand of the 32-key product
                 const int off = (mt >> 1) * 512 + lane * 8 + 4 * (mt & 1);
-                u32x2 v0 = *reinterpret_cast<const u32x2 *>(vb + off);
-                u32x2 v1 = *reinterpret_cast<const u32x2 *>(vb + 2 * kBlockHalfs + off);
-                if constexpr (MASKED) {
-                    if (vis[0] < PS) v0 = mask4(v0, vis[0], grp);
-                    if (vis[1] < PS) v1 = mask4(v1, vis[1], grp);
-                }
+                const u32x2 v0 = *reinterpret_cast<const u32x2 *>(vb + off);
+                const u32x2 v1 = *reinterpret_cast<const u32x2 *>(vb + 2 * kBlockHalfs + off);
                 st.oacc[mt] = mfma32(u32x4{v0.x, v0.y, v1.x, v1.y}, pb, st.oacc[mt]);
             }
             if constexpr (R > 0) {
@@ -554,13 +573,7 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
 #pragma unroll
             for (int q2 = 0; q2 < 4; ++q2) {
                 const u32x4 v0 = *reinterpret_cast<const u32x4 *>(vb + q2 * 512 + lane * 8);
-                u32x2 a = u32x2{v0.x, v0.y}, b = u32x2{v0.z, v0.w};
-                if constexpr (MASKED) {
-                    if (vis[0] < PS) {
-                        a = mask4(a, vis[0], grp);
-                        b = mask4(b, vis[0], grp);
-                    }
-                }
+                const u32x2 a = u32x2{v0.x, v0.y}, b = u32x2{v0.z, v0.w};
                 st.oacc[2 * q2] = mfma16(a, pf[0], st.oacc[2 * q2]);
                 st.oacc[2 * q2 + 1] = mfma16(b, pf[0], st.oacc[2 * q2 + 1]);
             }
@@ -577,14 +590,9 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
 
     using I1 = std::integral_constant<int, 1>;
     using I2 = std::integral_constant<int, 2>;
-    using TT = std::integral_constant<bool, true>;
     using NSF = std::integral_constant<int, NSR>;
-    // Every step runs the masked form: the value and rCache masks are skipped (uniform
-    // branches) on full pages, and the key mask costs a compare and a select per score.
-    // A second, unmasked instantiation chosen per step produced results that varied from
-    // call to call (cause not identified), so there is only this one.
     auto run_step = [&](auto nsa_tag, auto np_tag, int buf, int stage, CFrag &c) __attribute__((always_inline)) {
-        step(nsa_tag, np_tag, TT{}, buf, stage, c);
+        step(nsa_tag, np_tag, buf, stage, c);
     };
 
     CFrag ca, cb;
@@ -598,19 +606,19 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
             load_blocks(I1{}, N0{}, 0, bx);
             load_blocks(I1{}, I1{}, 1, bx);
             load_c(NSF{}, I2{}, 0, ca);
-            store_blocks(I1{}, N0{}, 0, bx);
+            store_blocks(I1{}, N0{}, 0, 0, bx);
             load_blocks(I1{}, N0{}, 2, bx);
             __syncthreads();
             for (int s = 0;;) {
                 load_c(NSF{}, I2{}, s + 1, cb);
                 run_step(NSF{}, I2{}, s & 1, s, ca);
-                store_blocks(I1{}, I1{}, (s + 1) & 1, bx);
+                store_blocks(I1{}, I1{}, (s + 1) & 1, s + 1, bx);
                 load_blocks(I1{}, I1{}, s + 3, bx);
                 __syncthreads();
                 if (++s >= n_stages) break;
                 load_c(NSF{}, I2{}, s + 1, ca);
                 run_step(NSF{}, I2{}, s & 1, s, cb);
-                store_blocks(I1{}, N0{}, (s + 1) & 1, bx);
+                store_blocks(I1{}, N0{}, (s + 1) & 1, s + 1, bx);
                 load_blocks(I1{}, N0{}, s + 3, bx);
                 __syncthreads();
                 if (++s >= n_stages) break;
@@ -621,19 +629,19 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
         auto run = [&](auto nsa_tag, auto np_tag) __attribute__((always_inline)) {
             load_blocks(I2{}, N0{}, 0, bx);
             load_c(nsa_tag, np_tag, 0, ca);
-            store_blocks(I2{}, N0{}, 0, bx);
+            store_blocks(I2{}, N0{}, 0, 0, bx);
             load_blocks(I2{}, N0{}, 1, bx);
             __syncthreads();
             for (int s = 0;;) {
                 load_c(nsa_tag, np_tag, s + 1, cb);
                 run_step(nsa_tag, np_tag, s & 1, s, ca);
-                store_blocks(I2{}, N0{}, (s + 1) & 1, bx);
+                store_blocks(I2{}, N0{}, (s + 1) & 1, s + 1, bx);
                 load_blocks(I2{}, N0{}, s + 2, bx);
                 __syncthreads();
                 if (++s >= n_stages) break;
                 load_c(nsa_tag, np_tag, s + 1, ca);
                 run_step(nsa_tag, np_tag, s & 1, s, cb);
-                store_blocks(I2{}, N0{}, (s + 1) & 1, bx);
+                store_blocks(I2{}, N0{}, (s + 1) & 1, s + 1, bx);
                 load_blocks(I2{}, N0{}, s + 2, bx);
                 __syncthreads();
                 if (++s >= n_stages) break;

@@ -293,8 +293,11 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
                     for (int t = 0; t < RT; ++t) {
                         const u32x2 c = ldg64(rb + t * 512 + lane * 4);
                         const u32x2 ck = (16 * t + 4 * grp < R) ? c : u32x2{0, 0};
-                        sacc[kt][0] = mfma16(ck, wq[0][t], sacc[kt][0]);
-                        sacc[kt][1] = mfma16(ck, wq[1][t], sacc[kt][1]);
+                        // zero-padded 16x16x32 form: the accumulator chain stays on one
+                        // instruction form (see the decode kernel)
+                        const u32x4 a = u32x4{ck.x, ck.y, 0u, 0u};
+                        sacc[kt][0] = mfma32(a, u32x4{wq[0][t].x, wq[0][t].y, 0u, 0u}, sacc[kt][0]);
+                        sacc[kt][1] = mfma32(a, u32x4{wq[1][t].x, wq[1][t].y, 0u, 0u}, sacc[kt][1]);
                     }
                 }
             }
