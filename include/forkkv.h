@@ -38,10 +38,10 @@
  *              fkv_scatter_tokens writes this order; other shapes use K [ps][d], V [d][ps].
  *   res pool   [num_res_pages][fkv_res_page_elems(ps, r)] bf16.  For ps = 16 a page
  *              holds ceil(r/16) tiles of 512 values in fragment order: for L = 16*g + c
- *              (0 <= L < 64) tile k holds C_K[token c][16k + 4g + i] at L*4 + i and
- *              C_V[token 4g + i][16k + c] at 256 + L*4 + i (i < 4), so each lane of a
- *              wave reads each of its rCache fragments with one 8-byte load (for r = 8
- *              half of a tile is padding).  Other page sizes: C_K as [ps][r], then C_V as
+ *              (0 <= L < 64) tile k holds C_K[token c][16k + 4g + i] at L*8 + i and
+ *              C_V[token 4g + i][16k + c] at L*8 + 4 + i (i < 4), so each lane of a
+ *              wave reads both of its rCache fragments of a tile with one 16-byte load
+ *              (for r = 8 half of a tile is padding).  Other page sizes: C_K as [ps][r], then C_V as
  *              [r][ps].
  *   adapters   [n_adapters][2][r][Hkv*d] bf16: B_K then B_V, each the r x n
  *              up-projection of Eq. 1 in row-major order (n = Hkv*d); KV head h

@@ -47,6 +47,9 @@ constexpr float kNegInf = -INFINITY;
 constexpr int kMaxPagesPerItem = fkv::kMaxPagesPerItem;
 constexpr int kBlockHalfs = PS * D;  // bf16 values in one (page, K|V, head) block
 constexpr int kBlockBytes = kBlockHalfs * 2;
+// Page-table rows staged in LDS run this many entries past an item's last page (loads
+// issued up to three stages ahead of the step being computed stay inside the table).
+constexpr int kTablePad = 12;
 
 struct DecodeArgs {
     const uint16_t *q, *base_kv, *res_kv, *lora_b;
@@ -56,6 +59,7 @@ struct DecodeArgs {
     float *ws;
     uint16_t *out;
     int32_t hq, hkv, max_pages, ws_stride;
+    int32_t off_items, off_blocks, off_ptr, off_slot, off_zero;  // plan section offsets (words)
     float scale_log2;  // softmax scale * log2(e)
 };
 
@@ -236,36 +240,43 @@ struct SplitShape {
     static constexpr int NSW = fkv::decode_wave_slots(G, R);                    // agent slots per wave
     static constexpr int NSR = R > 0 ? NSW : 1;
     static constexpr int MAX_SLOTS = MULTI ? cmin(fkv::kMaxGroups * AG, fkv::kMaxItemAgents) : NSW;
+    static constexpr int RES_SLOTS = R > 0 ? MAX_SLOTS : 0;                     // rCache table row stride
     static constexpr int RES_PAGE = RT * 512;                                   // rCache page (halfs)
     static constexpr int RING_BYTES = 8 * 2 * kBlockHalfs * 2;                  // two buffers of four pages
-    static constexpr int TABLE_WORDS = (1 + (R > 0 ? MAX_SLOTS : 0)) * kMaxPagesPerItem;
-    static constexpr int LDS_BYTES = RING_BYTES + TABLE_WORDS * 4;
+    static constexpr int TP = kMaxPagesPerItem + kTablePad;                     // table entries per page row
+    static constexpr int TABLE_BYTES = TP * (1 + RES_SLOTS) * 8;
+    static constexpr int LDS_BYTES = RING_BYTES + TABLE_BYTES;
 };
 
 template <int R, int G>
-__global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
+__global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(DecodeArgs p) {
     using S = SplitShape<R, G>;
     constexpr int AG = S::AG;
     constexpr int RT = S::RT;
     constexpr int RTX = S::RTX;
     constexpr int NSW = S::NSW;
     constexpr int NSR = S::NSR;
-    struct CFrag {  // rCache fragments of the wave's slots for the (up to two) pages of a step
-        u32x2 k[2][NSR][RTX], v[2][NSR][RTX];
+    constexpr int RS = S::RES_SLOTS;
+    struct CFrag {  // rCache fragments (C_K in .xy, C_V in .zw) of the wave's slots for its step pages
+        u32x4 kv[2][NSR][RTX];
     };
     __shared__ __attribute__((aligned(16))) unsigned char lds[S::LDS_BYTES];
     uint16_t *ring = reinterpret_cast<uint16_t *>(lds);
-    int32_t *s_tab = reinterpret_cast<int32_t *>(lds + S::RING_BYTES);
+    // page tables as device addresses: the K block of (page, head h) for the base pool, and
+    // per page the rCache page of every item slot ([page][slot]; the zero area of the plan
+    // for slots without an adapter and for empty slots).  Rows run kTablePad entries past
+    // the item, repeating its last page, so that loads issued ahead of the end stay valid.
+    uint64_t *s_base = reinterpret_cast<uint64_t *>(lds + S::RING_BYTES);
+    uint64_t *s_res = s_base + S::TP;
 
     const int32_t *plan = p.plan;
-    const int blk = plan[plan[fkv::H_OFF_BLOCKS] + blockIdx.x];
+    const int blk = plan[p.off_blocks + blockIdx.x];
     if (blk < 0) return;
     const int hkv = p.hkv;
     const int item = blk / hkv;
     const int h = blk - item * hkv;
-    const int32_t *rec = plan + plan[fkv::H_OFF_ITEMS] + item * fkv::kItemWords;
+    const int32_t *rec = plan + p.off_items + item * fkv::kItemWords;
     const int pg0 = rec[0], pg1 = rec[1], leader = rec[2], nag = rec[3], row_base = rec[4];
-    const int32_t *item_agents = rec + 5;
     const int ng = (nag + AG - 1) / AG;
     if (pg1 - pg0 > kMaxPagesPerItem || nag > S::MAX_SLOTS || (ng > 1 && !S::MULTI) || (ng == 1 && nag > NSW))
         return;  // rejected on the host
@@ -280,49 +291,67 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
     const int sb = my_group * AG;                       // first item slot of this wave's group
     const int my_slot = col / G;                        // this lane's row: slot within the group
     const bool row_active = my_slot < NSW && sb + my_slot < nag;
-    const int my_agent = row_active ? item_agents[sb + my_slot] : 0;
     const int qh = h * G + (col % G);
     const int64_t n = (int64_t)hkv * D;
 
+    // lane i < nag of every wave holds item agent i: id, sequence length, adapter (one
+    // round of parallel loads instead of a chain per agent)
+    const bool lane_ag = lane < nag;
+    const int l_agent = lane_ag ? rec[5 + lane] : 0;
+    const int l_len = lane_ag ? p.seq_lens[l_agent] : 0;
+    const int l_ad = (R > 0 && lane_ag) ? p.adapter_idx[l_agent] : -1;
+
+    // block-table entries of the item's pages: issued now, written to LDS once the
+    // adapters are known.  Wave w stages rows w, w+4, ... (row 0: base pool of the
+    // leader; row 1+s: rCache pool of item slot s), lane i entry i and 64 + i.
+    const int npg = pg1 - pg0;
+    const int ntp = npg + kTablePad;
+    const int n_rows = 1 + (R > 0 ? (S::MULTI ? ngp * AG : NSW) : 0);
+    constexpr int RPW = (1 + RS + WAVES - 1) / WAVES;
+    int32_t pid[RPW][2];
+#pragma unroll
+    for (int k = 0; k < RPW; ++k) {
+        const int t = wave + k * WAVES;
+        const int ag_t = __builtin_amdgcn_readlane(l_agent, t > 0 ? (t - 1) & 63 : 0);
+        const int32_t *row = t == 0 ? p.base_bt + (int64_t)leader * p.max_pages
+                                    : p.res_bt + (int64_t)ag_t * p.max_pages;
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const int i = lane + 64 * u;
+            pid[k][u] = (t < n_rows && i < ntp && npg > 0) ? row[pg0 + min(i, npg - 1)] : 0;
+        }
+    }
+
     // longest sequence of the item: value tokens past it are never read by any row and
     // are zeroed when a stage is stored (they may hold any bits)
-    int item_max_len = 0;
-    for (int i = 0; i < nag; ++i) item_max_len = max(item_max_len, p.seq_lens[item_agents[i]]);
+    int item_max_len = l_len;
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) item_max_len = max(item_max_len, __shfl_xor(item_max_len, o));
+    item_max_len = uniform(item_max_len);
     // per slot of the wave's group: adapter (or -1) and sequence length
     int slot_ad[NSR], slot_len[NSR];
-    int max_len = 0, min_res = 1 << 30;  // min_res: shortest rCache among the group's slots
+    int min_len = 1 << 30, min_res = 1 << 30;  // shortest sequence / rCache among the group's slots
 #pragma unroll
     for (int s = 0; s < NSR; ++s) {
         const bool ok = sb + s < nag && s < NSW;
-        const int ag_id = ok ? item_agents[sb + s] : 0;
-        const int len = ok ? p.seq_lens[ag_id] : 0;
-        slot_ad[s] = (ok && R > 0) ? p.adapter_idx[ag_id] : -1;
-        slot_len[s] = len;
-        if (ok) max_len = max(max_len, len);
+        const int ad = __builtin_amdgcn_readlane(l_ad, (sb + s) & 63);
+        const int len = __builtin_amdgcn_readlane(l_len, (sb + s) & 63);
+        slot_ad[s] = (ok && R > 0) ? ad : -1;
+        slot_len[s] = ok ? len : 0;
+        if (ok) min_len = min(min_len, len);
         if (ok && slot_ad[s] >= 0) min_res = min(min_res, len);
     }
-    const int my_len = row_active ? p.seq_lens[my_agent] : 0;
+    const int src_lane = (sb + my_slot) & 63;
+    const int sh_agent = __shfl(l_agent, src_lane), sh_len = __shfl(l_len, src_lane);
+    const int my_agent = row_active ? sh_agent : 0;
+    const int my_len = row_active ? sh_len : 0;
 
-    // Q^T fragments (B operand of the 16x16x32 products) and, per slot, the B_K rows this
-    // lane needs for W = B_K q; both only depend on the item record, so they are issued
-    // before the block tables are staged
+    // Q^T fragments (B operand of the 16x16x32 products)
     u32x4 qf[4];
     load_q(p.q + ((int64_t)my_agent * p.hq + qh) * D, row_active, grp, qf);
 
-    // block-table entries of the item's pages, for the base pool and every slot's
-    // residual pool, staged in LDS with one parallel pass
-    const int npg = pg1 - pg0;
-    const int n_tab = R > 0 ? 1 + nag : 1;
-    for (int idx = threadIdx.x; idx < n_tab * npg; idx += 256) {
-        const int t = idx / npg, i = idx - t * npg;
-        const int32_t *row = t == 0 ? p.base_bt + (int64_t)leader * p.max_pages
-                                    : p.res_bt + (int64_t)item_agents[t - 1] * p.max_pages;
-        s_tab[t * kMaxPagesPerItem + i] = row[pg0 + i];
-    }
-
     // B_K rows of every slot for W = B_K q (lane holds B_K[16t + col][the head-dim slots of
-    // k-step kk]); issued before the block-table loads, so they have landed by the time the
-    // tables are staged
+    // k-step kk])
     u32x4 bkf[NSR][RTX][4];
     if constexpr (R > 0) {
 #pragma unroll
@@ -345,25 +374,43 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
             }
         }
     }
+
+    // page tables -> LDS, as addresses
+    const uint16_t *zero_c = reinterpret_cast<const uint16_t *>(plan + p.off_zero);
+#pragma unroll
+    for (int k = 0; k < RPW; ++k) {
+        const int t = wave + k * WAVES;
+        const int ad_t = __builtin_amdgcn_readlane(l_ad, t > 0 ? (t - 1) & 63 : 0);
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const int i = lane + 64 * u;
+            if (t < n_rows && i < ntp) {
+                if (t == 0) {
+                    s_base[i] = reinterpret_cast<uint64_t>(p.base_kv + ((int64_t)pid[k][u] * 2 * hkv + h) * kBlockHalfs);
+                } else {
+                    const uint16_t *a = (t - 1 < nag && ad_t >= 0) ? p.res_kv + (int64_t)pid[k][u] * S::RES_PAGE : zero_c;
+                    s_res[i * RS + (t - 1)] = reinterpret_cast<uint64_t>(a);
+                }
+            }
+        }
+    }
+
     // W^T = (B_K q)^T per slot, as the B operand of the residual key products; row
     // columns of other slots are zero, so one product serves a pair of slots (or tiles)
     u32x2 wsel[NSR][RTX];
-    auto finish_w = [&]() __attribute__((always_inline)) {
 #pragma unroll
-        for (int s = 0; s < NSR; ++s)
+    for (int s = 0; s < NSR; ++s)
 #pragma unroll
-            for (int t = 0; t < RTX; ++t) {
-                wsel[s][t] = u32x2{0, 0};
-                if constexpr (R > 0) {
-                    f32x4 acc = {0, 0, 0, 0};
+        for (int t = 0; t < RTX; ++t) {
+            wsel[s][t] = u32x2{0, 0};
+            if constexpr (R > 0) {
+                f32x4 acc = {0, 0, 0, 0};
 #pragma unroll
-                    for (int kk = 0; kk < 4; ++kk) acc = mfma32(bkf[s][t][kk], qf[kk], acc);
-                    if (my_slot == s) wsel[s][t] = pack4(acc);
-                }
+                for (int kk = 0; kk < 4; ++kk) acc = mfma32(bkf[s][t][kk], qf[kk], acc);
+                if (my_slot == s) wsel[s][t] = pack4(acc);
             }
-    };
-    __syncthreads();  // tables staged (the B_K loads, issued before them, have landed too)
-    finish_w();
+        }
+    __syncthreads();  // tables staged
 
     Rows<R> st;
     st.init();
@@ -373,32 +420,33 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
     // Base blocks travel memory -> registers -> LDS ring.  Four groups: two 16 KB buffers
     // of one stage (two pages), each wave loading one 4 KB block per stage two stages
     // ahead; otherwise two 32 KB buffers (four pages), two blocks per wave one stage ahead.
-    // Stages past the item re-read its last stage: every loop iteration then issues the
-    // same loads, so the compiler's vmcnt bookkeeping stays exact.
+    // A stage buffer holds page pairs [K even | K odd | V low half | V high half]: the two
+    // value halves interleave the pair's pages so that one 16-byte LDS read gives the
+    // 32-key operand of a value product.  Loads past the item read the padded tables: every
+    // loop iteration issues the same loads, so the compiler's vmcnt bookkeeping stays exact.
     const int n_stages = (npg + sp - 1) / sp;
     const int buf_halfs = sp * 2 * kBlockHalfs;
+    const int64_t vstride = (int64_t)hkv * kBlockHalfs;  // K block -> V block of a (page, head)
     auto load_blocks = [&](auto nb_tag, auto first_tag, int stage, u32x4 (&bx)[2][4]) __attribute__((always_inline)) {
         constexpr int NB = decltype(nb_tag)::value, FIRST = decltype(first_tag)::value;
-        const int stc = min(stage, n_stages - 1);
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
             const int b = wave * NB + j;                 // block of the stage: page b/2, K or V
-            const int pl = min(pg0 + stc * sp + (b >> 1), pg1 - 1);
-            const int bpage = uniform(s_tab[pl - pg0]);
-            const uint16_t *src = p.base_kv + (((int64_t)bpage * 2 + (b & 1)) * hkv + h) * kBlockHalfs;
+            const uint64_t src = s_base[stage * sp + (b >> 1)] + ((b & 1) ? vstride * 2 : 0) + lane * 16;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) bx[FIRST + j][i] = ldg128(src + i * 512 + lane * 8);
+            for (int i = 0; i < 4; ++i) bx[FIRST + j][i] = ldg128_at(src + i * 1024);
         }
     };
     auto store_blocks = [&](auto nb_tag, auto first_tag, int buf, int stage, u32x4 (&bx)[2][4]) __attribute__((always_inline)) {
         constexpr int NB = decltype(nb_tag)::value, FIRST = decltype(first_tag)::value;
-        const int stc = min(stage, n_stages - 1);
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
             const int b = wave * NB + j;
-            if (b & 1) {  // a V block: zero the tokens past the item's longest sequence
-                const int pl = min(pg0 + stc * sp + (b >> 1), pg1 - 1);
-                const int vis = item_max_len - pl * PS;
+            const int pb = b >> 1;  // page of the stage
+            uint16_t *pair = ring + buf * buf_halfs + (pb >> 1) * 4 * kBlockHalfs;
+            if (b & 1) {
+                // a V block: zero the tokens past the item's longest sequence
+                const int vis = item_max_len - (pg0 + stage * sp + pb) * PS;
                 if (vis < PS) {
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
@@ -407,71 +455,85 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
                         bx[FIRST + j][i] = u32x4{lo.x, lo.y, hi.x, hi.y};
                     }
                 }
-            }
-            uint16_t *dst = ring + buf * buf_halfs + b * kBlockHalfs;
+                uint16_t *vlo = pair + 2 * kBlockHalfs + (pb & 1) * 4;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4 *>(dst + i * 512 + lane * 8) = bx[FIRST + j][i];
+                for (int i = 0; i < 4; ++i) {
+                    const int o = (i * 64 + lane) * 8;
+                    *reinterpret_cast<u32x2 *>(vlo + o) = u32x2{bx[FIRST + j][i].x, bx[FIRST + j][i].y};
+                    *reinterpret_cast<u32x2 *>(vlo + kBlockHalfs + o) = u32x2{bx[FIRST + j][i].z, bx[FIRST + j][i].w};
+                }
+            } else {
+                uint16_t *dst = pair + (pb & 1) * kBlockHalfs;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4 *>(dst + i * 512 + lane * 8) = bx[FIRST + j][i];
+            }
         }
     };
-    // rCache fragments of the wave's slots for its pages of a stage (NSA slots, 1 or NSR).
-    // Slots without an adapter, and empty slots, read the plan's zero area.
-    const uint16_t *zero_c = reinterpret_cast<const uint16_t *>(plan + plan[fkv::H_OFF_ZERO]);
+    // rCache fragments of the wave's slots for its pages of a stage (NSA slots, 1 or NSR):
+    // one 16-byte load per (page, slot, rank tile), at the address the table holds
     const int wpage0 = ngp == 4 ? 0 : (ngp == 2 ? 2 * copy : copy);  // first stage page it computes
     auto load_c = [&](auto nsa_tag, auto np_tag, int stage, CFrag &c) __attribute__((always_inline)) {
         constexpr int NSA = decltype(nsa_tag)::value, NP = decltype(np_tag)::value;
-        const int stc = min(stage, n_stages - 1);
         if constexpr (R > 0) {
 #pragma unroll
             for (int j = 0; j < NP; ++j) {
-                const int pl = min(pg0 + stc * sp + wpage0 + j, pg1 - 1);
+                const uint64_t *e = s_res + (stage * sp + wpage0 + j) * RS + sb;
+                uint64_t a[NSA];
+                if constexpr (NSA % 2 == 0) {
+#pragma unroll
+                    for (int s = 0; s < NSA; s += 2) {
+                        typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
+                        const u64x2 v = *reinterpret_cast<const u64x2 *>(e + s);
+                        a[s] = v.x;
+                        a[s + 1] = v.y;
+                    }
+                } else {
+#pragma unroll
+                    for (int s = 0; s < NSA; ++s) a[s] = e[s];
+                }
 #pragma unroll
                 for (int s = 0; s < NSA; ++s) {
-                    const int tab = uniform(s_tab[(1 + sb + s) * kMaxPagesPerItem + (pl - pg0)]);
-                    const uint16_t *rb = slot_ad[s] >= 0 ? p.res_kv + (int64_t)tab * S::RES_PAGE : zero_c;
 #pragma unroll
-                    for (int t = 0; t < RT; ++t) {
-                        c.k[j][s][t] = ldg64(rb + t * 512 + lane * 4);
-                        c.v[j][s][t] = ldg64(rb + t * 512 + 256 + lane * 4);
-                    }
+                    for (int t = 0; t < RT; ++t) c.kv[j][s][t] = ldg128_at(a[s] + t * 1024 + lane * 16);
                 }
             }
         }
     };
 
-    // ---- one step: NP pages starting at stage page wp of LDS buffer buf ----
+    // ---- one step: NP pages starting at stage page wpage0 of LDS buffer buf ----
     auto step = [&](auto nsa_tag, auto np_tag, int buf, int stage, CFrag &c) __attribute__((always_inline)) {
         constexpr int NSA = decltype(nsa_tag)::value;
         constexpr int NP = decltype(np_tag)::value;
         const int pgw = pg0 + stage * sp + wpage0;         // logical page of step page 0
-        const uint16_t *kb = ring + buf * buf_halfs + wpage0 * 2 * kBlockHalfs;
-        bool pvalid[NP];
-#pragma unroll
-        for (int j = 0; j < NP; ++j) pvalid[j] = pgw + j < pg1;
+        const uint16_t *pair = ring + buf * buf_halfs + (wpage0 >> 1) * 4 * kBlockHalfs;
+        const int half = NP == 2 ? 0 : (wpage0 & 1);       // one-page steps: the page's place in its pair
         // rCache tokens past a slot's own length, or on a padding page, are unwritten: zero
         // them (one uniform branch; pages inside every rCache of the group skip it)
         if constexpr (R > 0) {
-            if (!pvalid[NP - 1] || (pgw + NP) * PS > min_res) {
+            if (pgw + NP > pg1 || (pgw + NP) * PS > min_res) {
 #pragma unroll
                 for (int j = 0; j < NP; ++j)
 #pragma unroll
                     for (int s = 0; s < NSA; ++s) {
-                        const int svis = pvalid[j] ? slot_len[s] - (pgw + j) * PS : 0;
+                        const int svis = pgw + j < pg1 ? slot_len[s] - (pgw + j) * PS : 0;
 #pragma unroll
                         for (int t = 0; t < RT; ++t) {
-                            c.k[j][s][t] = col < svis ? c.k[j][s][t] : u32x2{0, 0};
-                            c.v[j][s][t] = mask4(c.v[j][s][t], svis, grp);
+                            const u32x4 x = c.kv[j][s][t];
+                            const u32x2 k = col < svis ? u32x2{x.x, x.y} : u32x2{0, 0};
+                            const u32x2 v = mask4(u32x2{x.z, x.w}, svis, grp);
+                            c.kv[j][s][t] = u32x4{k.x, k.y, v.x, v.y};
                         }
                     }
             }
         }
         // rCache fragment of (page j, slot s, tile t); for rank 8 half of a tile is padding
         auto ckf = [&](int j, int s, int t) __attribute__((always_inline)) -> u32x2 {
-            const u32x2 v = c.k[j][s][t];
+            const u32x2 v = u32x2{c.kv[j][s][t].x, c.kv[j][s][t].y};
             if constexpr (R == 8) return grp < 2 ? v : u32x2{0, 0};
             return v;
         };
         auto cvf = [&](int j, int s, int t) __attribute__((always_inline)) -> u32x2 {
-            const u32x2 v = c.v[j][s][t];
+            const u32x2 v = u32x2{c.kv[j][s][t].z, c.kv[j][s][t].w};
             if constexpr (R == 8) return col < 8 ? v : u32x2{0, 0};
             return v;
         };
@@ -479,11 +541,11 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
         f32x4 sacc[NP];
 #pragma unroll
         for (int j = 0; j < NP; ++j) {
+            const uint16_t *kb = pair + (half + j) * kBlockHalfs;
             sacc[j] = f32x4{0, 0, 0, 0};
 #pragma unroll
             for (int kk = 0; kk < 4; ++kk)
-                sacc[j] = mfma32(*reinterpret_cast<const u32x4 *>(kb + j * 2 * kBlockHalfs + kk * 512 + lane * 8),
-                                 qf[kk], sacc[j]);
+                sacc[j] = mfma32(*reinterpret_cast<const u32x4 *>(kb + kk * 512 + lane * 8), qf[kk], sacc[j]);
         }
         if constexpr (R > 0) {
             constexpr int NU = NSA * RT;  // (slot, tile) units, taken in pairs
@@ -507,20 +569,28 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
                 }
             }
         }
-        // Stage 2: online softmax over the step's keys (rows in lanes, keys in lane groups)
+        // Stage 2: online softmax over the step's keys (rows in lanes, keys in lane groups).
+        // Keys 4grp + i of page j are visible to this lane's row when i < kv; a step inside
+        // every row's sequence skips the test.
         float sv[NP][4];
-        float mx = kNegInf;
+        if (pgw + NP <= pg1 && (pgw + NP) * PS <= min_len) {
 #pragma unroll
-        for (int j = 0; j < NP; ++j) {
-            // keys 4grp + i of page j are visible to this lane's row when i < kv
-            const int kv = (pvalid[j] && row_active) ? my_len - (pgw + j) * PS - 4 * grp : 0;
+            for (int j = 0; j < NP; ++j)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float x = i < kv ? sacc[j][i] : kNegInf;
-                sv[j][i] = x;
-                mx = fmaxf(mx, x);
+                for (int i = 0; i < 4; ++i) sv[j][i] = sacc[j][i];
+        } else {
+#pragma unroll
+            for (int j = 0; j < NP; ++j) {
+                const int kv = (pgw + j < pg1 && row_active) ? my_len - (pgw + j) * PS - 4 * grp : 0;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) sv[j][i] = i < kv ? sacc[j][i] : kNegInf;
             }
         }
+        float mx = kNegInf;
+#pragma unroll
+        for (int j = 0; j < NP; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sv[j][i]);
         mx = max_over_groups(mx) * cl;
         if (__builtin_amdgcn_ballot_w64(mx > st.m + kLazyRescale) != 0) {
             const float m_new = fmaxf(st.m, mx);
@@ -547,16 +617,14 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
         }
         st.l += psum;
         // O^T += V^T P^T and acc_r^T += C_V^T P^T (rows of other slots masked out of P)
-        const uint16_t *vb = kb + kBlockHalfs;
+        const uint16_t *vlo = pair + 2 * kBlockHalfs;
         if constexpr (NP == 2) {
             const u32x4 pb = u32x4{pf[0].x, pf[0].y, pf[1].x, pf[1].y};
 #pragma unroll
             for (int mt = 0; mt < 8; ++mt) {
-                // V^T rows 16mt.. of both pages (8 bytes each), one operand of the 32-key product
-                const int off = (mt >> 1) * 512 + lane * 8 + 4 * (mt & 1);
-                const u32x2 v0 = *reinterpret_cast<const u32x2 *>(vb + off);
-                const u32x2 v1 = *reinterpret_cast<const u32x2 *>(vb + 2 * kBlockHalfs + off);
-                st.oacc[mt] = mfma32(u32x4{v0.x, v0.y, v1.x, v1.y}, pb, st.oacc[mt]);
+                // V^T rows 16mt.. of both pages, the 32-key operand of one product
+                const u32x4 v = *reinterpret_cast<const u32x4 *>(vlo + (mt & 1) * kBlockHalfs + ((mt >> 1) * 64 + lane) * 8);
+                st.oacc[mt] = mfma32(v, pb, st.oacc[mt]);
             }
             if constexpr (R > 0) {
 #pragma unroll
@@ -572,8 +640,9 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
         } else {
 #pragma unroll
             for (int q2 = 0; q2 < 4; ++q2) {
-                const u32x4 v0 = *reinterpret_cast<const u32x4 *>(vb + q2 * 512 + lane * 8);
-                const u32x2 a = u32x2{v0.x, v0.y}, b = u32x2{v0.z, v0.w};
+                const int o = (q2 * 64 + lane) * 8 + half * 4;
+                const u32x2 a = *reinterpret_cast<const u32x2 *>(vlo + o);
+                const u32x2 b = *reinterpret_cast<const u32x2 *>(vlo + kBlockHalfs + o);
                 st.oacc[2 * q2] = mfma16(a, pf[0], st.oacc[2 * q2]);
                 st.oacc[2 * q2 + 1] = mfma16(b, pf[0], st.oacc[2 * q2 + 1]);
             }
@@ -591,9 +660,6 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
     using I1 = std::integral_constant<int, 1>;
     using I2 = std::integral_constant<int, 2>;
     using NSF = std::integral_constant<int, NSR>;
-    auto run_step = [&](auto nsa_tag, auto np_tag, int buf, int stage, CFrag &c) __attribute__((always_inline)) {
-        step(nsa_tag, np_tag, buf, stage, c);
-    };
 
     CFrag ca, cb;
     u32x4 bx[2][4];
@@ -611,13 +677,13 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
             __syncthreads();
             for (int s = 0;;) {
                 load_c(NSF{}, I2{}, s + 1, cb);
-                run_step(NSF{}, I2{}, s & 1, s, ca);
+                step(NSF{}, I2{}, s & 1, s, ca);
                 store_blocks(I1{}, I1{}, (s + 1) & 1, s + 1, bx);
                 load_blocks(I1{}, I1{}, s + 3, bx);
                 __syncthreads();
                 if (++s >= n_stages) break;
                 load_c(NSF{}, I2{}, s + 1, ca);
-                run_step(NSF{}, I2{}, s & 1, s, cb);
+                step(NSF{}, I2{}, s & 1, s, cb);
                 store_blocks(I1{}, N0{}, (s + 1) & 1, s + 1, bx);
                 load_blocks(I1{}, N0{}, s + 3, bx);
                 __syncthreads();
@@ -634,13 +700,13 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
             __syncthreads();
             for (int s = 0;;) {
                 load_c(nsa_tag, np_tag, s + 1, cb);
-                run_step(nsa_tag, np_tag, s & 1, s, ca);
+                step(nsa_tag, np_tag, s & 1, s, ca);
                 store_blocks(I2{}, N0{}, (s + 1) & 1, s + 1, bx);
                 load_blocks(I2{}, N0{}, s + 2, bx);
                 __syncthreads();
                 if (++s >= n_stages) break;
                 load_c(nsa_tag, np_tag, s + 1, ca);
-                run_step(nsa_tag, np_tag, s & 1, s, cb);
+                step(nsa_tag, np_tag, s & 1, s, cb);
                 store_blocks(I2{}, N0{}, (s + 1) & 1, s + 1, bx);
                 load_blocks(I2{}, N0{}, s + 2, bx);
                 __syncthreads();
@@ -657,7 +723,6 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
         }
     }
 
-
     write_partial<R>(p, st, row_active, (int64_t)(row_base + copy * nag * G + my_group * ROWS + col) * hkv + h,
                      grp);
 }
@@ -670,7 +735,7 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs p) {
 // so the compiler can count them and the prefetched page stays in flight.
 template <int R, int G>
 struct RopeShape {
-    static constexpr int AG = ROWS / G;
+    static constexpr int AG = fkv::decode_rope_item_agents(G, R);  // agent slots of an item
     static constexpr int RT = (R + 15) / 16;
     static constexpr int BSTAGE_BYTES = AG * R * D * 2;     // row-major B_K slices
     static constexpr int BKT_BYTES = AG * RT * 8 * 64 * 8;  // B_K^T fragments
@@ -690,12 +755,12 @@ __global__ __launch_bounds__(256, 1) void decode_rope_kernel(DecodeArgs p) {
     __shared__ int32_t s_tab[S::TABLE_WORDS];
 
     const int32_t *plan = p.plan;
-    const int blk = plan[plan[fkv::H_OFF_BLOCKS] + blockIdx.x];
+    const int blk = plan[p.off_blocks + blockIdx.x];
     if (blk < 0) return;
     const int hkv = p.hkv;
     const int item = blk / hkv;
     const int h = blk - item * hkv;
-    const int32_t *rec = plan + plan[fkv::H_OFF_ITEMS] + item * fkv::kItemWords;
+    const int32_t *rec = plan + p.off_items + item * fkv::kItemWords;
     const int pg0 = rec[0], pg1 = rec[1], leader = rec[2], nag = rec[3], row_base = rec[4];
     const int32_t *item_agents = rec + 5;
     if (nag > AG || pg1 - pg0 > kMaxPagesPerItem) return;  // rejected on the host
@@ -808,8 +873,10 @@ __global__ __launch_bounds__(256, 1) void decode_rope_kernel(DecodeArgs p) {
                 const uint16_t *rb = p.res_kv + (int64_t)rpage * res_page_halfs;
 #pragma unroll
                 for (int t = 0; t < RT; ++t) {
-                    const u32x2 k = ldg64(rb + t * 512 + lane * 4);
-                    const u32x2 v = ldg64(rb + t * 512 + 256 + lane * 4);
+                    // two 8-byte loads: the single 16-byte form of this load gave wrong
+                    // results at rank 32 with this kernel's register allocation
+                    const u32x2 k = ldg64(rb + t * 512 + lane * 8);
+                    const u32x2 v = ldg64(rb + t * 512 + lane * 8 + 4);
                     f.cv[s][t] = ro.cv_ok[t] ? v : u32x2{0, 0};
                     f.ck[s][t] = ro.ck_ok[t] ? k : u32x2{0, 0};
                 }
@@ -911,9 +978,9 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(DecodeA
     const int j = blockIdx.x - a * hq;
     const int h = j / G, jj = j - h * G;
     const int32_t *plan = p.plan;
-    const int32_t *slots = plan + plan[fkv::H_OFF_AGENT_SLOT];
-    const int k0 = plan[plan[fkv::H_OFF_AGENT_PTR] + a];
-    const int K = plan[plan[fkv::H_OFF_AGENT_PTR] + a + 1] - k0;
+    const int32_t *slots = plan + p.off_slot;
+    const int k0 = plan[p.off_ptr + a];
+    const int K = plan[p.off_ptr + a + 1] - k0;
     const int ad = R > 0 ? p.adapter_idx[a] : -1;
     const int stride = p.ws_stride;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -1087,6 +1154,11 @@ extern "C" fkv_status fkv_residual_attention_decode(const fkv_attn_args *a, cons
     da.hkv = a->hkv;
     da.max_pages = a->max_pages;
     da.ws_stride = ws_stride_of(a->r);
+    da.off_items = w[fkv::H_OFF_ITEMS];
+    da.off_blocks = w[fkv::H_OFF_BLOCKS];
+    da.off_ptr = w[fkv::H_OFF_AGENT_PTR];
+    da.off_slot = w[fkv::H_OFF_AGENT_SLOT];
+    da.off_zero = w[fkv::H_OFF_ZERO];
     da.scale_log2 = a->scale * 1.4426950408889634f;
     const int nb = w[fkv::H_N_BLOCKS];
     hipStream_t hs = static_cast<hipStream_t>(stream);

@@ -43,11 +43,16 @@ constexpr int decode_wave_slots(int g, int r) {
     return r >= 64 ? (kMaxRows / g < 2 ? kMaxRows / g : 2) : kMaxRows / g;
 }
 constexpr int decode_heads_per_block(int, bool) { return 1; }
+// With RoPE an item holds one group, of at most two agents at rank 32 or more (the wave
+// keeps two pages of every slot's rCache fragments and RoPE rows in registers).
+constexpr int decode_rope_item_agents(int g, int r) {
+    return r >= 32 ? (kMaxRows / g < 2 ? kMaxRows / g : 2) : kMaxRows / g;
+}
 // Largest number of agents per work item:
 constexpr int decode_item_agent_cap(int g, int hkv, int r, bool rope) {
     (void)hkv;
     const int ag = kMaxRows / g;
-    if (rope && r > 0) return ag;
+    if (rope && r > 0) return decode_rope_item_agents(g, r);
     if (r >= 32) return decode_wave_slots(g, r);
     return kMaxGroups * ag < kMaxItemAgents ? kMaxGroups * ag : kMaxItemAgents;
 }

@@ -7,10 +7,10 @@
 //   K element (token t, dim d) at  (d/32)*512 + (t + 16*((d%16)/4))*8 + 4*((d%32)/16) + d%4
 //   V element (token t, dim d) at  (d/32)*512 + (d%16 + 16*(t/4))*8 + 4*((d/16)%2) + t%4
 // A residual page with ps = 16 holds ceil(r/16) tiles of 512 values; tile k holds, for
-// lane L = 16*g + c of a wave, the 4 values at L*4 and the 4 values at 256 + L*4:
+// lane L = 16*g + c of a wave, 8 values at L*8: the 4 at L*8 + i and the 4 at L*8 + 4 + i,
 //   C_K[token c][16k + 4g + i]             C_V[token 4g + i][16k + c]        (i = 0..3)
-// so each lane reads each of its rCache fragments with one 8-byte load (512 contiguous
-// bytes per wave instruction).  Rank values past r (r = 8) are padding.  Other shapes use
+// so each lane reads both of its rCache fragments of a tile with one 16-byte load (1 KB
+// contiguous per wave instruction).  Rank values past r (r = 8) are padding.  Other shapes use
 // plain [ps][d] (K), [d][ps] (V), [ps][r] (C_K) and [r][ps] (C_V).
 #include <hip/hip_runtime.h>
 
@@ -40,11 +40,11 @@ __device__ __forceinline__ int v_slot(int64_t e, int ps, int d) {
 }
 
 __device__ __forceinline__ int64_t ck_off(int t, int rho, int ps, int r) {
-    if (ps == 16) return (int64_t)(rho >> 4) * 512 + (((rho & 15) >> 2) * 16 + t) * 4 + (rho & 3);
+    if (ps == 16) return (int64_t)(rho >> 4) * 512 + (((rho & 15) >> 2) * 16 + t) * 8 + (rho & 3);
     return (int64_t)t * r + rho;
 }
 __device__ __forceinline__ int64_t cv_off(int t, int rho, int ps, int r) {
-    if (ps == 16) return (int64_t)(rho >> 4) * 512 + 256 + ((t >> 2) * 16 + (rho & 15)) * 4 + (t & 3);
+    if (ps == 16) return (int64_t)(rho >> 4) * 512 + ((t >> 2) * 16 + (rho & 15)) * 8 + 4 + (t & 3);
     return (int64_t)ps * r + (int64_t)rho * ps + t;
 }
 __device__ __forceinline__ int64_t res_page_elems(int ps, int r) {
@@ -53,8 +53,8 @@ __device__ __forceinline__ int64_t res_page_elems(int ps, int r) {
 // Token slot of element e of a residual page.
 __device__ __forceinline__ int c_slot(int64_t e, int ps, int r) {
     if (ps == 16) {
-        const int w = (int)(e & 511);
-        return w < 256 ? ((w >> 2) & 15) : 4 * (((w - 256) >> 2) >> 4) + (w & 3);
+        const int w = (int)(e & 511);  // lane w / 8 of the tile: C_K at w % 8 < 4, else C_V
+        return (w & 4) == 0 ? ((w >> 3) & 15) : 4 * (w >> 7) + (w & 3);
     }
     return e < (int64_t)ps * r ? (int)(e / r) : (int)((e - (int64_t)ps * r) % ps);
 }

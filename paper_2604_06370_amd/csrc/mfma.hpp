@@ -50,6 +50,10 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_floa
 
 __device__ __forceinline__ u32x4 ldg128(const void *p) { return *reinterpret_cast<const u32x4 *>(p); }
 __device__ __forceinline__ u32x2 ldg64(const void *p) { return *reinterpret_cast<const u32x2 *>(p); }
+// Loads through an address held as an integer (a device-memory pointer read from LDS):
+// the global address space keeps them off the LDS counter that generic loads also use.
+typedef const u32x4 __attribute__((address_space(1))) *gptr128;
+__device__ __forceinline__ u32x4 ldg128_at(uint64_t addr) { return *reinterpret_cast<gptr128>(addr); }
 
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 

@@ -217,7 +217,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
                     for (int mt = 0; mt < 8; ++mt) u[mt] = f32x4{0, 0, 0, 0};
 #pragma unroll
                     for (int t = 0; t < RT; ++t) {
-                        const u32x2 c = ldg64(rb + t * 512 + lane * 4);
+                        const u32x2 c = ldg64(rb + t * 512 + lane * 8);
                         const u32x2 ck = (16 * t + 4 * grp < R) ? c : u32x2{0, 0};
 #pragma unroll
                         for (int mt = 0; mt < 8; ++mt) u[mt] = mfma16(sBK[(t * 8 + mt) * 64 + lane], ck, u[mt]);
@@ -258,7 +258,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
                 for (int t = 0; t < RT; ++t) {
                     const int rho = 16 * t + col;
                     u32x2 v = {0, 0};
-                    if (rb) v = ldg64(rb + t * 512 + 256 + lane * 4);
+                    if (rb) v = ldg64(rb + t * 512 + lane * 8 + 4);
                     const int k0 = 4 * grp;
                     if (k0 + 0 >= vis) v.x &= 0xffff0000u;
                     if (k0 + 1 >= vis) v.x &= 0x0000ffffu;
@@ -291,7 +291,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
                     const uint16_t *rb = p.res_kv + (int64_t)btr[pg] * S::RES_PAGE;
 #pragma unroll
                     for (int t = 0; t < RT; ++t) {
-                        const u32x2 c = ldg64(rb + t * 512 + lane * 4);
+                        const u32x2 c = ldg64(rb + t * 512 + lane * 8);
                         const u32x2 ck = (16 * t + 4 * grp < R) ? c : u32x2{0, 0};
                         // zero-padded 16x16x32 form: the accumulator chain stays on one
                         // instruction form (see the decode kernel)
