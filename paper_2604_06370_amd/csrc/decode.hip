@@ -59,7 +59,7 @@ struct DecodeArgs {
     float *ws;
     uint16_t *out;
     int32_t hq, hkv, max_pages, ws_stride;
-    int32_t off_items, off_blocks, off_ptr, off_slot, off_zero;  // plan section offsets (words)
+    int32_t off_items, off_blocks, off_ptr, off_zero;  // plan section offsets (words)
     float scale_log2;  // softmax scale * log2(e)
 };
 
@@ -276,7 +276,7 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
     const int item = blk / hkv;
     const int h = blk - item * hkv;
     const int32_t *rec = plan + p.off_items + item * fkv::kItemWords;
-    const int pg0 = rec[0], pg1 = rec[1], leader = rec[2], nag = rec[3], row_base = rec[4];
+    const int pg0 = rec[0], pg1 = rec[1], leader = rec[2], nag = rec[3];
     const int ng = (nag + AG - 1) / AG;
     if (pg1 - pg0 > kMaxPagesPerItem || nag > S::MAX_SLOTS || (ng > 1 && !S::MULTI) || (ng == 1 && nag > NSW))
         return;  // rejected on the host
@@ -298,6 +298,7 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
     // round of parallel loads instead of a chain per agent)
     const bool lane_ag = lane < nag;
     const int l_agent = lane_ag ? rec[5 + lane] : 0;
+    const int l_part = lane_ag ? rec[5 + fkv::kMaxItemAgents + lane] : 0;  // first partial of the slot
     const int l_len = lane_ag ? p.seq_lens[l_agent] : 0;
     const int l_ad = (R > 0 && lane_ag) ? p.adapter_idx[l_agent] : -1;
 
@@ -343,17 +344,22 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
     }
     const int src_lane = (sb + my_slot) & 63;
     const int sh_agent = __shfl(l_agent, src_lane), sh_len = __shfl(l_len, src_lane);
+    const int my_part = __shfl(l_part, src_lane) + copy;  // this lane's row's partial
     const int my_agent = row_active ? sh_agent : 0;
     const int my_len = row_active ? sh_len : 0;
 
     // Q^T fragments (B operand of the 16x16x32 products)
+    const uint16_t *qrow = p.q + ((int64_t)my_agent * p.hq + qh) * D;
     u32x4 qf[4];
-    load_q(p.q + ((int64_t)my_agent * p.hq + qh) * D, row_active, grp, qf);
+    load_q(qrow, row_active, grp, qf);
 
-    // B_K rows of every slot for W = B_K q (lane holds B_K[16t + col][the head-dim slots of
-    // k-step kk])
-    u32x4 bkf[NSR][RTX][4];
+    // W = B_K q: the contraction over the head dim may take any order that both operands
+    // share, so it uses the natural one (lane holds dims 32kk + 8grp .. +7), in which each
+    // lane reads 16 contiguous bytes of a B_K row and of q
+    u32x4 bkf[NSR][RTX][4], qn[4];
     if constexpr (R > 0) {
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) qn[kk] = row_active ? ldg128(qrow + 32 * kk + 8 * grp) : u32x4{0, 0, 0, 0};
 #pragma unroll
         for (int s = 0; s < NSR; ++s) {
             const uint16_t *bk = p.lora_b + (int64_t)(slot_ad[s] >= 0 ? slot_ad[s] : 0) * 2 * R * n + (int64_t)h * D;
@@ -362,15 +368,8 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
                 const int rho = 16 * t + col;
                 const int64_t ro = (int64_t)(rho < R ? rho : 0) * n;
 #pragma unroll
-                for (int kk = 0; kk < 4; ++kk) {
-                    u32x4 a = {0, 0, 0, 0};
-                    if (slot_ad[s] >= 0 && rho < R) {
-                        const u32x2 lo = ldg64(bk + ro + 32 * kk + 4 * grp);
-                        const u32x2 hi = ldg64(bk + ro + 32 * kk + 16 + 4 * grp);
-                        a = u32x4{lo.x, lo.y, hi.x, hi.y};
-                    }
-                    bkf[s][t][kk] = a;
-                }
+                for (int kk = 0; kk < 4; ++kk)
+                    bkf[s][t][kk] = (slot_ad[s] >= 0 && rho < R) ? ldg128(bk + ro + 32 * kk + 8 * grp) : u32x4{0, 0, 0, 0};
             }
         }
     }
@@ -406,7 +405,7 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
             if constexpr (R > 0) {
                 f32x4 acc = {0, 0, 0, 0};
 #pragma unroll
-                for (int kk = 0; kk < 4; ++kk) acc = mfma32(bkf[s][t][kk], qf[kk], acc);
+                for (int kk = 0; kk < 4; ++kk) acc = mfma32(bkf[s][t][kk], qn[kk], acc);
                 if (my_slot == s) wsel[s][t] = pack4(acc);
             }
         }
@@ -723,8 +722,7 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
         }
     }
 
-    write_partial<R>(p, st, row_active, (int64_t)(row_base + copy * nag * G + my_group * ROWS + col) * hkv + h,
-                     grp);
+    write_partial<R>(p, st, row_active, ((int64_t)my_part * G + col % G) * hkv + h, grp);
 }
 
 
@@ -761,7 +759,7 @@ __global__ __launch_bounds__(256, 1) void decode_rope_kernel(DecodeArgs p) {
     const int item = blk / hkv;
     const int h = blk - item * hkv;
     const int32_t *rec = plan + p.off_items + item * fkv::kItemWords;
-    const int pg0 = rec[0], pg1 = rec[1], leader = rec[2], nag = rec[3], row_base = rec[4];
+    const int pg0 = rec[0], pg1 = rec[1], leader = rec[2], nag = rec[3];
     const int32_t *item_agents = rec + 5;
     if (nag > AG || pg1 - pg0 > kMaxPagesPerItem) return;  // rejected on the host
 
@@ -771,6 +769,7 @@ __global__ __launch_bounds__(256, 1) void decode_rope_kernel(DecodeArgs p) {
     const int my_slot_l = col / G;
     const bool row_active = my_slot_l < nag;
     const int my_agent = row_active ? item_agents[my_slot_l] : 0;
+    const int my_part = row_active ? item_agents[fkv::kMaxItemAgents + my_slot_l] + wave : 0;  // wave = copy
     const int qh = h * G + (col % G);
 
     const int npg = pg1 - pg0;
@@ -958,53 +957,70 @@ __global__ __launch_bounds__(256, 1) void decode_rope_kernel(DecodeArgs p) {
     else if (nag == 3) run_pages(I3{});
     else run_pages(I4{});
 
-    write_partial<R>(p, st, row_active, (int64_t)(row_base + wave * nag * G + col) * hkv + h, grp);
+    write_partial<R>(p, st, row_active, ((int64_t)my_part * G + col % G) * hkv + h, grp);
 }
 
 
 // Log-sum-exp merge of one agent's partials and Stage 3 of Algorithm 1 for one query
 // head j (KV head h = j / G): O = (sum_k w_k acc_k + (sum_k w_k acc_r,k) . B_V[h]) / L
-// with w_k = 2^(m_k - M), M = max_k m_k, L = sum_k w_k l_k.  Wave w folds partials
-// k = w, w+4, ... with a running maximum (lane c holds columns c, c+64, c+128 of the
-// record), the four waves are merged through LDS, then B_V is applied once.
+// with w_k = 2^(m_k - M), M = max_k m_k, L = sum_k w_k l_k.  An agent's partials are
+// contiguous, so the records are addressed directly: in rounds of 64, wave w issues the
+// loads of partials w, w+4, ... together and folds them with a running maximum (lane c
+// holds columns c, c+64, c+128 of a record).  The four waves are merged through LDS and
+// B_V (prefetched at the start, as it does not depend on the partials) is applied once.
 constexpr int kCombineThreads = 256;
+constexpr int kCombineRound = 64;  // partials per round
 
 template <int R, int G>
 __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(DecodeArgs p) {
     constexpr int NCOL = D + R;
     constexpr int NC = (NCOL + 63) / 64;
+    constexpr int U = kCombineRound / WAVES;  // partials per wave and round
+    constexpr int RH = (R + 1) / 2;            // rank rows per half of the workgroup
     const int hq = p.hq;
     const int a = blockIdx.x / hq;
     const int j = blockIdx.x - a * hq;
     const int h = j / G, jj = j - h * G;
     const int32_t *plan = p.plan;
-    const int32_t *slots = plan + p.off_slot;
     const int k0 = plan[p.off_ptr + a];
     const int K = plan[p.off_ptr + a + 1] - k0;
     const int ad = R > 0 ? p.adapter_idx[a] : -1;
     const int stride = p.ws_stride;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int add = jj * p.hkv + h;
+    // record of partial k0 + k for query head j: ((k0 + k) * G + jj) * hkv + h
+    const float *rec0 = p.ws + ((int64_t)k0 * G * p.hkv + jj * p.hkv + h) * stride;
+    const int64_t kstride = (int64_t)G * p.hkv * stride;
+    const int d = tid & (D - 1), half = tid >> 7;
     __shared__ float sM[4], sL[4];
     __shared__ float sAcc[4][NCOL];
     __shared__ float sFin[NCOL];
     __shared__ float sOut[D];
 
+    // B_V[rho][h*D + d] for this thread's half of the rank
+    float bv[RH > 0 ? RH : 1];
+    if constexpr (R > 0) {
+        const uint16_t *bvp = p.lora_b + ((int64_t)(ad >= 0 ? ad : 0) * 2 + 1) * R * p.hkv * D + (int64_t)h * D + d;
+#pragma unroll
+        for (int i = 0; i < RH; ++i) {
+            const int rho = half * RH + i;
+            bv[i] = (ad >= 0 && rho < R) ? bf16_to_f32(bvp[(int64_t)rho * p.hkv * D]) : 0.f;
+        }
+    }
+
     float M = kNegInf, L = 0.f, acc[NC];
 #pragma unroll
     for (int c = 0; c < NC; ++c) acc[c] = 0.f;
-    constexpr int U = 4;
-    for (int kb = wave; kb < K; kb += 4 * U) {
+    for (int kb = 0; kb < K; kb += kCombineRound) {
         float mv[U], lv[U], v[U][NC];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int k = kb + 4 * u;
-            const int kc = k < K ? k : kb;
-            const float *src = p.ws + (int64_t)(slots[k0 + kc] + add) * stride;
-            mv[u] = k < K ? src[NCOL] : kNegInf;
-            lv[u] = src[NCOL + 1];
+            const int idx = wave + WAVES * u;
+            const bool ok = kb + idx < K;
+            const float *src = rec0 + (int64_t)(kb + idx) * kstride;
+            mv[u] = ok ? src[NCOL] : kNegInf;
+            lv[u] = ok ? src[NCOL + 1] : 0.f;
 #pragma unroll
-            for (int c = 0; c < NC; ++c) v[u][c] = lane + 64 * c < NCOL ? src[lane + 64 * c] : 0.f;
+            for (int c = 0; c < NC; ++c) v[u][c] = (ok && lane + 64 * c < NCOL) ? src[lane + 64 * c] : 0.f;
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -1039,17 +1055,12 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(DecodeA
     __syncthreads();
     // Stage 3: O = (acc + acc_r . B_V) / L; the rank sum is split over the two halves of
     // the workgroup
-    const int d = tid & (D - 1), half = tid >> 7;
     float o = half == 0 ? sFin[d] : 0.f;
     if constexpr (R > 0) {
-        if (ad >= 0) {
-            constexpr int RH = (R + 1) / 2;
-            const uint16_t *bv = p.lora_b + ((int64_t)ad * 2 + 1) * R * p.hkv * D + (int64_t)h * D + d;
 #pragma unroll
-            for (int i = 0; i < RH; ++i) {
-                const int rho = half * RH + i;
-                if (rho < R) o += sFin[D + rho] * bf16_to_f32(bv[(int64_t)rho * p.hkv * D]);
-            }
+        for (int i = 0; i < RH; ++i) {
+            const int rho = half * RH + i;
+            if (rho < R) o += sFin[D + rho] * bv[i];
         }
     }
     if (half == 1) sOut[d] = o;
@@ -1157,7 +1168,6 @@ extern "C" fkv_status fkv_residual_attention_decode(const fkv_attn_args *a, cons
     da.off_items = w[fkv::H_OFF_ITEMS];
     da.off_blocks = w[fkv::H_OFF_BLOCKS];
     da.off_ptr = w[fkv::H_OFF_AGENT_PTR];
-    da.off_slot = w[fkv::H_OFF_AGENT_SLOT];
     da.off_zero = w[fkv::H_OFF_ZERO];
     da.scale_log2 = a->scale * 1.4426950408889634f;
     const int nb = w[fkv::H_N_BLOCKS];

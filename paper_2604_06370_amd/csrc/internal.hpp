@@ -15,23 +15,25 @@ void clear_error();
 
 // Decode plan, host side.  Serialised layout (all int32):
 //   header[kHeaderWords]
-//   items   [n_items][kItemWords]  {page_begin, page_end, leader, n_ag, row_base, agent[16]}
+//   items   [n_items][kItemWords]  {page_begin, page_end, leader, n_ag, copies, agent[16],
+//                                   partial[16]}  (partial[j] + c: partial of slot j, copy c)
 //   blocks  [n_blocks]             item * (hkv / H) + head block, or -1 for an idle block
 //                                  (H = heads per block, header word H_HEADS_PER_BLOCK)
-//   agent_ptr [n_agents+1]         CSR over the partial rows of each agent
-//   agent_slot[...]                (row_base + (copy*n_ag + slot)*g) * hkv  (add jj*hkv + head
-//                                  for query head jj)
+//   agent_ptr [n_agents+1]         agent a owns partials agent_ptr[a] .. agent_ptr[a+1]-1; query
+//                                  head jj of KV head h of partial p is workspace record
+//                                  (p * g + jj) * hkv + h
+//   (header word H_OFF_AGENT_SLOT is unused and equals H_OFF_ZERO)
 //   zero      [kZeroWords]         zeros, 16-byte aligned (read in place of the rCache of an
 //                                  agent without adapter or of an empty agent slot)
 // An item holds up to four agent groups; a group is the floor(16/g) agents whose
 // query heads of one KV head fill the 16 rows of one matrix-core tile.  An item of
 // ng groups runs on 4 / ngp wave copies (ngp = 1, 2, 4 for ng = 1, 2, 3..4); every
-// copy writes its own partial rows, so the item owns copies * n_ag * g rows.
+// copy writes its own partial, so the item owns copies * n_ag partials (g rows each).
 constexpr int kHeaderWords = 24;
 constexpr int kMaxRows = 16;        // query rows of one agent group (one wave's row tile)
 constexpr int kMaxGroups = 4;       // agent groups per item (one wave each)
 constexpr int kMaxItemAgents = 16;  // agents per item
-constexpr int kItemWords = 5 + kMaxItemAgents;
+constexpr int kItemWords = 5 + 2 * kMaxItemAgents;
 constexpr int kMaxPagesPerItem = 64;  // upper bound of pages_per_split (block tables are staged in LDS)
 
 // Decode: one workgroup per (work item, KV head).  Without RoPE and with rank below 32 an

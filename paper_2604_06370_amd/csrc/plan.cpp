@@ -127,7 +127,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     // 4. work items, clustered by (segment, split).  An item of ng agent groups runs its
     //    groups on 4 / ngp wave copies (ngp = ng rounded up to 1, 2 or 4), each writing its
     //    own partial rows: rows = copies * agents * g.
-    struct Item { int32_t p0, p1, row_base, copies; double cost; std::vector<int32_t> agents; };
+    struct Item { int32_t p0, p1, copies; double cost; std::vector<int32_t> agents; };
     std::vector<Item> items;
     std::vector<std::pair<int32_t, int32_t>> clusters;  // [first item, item count)
     std::vector<double> cluster_cost;
@@ -146,7 +146,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
             for (size_t c : chunks) {
                 const int32_t ng = (int32_t)((c + ag - 1) / ag);
                 const int32_t ngp = ng == 1 ? 1 : (ng == 2 ? 2 : 4);
-                Item it{p0, p1, (int32_t)total_rows, fkv::kMaxGroups / ngp, 0.0, {}};
+                Item it{p0, p1, fkv::kMaxGroups / ngp, 0.0, {}};
                 for (size_t j = k; j < k + c; ++j) it.agents.push_back(s.agents[j]);
                 k += c;
                 total_rows += (int64_t)it.copies * (int64_t)c * g;
@@ -185,16 +185,19 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     for (auto &l : per_xcd) depth = std::max(depth, l.size());
     const int32_t n_blocks = (int32_t)(depth * kNumXcd);
 
-    // 6. partial rows per agent (CSR): copy c of agent slot j, query head jj of head h lives
-    //    at partial index (row_base + (c * n_agents_in_item + j) * g + jj) * hkv + h
-    std::vector<std::vector<int32_t>> slots(A);
-    for (int32_t w = 0; w < n_items; ++w) {
-        const int64_t nag = (int64_t)items[w].agents.size();
-        for (int32_t c = 0; c < items[w].copies; ++c)
-            for (int64_t j = 0; j < nag; ++j)
-                slots[items[w].agents[j]].push_back(
-                    (int32_t)(((int64_t)items[w].row_base + ((int64_t)c * nag + j) * g) * hkv));
-    }
+    // 6. partials, contiguous per agent (CSR): agent a owns [ptr[a], ptr[a+1]); slot j of an
+    //    item writes its copies c to partials first[j] + c
+    std::vector<int32_t> ptr(A + 1, 0);
+    for (const auto &it : items)
+        for (int32_t a : it.agents) ptr[a + 1] += it.copies;
+    for (int32_t a = 0; a < A; ++a) ptr[a + 1] += ptr[a];
+    std::vector<int32_t> next(ptr.begin(), ptr.end() - 1);
+    std::vector<std::vector<int32_t>> first(n_items);
+    for (int32_t w = 0; w < n_items; ++w)
+        for (int32_t a : items[w].agents) {
+            first[w].push_back(next[a]);
+            next[a] += items[w].copies;
+        }
 
     // 7. serialise
     auto *pl = new fkv_plan();
@@ -202,13 +205,10 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     pl->g = g;
     pl->n_agents = A;
     pl->max_pages_used = P;
-    int64_t total_slots = 0;
-    for (auto &v : slots) total_slots += (int64_t)v.size();
     const int64_t off_items = fkv::kHeaderWords;
     const int64_t off_blocks = off_items + (int64_t)n_items * fkv::kItemWords;
     const int64_t off_ptr = off_blocks + n_blocks;
-    const int64_t off_slot = off_ptr + A + 1;
-    const int64_t off_zero = (off_slot + total_slots + 3) / 4 * 4;
+    const int64_t off_zero = (off_ptr + A + 1 + 3) / 4 * 4;
     const int64_t total = off_zero + fkv::kZeroWords;
     if (total > INT32_MAX) {
         delete pl;
@@ -226,7 +226,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     w[fkv::H_OFF_ITEMS] = (int32_t)off_items;
     w[fkv::H_OFF_BLOCKS] = (int32_t)off_blocks;
     w[fkv::H_OFF_AGENT_PTR] = (int32_t)off_ptr;
-    w[fkv::H_OFF_AGENT_SLOT] = (int32_t)off_slot;
+    w[fkv::H_OFF_AGENT_SLOT] = (int32_t)off_zero;
     w[fkv::H_TOTAL_WORDS] = (int32_t)total;
     w[fkv::H_PAGES_PER_SPLIT] = pps_max;
     w[fkv::H_PAGE_SIZE] = ps;
@@ -243,20 +243,18 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
         r[1] = items[i].p1;
         r[2] = items[i].agents[0];
         r[3] = (int32_t)items[i].agents.size();
-        r[4] = items[i].row_base;
-        for (int32_t j = 0; j < fkv::kMaxItemAgents; ++j) r[5 + j] = j < r[3] ? items[i].agents[j] : -1;
+        r[4] = items[i].copies;
+        for (int32_t j = 0; j < fkv::kMaxItemAgents; ++j) {
+            r[5 + j] = j < r[3] ? items[i].agents[j] : -1;
+            r[5 + fkv::kMaxItemAgents + j] = j < r[3] ? first[i][j] : -1;
+        }
     }
     for (int32_t b = 0; b < n_blocks; ++b) {
         const auto &lst = per_xcd[b % kNumXcd];
         const size_t k = (size_t)(b / kNumXcd);
         w[off_blocks + b] = k < lst.size() ? lst[k] : -1;
     }
-    int64_t pos = off_slot;
-    for (int32_t a = 0; a < A; ++a) {
-        w[off_ptr + a] = (int32_t)(pos - off_slot);
-        for (int32_t s : slots[a]) w[pos++] = s;
-    }
-    w[off_ptr + A] = (int32_t)(pos - off_slot);
+    for (int32_t a = 0; a <= A; ++a) w[off_ptr + a] = ptr[a];
     for (auto &s : segs) {
         pl->seg_first_page.push_back(s.first);
         pl->seg_n_pages.push_back(s.n);

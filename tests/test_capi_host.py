@@ -213,18 +213,20 @@ def test_attention_entry_points_reject_bad_arguments_before_launching():
 
 def _parse_plan(words):
     """Decode the serialised plan (layout of internal.hpp) into items, blocks and the CSR."""
-    H = dict(n_items=1, n_blocks=2, n_agents=3, hkv=4, g=5, off_items=7, off_blocks=8, off_ptr=9, off_slot=10,
+    H = dict(n_items=1, n_blocks=2, n_agents=3, hkv=4, g=5, off_items=7, off_blocks=8, off_ptr=9,
              total_rows=15, max_item_agents=16, heads_per_block=17, rank=18, rope=19)
     h = {k: int(words[v]) for k, v in H.items()}
     items = []
+    iw = 5 + 2 * 16
     for i in range(h["n_items"]):
-        r = words[h["off_items"] + 21 * i: h["off_items"] + 21 * (i + 1)]
-        items.append(dict(p0=int(r[0]), p1=int(r[1]), leader=int(r[2]), nag=int(r[3]), row_base=int(r[4]),
-                          agents=[int(x) for x in r[5:5 + int(r[3])]], pad=[int(x) for x in r[5 + int(r[3]):]]))
+        r = words[h["off_items"] + iw * i: h["off_items"] + iw * (i + 1)]
+        nag = int(r[3])
+        items.append(dict(p0=int(r[0]), p1=int(r[1]), leader=int(r[2]), nag=nag, copies=int(r[4]),
+                          agents=[int(x) for x in r[5:5 + nag]], pad=[int(x) for x in r[5 + nag:21]],
+                          first=[int(x) for x in r[21:21 + nag]], first_pad=[int(x) for x in r[21 + nag:37]]))
     blocks = words[h["off_blocks"]: h["off_blocks"] + h["n_blocks"]]
     ptr = words[h["off_ptr"]: h["off_ptr"] + h["n_agents"] + 1]
-    slots = words[h["off_slot"]: h["off_slot"] + int(ptr[-1])]
-    return h, items, blocks, ptr, slots
+    return h, items, blocks, ptr
 
 
 def _synthetic_tables(rng, n_agents, groups, prefix_pages, mid_pages, max_suffix_pages, ps=16):
@@ -264,7 +266,7 @@ def test_decode_plan_items_cover_every_agent_page_once(hq, hkv, r, rope, pps):
         bb, sl = _synthetic_tables(rng, n_agents, groups, pre, mid, suf)
         n_item = rt.decode_plan_default_agents(hq, hkv, r, rope)
         plan = rt.DecodePlan(bb, sl, hq, hkv, 16, pps, r=r, rope=rope)
-        h, items, blocks, ptr, slots = _parse_plan(plan.serialize())
+        h, items, blocks, ptr = _parse_plan(plan.serialize())
         assert h["max_item_agents"] == n_item and (h["rank"], h["rope"]) == (r, int(rope))
         assert n_item <= (16 // g if rope else 16) and n_item <= 4 * (16 // g)
         hpb = h["heads_per_block"]
@@ -272,29 +274,28 @@ def test_decode_plan_items_cover_every_agent_page_once(hq, hkv, r, rope, pps):
         # with head blocks (the LDS-staged kernel) one page of an item fits its 48 KB stage
         assert hpb == 1 or 8192 * hpb + n_item * 64 * r <= 48 * 1024
         seen = np.zeros(bb.shape, np.int32)
-        rows = np.zeros(h["total_rows"], np.int32)
+        owned = [[] for _ in range(n_agents)]
         for it in items:
             assert 0 <= it["p0"] < it["p1"] and it["p1"] - it["p0"] <= 256
             assert 1 <= it["nag"] <= h["max_item_agents"] and it["leader"] == it["agents"][0]
-            assert all(x == -1 for x in it["pad"])
+            assert all(x == -1 for x in it["pad"]) and all(x == -1 for x in it["first_pad"])
             for a in it["agents"]:
                 assert it["p1"] <= (sl[a] + 15) // 16
                 assert (bb[a, it["p0"]:it["p1"]] == bb[it["leader"], it["p0"]:it["p1"]]).all()
                 seen[a, it["p0"]:it["p1"]] += 1
             ng = -(-it["nag"] // (16 // g))
-            it["copies"] = 4 // (1 if ng == 1 else 2 if ng == 2 else 4)
-            rows[it["row_base"]: it["row_base"] + it["copies"] * it["nag"] * g] += 1
+            assert it["copies"] == (4 if rope else 4 // (1 if ng == 1 else 2 if ng == 2 else 4))
+            for j, a in enumerate(it["agents"]):
+                owned[a] += [it["first"][j] + c for c in range(it["copies"])]
         for a in range(n_agents):
             npg = (sl[a] + 15) // 16
             assert (seen[a, :npg] == 1).all() and (seen[a, npg:] == 0).all()
-        assert (rows == 1).all()
+            # every partial of the agent is written by exactly one (item, slot, copy), and the
+            # agent's partials are the contiguous range the CSR names
+            assert sorted(owned[a]) == list(range(int(ptr[a]), int(ptr[a + 1])))
+        assert int(ptr[0]) == 0 and h["total_rows"] == int(ptr[-1]) * g
         ids = [b for b in blocks if b >= 0]
         assert sorted(ids) == list(range(len(items) * (hkv // hpb))) and len(blocks) % 8 == 0
-        for a in range(n_agents):
-            mine = sorted(int(s) // hkv for s in slots[ptr[a]:ptr[a + 1]])
-            want = sorted(it["row_base"] + (c * it["nag"] + it["agents"].index(a)) * g
-                          for it in items if a in it["agents"] for c in range(it["copies"]))
-            assert mine == want and all(int(s) % hkv == 0 for s in slots[ptr[a]:ptr[a + 1]])
         info = plan.info(128, r)
         assert info["workspace_bytes"] == h["total_rows"] * hkv * ((128 + r + 2 + 3) // 4 * 4) * 4
         plan.close()
