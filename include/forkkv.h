@@ -181,7 +181,8 @@ typedef struct {
     int32_t hq, hkv;
     int32_t page_size;
     int32_t max_pages;        /* row stride of base_bt */
-    int32_t pages_per_split;  /* pages per work item (<= 64); 0 = choose automatically */
+    int32_t pages_per_split;  /* pages per work item (<= 128 without RoPE, items of several agent
+                                 groups <= 64; <= 64 with RoPE); 0 = choose automatically */
     int32_t num_cus;          /* compute units to fill; 0 = 256 */
     int32_t max_item_agents;  /* agents sharing one work item; 0 = as many as the kernel takes
                                  (fkv_decode_plan_default_agents); larger values are clamped */
@@ -204,9 +205,16 @@ typedef struct {
  * head layout. */
 int32_t fkv_decode_plan_default_agents(int32_t hq, int32_t hkv, int32_t r, int32_t rope);
 
-/* Build a plan from host block tables (base_bt [n_agents][max_pages], seq_lens [n_agents]). */
+/* Build a plan from host copies of the decode call's tables: base_bt and res_bt
+ * [n_agents][max_pages], seq_lens and adapter_idx [n_agents] (res_bt and adapter_idx may be
+ * NULL when r == 0 or RoPE is on).  Without RoPE the plan holds, per workgroup of the split
+ * kernel, the page ids, sequence lengths and adapters it reads, so the plan must be rebuilt
+ * whenever any of these tables changes (in a serving loop: every decode step).
+ * Errors: FKV_ERR_INVALID for null or inconsistent arguments, FKV_ERR_UNSUPPORTED for
+ * head layouts or ranks the kernels do not take. */
 fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *params, const int32_t *base_bt,
-                                  const int32_t *seq_lens, fkv_plan **out);
+                                  const int32_t *res_bt, const int32_t *seq_lens, const int32_t *adapter_idx,
+                                  fkv_plan **out);
 void fkv_decode_plan_destroy(fkv_plan *plan);
 /* Sizes of the plan; workspace_bytes is computed for head dim d and rank r. */
 fkv_status fkv_decode_plan_info(const fkv_plan *plan, int32_t d, int32_t r, fkv_plan_info *out);

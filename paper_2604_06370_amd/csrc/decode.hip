@@ -47,9 +47,6 @@ constexpr float kNegInf = -INFINITY;
 constexpr int kMaxPagesPerItem = fkv::kMaxPagesPerItem;
 constexpr int kBlockHalfs = PS * D;  // bf16 values in one (page, K|V, head) block
 constexpr int kBlockBytes = kBlockHalfs * 2;
-// Page-table rows staged in LDS run this many entries past an item's last page (loads
-// issued up to three stages ahead of the step being computed stay inside the table).
-constexpr int kTablePad = 12;
 
 struct DecodeArgs {
     const uint16_t *q, *base_kv, *res_kv, *lora_b;
@@ -59,7 +56,7 @@ struct DecodeArgs {
     float *ws;
     uint16_t *out;
     int32_t hq, hkv, max_pages, ws_stride;
-    int32_t off_items, off_blocks, off_ptr, off_zero;  // plan section offsets (words)
+    int32_t off_items, off_blocks, off_ptr, off_zero, off_desc;  // plan section offsets (words)
     float scale_log2;  // softmax scale * log2(e)
 };
 
@@ -240,12 +237,8 @@ struct SplitShape {
     static constexpr int NSW = fkv::decode_wave_slots(G, R);                    // agent slots per wave
     static constexpr int NSR = R > 0 ? NSW : 1;
     static constexpr int MAX_SLOTS = MULTI ? cmin(fkv::kMaxGroups * AG, fkv::kMaxItemAgents) : NSW;
-    static constexpr int RES_SLOTS = R > 0 ? MAX_SLOTS : 0;                     // rCache table row stride
     static constexpr int RES_PAGE = RT * 512;                                   // rCache page (halfs)
     static constexpr int RING_BYTES = 8 * 2 * kBlockHalfs * 2;                  // two buffers of four pages
-    static constexpr int TP = kMaxPagesPerItem + kTablePad;                     // table entries per page row
-    static constexpr int TABLE_BYTES = TP * (1 + RES_SLOTS) * 8;
-    static constexpr int LDS_BYTES = RING_BYTES + TABLE_BYTES;
 };
 
 template <int R, int G>
@@ -256,30 +249,28 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
     constexpr int RTX = S::RTX;
     constexpr int NSW = S::NSW;
     constexpr int NSR = S::NSR;
-    constexpr int RS = S::RES_SLOTS;
     struct CFrag {  // rCache fragments (C_K in .xy, C_V in .zw) of the wave's slots for its step pages
         u32x4 kv[2][NSR][RTX];
     };
-    __shared__ __attribute__((aligned(16))) unsigned char lds[S::LDS_BYTES];
+    __shared__ __attribute__((aligned(16))) unsigned char lds[S::RING_BYTES];
     uint16_t *ring = reinterpret_cast<uint16_t *>(lds);
-    // page tables as device addresses: the K block of (page, head h) for the base pool, and
-    // per page the rCache page of every item slot ([page][slot]; the zero area of the plan
-    // for slots without an adapter and for empty slots).  Rows run kTablePad entries past
-    // the item, repeating its last page, so that loads issued ahead of the end stay valid.
-    uint64_t *s_base = reinterpret_cast<uint64_t *>(lds + S::RING_BYTES);
-    uint64_t *s_res = s_base + S::TP;
 
-    const int32_t *plan = p.plan;
-    const int blk = plan[p.off_blocks + blockIdx.x];
-    if (blk < 0) return;
+    // The block's descriptor holds everything the prologue needs (page range, head, every
+    // slot's agent, length, adapter and first partial, the base page ids and each slot's
+    // rCache page ids), at an address that depends on blockIdx only: one round of
+    // independent loads, after which the first base pages, rCache rows, queries and B_K
+    // slices are all requested together.
+    const int32_t *desc = p.plan + p.off_desc + (int64_t)blockIdx.x * fkv::kDescWords;
+    const int pg0 = desc[fkv::kDescPg0], pg1 = desc[fkv::kDescPg1], nag = desc[fkv::kDescNag];
+    const int h = desc[fkv::kDescHead];
+    const int item_max_len = desc[fkv::kDescMaxLen];
+    const int rstride = desc[fkv::kDescResStride];  // page ids per slot row of the residual table
+    const int npg = pg1 - pg0;
     const int hkv = p.hkv;
-    const int item = blk / hkv;
-    const int h = blk - item * hkv;
-    const int32_t *rec = plan + p.off_items + item * fkv::kItemWords;
-    const int pg0 = rec[0], pg1 = rec[1], leader = rec[2], nag = rec[3];
     const int ng = (nag + AG - 1) / AG;
-    if (pg1 - pg0 > kMaxPagesPerItem || nag > S::MAX_SLOTS || (ng > 1 && !S::MULTI) || (ng == 1 && nag > NSW))
-        return;  // rejected on the host
+    if (nag <= 0 || npg <= 0 || nag > S::MAX_SLOTS || (ng > 1 && !S::MULTI) || (ng == 1 && nag > NSW) ||
+        npg > (ng > 2 ? fkv::kMaxPagesMulti : fkv::kMaxPagesSingle) || (ng > 2 ? rstride != 64 : rstride != 128))
+        return;  // idle block, or rejected on the host
     const int ngp = ng == 1 ? 1 : (ng == 2 ? 2 : 4);   // groups rounded to a divisor of 4
     const int sp = ngp == 4 ? 2 : 4;                   // pages per stage
 
@@ -294,41 +285,40 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
     const int qh = h * G + (col % G);
     const int64_t n = (int64_t)hkv * D;
 
-    // lane i < nag of every wave holds item agent i: id, sequence length, adapter (one
-    // round of parallel loads instead of a chain per agent)
+    // lane i < nag of every wave holds item slot i: agent, sequence length, adapter, first
+    // partial; lane i (and 64 + i) holds the base page id of item page i and, per slot s
+    // of this wave's group, that slot's rCache page id (-1: no adapter)
     const bool lane_ag = lane < nag;
-    const int l_agent = lane_ag ? rec[5 + lane] : 0;
-    const int l_part = lane_ag ? rec[5 + fkv::kMaxItemAgents + lane] : 0;  // first partial of the slot
-    const int l_len = lane_ag ? p.seq_lens[l_agent] : 0;
-    const int l_ad = (R > 0 && lane_ag) ? p.adapter_idx[l_agent] : -1;
-
-    // block-table entries of the item's pages: issued now, written to LDS once the
-    // adapters are known.  Wave w stages rows w, w+4, ... (row 0: base pool of the
-    // leader; row 1+s: rCache pool of item slot s), lane i entry i and 64 + i.
-    const int npg = pg1 - pg0;
-    const int ntp = npg + kTablePad;
-    const int n_rows = 1 + (R > 0 ? (S::MULTI ? ngp * AG : NSW) : 0);
-    constexpr int RPW = (1 + RS + WAVES - 1) / WAVES;
-    int32_t pid[RPW][2];
+    const int l_agent = lane_ag ? desc[fkv::kDescAgent + lane] : 0;
+    const int l_len = lane_ag ? desc[fkv::kDescLen + lane] : 0;
+    const int l_ad = (R > 0 && lane_ag) ? desc[fkv::kDescAdapter + lane] : -1;
+    const int l_part = lane_ag ? desc[fkv::kDescPart + lane] : 0;
+    const int bid0 = desc[fkv::kDescBase + min(lane, npg - 1)];
+    const int bid1 = desc[fkv::kDescBase + min(64 + lane, npg - 1)];
+    int rid0[NSR], rid1[NSR];
 #pragma unroll
-    for (int k = 0; k < RPW; ++k) {
-        const int t = wave + k * WAVES;
-        const int ag_t = __builtin_amdgcn_readlane(l_agent, t > 0 ? (t - 1) & 63 : 0);
-        const int32_t *row = t == 0 ? p.base_bt + (int64_t)leader * p.max_pages
-                                    : p.res_bt + (int64_t)ag_t * p.max_pages;
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-            const int i = lane + 64 * u;
-            pid[k][u] = (t < n_rows && i < ntp && npg > 0) ? row[pg0 + min(i, npg - 1)] : 0;
-        }
+    for (int s = 0; s < NSR; ++s) {
+        const bool ok = R > 0 && s < NSW && sb + s < nag;
+        const int32_t *row = desc + fkv::kDescRes + (ok ? sb + s : 0) * rstride;
+        rid0[s] = ok ? row[min(lane, npg - 1)] : -1;
+        rid1[s] = (ok && rstride > 64) ? row[min(64 + lane, npg - 1)] : -1;
     }
+    // device address of the K block of (item page k, head h); V follows hkv blocks later.
+    // Pages past the item repeat its last page, so loads issued ahead of the end stay valid.
+    auto base_addr = [&](int k) __attribute__((always_inline)) -> uint64_t {
+        k = min(k, npg - 1);
+        const int id = k < 64 ? __builtin_amdgcn_readlane(bid0, k) : __builtin_amdgcn_readlane(bid1, k - 64);
+        return reinterpret_cast<uint64_t>(p.base_kv + ((int64_t)id * 2 * hkv + h) * kBlockHalfs);
+    };
+    // device address of the rCache page of (item page k, wave slot s); the plan's zero area
+    // stands in for a slot without adapter
+    const uint16_t *zero_c = reinterpret_cast<const uint16_t *>(p.plan + p.off_zero);
+    auto res_addr = [&](int k, int s) __attribute__((always_inline)) -> uint64_t {
+        k = min(k, npg - 1);
+        const int id = k < 64 ? __builtin_amdgcn_readlane(rid0[s], k) : __builtin_amdgcn_readlane(rid1[s], k - 64);
+        return reinterpret_cast<uint64_t>(id >= 0 ? p.res_kv + (int64_t)id * S::RES_PAGE : zero_c);
+    };
 
-    // longest sequence of the item: value tokens past it are never read by any row and
-    // are zeroed when a stage is stored (they may hold any bits)
-    int item_max_len = l_len;
-#pragma unroll
-    for (int o = 1; o < 16; o <<= 1) item_max_len = max(item_max_len, __shfl_xor(item_max_len, o));
-    item_max_len = uniform(item_max_len);
     // per slot of the wave's group: adapter (or -1) and sequence length
     int slot_ad[NSR], slot_len[NSR];
     int min_len = 1 << 30, min_res = 1 << 30;  // shortest sequence / rCache among the group's slots
@@ -348,68 +338,50 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
     const int my_agent = row_active ? sh_agent : 0;
     const int my_len = row_active ? sh_len : 0;
 
-    // Q^T fragments (B operand of the 16x16x32 products)
-    const uint16_t *qrow = p.q + ((int64_t)my_agent * p.hq + qh) * D;
-    u32x4 qf[4];
-    load_q(qrow, row_active, grp, qf);
+    // Query fragments and W = B_K q.  Their loads are issued after the first base pages
+    // and rCache rows have been requested (each pipeline below calls this right after its
+    // first loads), so the prologue's latency overlaps the start of the stream.
+    u32x4 qf[4];        // Q^T fragments (B operand of the 16x16x32 products)
+    u32x2 wsel[NSR][RTX];
+    auto prologue_products = [&]() __attribute__((always_inline)) {
+        const uint16_t *qrow = p.q + ((int64_t)my_agent * p.hq + qh) * D;
+        load_q(qrow, row_active, grp, qf);
 
-    // W = B_K q: the contraction over the head dim may take any order that both operands
-    // share, so it uses the natural one (lane holds dims 32kk + 8grp .. +7), in which each
-    // lane reads 16 contiguous bytes of a B_K row and of q
-    u32x4 bkf[NSR][RTX][4], qn[4];
-    if constexpr (R > 0) {
+        // W = B_K q: the contraction over the head dim may take any order that both
+        // operands share, so it uses the natural one (lane holds dims 32kk + 8grp .. +7),
+        // in which each lane reads 16 contiguous bytes of a B_K row and of q
+        u32x4 bkf[NSR][RTX][4], qn[4];
+        if constexpr (R > 0) {
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) qn[kk] = row_active ? ldg128(qrow + 32 * kk + 8 * grp) : u32x4{0, 0, 0, 0};
+            for (int kk = 0; kk < 4; ++kk) qn[kk] = row_active ? ldg128(qrow + 32 * kk + 8 * grp) : u32x4{0, 0, 0, 0};
 #pragma unroll
-        for (int s = 0; s < NSR; ++s) {
-            const uint16_t *bk = p.lora_b + (int64_t)(slot_ad[s] >= 0 ? slot_ad[s] : 0) * 2 * R * n + (int64_t)h * D;
+            for (int s = 0; s < NSR; ++s) {
+                const uint16_t *bk = p.lora_b + (int64_t)(slot_ad[s] >= 0 ? slot_ad[s] : 0) * 2 * R * n + (int64_t)h * D;
 #pragma unroll
-            for (int t = 0; t < RT; ++t) {
-                const int rho = 16 * t + col;
-                const int64_t ro = (int64_t)(rho < R ? rho : 0) * n;
+                for (int t = 0; t < RT; ++t) {
+                    const int rho = 16 * t + col;
+                    const int64_t ro = (int64_t)(rho < R ? rho : 0) * n;
 #pragma unroll
-                for (int kk = 0; kk < 4; ++kk)
-                    bkf[s][t][kk] = (slot_ad[s] >= 0 && rho < R) ? ldg128(bk + ro + 32 * kk + 8 * grp) : u32x4{0, 0, 0, 0};
-            }
-        }
-    }
-
-    // page tables -> LDS, as addresses
-    const uint16_t *zero_c = reinterpret_cast<const uint16_t *>(plan + p.off_zero);
-#pragma unroll
-    for (int k = 0; k < RPW; ++k) {
-        const int t = wave + k * WAVES;
-        const int ad_t = __builtin_amdgcn_readlane(l_ad, t > 0 ? (t - 1) & 63 : 0);
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-            const int i = lane + 64 * u;
-            if (t < n_rows && i < ntp) {
-                if (t == 0) {
-                    s_base[i] = reinterpret_cast<uint64_t>(p.base_kv + ((int64_t)pid[k][u] * 2 * hkv + h) * kBlockHalfs);
-                } else {
-                    const uint16_t *a = (t - 1 < nag && ad_t >= 0) ? p.res_kv + (int64_t)pid[k][u] * S::RES_PAGE : zero_c;
-                    s_res[i * RS + (t - 1)] = reinterpret_cast<uint64_t>(a);
+                    for (int kk = 0; kk < 4; ++kk)
+                        bkf[s][t][kk] = (slot_ad[s] >= 0 && rho < R) ? ldg128(bk + ro + 32 * kk + 8 * grp) : u32x4{0, 0, 0, 0};
                 }
             }
         }
-    }
-
-    // W^T = (B_K q)^T per slot, as the B operand of the residual key products; row
-    // columns of other slots are zero, so one product serves a pair of slots (or tiles)
-    u32x2 wsel[NSR][RTX];
+        // W^T = (B_K q)^T per slot, as the B operand of the residual key products; row
+        // columns of other slots are zero, so one product serves a pair of slots (or tiles)
 #pragma unroll
-    for (int s = 0; s < NSR; ++s)
+        for (int s = 0; s < NSR; ++s)
 #pragma unroll
-        for (int t = 0; t < RTX; ++t) {
-            wsel[s][t] = u32x2{0, 0};
-            if constexpr (R > 0) {
-                f32x4 acc = {0, 0, 0, 0};
+            for (int t = 0; t < RTX; ++t) {
+                wsel[s][t] = u32x2{0, 0};
+                if constexpr (R > 0) {
+                    f32x4 acc = {0, 0, 0, 0};
 #pragma unroll
-                for (int kk = 0; kk < 4; ++kk) acc = mfma32(bkf[s][t][kk], qn[kk], acc);
-                if (my_slot == s) wsel[s][t] = pack4(acc);
+                    for (int kk = 0; kk < 4; ++kk) acc = mfma32(bkf[s][t][kk], qn[kk], acc);
+                    if (my_slot == s) wsel[s][t] = pack4(acc);
+                }
             }
-        }
-    __syncthreads();  // tables staged
+    };
 
     Rows<R> st;
     st.init();
@@ -431,7 +403,7 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
             const int b = wave * NB + j;                 // block of the stage: page b/2, K or V
-            const uint64_t src = s_base[stage * sp + (b >> 1)] + ((b & 1) ? vstride * 2 : 0) + lane * 16;
+            const uint64_t src = base_addr(stage * sp + (b >> 1)) + ((b & 1) ? vstride * 2 : 0) + lane * 16;
 #pragma unroll
             for (int i = 0; i < 4; ++i) bx[FIRST + j][i] = ldg128_at(src + i * 1024);
         }
@@ -476,20 +448,9 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
         if constexpr (R > 0) {
 #pragma unroll
             for (int j = 0; j < NP; ++j) {
-                const uint64_t *e = s_res + (stage * sp + wpage0 + j) * RS + sb;
                 uint64_t a[NSA];
-                if constexpr (NSA % 2 == 0) {
 #pragma unroll
-                    for (int s = 0; s < NSA; s += 2) {
-                        typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
-                        const u64x2 v = *reinterpret_cast<const u64x2 *>(e + s);
-                        a[s] = v.x;
-                        a[s + 1] = v.y;
-                    }
-                } else {
-#pragma unroll
-                    for (int s = 0; s < NSA; ++s) a[s] = e[s];
-                }
+                for (int s = 0; s < NSA; ++s) a[s] = res_addr(stage * sp + wpage0 + j, s);
 #pragma unroll
                 for (int s = 0; s < NSA; ++s) {
 #pragma unroll
@@ -671,6 +632,7 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
             load_blocks(I1{}, N0{}, 0, bx);
             load_blocks(I1{}, I1{}, 1, bx);
             load_c(NSF{}, I2{}, 0, ca);
+            prologue_products();
             store_blocks(I1{}, N0{}, 0, 0, bx);
             load_blocks(I1{}, N0{}, 2, bx);
             __syncthreads();
@@ -694,6 +656,7 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
         auto run = [&](auto nsa_tag, auto np_tag) __attribute__((always_inline)) {
             load_blocks(I2{}, N0{}, 0, bx);
             load_c(nsa_tag, np_tag, 0, ca);
+            prologue_products();
             store_blocks(I2{}, N0{}, 0, 0, bx);
             load_blocks(I2{}, N0{}, 1, bx);
             __syncthreads();
@@ -1145,8 +1108,10 @@ extern "C" fkv_status fkv_residual_attention_decode(const fkv_attn_args *a, cons
     if (w[fkv::H_MAX_ITEM_AGENTS] > fkv::decode_item_agent_cap(g, a->hkv, a->r, rope_on))
         return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: the plan puts more agents in a work item "
                                           "than this kernel takes");
-    if (w[fkv::H_PAGES_PER_SPLIT] > fkv::kMaxPagesPerItem)
-        return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: plan items longer than 64 pages");
+    if (w[fkv::H_PAGES_PER_SPLIT] > (rope_on ? fkv::kMaxPagesPerItem : fkv::kMaxPagesSingle))
+        return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: plan items longer than the kernel takes");
+    if (!rope_on && w[fkv::H_OFF_DESC] < 0)
+        return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: plan has no block descriptors");
     DecodeArgs da;
     da.q = static_cast<const uint16_t *>(a->q);
     da.base_kv = static_cast<const uint16_t *>(a->base_kv);
@@ -1169,6 +1134,7 @@ extern "C" fkv_status fkv_residual_attention_decode(const fkv_attn_args *a, cons
     da.off_blocks = w[fkv::H_OFF_BLOCKS];
     da.off_ptr = w[fkv::H_OFF_AGENT_PTR];
     da.off_zero = w[fkv::H_OFF_ZERO];
+    da.off_desc = w[fkv::H_OFF_DESC];
     da.scale_log2 = a->scale * 1.4426950408889634f;
     const int nb = w[fkv::H_N_BLOCKS];
     hipStream_t hs = static_cast<hipStream_t>(stream);

@@ -35,6 +35,30 @@ constexpr int kMaxGroups = 4;       // agent groups per item (one wave each)
 constexpr int kMaxItemAgents = 16;  // agents per item
 constexpr int kItemWords = 5 + 2 * kMaxItemAgents;
 constexpr int kMaxPagesPerItem = 64;  // upper bound of pages_per_split (block tables are staged in LDS)
+// RoPE-off plans: item page limits of the split kernel, whose page ids travel in lane
+// registers (two per table row: lanes 0..63 and 64..127)
+constexpr int kMaxPagesMulti = 64;    // items of three or four agent groups
+constexpr int kMaxPagesSingle = 128;  // items of one or two agent groups
+
+// Block descriptors (RoPE-off plans): block b of the split kernel reads the
+// kDescWords words at off_desc + b * kDescWords:
+//   [kDescPg0, kDescPg1)  item page range        kDescNag   agents in the item (0: idle block)
+//   kDescHead             KV head                kDescMaxLen longest sequence of the item
+//   kDescResStride        row stride of the rCache page-id table (64 for three or four
+//                         agent groups, else 128)
+//   kDescAgent/Len/Adapter/Part + slot   agent, sequence length, adapter (-1: none) and
+//                         first partial of each item slot
+//   kDescBase + i         base page id of item page i (the pages every agent shares)
+//   kDescRes + s * stride + i   rCache page id of slot s at item page i (-1: no adapter)
+enum DescField { kDescPg0 = 0, kDescPg1, kDescNag, kDescHead, kDescMaxLen, kDescResStride, kDescItem, kDescCopies };
+constexpr int kDescAgent = 8;
+constexpr int kDescLen = kDescAgent + kMaxItemAgents;
+constexpr int kDescAdapter = kDescLen + kMaxItemAgents;
+constexpr int kDescPart = kDescAdapter + kMaxItemAgents;
+constexpr int kDescBase = kDescPart + kMaxItemAgents;
+constexpr int kDescRes = kDescBase + kMaxPagesSingle;
+constexpr int kDescResWords = kMaxItemAgents * kMaxPagesMulti;  // = 8 slots x 128 pages as well
+constexpr int kDescWords = kDescRes + kDescResWords;
 
 // Decode: one workgroup per (work item, KV head).  Without RoPE and with rank below 32 an
 // item holds up to four agent groups (their base pages are shared through LDS); with
@@ -63,7 +87,7 @@ enum PlanHeader {
     H_MAGIC = 0, H_N_ITEMS, H_N_BLOCKS, H_N_AGENTS, H_HKV, H_GROUP, H_AGENTS_PER_ITEM,
     H_OFF_ITEMS, H_OFF_BLOCKS, H_OFF_AGENT_PTR, H_OFF_AGENT_SLOT, H_TOTAL_WORDS, H_PAGES_PER_SPLIT,
     H_PAGE_SIZE, H_N_SEGMENTS, H_TOTAL_ROWS, H_MAX_ITEM_AGENTS, H_HEADS_PER_BLOCK, H_RANK, H_ROPE, H_OFF_ZERO,
-    H_FIELDS
+    H_OFF_DESC, H_FIELDS
 };
 constexpr int kZeroWords = 1024;  // zeroed area of a plan: stand-in rCache page for agents without one
 static_assert(H_FIELDS <= kHeaderWords, "plan header fields overflow the header");

@@ -20,14 +20,22 @@
 
 namespace {
 constexpr int kNumXcd = 8;
+// Estimated time of one item page (in units of a single agent's page) and of an item's
+// prologue, used to size and order the work items.
+double item_page_cost(int32_t agents) { return 1.0 + (double)agents / 32.0; }
+constexpr double kItemOverhead = 8.0;
 }
 
 extern "C" {
 
 fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32_t *base_bt,
-                                  const int32_t *seq_lens, fkv_plan **out) {
+                                  const int32_t *res_bt, const int32_t *seq_lens, const int32_t *adapter_idx,
+                                  fkv_plan **out) {
     fkv::clear_error();
     if (!prm || !base_bt || !seq_lens || !out) return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: null argument");
+    if (prm->r > 0 && prm->rope == 0 && (!res_bt || !adapter_idx))
+        return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: res_bt and adapter_idx are required for r > 0 "
+                                          "without RoPE");
     const int32_t A = prm->n_agents, ps = prm->page_size, mp = prm->max_pages;
     if (A < 1 || prm->hkv < 1 || prm->hq < 1 || ps < 1 || mp < 1 || prm->pages_per_split < 0)
         return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: bad sizes");
@@ -95,34 +103,73 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
         }
         return out;
     };
-    // 3. pages per item: one split size for every segment, chosen so that there are
-    //    about three (item, head block) workgroups per compute unit (with two resident
-    //    workgroups per unit and items of up to four agent groups this measured best:
-    //    longer units pay the per-unit prologue less often, shorter ones balance the
-    //    tail better).  Splits of a segment are made equal instead of a full-size run
-    //    plus a short remainder.
+    // 3. pages per item.
+    //    RoPE off: the split kernel keeps two workgroups per compute unit resident, so the
+    //    items are sized for one round of 2 * num_cus workgroups of equal estimated time.
+    //    A page of an item with more agents costs more (its agents' rCache rows and more
+    //    matrix-core work per base byte; about 1.5x a single agent's page at 16 agents), and
+    //    every item pays a fixed prologue of about eight pages.  The target time per item is
+    //    the smallest for which the splits fit that round (or, when the page limits of an
+    //    item forbid it, the fewest rounds that hold them).  Splits of a segment are equal.
+    //    RoPE on: about three (item, head block) workgroups per compute unit, 64 pages at
+    //    most per item.
     const int64_t cus = prm->num_cus > 0 ? prm->num_cus : 256;
     const int32_t nhb_units = prm->hkv / hpb;
     std::vector<int32_t> seg_pps(segs.size());
     {
-        int64_t units = 0;  // (page x agent chunk) units per head block
-        for (auto &s : segs) units += (int64_t)s.n * (int64_t)chunk_sizes(s.agents.size()).size();
-        // about three (item, head block) workgroups per compute unit
-        const int32_t auto_pps = (int32_t)std::max<int64_t>(
-            4, std::min<int64_t>(fkv::kMaxPagesPerItem, (units * nhb_units + 3 * cus - 1) / (3 * cus)));
+        struct SegCost { int32_t n, cap; double cpp; };  // pages, page limit, cost per page
+        std::vector<SegCost> sc(segs.size());
         for (size_t i = 0; i < segs.size(); ++i) {
-            int32_t pps = prm->pages_per_split > 0 ? prm->pages_per_split : auto_pps;
-            if (pps > fkv::kMaxPagesPerItem)
-                return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: pages_per_split above 64");
-            if (prm->pages_per_split == 0) {
-                const int32_t n_split = (segs[i].n + pps - 1) / pps;
-                pps = (segs[i].n + n_split - 1) / n_split;
+            const std::vector<size_t> ch = chunk_sizes(segs[i].agents.size());
+            double cpp = 0;
+            int32_t cap = fkv::kMaxPagesSingle;
+            for (size_t c : ch) {  // every chunk is an item of its own: the largest sets the time
+                cpp = std::max(cpp, item_page_cost((int32_t)c));
+                if ((c + ag - 1) / ag > 2) cap = fkv::kMaxPagesMulti;
+            }
+            if (rope) cap = fkv::kMaxPagesPerItem;
+            sc[i] = {segs[i].n, cap, cpp};
+        }
+        const double ovh = kItemOverhead;
+        auto n_split = [&](const SegCost &s, double T) {
+            const int64_t by_cap = (s.n + s.cap - 1) / s.cap;
+            const int64_t by_cost = (int64_t)std::ceil((double)s.n * s.cpp / std::max(T - ovh, 1e-9));
+            return std::max<int64_t>(1, std::max(by_cap, by_cost));
+        };
+        auto n_items_at = [&](double T) {
+            int64_t k = 0;
+            for (size_t i = 0; i < sc.size(); ++i) k += n_split(sc[i], T) * (int64_t)chunk_sizes(segs[i].agents.size()).size();
+            return k;
+        };
+        double total = 0;
+        for (auto &s : sc) total += s.n * s.cpp;
+        const int64_t slots = std::max<int64_t>(1, 2 * cus / nhb_units);  // items per round
+        const int64_t min_items = n_items_at(1e30);
+        const int64_t rounds = (min_items + slots - 1) / slots;
+        double lo = ovh, hi = ovh + total + 1.0;
+        for (int it = 0; it < 60; ++it) {
+            const double mid = 0.5 * (lo + hi);
+            if (n_items_at(mid) <= rounds * slots) hi = mid; else lo = mid;
+        }
+        const int32_t rope_pps = (int32_t)std::max<int64_t>(
+            4, std::min<int64_t>(fkv::kMaxPagesPerItem, [&] {
+                int64_t units = 0;
+                for (auto &s : segs) units += (int64_t)s.n * (int64_t)chunk_sizes(s.agents.size()).size();
+                return (units * nhb_units + 3 * cus - 1) / (3 * cus);
+            }()));
+        for (size_t i = 0; i < segs.size(); ++i) {
+            int32_t pps;
+            if (prm->pages_per_split > 0) {
+                if (prm->pages_per_split > fkv::kMaxPagesSingle)
+                    return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: pages_per_split above 128");
+                pps = std::min(prm->pages_per_split, sc[i].cap);
+            } else {
+                const int64_t k = rope ? (segs[i].n + rope_pps - 1) / rope_pps : n_split(sc[i], hi);
+                pps = (int32_t)((segs[i].n + k - 1) / k);
             }
             seg_pps[i] = pps;
         }
     }
-    const double per_page_base = 8.0 * hpb;
-    const double unit_overhead = 12.0 * per_page_base;
 
     // 4. work items, clustered by (segment, split).  An item of ng agent groups runs its
     //    groups on 4 / ngp wave copies (ngp = ng rounded up to 1, 2 or 4), each writing its
@@ -150,7 +197,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
                 for (size_t j = k; j < k + c; ++j) it.agents.push_back(s.agents[j]);
                 k += c;
                 total_rows += (int64_t)it.copies * (int64_t)c * g;
-                it.cost = unit_overhead + (double)(p1 - p0) * (per_page_base + (double)c);
+                it.cost = kItemOverhead + (double)(p1 - p0) * item_page_cost((int32_t)c);
                 cost += it.cost;
                 items.push_back(std::move(it));
             }
@@ -209,7 +256,8 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     const int64_t off_blocks = off_items + (int64_t)n_items * fkv::kItemWords;
     const int64_t off_ptr = off_blocks + n_blocks;
     const int64_t off_zero = (off_ptr + A + 1 + 3) / 4 * 4;
-    const int64_t total = off_zero + fkv::kZeroWords;
+    const int64_t off_desc = off_zero + fkv::kZeroWords;
+    const int64_t total = off_desc + (rope ? 0 : (int64_t)n_blocks * fkv::kDescWords);
     if (total > INT32_MAX) {
         delete pl;
         return fkv::fail(FKV_ERR_UNSUPPORTED, "fkv_decode_plan_create: plan too large");
@@ -237,6 +285,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     w[fkv::H_RANK] = prm->r;
     w[fkv::H_ROPE] = rope ? 1 : 0;
     w[fkv::H_OFF_ZERO] = (int32_t)off_zero;
+    w[fkv::H_OFF_DESC] = rope ? -1 : (int32_t)off_desc;
     for (int32_t i = 0; i < n_items; ++i) {
         int32_t *r = &w[off_items + (int64_t)i * fkv::kItemWords];
         r[0] = items[i].p0;
@@ -255,6 +304,43 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
         w[off_blocks + b] = k < lst.size() ? lst[k] : -1;
     }
     for (int32_t a = 0; a <= A; ++a) w[off_ptr + a] = ptr[a];
+    if (!rope) {
+        // block descriptors: everything the split kernel's prologue reads, at an address
+        // that depends on the block index only
+        for (int32_t b = 0; b < n_blocks; ++b) {
+            int32_t *d = &w[off_desc + (int64_t)b * fkv::kDescWords];
+            const int32_t blk = w[off_blocks + b];
+            if (blk < 0) continue;  // idle: nag = 0
+            const int32_t i = blk / nhb;
+            const Item &it = items[i];
+            const int32_t nag = (int32_t)it.agents.size();
+            const int32_t ng = (nag + ag - 1) / ag;
+            const int32_t stride = ng > 2 ? fkv::kMaxPagesMulti : fkv::kMaxPagesSingle;
+            int32_t max_len = 0;
+            for (int32_t a : it.agents) max_len = std::max(max_len, seq_lens[a]);
+            d[fkv::kDescPg0] = it.p0;
+            d[fkv::kDescPg1] = it.p1;
+            d[fkv::kDescNag] = nag;
+            d[fkv::kDescHead] = (blk % nhb) * hpb;
+            d[fkv::kDescMaxLen] = max_len;
+            d[fkv::kDescResStride] = stride;
+            d[fkv::kDescItem] = i;
+            d[fkv::kDescCopies] = it.copies;
+            const int32_t leader = it.agents[0];
+            for (int32_t k = it.p0; k < it.p1; ++k)
+                d[fkv::kDescBase + (k - it.p0)] = base_bt[(int64_t)leader * mp + k];
+            for (int32_t j = 0; j < nag; ++j) {
+                const int32_t a = it.agents[j];
+                const int32_t ad = prm->r > 0 ? adapter_idx[a] : -1;
+                d[fkv::kDescAgent + j] = a;
+                d[fkv::kDescLen + j] = seq_lens[a];
+                d[fkv::kDescAdapter + j] = ad;
+                d[fkv::kDescPart + j] = first[i][j];
+                for (int32_t k = it.p0; k < it.p1; ++k)
+                    d[fkv::kDescRes + j * stride + (k - it.p0)] = ad >= 0 ? res_bt[(int64_t)a * mp + k] : -1;
+            }
+        }
+    }
     for (auto &s : segs) {
         pl->seg_first_page.push_back(s.first);
         pl->seg_n_pages.push_back(s.n);

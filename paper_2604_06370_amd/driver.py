@@ -115,7 +115,8 @@ class LoadedWorkload:
         agents = list(wl.decode_agents() if agents is None else agents)
         bb, rb, sl = self.tree.block_tables(agents, self.max_pages)
         plan = rt.DecodePlan(bb, sl, wl.hq, wl.hkv, wl.page_size, self.pages_per_split,
-                             max_item_agents=self.item_agents, r=wl.r, rope=self.rope)
+                             max_item_agents=self.item_agents, r=wl.r, rope=self.rope, res_bt=rb,
+                             adapter_idx=self.adapter_idx_host[agents])
         info = plan.info(wl.d, wl.r)
         dev = self.device
         q_rows = torch.tensor([int(wl.q_offset[a]) for a in agents], device=dev)

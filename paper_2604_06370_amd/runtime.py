@@ -125,13 +125,21 @@ class DecodePlan:
 
     def __init__(self, base_bt: np.ndarray, seq_lens: np.ndarray, hq: int, hkv: int, page_size: int,
                  pages_per_split: int = 0, num_cus: int = 0, max_item_agents: int = 0, r: int = 0,
-                 rope: bool = False):
+                 rope: bool = False, res_bt: Optional[np.ndarray] = None,
+                 adapter_idx: Optional[np.ndarray] = None):
         bb = np.ascontiguousarray(base_bt, dtype=np.int32)
         sl = np.ascontiguousarray(seq_lens, dtype=np.int32)
+        rb = np.ascontiguousarray(res_bt, dtype=np.int32) if res_bt is not None else None
+        ad = np.ascontiguousarray(adapter_idx, dtype=np.int32) if adapter_idx is not None else None
+        if rb is not None and rb.shape != bb.shape:
+            raise ValueError("res_bt must have the shape of base_bt")
+        if ad is not None and ad.shape != (bb.shape[0],):
+            raise ValueError("adapter_idx must hold one entry per agent")
         prm = N.fkv_decode_plan_params(bb.shape[0], hq, hkv, page_size, bb.shape[1], pages_per_split, num_cus,
                                        max_item_agents, r, int(bool(rope)))
         h = N.c_vp()
-        check(N.fkv_decode_plan_create(ctypes.byref(prm), _ptr(bb), _ptr(sl), ctypes.byref(h)),
+        check(N.fkv_decode_plan_create(ctypes.byref(prm), _ptr(bb), _ptr(rb) if rb is not None else None, _ptr(sl),
+                                       _ptr(ad) if ad is not None else None, ctypes.byref(h)),
               "fkv_decode_plan_create")
         self._h = h
         self.n_agents = bb.shape[0]

@@ -159,7 +159,8 @@ def test_decode_plan_segments_follow_the_fork_tree():
         t.fork(a, a, toks)
         agents.append(a)
     bb, rb, sl = t.block_tables(agents, 64)
-    plan = rt.DecodePlan(bb, sl, hq=8, hkv=2, page_size=ps, pages_per_split=8, r=16)
+    plan = rt.DecodePlan(bb, sl, hq=8, hkv=2, page_size=ps, pages_per_split=8, r=16, res_bt=rb,
+                         adapter_idx=np.arange(len(agents), dtype=np.int32))
     segs = plan.segments()
     assert segs[0] == (0, 32, [0, 1, 2, 3, 4, 5])
     assert (32, 4, [0, 2]) in segs and (32, 4, [1, 3]) in segs
@@ -214,7 +215,7 @@ def test_attention_entry_points_reject_bad_arguments_before_launching():
 def _parse_plan(words):
     """Decode the serialised plan (layout of internal.hpp) into items, blocks and the CSR."""
     H = dict(n_items=1, n_blocks=2, n_agents=3, hkv=4, g=5, off_items=7, off_blocks=8, off_ptr=9,
-             total_rows=15, max_item_agents=16, heads_per_block=17, rank=18, rope=19)
+             total_rows=15, max_item_agents=16, heads_per_block=17, rank=18, rope=19, off_desc=21)
     h = {k: int(words[v]) for k, v in H.items()}
     items = []
     iw = 5 + 2 * 16
@@ -227,6 +228,23 @@ def _parse_plan(words):
     blocks = words[h["off_blocks"]: h["off_blocks"] + h["n_blocks"]]
     ptr = words[h["off_ptr"]: h["off_ptr"] + h["n_agents"] + 1]
     return h, items, blocks, ptr
+
+
+# block descriptor layout (RoPE-off plans): header words, then per-slot arrays, base ids, rCache ids
+DESC_AGENT, DESC_LEN, DESC_AD, DESC_PART, DESC_BASE, DESC_RES = 8, 24, 40, 56, 72, 200
+DESC_WORDS = DESC_RES + 16 * 64
+
+
+def _parse_desc(words, h):
+    out = []
+    for b in range(h["n_blocks"]):
+        d = np.asarray(words[h["off_desc"] + b * DESC_WORDS: h["off_desc"] + (b + 1) * DESC_WORDS])
+        nag = int(d[2])
+        out.append(dict(p0=int(d[0]), p1=int(d[1]), nag=nag, head=int(d[3]), max_len=int(d[4]), stride=int(d[5]),
+                        item=int(d[6]), copies=int(d[7]), agents=d[DESC_AGENT:DESC_AGENT + nag].tolist(),
+                        lens=d[DESC_LEN:DESC_LEN + nag].tolist(), ads=d[DESC_AD:DESC_AD + nag].tolist(),
+                        parts=d[DESC_PART:DESC_PART + nag].tolist(), base=d[DESC_BASE:DESC_RES], res=d[DESC_RES:]))
+    return out
 
 
 def _synthetic_tables(rng, n_agents, groups, prefix_pages, mid_pages, max_suffix_pages, ps=16):
@@ -264,9 +282,12 @@ def test_decode_plan_items_cover_every_agent_page_once(hq, hkv, r, rope, pps):
     g = hq // hkv
     for n_agents, groups, pre, mid, suf in [(16, 1, 300, 0, 40), (37, 3, 64, 9, 5), (5, 5, 0, 3, 2)]:
         bb, sl = _synthetic_tables(rng, n_agents, groups, pre, mid, suf)
+        rb = (bb + 7) * 3 + np.arange(bb.shape[1])[None, :]  # any distinct ids
+        ad = np.where(np.arange(n_agents) % 5 == 4, -1, (np.arange(n_agents) * 7) % 11).astype(np.int32)
         n_item = rt.decode_plan_default_agents(hq, hkv, r, rope)
-        plan = rt.DecodePlan(bb, sl, hq, hkv, 16, pps, r=r, rope=rope)
-        h, items, blocks, ptr = _parse_plan(plan.serialize())
+        plan = rt.DecodePlan(bb, sl, hq, hkv, 16, pps, r=r, rope=rope, res_bt=rb, adapter_idx=ad)
+        words = plan.serialize()
+        h, items, blocks, ptr = _parse_plan(words)
         assert h["max_item_agents"] == n_item and (h["rank"], h["rope"]) == (r, int(rope))
         assert n_item <= (16 // g if rope else 16) and n_item <= 4 * (16 // g)
         hpb = h["heads_per_block"]
@@ -296,6 +317,30 @@ def test_decode_plan_items_cover_every_agent_page_once(hq, hkv, r, rope, pps):
         assert int(ptr[0]) == 0 and h["total_rows"] == int(ptr[-1]) * g
         ids = [b for b in blocks if b >= 0]
         assert sorted(ids) == list(range(len(items) * (hkv // hpb))) and len(blocks) % 8 == 0
+        if rope:
+            assert h["off_desc"] == -1
+        else:
+            # each block's descriptor restates its item and head, the leader's base page ids
+            # and every slot's rCache page ids (-1 without adapter), within the page limits
+            for blk, dsc in zip(blocks, _parse_desc(words, h)):
+                if blk < 0:
+                    assert dsc["nag"] == 0
+                    continue
+                it = items[blk // hkv]
+                assert (dsc["p0"], dsc["p1"], dsc["nag"], dsc["head"], dsc["item"], dsc["copies"]) == \
+                    (it["p0"], it["p1"], it["nag"], blk % hkv, blk // hkv, it["copies"])
+                npg = it["p1"] - it["p0"]
+                ng = -(-it["nag"] // (16 // g))
+                assert dsc["stride"] == (64 if ng > 2 else 128) and npg <= dsc["stride"]
+                assert dsc["agents"] == it["agents"] and dsc["parts"] == it["first"]
+                assert dsc["lens"] == [int(sl[a]) for a in it["agents"]] and dsc["max_len"] == max(dsc["lens"])
+                exp_ad = [int(ad[a]) if r > 0 else -1 for a in it["agents"]]
+                assert dsc["ads"] == exp_ad
+                assert (dsc["base"][:npg] == bb[it["leader"], it["p0"]:it["p1"]]).all()
+                for j, a in enumerate(it["agents"]):
+                    row = dsc["res"][j * dsc["stride"]: j * dsc["stride"] + npg]
+                    exp = rb[a, it["p0"]:it["p1"]] if exp_ad[j] >= 0 else np.full(npg, -1)
+                    assert (row == exp).all()
         info = plan.info(128, r)
         assert info["workspace_bytes"] == h["total_rows"] * hkv * ((128 + r + 2 + 3) // 4 * 4) * 4
         plan.close()
