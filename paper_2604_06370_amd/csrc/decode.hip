@@ -61,6 +61,72 @@ struct DecodeArgs {
 };
 
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
+
+// Base-page ring of the multi-group decode path: kRing stages of two pages (K and V
+// blocks of one head), written by direct memory-to-LDS copies.
+typedef __attribute__((address_space(3))) u32x4 LdsU32x4;
+constexpr int kRing = 4;
+constexpr int kStageBytes = 4 * kBlockBytes;
+
+// Copies from global memory straight into LDS (buffer_load ... lds).  The buffer
+// resource names one 4 KB block (its address is wave-uniform); lane i's 16 bytes at
+// block offset voff (its own) land at dst + 16 i.  The per-lane offset registers are
+// the same for every block, so no address register is rewritten while copies are in
+// flight.
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+__device__ void raw_buffer_load_lds(i32x4 rsrc, __attribute__((address_space(3))) uint32_t *lds, int size, int voffset,
+                                    int soffset, int offset, int aux) __asm("llvm.amdgcn.raw.buffer.load.lds");
+__device__ __forceinline__ i32x4 block_rsrc(uint64_t base, int bytes = kBlockBytes) {
+    i32x4 r;
+    r.x = __builtin_amdgcn_readfirstlane((int)(uint32_t)base);
+    r.y = __builtin_amdgcn_readfirstlane((int)(uint32_t)(base >> 32));
+    r.z = bytes;       // bytes addressable through the resource
+    r.w = 0x00020000;  // raw 32-bit data format
+    return r;
+}
+// 16-byte buffer load into registers (the same per-lane offset register for every block,
+// a wave-uniform resource naming the block).
+__device__ i32x4 raw_buffer_load_b128(i32x4 rsrc, int voffset, int soffset, int aux) __asm("llvm.amdgcn.raw.buffer.load.v4i32");
+__device__ __forceinline__ u32x4 buf_load16(i32x4 rsrc, int voff) {
+    return __builtin_bit_cast(u32x4, raw_buffer_load_b128(rsrc, voff, 0, 0));
+}
+__device__ __forceinline__ void lds_dma16(i32x4 rsrc, int voff, LdsU32x4 *dst) {
+    raw_buffer_load_lds(rsrc, reinterpret_cast<__attribute__((address_space(3))) uint32_t *>(dst), 16, voff, 0, 0, 0);
+}
+
+// LDS byte address of a ring location.
+__device__ __forceinline__ uint32_t lds_addr(const LdsU32x4 *p) {
+    return (uint32_t)reinterpret_cast<uintptr_t>(p);
+}
+// Four 16-byte LDS reads at addr, addr + 1 KB, + 2 KB, + 3 KB (addr: this lane's byte
+// address), completed before the group ends.
+__device__ __forceinline__ void lds_read4(uint32_t addr, u32x4 (&out)[4]) {
+    asm volatile(
+        "ds_read_b128 %0, %4\n\t"
+        "ds_read_b128 %1, %4 offset:1024\n\t"
+        "ds_read_b128 %2, %4 offset:2048\n\t"
+        "ds_read_b128 %3, %4 offset:3072\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(out[0]), "=&v"(out[1]), "=&v"(out[2]), "=&v"(out[3])  // early clobber: the address stays intact
+        : "v"(addr)
+        : "memory");
+}
+
+// Wait until at most N vector-memory operations of this wave are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+// Ring stage hand-over: this wave's copies older than its last N vector-memory operations
+// have landed in LDS (and its LDS reads of the previous stage completed inside their own
+// instruction groups), then all waves meet.  A plain barrier: the copies are ordered by
+// the count, not by a memory fence that would wait for every copy still in flight.
+template <int N>
+__device__ __forceinline__ void stage_barrier() {
+    wait_vmcnt<N>();
+    __builtin_amdgcn_s_barrier();
+}
 constexpr int cmin(int a, int b) { return a < b ? a : b; }
 
 // Partial row record in the workspace (floats): acc[D], acc_r[R], m, l; stride
@@ -238,7 +304,6 @@ struct SplitShape {
     static constexpr int NSR = R > 0 ? NSW : 1;
     static constexpr int MAX_SLOTS = MULTI ? cmin(fkv::kMaxGroups * AG, fkv::kMaxItemAgents) : NSW;
     static constexpr int RES_PAGE = RT * 512;                                   // rCache page (halfs)
-    static constexpr int RING_BYTES = 8 * 2 * kBlockHalfs * 2;                  // two buffers of four pages
 };
 
 template <int R, int G>
@@ -252,8 +317,7 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
     struct CFrag {  // rCache fragments (C_K in .xy, C_V in .zw) of the wave's slots for its step pages
         u32x4 kv[2][NSR][RTX];
     };
-    __shared__ __attribute__((aligned(16))) unsigned char lds[S::RING_BYTES];
-    uint16_t *ring = reinterpret_cast<uint16_t *>(lds);
+    __shared__ __attribute__((aligned(16))) u32x4 lds_ring[kRing * kStageBytes / 16];
 
     // The block's descriptor holds everything the prologue needs (page range, head, every
     // slot's agent, length, adapter and first partial, the base page ids and each slot's
@@ -272,7 +336,6 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
         npg > (ng > 2 ? fkv::kMaxPagesMulti : fkv::kMaxPagesSingle) || (ng > 2 ? rstride != 64 : rstride != 128))
         return;  // idle block, or rejected on the host
     const int ngp = ng == 1 ? 1 : (ng == 2 ? 2 : 4);   // groups rounded to a divisor of 4
-    const int sp = ngp == 4 ? 2 : 4;                   // pages per stage
 
     const int lane = threadIdx.x & 63;
     const int wave = uniform(threadIdx.x >> 6);
@@ -305,9 +368,12 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
     }
     // device address of the K block of (item page k, head h); V follows hkv blocks later.
     // Pages past the item repeat its last page, so loads issued ahead of the end stay valid.
+    // (both table halves are read and the half is chosen on the scalar unit: no branch and
+    // no vector temporary)
     auto base_addr = [&](int k) __attribute__((always_inline)) -> uint64_t {
         k = min(k, npg - 1);
-        const int id = k < 64 ? __builtin_amdgcn_readlane(bid0, k) : __builtin_amdgcn_readlane(bid1, k - 64);
+        const int lo = __builtin_amdgcn_readlane(bid0, k & 63), hi = __builtin_amdgcn_readlane(bid1, k & 63);
+        const int id = k < 64 ? lo : hi;
         return reinterpret_cast<uint64_t>(p.base_kv + ((int64_t)id * 2 * hkv + h) * kBlockHalfs);
     };
     // device address of the rCache page of (item page k, wave slot s); the plan's zero area
@@ -315,7 +381,8 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
     const uint16_t *zero_c = reinterpret_cast<const uint16_t *>(p.plan + p.off_zero);
     auto res_addr = [&](int k, int s) __attribute__((always_inline)) -> uint64_t {
         k = min(k, npg - 1);
-        const int id = k < 64 ? __builtin_amdgcn_readlane(rid0[s], k) : __builtin_amdgcn_readlane(rid1[s], k - 64);
+        const int lo = __builtin_amdgcn_readlane(rid0[s], k & 63), hi = __builtin_amdgcn_readlane(rid1[s], k & 63);
+        const int id = k < 64 ? lo : hi;
         return reinterpret_cast<uint64_t>(id >= 0 ? p.res_kv + (int64_t)id * S::RES_PAGE : zero_c);
     };
 
@@ -386,87 +453,34 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
     Rows<R> st;
     st.init();
     const float cl = p.scale_log2;
+    const int64_t vbytes = (int64_t)hkv * kBlockBytes;  // K block -> V block of a (page, head)
 
-    // ---- loads ----
-    // Base blocks travel memory -> registers -> LDS ring.  Four groups: two 16 KB buffers
-    // of one stage (two pages), each wave loading one 4 KB block per stage two stages
-    // ahead; otherwise two 32 KB buffers (four pages), two blocks per wave one stage ahead.
-    // A stage buffer holds page pairs [K even | K odd | V low half | V high half]: the two
-    // value halves interleave the pair's pages so that one 16-byte LDS read gives the
-    // 32-key operand of a value product.  Loads past the item read the padded tables: every
-    // loop iteration issues the same loads, so the compiler's vmcnt bookkeeping stays exact.
-    const int n_stages = (npg + sp - 1) / sp;
-    const int buf_halfs = sp * 2 * kBlockHalfs;
-    const int64_t vstride = (int64_t)hkv * kBlockHalfs;  // K block -> V block of a (page, head)
-    auto load_blocks = [&](auto nb_tag, auto first_tag, int stage, u32x4 (&bx)[2][4]) __attribute__((always_inline)) {
-        constexpr int NB = decltype(nb_tag)::value, FIRST = decltype(first_tag)::value;
-#pragma unroll
-        for (int j = 0; j < NB; ++j) {
-            const int b = wave * NB + j;                 // block of the stage: page b/2, K or V
-            const uint64_t src = base_addr(stage * sp + (b >> 1)) + ((b & 1) ? vstride * 2 : 0) + lane * 16;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) bx[FIRST + j][i] = ldg128_at(src + i * 1024);
-        }
-    };
-    auto store_blocks = [&](auto nb_tag, auto first_tag, int buf, int stage, u32x4 (&bx)[2][4]) __attribute__((always_inline)) {
-        constexpr int NB = decltype(nb_tag)::value, FIRST = decltype(first_tag)::value;
-#pragma unroll
-        for (int j = 0; j < NB; ++j) {
-            const int b = wave * NB + j;
-            const int pb = b >> 1;  // page of the stage
-            uint16_t *pair = ring + buf * buf_halfs + (pb >> 1) * 4 * kBlockHalfs;
-            if (b & 1) {
-                // a V block: zero the tokens past the item's longest sequence
-                const int vis = item_max_len - (pg0 + stage * sp + pb) * PS;
-                if (vis < PS) {
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const u32x2 lo = mask4(u32x2{bx[FIRST + j][i].x, bx[FIRST + j][i].y}, vis, grp);
-                        const u32x2 hi = mask4(u32x2{bx[FIRST + j][i].z, bx[FIRST + j][i].w}, vis, grp);
-                        bx[FIRST + j][i] = u32x4{lo.x, lo.y, hi.x, hi.y};
-                    }
-                }
-                uint16_t *vlo = pair + 2 * kBlockHalfs + (pb & 1) * 4;
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int o = (i * 64 + lane) * 8;
-                    *reinterpret_cast<u32x2 *>(vlo + o) = u32x2{bx[FIRST + j][i].x, bx[FIRST + j][i].y};
-                    *reinterpret_cast<u32x2 *>(vlo + kBlockHalfs + o) = u32x2{bx[FIRST + j][i].z, bx[FIRST + j][i].w};
-                }
-            } else {
-                uint16_t *dst = pair + (pb & 1) * kBlockHalfs;
-#pragma unroll
-                for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4 *>(dst + i * 512 + lane * 8) = bx[FIRST + j][i];
-            }
-        }
-    };
-    // rCache fragments of the wave's slots for its pages of a stage (NSA slots, 1 or NSR):
-    // one 16-byte load per (page, slot, rank tile), at the address the table holds
-    const int wpage0 = ngp == 4 ? 0 : (ngp == 2 ? 2 * copy : copy);  // first stage page it computes
-    auto load_c = [&](auto nsa_tag, auto np_tag, int stage, CFrag &c) __attribute__((always_inline)) {
+    // rCache fragments of the wave's slots (NSA: 1 or NSR) for NP item pages from k0: one
+    // 16-byte load per (page, slot, rank tile), at the address the descriptor names
+    auto load_c = [&](auto nsa_tag, auto np_tag, int k0, CFrag &c) __attribute__((always_inline)) {
         constexpr int NSA = decltype(nsa_tag)::value, NP = decltype(np_tag)::value;
         if constexpr (R > 0) {
 #pragma unroll
-            for (int j = 0; j < NP; ++j) {
-                uint64_t a[NSA];
-#pragma unroll
-                for (int s = 0; s < NSA; ++s) a[s] = res_addr(stage * sp + wpage0 + j, s);
+            for (int j = 0; j < NP; ++j)
 #pragma unroll
                 for (int s = 0; s < NSA; ++s) {
+                    const i32x4 rs = block_rsrc(res_addr(k0 + j, s), RT * 1024);
 #pragma unroll
-                    for (int t = 0; t < RT; ++t) c.kv[j][s][t] = ldg128_at(a[s] + t * 1024 + lane * 16);
+                    for (int t = 0; t < RT; ++t) c.kv[j][s][t] = buf_load16(rs, lane * 16 + t * 1024);
                 }
-            }
         }
     };
 
-    // ---- one step: NP pages starting at stage page wpage0 of LDS buffer buf ----
-    auto step = [&](auto nsa_tag, auto np_tag, int buf, int stage, CFrag &c) __attribute__((always_inline)) {
+    // ---- Stages 1-2 for NP item pages from k0, fragments in registers ----
+    // kf[j][kk]: K fragments of page j (A operand of S^T = K Q^T, 32 head dims per kk);
+    // vf[j][q2]: the page's value chunk q2 in its stored order, dims 32q2 + col (.xy) and
+    // 32q2 + 16 + col (.zw) of tokens 4grp .. 4grp + 3.  For two pages the value product
+    // takes 32 keys: the pair's two 8-byte halves form one 16x16x32 operand.
+    auto compute = [&](auto nsa_tag, auto np_tag, int k0, auto &&get_k, auto &&get_v, CFrag &c)
+        __attribute__((always_inline)) {
         constexpr int NSA = decltype(nsa_tag)::value;
         constexpr int NP = decltype(np_tag)::value;
-        const int pgw = pg0 + stage * sp + wpage0;         // logical page of step page 0
-        const uint16_t *pair = ring + buf * buf_halfs + (wpage0 >> 1) * 4 * kBlockHalfs;
-        const int half = NP == 2 ? 0 : (wpage0 & 1);       // one-page steps: the page's place in its pair
+        const int pgw = pg0 + k0;  // logical page of step page 0
         // rCache tokens past a slot's own length, or on a padding page, are unwritten: zero
         // them (one uniform branch; pages inside every rCache of the group skip it)
         if constexpr (R > 0) {
@@ -498,14 +512,14 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
             return v;
         };
         // scores S^T = K_base Q^T + C_K (W)^T
+        u32x4 kf[NP][4];
+        get_k(kf);
         f32x4 sacc[NP];
 #pragma unroll
         for (int j = 0; j < NP; ++j) {
-            const uint16_t *kb = pair + (half + j) * kBlockHalfs;
             sacc[j] = f32x4{0, 0, 0, 0};
 #pragma unroll
-            for (int kk = 0; kk < 4; ++kk)
-                sacc[j] = mfma32(*reinterpret_cast<const u32x4 *>(kb + kk * 512 + lane * 8), qf[kk], sacc[j]);
+            for (int kk = 0; kk < 4; ++kk) sacc[j] = mfma32(kf[j][kk], qf[kk], sacc[j]);
         }
         if constexpr (R > 0) {
             constexpr int NU = NSA * RT;  // (slot, tile) units, taken in pairs
@@ -576,15 +590,30 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
             pf[j] = pack4(pv);
         }
         st.l += psum;
+        u32x4 vf[NP][4];
+        get_v(vf);
+        // value tokens past the item's longest sequence (or on a padding page) may hold any
+        // bits: zero them so that their zero weights cannot meet a NaN
+        if (pgw + NP > pg1 || (pgw + NP) * PS > item_max_len) {
+#pragma unroll
+            for (int j = 0; j < NP; ++j) {
+                const int vis = pgw + j < pg1 ? item_max_len - (pgw + j) * PS : 0;
+#pragma unroll
+                for (int q2 = 0; q2 < 4; ++q2) {
+                    const u32x2 lo = mask4(u32x2{vf[j][q2].x, vf[j][q2].y}, vis, grp);
+                    const u32x2 hi = mask4(u32x2{vf[j][q2].z, vf[j][q2].w}, vis, grp);
+                    vf[j][q2] = u32x4{lo.x, lo.y, hi.x, hi.y};
+                }
+            }
+        }
         // O^T += V^T P^T and acc_r^T += C_V^T P^T (rows of other slots masked out of P)
-        const uint16_t *vlo = pair + 2 * kBlockHalfs;
         if constexpr (NP == 2) {
             const u32x4 pb = u32x4{pf[0].x, pf[0].y, pf[1].x, pf[1].y};
 #pragma unroll
-            for (int mt = 0; mt < 8; ++mt) {
-                // V^T rows 16mt.. of both pages, the 32-key operand of one product
-                const u32x4 v = *reinterpret_cast<const u32x4 *>(vlo + (mt & 1) * kBlockHalfs + ((mt >> 1) * 64 + lane) * 8);
-                st.oacc[mt] = mfma32(v, pb, st.oacc[mt]);
+            for (int q2 = 0; q2 < 4; ++q2) {
+                st.oacc[2 * q2] = mfma32(u32x4{vf[0][q2].x, vf[0][q2].y, vf[1][q2].x, vf[1][q2].y}, pb, st.oacc[2 * q2]);
+                st.oacc[2 * q2 + 1] =
+                    mfma32(u32x4{vf[0][q2].z, vf[0][q2].w, vf[1][q2].z, vf[1][q2].w}, pb, st.oacc[2 * q2 + 1]);
             }
             if constexpr (R > 0) {
 #pragma unroll
@@ -600,11 +629,8 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
         } else {
 #pragma unroll
             for (int q2 = 0; q2 < 4; ++q2) {
-                const int o = (q2 * 64 + lane) * 8 + half * 4;
-                const u32x2 a = *reinterpret_cast<const u32x2 *>(vlo + o);
-                const u32x2 b = *reinterpret_cast<const u32x2 *>(vlo + kBlockHalfs + o);
-                st.oacc[2 * q2] = mfma16(a, pf[0], st.oacc[2 * q2]);
-                st.oacc[2 * q2 + 1] = mfma16(b, pf[0], st.oacc[2 * q2 + 1]);
+                st.oacc[2 * q2] = mfma16(u32x2{vf[0][q2].x, vf[0][q2].y}, pf[0], st.oacc[2 * q2]);
+                st.oacc[2 * q2 + 1] = mfma16(u32x2{vf[0][q2].z, vf[0][q2].w}, pf[0], st.oacc[2 * q2 + 1]);
             }
             if constexpr (R > 0) {
 #pragma unroll
@@ -621,68 +647,139 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
     using I2 = std::integral_constant<int, 2>;
     using NSF = std::integral_constant<int, NSR>;
 
-    CFrag ca, cb;
-    u32x4 bx[2][4];
-    using N0 = std::integral_constant<int, 0>;
-    if (npg <= 0) {
-        // an empty item only reports empty partial rows
-    } else if (ngp == 4) {
-        // four groups: bx[1] holds stage s+1 and bx[0] stage s+2 while stage s is computed
+    if (ngp > 1) {
         if constexpr (S::MULTI) {
-            load_blocks(I1{}, N0{}, 0, bx);
-            load_blocks(I1{}, I1{}, 1, bx);
-            load_c(NSF{}, I2{}, 0, ca);
-            prologue_products();
-            store_blocks(I1{}, N0{}, 0, 0, bx);
-            load_blocks(I1{}, N0{}, 2, bx);
-            __syncthreads();
-            for (int s = 0;;) {
-                load_c(NSF{}, I2{}, s + 1, cb);
-                step(NSF{}, I2{}, s & 1, s, ca);
-                store_blocks(I1{}, I1{}, (s + 1) & 1, s + 1, bx);
-                load_blocks(I1{}, I1{}, s + 3, bx);
-                __syncthreads();
-                if (++s >= n_stages) break;
-                load_c(NSF{}, I2{}, s + 1, ca);
-                step(NSF{}, I2{}, s & 1, s, cb);
-                store_blocks(I1{}, N0{}, (s + 1) & 1, s + 1, bx);
-                load_blocks(I1{}, N0{}, s + 3, bx);
-                __syncthreads();
-                if (++s >= n_stages) break;
-            }
+            // Several agent groups share each base page through an LDS ring of kRing stages
+            // of two pages ([K p0 | V p0 | K p1 | V p1], 4 KB each).  Memory writes a stage
+            // straight into LDS (global_load_lds, no registers): wave w copies block w of
+            // stage s + kRing - 1 while stage s is computed.  Four groups: every wave computes
+            // both pages for its group; two groups: wave (group, copy) computes page `copy`.
+            // rCache fragments go to registers two stages ahead.
+            constexpr int NPW_MAX = 2;
+            const int npw = ngp == 4 ? 2 : 1;
+            const int n_stages = (npg + 1) / 2;
+            auto dma_stage = [&](int stage, LdsU32x4 *__restrict__ buf) __attribute__((always_inline)) {
+                const i32x4 rs = block_rsrc(base_addr(2 * stage + (wave >> 1)) + ((wave & 1) ? vbytes : 0));
+                LdsU32x4 *dst = buf + wave * (kBlockBytes / 16);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) lds_dma16(rs, lane * 16 + i * 1024, dst + i * 64);
+            };
+            auto ring_buf = [&](int stage) __attribute__((always_inline)) -> LdsU32x4 * {
+                return (LdsU32x4 *)(lds_ring + (stage % kRing) * (kStageBytes / 16));
+            };
+            // One iteration: request the rCache rows of stage s + 2, copy stage s + kRing - 1
+            // into its ring buffer, compute stage s.  The ring is read with explicit LDS
+            // reads whose wait is part of the same instruction group: the compiler sees no
+            // LDS load that it would have to order after the copies still in flight, which
+            // are waited for (by count) before the barrier that precedes each stage.
+            auto iterate = [&](auto nsa_tag, auto np_tag, int s, CFrag &c_now, CFrag &c_next2) __attribute__((always_inline)) {
+                constexpr int NP = decltype(np_tag)::value;
+                load_c(nsa_tag, np_tag, 2 * (s + 2) + (NP == 2 ? 0 : copy), c_next2);
+                dma_stage(s + kRing - 1, ring_buf(s + kRing - 1));
+                const uint32_t cur = lds_addr(ring_buf(s)) + lane * 16;
+                auto get_k = [&](u32x4 (&kf)[NP][4]) __attribute__((always_inline)) {
+#pragma unroll
+                    for (int j = 0; j < NP; ++j) lds_read4(cur + (NP == 2 ? j : copy) * 2 * kBlockBytes, kf[j]);
+                };
+                auto get_v = [&](u32x4 (&vf)[NP][4]) __attribute__((always_inline)) {
+#pragma unroll
+                    for (int j = 0; j < NP; ++j) lds_read4(cur + (NP == 2 ? j : copy) * 2 * kBlockBytes + kBlockBytes, vf[j]);
+                };
+                compute(nsa_tag, np_tag, 2 * s + (NP == 2 ? 0 : copy), get_k, get_v, c_now);
+            };
+            auto run = [&](auto nsa_tag, auto np_tag) __attribute__((always_inline)) {
+                constexpr int NP = decltype(np_tag)::value;
+                constexpr int NC = R > 0 ? decltype(nsa_tag)::value * NP * RT : 0;  // rCache loads per iteration
+                // vm operations issued after a stage's copies until that stage is computed:
+                // kRing - 2 further iterations
+                constexpr int kWait = (kRing - 2) * (4 + NC);
+                static_assert(kWait < 64, "vmcnt range");
+                CFrag c0, c1, c2;
+                load_c(nsa_tag, np_tag, NP == 2 ? 0 : copy, c0);
+                load_c(nsa_tag, np_tag, 2 + (NP == 2 ? 0 : copy), c1);
+#pragma unroll
+                for (int k = 0; k < kRing - 1; ++k) dma_stage(k, ring_buf(k));
+                prologue_products();
+                for (int s = 0;;) {
+                    stage_barrier<kWait>();
+                    iterate(nsa_tag, np_tag, s, c0, c2);
+                    if (++s >= n_stages) break;
+                    stage_barrier<kWait>();
+                    iterate(nsa_tag, np_tag, s, c1, c0);
+                    if (++s >= n_stages) break;
+                    stage_barrier<kWait>();
+                    iterate(nsa_tag, np_tag, s, c2, c1);
+                    if (++s >= n_stages) break;
+                }
+                wait_vmcnt<0>();  // no copy into LDS outlives the block
+            };
+            (void)npw;
+            if (ngp == 4) run(NSF{}, I2{});
+            else run(NSF{}, I1{});
         }
     } else {
-        // one or two groups: bx holds stage s+1 while stage s is computed
-        auto run = [&](auto nsa_tag, auto np_tag) __attribute__((always_inline)) {
-            load_blocks(I2{}, N0{}, 0, bx);
-            load_c(nsa_tag, np_tag, 0, ca);
+        // One agent group: no page is shared between waves.  Wave w computes item pages
+        // w, w + 4, ... straight from registers (the stored fragment order is the operand
+        // order), with the next two pages and their rCache rows in flight.
+        struct PageRegs {
+            u32x4 k[1][4], v[1][4];
+            CFrag c;
+        };
+        auto load_page = [&](auto nsa_tag, int k, PageRegs &pr) __attribute__((always_inline)) {
+            const uint64_t a = base_addr(k);
+            const i32x4 rk = block_rsrc(a), rv = block_rsrc(a + vbytes);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) pr.k[0][i] = buf_load16(rk, lane * 16 + i * 1024);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) pr.v[0][i] = buf_load16(rv, lane * 16 + i * 1024);
+            load_c(nsa_tag, I1{}, k, pr.c);
+        };
+        auto regs_k = [](PageRegs &pr) {
+            return [&pr](u32x4 (&kf)[1][4]) __attribute__((always_inline)) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) kf[0][i] = pr.k[0][i];
+            };
+        };
+        auto regs_v = [](PageRegs &pr) {
+            return [&pr](u32x4 (&vf)[1][4]) __attribute__((always_inline)) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) vf[0][i] = pr.v[0][i];
+            };
+        };
+        const int n_my = wave < npg ? (npg - wave + WAVES - 1) / WAVES : 0;
+        // one agent: two pages in flight; several agents (more rCache rows per page): one
+        auto run2 = [&](auto nsa_tag) __attribute__((always_inline)) {
+            PageRegs pa, pb;
+            load_page(nsa_tag, wave, pa);
             prologue_products();
-            store_blocks(I2{}, N0{}, 0, 0, bx);
-            load_blocks(I2{}, N0{}, 1, bx);
-            __syncthreads();
-            for (int s = 0;;) {
-                load_c(nsa_tag, np_tag, s + 1, cb);
-                step(nsa_tag, np_tag, s & 1, s, ca);
-                store_blocks(I2{}, N0{}, (s + 1) & 1, s + 1, bx);
-                load_blocks(I2{}, N0{}, s + 2, bx);
-                __syncthreads();
-                if (++s >= n_stages) break;
-                load_c(nsa_tag, np_tag, s + 1, ca);
-                step(nsa_tag, np_tag, s & 1, s, cb);
-                store_blocks(I2{}, N0{}, (s + 1) & 1, s + 1, bx);
-                load_blocks(I2{}, N0{}, s + 2, bx);
-                __syncthreads();
-                if (++s >= n_stages) break;
+            for (int i = 0; i < n_my;) {
+                load_page(nsa_tag, wave + WAVES * (i + 1), pb);
+                compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pa), regs_v(pa), pa.c);
+                if (++i >= n_my) break;
+                load_page(nsa_tag, wave + WAVES * (i + 1), pa);
+                compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pb), regs_v(pb), pb.c);
+                if (++i >= n_my) break;
             }
         };
-        // two groups: steps of two pages; one group: one page per wave and stage
-        if (ngp == 2) {
-            if constexpr (S::MULTI) run(NSF{}, I2{});
-        } else if (R > 0 && nag == 1) {
-            run(I1{}, I1{});
-        } else {
-            run(NSF{}, I1{});
-        }
+        auto run1 = [&](auto nsa_tag) __attribute__((always_inline)) {
+            PageRegs pa, pb, pc;
+            load_page(nsa_tag, wave, pa);
+            load_page(nsa_tag, wave + WAVES, pb);
+            prologue_products();
+            for (int i = 0; i < n_my;) {
+                load_page(nsa_tag, wave + WAVES * (i + 2), pc);
+                compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pa), regs_v(pa), pa.c);
+                if (++i >= n_my) break;
+                load_page(nsa_tag, wave + WAVES * (i + 2), pa);
+                compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pb), regs_v(pb), pb.c);
+                if (++i >= n_my) break;
+                load_page(nsa_tag, wave + WAVES * (i + 2), pb);
+                compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pc), regs_v(pc), pc.c);
+                if (++i >= n_my) break;
+            }
+        };
+        if (R == 0 || nag == 1) run1(I1{});
+        else run2(NSF{});
     }
 
     write_partial<R>(p, st, row_active, ((int64_t)my_part * G + col % G) * hkv + h, grp);

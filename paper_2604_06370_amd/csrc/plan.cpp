@@ -14,6 +14,8 @@
 // one item) are placed on one XCD so those re-reads hit that XCD's L2.
 #include <algorithm>
 #include <cmath>
+#include <functional>
+#include <queue>
 #include <unordered_map>
 
 #include "internal.hpp"
@@ -22,8 +24,8 @@ namespace {
 constexpr int kNumXcd = 8;
 // Estimated time of one item page (in units of a single agent's page) and of an item's
 // prologue, used to size and order the work items.
-double item_page_cost(int32_t agents) { return 1.0 + (double)agents / 32.0; }
-constexpr double kItemOverhead = 8.0;
+double item_page_cost(int32_t agents) { return 1.0 + 0.095 * (double)agents; }
+constexpr double kItemOverhead = 24.0;
 }
 
 extern "C" {
@@ -104,13 +106,11 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
         return out;
     };
     // 3. pages per item.
-    //    RoPE off: the split kernel keeps two workgroups per compute unit resident, so the
-    //    items are sized for one round of 2 * num_cus workgroups of equal estimated time.
-    //    A page of an item with more agents costs more (its agents' rCache rows and more
-    //    matrix-core work per base byte; about 1.5x a single agent's page at 16 agents), and
-    //    every item pays a fixed prologue of about eight pages.  The target time per item is
-    //    the smallest for which the splits fit that round (or, when the page limits of an
-    //    item forbid it, the fewest rounds that hold them).  Splits of a segment are equal.
+    //    RoPE off: the split kernel keeps two workgroups per compute unit resident.  A page
+    //    of an item with more agents costs more (its agents' rCache rows and more
+    //    matrix-core work per base byte; about 2.5x a single agent's page at 16 agents, as
+    //    measured), and every item pays a fixed prologue worth about 24 pages (see below
+    //    for how the split sizes are chosen).  Splits of a segment are equal.
     //    RoPE on: about three (item, head block) workgroups per compute unit, 64 pages at
     //    most per item.
     const int64_t cus = prm->num_cus > 0 ? prm->num_cus : 256;
@@ -130,27 +130,58 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
             if (rope) cap = fkv::kMaxPagesPerItem;
             sc[i] = {segs[i].n, cap, cpp};
         }
-        const double ovh = kItemOverhead;
-        auto n_split = [&](const SegCost &s, double T) {
-            const int64_t by_cap = (s.n + s.cap - 1) / s.cap;
-            const int64_t by_cost = (int64_t)std::ceil((double)s.n * s.cpp / std::max(T - ovh, 1e-9));
-            return std::max<int64_t>(1, std::max(by_cap, by_cost));
-        };
-        auto n_items_at = [&](double T) {
-            int64_t k = 0;
-            for (size_t i = 0; i < sc.size(); ++i) k += n_split(sc[i], T) * (int64_t)chunk_sizes(segs[i].agents.size()).size();
-            return k;
-        };
-        double total = 0;
-        for (auto &s : sc) total += s.n * s.cpp;
         const int64_t slots = std::max<int64_t>(1, 2 * cus / nhb_units);  // items per round
-        const int64_t min_items = n_items_at(1e30);
-        const int64_t rounds = (min_items + slots - 1) / slots;
-        double lo = ovh, hi = ovh + total + 1.0;
-        for (int it = 0; it < 60; ++it) {
-            const double mid = 0.5 * (lo + hi);
-            if (n_items_at(mid) <= rounds * slots) hi = mid; else lo = mid;
+        // Items of three or four agent groups stream every base page through LDS to four
+        // waves and are bound by the compute unit's vector-memory issue rate, so two of them
+        // on one compute unit slow each other down: they get at most one workgroup per
+        // compute unit (pages split evenly over that budget, within their page limit).  The
+        // other items take a uniform page count, chosen by a simulated greedy longest-first
+        // fill of the resident slots (what the dispatcher does with the block order below).
+        auto is_multi = [&](size_t i) { return sc[i].cap == fkv::kMaxPagesMulti && !rope; };
+        int64_t multi_pages = 0;
+        for (size_t i = 0; i < sc.size(); ++i)
+            if (is_multi(i)) {
+                multi_pages += (int64_t)sc[i].n * (int64_t)chunk_sizes(segs[i].agents.size()).size();
+            }
+        const int64_t multi_budget = std::max<int64_t>(1, cus / nhb_units);
+        const int32_t multi_pps = multi_pages > 0
+            ? (int32_t)std::min<int64_t>(fkv::kMaxPagesMulti, std::max<int64_t>(4, (multi_pages + multi_budget - 1) / multi_budget))
+            : fkv::kMaxPagesMulti;
+        std::vector<int32_t> cand_pps(sc.size());
+        auto sim = [&](auto &&pages_of) {
+            std::vector<double> costs;
+            for (size_t i = 0; i < sc.size(); ++i) {
+                const int32_t pps_i = pages_of(i);
+                const int64_t k = (sc[i].n + pps_i - 1) / pps_i;
+                const int32_t pages = (int32_t)((sc[i].n + k - 1) / k);
+                for (size_t c : chunk_sizes(segs[i].agents.size()))
+                    for (int64_t j = 0; j < k; ++j) costs.push_back(kItemOverhead + pages * item_page_cost((int32_t)c));
+            }
+            std::sort(costs.begin(), costs.end(), std::greater<double>());
+            std::priority_queue<double, std::vector<double>, std::greater<double>> free_at;
+            for (int64_t s = 0; s < slots; ++s) free_at.push(0.0);
+            double end = 0;
+            for (double c : costs) {
+                const double t0 = free_at.top();
+                free_at.pop();
+                free_at.push(t0 + c);
+                end = std::max(end, t0 + c);
+            }
+            return end;
+        };
+        // (the largest page count whose estimate is within 1% of the best: fewer items, fewer
+        // partial rows to merge)
+        const int32_t cands[] = {32, 40, 48, 56, 64, 80, 96, 112, 128};
+        double est[9], best = 1e300;
+        for (int c = 0; c < 9; ++c) {
+            const int32_t u = cands[c];
+            est[c] = sim([&](size_t i) { return is_multi(i) ? multi_pps : std::min(u, sc[i].cap); });
+            best = std::min(best, est[c]);
         }
+        int32_t best_u = 64;
+        for (int c = 8; c >= 0; --c)
+            if (est[c] <= best * 1.01) { best_u = cands[c]; break; }
+        for (size_t i = 0; i < sc.size(); ++i) cand_pps[i] = is_multi(i) ? multi_pps : std::min(best_u, sc[i].cap);
         const int32_t rope_pps = (int32_t)std::max<int64_t>(
             4, std::min<int64_t>(fkv::kMaxPagesPerItem, [&] {
                 int64_t units = 0;
@@ -164,7 +195,8 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
                     return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: pages_per_split above 128");
                 pps = std::min(prm->pages_per_split, sc[i].cap);
             } else {
-                const int64_t k = rope ? (segs[i].n + rope_pps - 1) / rope_pps : n_split(sc[i], hi);
+                const int32_t target = rope ? rope_pps : cand_pps[i];
+                const int64_t k = (segs[i].n + target - 1) / target;
                 pps = (int32_t)((segs[i].n + k - 1) / k);
             }
             seg_pps[i] = pps;
