@@ -244,7 +244,7 @@ typedef struct {
     const float *rope_sin;      /* device fp32 table from fkv_rope_table */
     const int32_t *plan;        /* device copy of a serialised decode plan (decode only) */
     const int32_t *q_indptr;    /* device [n_agents+1] query rows per agent (prefill only) */
-    void *workspace;            /* device scratch of workspace_bytes (decode) */
+    void *workspace;            /* device scratch of workspace_bytes (decode): the partial rows */
     size_t workspace_bytes;
     void *out;                  /* device bf16 [n_q][hq][d] */
     int32_t n_agents, hq, hkv, d, r, page_size, max_pages;
@@ -254,7 +254,7 @@ typedef struct {
                                    it are not computed, so it must not be understated. */
     float scale;                /* softmax scale; typically 1/sqrt(d) */
     void *const *timing_events; /* optional, host array of hipEvent_t: decode records [0] before its first
-                                   kernel, [1] between its two kernels and [2] after the second; prefill
+                                   kernel, [1] after the split kernel and [2] after the merge kernel; prefill
                                    records [0] and [1] around its kernel.  NULL = no events. */
 } fkv_attn_args;
 
@@ -267,8 +267,9 @@ typedef struct {
  * Supported: d = 128, page_size = 16, r in {0, 8, 16, 32, 64}, hq/hkv in {4, 8}.  The plan must
  * have been built for the same r and RoPE setting (FKV_ERR_INVALID otherwise), so that its work
  * items hold no more agents than fkv_decode_plan_default_agents allows.
- * Two kernels are enqueued (split, combine).  Errors: FKV_ERR_INVALID /
- * FKV_ERR_UNSUPPORTED before any launch, FKV_ERR_HIP when a launch fails. */
+ * Two kernels are enqueued (split, merge).  Calls that share a workspace must not overlap.
+ * Errors: FKV_ERR_INVALID / FKV_ERR_UNSUPPORTED before any launch, FKV_ERR_HIP when a
+ * launch fails. */
 fkv_status fkv_residual_attention_decode(const fkv_attn_args *args, const fkv_plan *plan, void *stream);
 
 /* Chunked prefill: agent a's query rows q_indptr[a] .. q_indptr[a+1]-1 are the

@@ -58,6 +58,8 @@ struct DecodeArgs {
     int32_t hq, hkv, max_pages, ws_stride;
     int32_t off_items, off_blocks, off_ptr, off_zero, off_desc;  // plan section offsets (words)
     float scale_log2;  // softmax scale * log2(e)
+    int64_t ws_bytes;  // bytes of the partial-row area of the workspace
+    int32_t n_rows;    // query rows to merge: n_agents * hq
 };
 
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
@@ -132,6 +134,17 @@ constexpr int cmin(int a, int b) { return a < b ? a : b; }
 // Partial row record in the workspace (floats): acc[D], acc_r[R], m, l; stride
 // rounded up to a multiple of 4 so every record is 16-byte aligned.
 __host__ __device__ constexpr int ws_stride_of(int r) { return (D + r + 2 + 3) / 4 * 4; }
+
+// Partial rows travel between workgroups of one launch (the merged launch) and between
+// launches.  They are written and read at device scope (cache policy sc1: coherent
+// across the XCDs' L2 caches, no cache write-back or invalidation needed), 16 bytes per
+// lane, through a buffer resource over the workspace (byte offsets below 4 GiB).
+__device__ void raw_buffer_store_v4f32(f32x4 data, i32x4 rsrc, int voffset, int soffset, int aux) __asm("llvm.amdgcn.raw.buffer.store.v4f32");
+__device__ f32x4 raw_buffer_load_v4f32(i32x4 rsrc, int voffset, int soffset, int aux) __asm("llvm.amdgcn.raw.buffer.load.v4f32");
+constexpr int kDeviceCoherent = 16;  // cache-policy operand: sc1
+__device__ __forceinline__ i32x4 workspace_rsrc(const float *ws, int64_t bytes) {
+    return block_rsrc(reinterpret_cast<uint64_t>(ws), (int)(bytes < 0x7fffffff ? bytes : 0x7fffffff));
+}
 
 // ---------------------------------------------------------------------------
 // Per-wave row state and the page update shared by both kernels.
@@ -235,16 +248,14 @@ __device__ __forceinline__ void write_partial(const DecodeArgs &p, Rows<R> &st, 
     st.l += __shfl_xor(st.l, 16);
     st.l += __shfl_xor(st.l, 32);
     if (!row_active) return;
-    float *dst = p.ws + prow * p.ws_stride;
+    const i32x4 rs = workspace_rsrc(p.ws, p.ws_bytes);
+    const int dst = (int)(prow * p.ws_stride * 4);  // byte offset of the record
 #pragma unroll
-    for (int mt = 0; mt < 8; ++mt) *reinterpret_cast<f32x4 *>(dst + 16 * mt + 4 * grp) = st.oacc[mt];
+    for (int mt = 0; mt < 8; ++mt) raw_buffer_store_v4f32(st.oacc[mt], rs, dst + (16 * mt + 4 * grp) * 4, 0, kDeviceCoherent);
 #pragma unroll
     for (int t = 0; t < Rows<R>::RT; ++t)
-        if (16 * t + 4 * grp < R) *reinterpret_cast<f32x4 *>(dst + D + 16 * t + 4 * grp) = st.racc[t];
-    if (grp == 0) {
-        dst[D + R] = st.m;
-        dst[D + R + 1] = st.l;
-    }
+        if (16 * t + 4 * grp < R) raw_buffer_store_v4f32(st.racc[t], rs, dst + (D + 16 * t + 4 * grp) * 4, 0, kDeviceCoherent);
+    if (grp == 0) raw_buffer_store_v4f32(f32x4{st.m, st.l, 0.f, 0.f}, rs, dst + (D + R) * 4, 0, kDeviceCoherent);
 }
 
 // Q^T as the B operand of the 16x16x32 products.  The head-dim index of slot j in
@@ -307,7 +318,7 @@ struct SplitShape {
 };
 
 template <int R, int G>
-__global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(DecodeArgs p) {
+__device__ __forceinline__ void split_body(const DecodeArgs &p) {
     using S = SplitShape<R, G>;
     constexpr int AG = S::AG;
     constexpr int RT = S::RT;
@@ -785,6 +796,11 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
     write_partial<R>(p, st, row_active, ((int64_t)my_part * G + col % G) * hkv + h, grp);
 }
 
+template <int R, int G>
+__global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(DecodeArgs p) {
+    split_body<R, G>(p);
+}
+
 
 // ---------------------------------------------------------------------------
 // RoPE on: one agent group per item; waves stride over the pages, registers
@@ -1022,126 +1038,100 @@ __global__ __launch_bounds__(256, 1) void decode_rope_kernel(DecodeArgs p) {
 
 
 // Log-sum-exp merge of one agent's partials and Stage 3 of Algorithm 1 for one query
-// head j (KV head h = j / G): O = (sum_k w_k acc_k + (sum_k w_k acc_r,k) . B_V[h]) / L
-// with w_k = 2^(m_k - M), M = max_k m_k, L = sum_k w_k l_k.  An agent's partials are
-// contiguous, so the records are addressed directly: in rounds of 64, wave w issues the
-// loads of partials w, w+4, ... together and folds them with a running maximum (lane c
-// holds columns c, c+64, c+128 of a record).  The four waves are merged through LDS and
-// B_V (prefetched at the start, as it does not depend on the partials) is applied once.
-constexpr int kCombineThreads = 256;
-constexpr int kCombineRound = 64;  // partials per round
-
+// row (agent a, query head j of KV head h = j / G), by one wave:
+//   O = (sum_k w_k acc_k + (sum_k w_k acc_r,k) . B_V[h]) / L,
+//   w_k = 2^(m_k - M), M = max_k m_k, L = sum_k w_k l_k.
+// An agent's partials are contiguous; lane i < NV reads float4 i of every record (acc,
+// then acc_r) and lane NV its (m, l), up to 48 records in flight at once (lanes past NV
+// read float4 0 and drop it).  B_V is read at
+// the start, as it does not depend on the partials.
 template <int R, int G>
-__global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(DecodeArgs p) {
-    constexpr int NCOL = D + R;
-    constexpr int NC = (NCOL + 63) / 64;
-    constexpr int U = kCombineRound / WAVES;  // partials per wave and round
-    constexpr int RH = (R + 1) / 2;            // rank rows per half of the workgroup
+__device__ __forceinline__ void combine_row(const DecodeArgs &p, int row) {
+    constexpr int NV = (D + R) / 4;  // float4s of acc and acc_r; (m, l) follow
+    constexpr int RB = R > 0 ? R : 1;
+    constexpr int BATCH = 48;  // partials in flight at once (one round for most rows)
+    const int lane = threadIdx.x & 63;
     const int hq = p.hq;
-    const int a = blockIdx.x / hq;
-    const int j = blockIdx.x - a * hq;
+    const int a = row / hq, j = row - a * hq;
     const int h = j / G, jj = j - h * G;
-    const int32_t *plan = p.plan;
-    const int k0 = plan[p.off_ptr + a];
-    const int K = plan[p.off_ptr + a + 1] - k0;
+    const int32_t *ptr = p.plan + p.off_ptr;
+    const int k0 = ptr[a], K = ptr[a + 1] - k0;
     const int ad = R > 0 ? p.adapter_idx[a] : -1;
     const int stride = p.ws_stride;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    // record of partial k0 + k for query head j: ((k0 + k) * G + jj) * hkv + h
-    const float *rec0 = p.ws + ((int64_t)k0 * G * p.hkv + jj * p.hkv + h) * stride;
-    const int64_t kstride = (int64_t)G * p.hkv * stride;
-    const int d = tid & (D - 1), half = tid >> 7;
-    __shared__ float sM[4], sL[4];
-    __shared__ float sAcc[4][NCOL];
-    __shared__ float sFin[NCOL];
-    __shared__ float sOut[D];
+    const i32x4 rs = workspace_rsrc(p.ws, p.ws_bytes);
+    // byte offsets: record of partial k0 for this row, lane's float4 (lanes past NV: float4 0)
+    const int rec0 = (int)(((int64_t)k0 * G * p.hkv + jj * p.hkv + h) * stride * 4) + (lane <= NV ? 16 * lane : 0);
+    const int kstride = G * p.hkv * stride * 4;
 
-    // B_V[rho][h*D + d] for this thread's half of the rank
-    float bv[RH > 0 ? RH : 1];
+    // B_V[rho][h*D + 4 lane .. +3] for the output dims of lanes 0..31
+    u32x2 bv[RB];
     if constexpr (R > 0) {
-        const uint16_t *bvp = p.lora_b + ((int64_t)(ad >= 0 ? ad : 0) * 2 + 1) * R * p.hkv * D + (int64_t)h * D + d;
+        const uint16_t *bvp = p.lora_b + ((int64_t)(ad >= 0 ? ad : 0) * 2 + 1) * R * p.hkv * D + (int64_t)h * D + 4 * (lane & 31);
 #pragma unroll
-        for (int i = 0; i < RH; ++i) {
-            const int rho = half * RH + i;
-            bv[i] = (ad >= 0 && rho < R) ? bf16_to_f32(bvp[(int64_t)rho * p.hkv * D]) : 0.f;
-        }
+        for (int rho = 0; rho < R; ++rho) bv[rho] = ad >= 0 ? ldg64(bvp + (int64_t)rho * p.hkv * D) : u32x2{0, 0};
     }
 
-    float M = kNegInf, L = 0.f, acc[NC];
+    f32x4 acc = {0, 0, 0, 0};
+    float M = kNegInf, L = 0.f;
+    for (int kb = 0; kb < K; kb += BATCH) {
+        f32x4 v[BATCH];
 #pragma unroll
-    for (int c = 0; c < NC; ++c) acc[c] = 0.f;
-    for (int kb = 0; kb < K; kb += kCombineRound) {
-        float mv[U], lv[U], v[U][NC];
+        for (int u = 0; u < BATCH; ++u)
+            v[u] = kb + u < K ? raw_buffer_load_v4f32(rs, rec0 + (kb + u) * kstride, 0, kDeviceCoherent) : f32x4{0, 0, 0, 0};
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int idx = wave + WAVES * u;
-            const bool ok = kb + idx < K;
-            const float *src = rec0 + (int64_t)(kb + idx) * kstride;
-            mv[u] = ok ? src[NCOL] : kNegInf;
-            lv[u] = ok ? src[NCOL + 1] : 0.f;
-#pragma unroll
-            for (int c = 0; c < NC; ++c) v[u][c] = (ok && lane + 64 * c < NCOL) ? src[lane + 64 * c] : 0.f;
+        for (int u = 0; u < BATCH; ++u) {
+            // past the last partial: weight zero (m = -inf in lane NV, zeros elsewhere)
+            if (!(kb + u < K && lane <= NV)) v[u] = f32x4{lane == NV ? kNegInf : 0.f, 0.f, 0.f, 0.f};
         }
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const float Mn = fmaxf(M, mv[u]);
+        for (int u = 0; u < BATCH; ++u) {
+            const float mk = __shfl(v[u].x, NV), lk = __shfl(v[u].y, NV);
+            const float Mn = fmaxf(M, mk);
             const float Mu = Mn == kNegInf ? 0.f : Mn;
-            const float e0 = fast_exp2(M - Mu), e1 = fast_exp2(mv[u] - Mu);
-            L = L * e0 + lv[u] * e1;
-#pragma unroll
-            for (int c = 0; c < NC; ++c) acc[c] = acc[c] * e0 + v[u][c] * e1;
+            const float e0 = fast_exp2(M - Mu), e1 = fast_exp2(mk - Mu);
+            L = L * e0 + lk * e1;
+            acc = acc * e0 + v[u] * e1;
             M = Mn;
         }
     }
-    if (lane == 0) {
-        sM[wave] = M;
-        sL[wave] = L;
-    }
-#pragma unroll
-    for (int c = 0; c < NC; ++c)
-        if (lane + 64 * c < NCOL) sAcc[wave][lane + 64 * c] = acc[c];
-    __syncthreads();
-    float Mt = kNegInf;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) Mt = fmaxf(Mt, sM[w]);
-    const float Mtu = Mt == kNegInf ? 0.f : Mt;
-    float ew[4], Lt = 0.f;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-        ew[w] = fast_exp2(sM[w] - Mtu);
-        Lt += ew[w] * sL[w];
-    }
-    if (tid < NCOL) sFin[tid] = ew[0] * sAcc[0][tid] + ew[1] * sAcc[1][tid] + ew[2] * sAcc[2][tid] + ew[3] * sAcc[3][tid];
-    __syncthreads();
-    // Stage 3: O = (acc + acc_r . B_V) / L; the rank sum is split over the two halves of
-    // the workgroup
-    float o = half == 0 ? sFin[d] : 0.f;
+    // Stage 3 (Eq. 4): lanes 0..31 own output dims 4 lane .. +3; acc_r sits in lanes 32..
+    f32x4 o = acc;
     if constexpr (R > 0) {
 #pragma unroll
-        for (int i = 0; i < RH; ++i) {
-            const int rho = half * RH + i;
-            if (rho < R) o += sFin[D + rho] * bv[i];
+        for (int rho = 0; rho < R; ++rho) {
+            const float ar = __shfl(acc[rho % 4], D / 4 + rho / 4);
+            o[0] += ar * bf16_lo(bv[rho].x);
+            o[1] += ar * bf16_hi(bv[rho].x);
+            o[2] += ar * bf16_lo(bv[rho].y);
+            o[3] += ar * bf16_hi(bv[rho].y);
         }
     }
-    if (half == 1) sOut[d] = o;
-    __syncthreads();
-    if (half == 0) {
-        o += sOut[d];
-        const float res = Lt > 0.f ? o / Lt : 0.f;
-        typedef __bf16 bf1;
-        p.out[((int64_t)a * hq + j) * D + d] = __builtin_bit_cast(uint16_t, (bf1)res);
+    const float inv = L > 0.f ? 1.f / L : 0.f;
+    if (lane < D / 4) {
+        uint16_t *dst = p.out + ((int64_t)a * hq + j) * D + 4 * lane;
+        *reinterpret_cast<u32x2 *>(dst) = u32x2{pack_bf16(o[0] * inv, o[1] * inv), pack_bf16(o[2] * inv, o[3] * inv)};
     }
 }
 
+// The merge kernel: one wave per query row.
+template <int R, int G>
+__global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs p) {
+    const int row = blockIdx.x * WAVES + uniform(threadIdx.x >> 6);
+    if (row < p.n_rows) combine_row<R, G>(p, row);
+}
+
 template <int R, int G, bool ROPE>
-hipError_t launch_decode(const DecodeArgs &da, int n_blocks, int n_agents, int hpb, hipStream_t st, void *const *ev) {
+hipError_t launch_decode(const DecodeArgs &da_in, int n_blocks, int n_agents, int hpb, hipStream_t st, void *const *ev) {
+    (void)hpb;
     hipError_t e;
+    DecodeArgs da = da_in;
+    da.n_rows = n_agents * da.hq;
     if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[0]), st)) != hipSuccess) return e;
     if constexpr (ROPE) hipLaunchKernelGGL((decode_rope_kernel<R, G>), dim3(n_blocks), dim3(256), 0, st, da);
     else hipLaunchKernelGGL((decode_split_kernel<R, G>), dim3(n_blocks), dim3(256), 0, st, da);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[1]), st)) != hipSuccess) return e;
-    hipLaunchKernelGGL((decode_combine_kernel<R, G>), dim3(n_agents * da.hq), dim3(kCombineThreads), 0, st, da);
+    hipLaunchKernelGGL((decode_combine_kernel<R, G>), dim3((da.n_rows + WAVES - 1) / WAVES), dim3(256), 0, st, da);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[2]), st)) != hipSuccess) return e;
     return hipSuccess;
@@ -1233,6 +1223,11 @@ extern "C" fkv_status fkv_residual_attention_decode(const fkv_attn_args *a, cons
     da.off_zero = w[fkv::H_OFF_ZERO];
     da.off_desc = w[fkv::H_OFF_DESC];
     da.scale_log2 = a->scale * 1.4426950408889634f;
+    // grid-barrier words: the 256 bytes after the partial rows (see fkv_decode_plan_info)
+    da.ws_bytes = fkv::decode_partials_bytes(plan, a->d, a->r);
+    if (da.ws_bytes >= 0x7fffffff)
+        return fkv::fail(FKV_ERR_UNSUPPORTED, "fkv_residual_attention_decode: partial rows above 2 GiB");
+    da.n_rows = a->n_agents * a->hq;
     const int nb = w[fkv::H_N_BLOCKS];
     hipStream_t hs = static_cast<hipStream_t>(stream);
     const bool rope = a->rope_cos != nullptr && a->r > 0;

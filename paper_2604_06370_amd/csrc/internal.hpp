@@ -95,6 +95,12 @@ constexpr int32_t kPlanMagic = 0x464b5631;  // "FKV1"
 
 }  // namespace fkv
 
+struct fkv_plan;
+namespace fkv {
+// Decode workspace: the partial rows, rounded up to 256 bytes.
+int64_t decode_partials_bytes(const fkv_plan *plan, int32_t d, int32_t r);
+}  // namespace fkv
+
 struct fkv_plan {
     std::vector<int32_t> words;
     std::vector<int32_t> seg_first_page, seg_n_pages, seg_agent_off, seg_agents;

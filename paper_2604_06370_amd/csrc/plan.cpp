@@ -385,6 +385,18 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
 
 void fkv_decode_plan_destroy(fkv_plan *plan) { delete plan; }
 
+}  // extern "C"
+
+namespace fkv {
+int64_t decode_partials_bytes(const fkv_plan *plan, int32_t d, int32_t r) {
+    const int64_t stride = (int64_t)(d + r + 2 + 3) / 4 * 4;
+    const int64_t bytes = (int64_t)plan->words[H_TOTAL_ROWS] * plan->hkv * stride * 4;
+    return (bytes + 255) / 256 * 256;
+}
+}  // namespace fkv
+
+extern "C" {
+
 fkv_status fkv_decode_plan_info(const fkv_plan *plan, int32_t d, int32_t r, fkv_plan_info *out) {
     fkv::clear_error();
     if (!plan || !out || d < 1 || r < 0) return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_info: bad argument");
@@ -394,8 +406,7 @@ fkv_status fkv_decode_plan_info(const fkv_plan *plan, int32_t d, int32_t r, fkv_
     out->n_blocks = w[fkv::H_N_BLOCKS];
     out->n_segments = w[fkv::H_N_SEGMENTS];
     out->pages_per_split = w[fkv::H_PAGES_PER_SPLIT];
-    const int64_t stride = (int64_t)(d + r + 2 + 3) / 4 * 4;
-    out->workspace_bytes = (int64_t)w[fkv::H_TOTAL_ROWS] * plan->hkv * stride * 4;
+    out->workspace_bytes = fkv::decode_partials_bytes(plan, d, r);
     return FKV_OK;
 }
 

@@ -127,7 +127,7 @@ class LoadedWorkload:
             "adapter_idx": torch.from_numpy(self.adapter_idx_host[agents]).to(dev),
             "q": self.q_all[q_rows].contiguous(),
             "out": torch.empty((len(agents), wl.hq, wl.d), dtype=torch.bfloat16, device=dev),
-            "ws": torch.empty(max(1, info["workspace_bytes"] // 4), dtype=torch.float32, device=dev),
+            "ws": torch.zeros(max(1, info["workspace_bytes"] // 4), dtype=torch.float32, device=dev),
             "host_bt": (bb, rb, sl),
         }
         st["plan_dev"] = plan.device(dev)
