@@ -186,6 +186,8 @@ def main():
     ap.add_argument("--pps", type=int, default=0, help="pages per split (0 = automatic)")
     ap.add_argument("--item-agents", type=int, default=0, help="agents per decode work item (0 = automatic)")
     ap.add_argument("--copies", type=int, default=3)
+    ap.add_argument("--event-every", type=int, default=5,
+                    help="record the kernel-timing events on every N-th timed step (1 = every step)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true", help="skip the chunked-prefill measurement")
     ap.add_argument("--prefill-config", type=int, default=3)
@@ -226,18 +228,25 @@ def main():
         handles = [(ctypes.c_void_p * 3)(*[e.cuda_event for e in trio]) for trio in ev]
         for i in range(warmup):
             lws[i % len(lws)].decode()
+        # timed steps: the library records its HIP events around the split kernel of every
+        # `event_every`-th step (an event record costs GPU time of its own, so recording
+        # them on every step would slow the very steps being timed)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
+        timed = []
         for i in range(steps):
             lw = lws[i % len(lws)]
-            lw._decode["args"].timing_events = ctypes.cast(handles[i], ctypes.c_void_p).value
+            rec = i % args.event_every == 0
+            lw._decode["args"].timing_events = ctypes.cast(handles[i], ctypes.c_void_p).value if rec else None
+            if rec:
+                timed.append(i)
             lw.decode()
         torch.cuda.synchronize()
         t1 = time.perf_counter()
         for lw in lws:
             lw._decode["args"].timing_events = None
-        split_ms = np.array([ev[i][0].elapsed_time(ev[i][1]) for i in range(steps)])
-        comb_ms = np.array([ev[i][1].elapsed_time(ev[i][2]) for i in range(steps)])
+        split_ms = np.array([ev[i][0].elapsed_time(ev[i][1]) for i in timed])
+        comb_ms = np.array([ev[i][1].elapsed_time(ev[i][2]) for i in timed])
         for lw in lws:
             lw.close()
         del lws
