@@ -1038,18 +1038,36 @@ __global__ __launch_bounds__(256, 1) void decode_rope_kernel(DecodeArgs p) {
 
 
 // Log-sum-exp merge of one agent's partials and Stage 3 of Algorithm 1 for one query
-// row (agent a, query head j of KV head h = j / G), by one wave:
+// row (agent a, query head j of KV head h = j / G), by one workgroup of CW waves:
 //   O = (sum_k w_k acc_k + (sum_k w_k acc_r,k) . B_V[h]) / L,
 //   w_k = 2^(m_k - M), M = max_k m_k, L = sum_k w_k l_k.
-// An agent's partials are contiguous; lane i < NV reads float4 i of every record (acc,
-// then acc_r) and lane NV its (m, l), up to 48 records in flight at once (lanes past NV
-// read float4 0 and drop it).  B_V is read at
-// the start, as it does not depend on the partials.
+// An agent's partials are contiguous; wave w merges partials w, w + CW, ... (all of its
+// share in flight at once): lane i < NV reads float4 i of every record (acc, then acc_r)
+// and lane NV its (m, l); lanes past NV read float4 0 and drop it.  The waves' results
+// meet in LDS and wave 0 merges them and applies Stage 3.  B_V is read at the start, as
+// it does not depend on the partials.
+#ifndef FKV_COMBINE_WAVES
+#define FKV_COMBINE_WAVES 4
+#endif
+constexpr int CW = FKV_COMBINE_WAVES;
+
+__device__ __forceinline__ void lse_merge(float &M, float &L, f32x4 &acc, float mk, float lk, const f32x4 &v) {
+    const float Mn = fmaxf(M, mk);
+    const float Mu = Mn == kNegInf ? 0.f : Mn;
+    const float e0 = fast_exp2(M - Mu), e1 = fast_exp2(mk - Mu);
+    L = L * e0 + lk * e1;
+    acc = acc * e0 + v * e1;
+    M = Mn;
+}
+
 template <int R, int G>
-__device__ __forceinline__ void combine_row(const DecodeArgs &p, int row) {
+__global__ __launch_bounds__(64 * CW) void decode_combine_kernel(DecodeArgs p) {
     constexpr int NV = (D + R) / 4;  // float4s of acc and acc_r; (m, l) follow
     constexpr int RB = R > 0 ? R : 1;
-    constexpr int BATCH = 48;  // partials in flight at once (one round for most rows)
+    constexpr int BATCH = (48 + CW - 1) / CW;  // partials in flight per wave
+    __shared__ f32x4 s_acc[CW > 1 ? CW - 1 : 1][NV + 1];
+    const int row = blockIdx.x;
+    const int wave = uniform(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     const int hq = p.hq;
     const int a = row / hq, j = row - a * hq;
@@ -1063,35 +1081,41 @@ __device__ __forceinline__ void combine_row(const DecodeArgs &p, int row) {
     const int rec0 = (int)(((int64_t)k0 * G * p.hkv + jj * p.hkv + h) * stride * 4) + (lane <= NV ? 16 * lane : 0);
     const int kstride = G * p.hkv * stride * 4;
 
-    // B_V[rho][h*D + 4 lane .. +3] for the output dims of lanes 0..31
+    // B_V[rho][h*D + 4 lane .. +3] for the output dims of lanes 0..31 (wave 0)
     u32x2 bv[RB];
     if constexpr (R > 0) {
-        const uint16_t *bvp = p.lora_b + ((int64_t)(ad >= 0 ? ad : 0) * 2 + 1) * R * p.hkv * D + (int64_t)h * D + 4 * (lane & 31);
+        if (wave == 0) {
+            const uint16_t *bvp = p.lora_b + ((int64_t)(ad >= 0 ? ad : 0) * 2 + 1) * R * p.hkv * D + (int64_t)h * D + 4 * (lane & 31);
 #pragma unroll
-        for (int rho = 0; rho < R; ++rho) bv[rho] = ad >= 0 ? ldg64(bvp + (int64_t)rho * p.hkv * D) : u32x2{0, 0};
+            for (int rho = 0; rho < R; ++rho) bv[rho] = ad >= 0 ? ldg64(bvp + (int64_t)rho * p.hkv * D) : u32x2{0, 0};
+        }
     }
 
     f32x4 acc = {0, 0, 0, 0};
     float M = kNegInf, L = 0.f;
-    for (int kb = 0; kb < K; kb += BATCH) {
+    for (int kb = wave; kb < K; kb += BATCH * CW) {
         f32x4 v[BATCH];
 #pragma unroll
         for (int u = 0; u < BATCH; ++u)
-            v[u] = kb + u < K ? raw_buffer_load_v4f32(rs, rec0 + (kb + u) * kstride, 0, kDeviceCoherent) : f32x4{0, 0, 0, 0};
+            v[u] = kb + u * CW < K ? raw_buffer_load_v4f32(rs, rec0 + (kb + u * CW) * kstride, 0, kDeviceCoherent)
+                                   : f32x4{0, 0, 0, 0};
 #pragma unroll
         for (int u = 0; u < BATCH; ++u) {
             // past the last partial: weight zero (m = -inf in lane NV, zeros elsewhere)
-            if (!(kb + u < K && lane <= NV)) v[u] = f32x4{lane == NV ? kNegInf : 0.f, 0.f, 0.f, 0.f};
+            if (!(kb + u * CW < K && lane <= NV)) v[u] = f32x4{lane == NV ? kNegInf : 0.f, 0.f, 0.f, 0.f};
         }
 #pragma unroll
-        for (int u = 0; u < BATCH; ++u) {
-            const float mk = __shfl(v[u].x, NV), lk = __shfl(v[u].y, NV);
-            const float Mn = fmaxf(M, mk);
-            const float Mu = Mn == kNegInf ? 0.f : Mn;
-            const float e0 = fast_exp2(M - Mu), e1 = fast_exp2(mk - Mu);
-            L = L * e0 + lk * e1;
-            acc = acc * e0 + v[u] * e1;
-            M = Mn;
+        for (int u = 0; u < BATCH; ++u) lse_merge(M, L, acc, __shfl(v[u].x, NV), __shfl(v[u].y, NV), v[u]);
+    }
+    if constexpr (CW > 1) {
+        // lane NV's acc holds (L, 0, 0, 0) scaled alongside; carry (M, L) there instead
+        if (wave > 0 && lane <= NV) s_acc[wave - 1][lane] = lane == NV ? f32x4{M, L, 0.f, 0.f} : acc;
+        __syncthreads();
+        if (wave > 0) return;
+#pragma unroll
+        for (int w = 0; w < CW - 1; ++w) {
+            const f32x4 v = lane <= NV ? s_acc[w][lane] : f32x4{0, 0, 0, 0};
+            lse_merge(M, L, acc, __shfl(v.x, NV), __shfl(v.y, NV), lane < NV ? v : f32x4{0, 0, 0, 0});
         }
     }
     // Stage 3 (Eq. 4): lanes 0..31 own output dims 4 lane .. +3; acc_r sits in lanes 32..
@@ -1113,13 +1137,6 @@ __device__ __forceinline__ void combine_row(const DecodeArgs &p, int row) {
     }
 }
 
-// The merge kernel: one wave per query row.
-template <int R, int G>
-__global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs p) {
-    const int row = blockIdx.x * WAVES + uniform(threadIdx.x >> 6);
-    if (row < p.n_rows) combine_row<R, G>(p, row);
-}
-
 template <int R, int G, bool ROPE>
 hipError_t launch_decode(const DecodeArgs &da_in, int n_blocks, int n_agents, int hpb, hipStream_t st, void *const *ev) {
     (void)hpb;
@@ -1131,7 +1148,7 @@ hipError_t launch_decode(const DecodeArgs &da_in, int n_blocks, int n_agents, in
     else hipLaunchKernelGGL((decode_split_kernel<R, G>), dim3(n_blocks), dim3(256), 0, st, da);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[1]), st)) != hipSuccess) return e;
-    hipLaunchKernelGGL((decode_combine_kernel<R, G>), dim3((da.n_rows + WAVES - 1) / WAVES), dim3(256), 0, st, da);
+    hipLaunchKernelGGL((decode_combine_kernel<R, G>), dim3(da.n_rows), dim3(64 * CW), 0, st, da);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[2]), st)) != hipSuccess) return e;
     return hipSuccess;
