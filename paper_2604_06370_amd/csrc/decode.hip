@@ -10,9 +10,9 @@
 //  - single-group items (private suffixes; every item with RoPE or rank >= 32): the
 //    waves stride over the pages with a register-double-buffered pipeline;
 //  - multi-group items (shared prefixes): stages of two pages; each base K/V block is
-//    loaded once into LDS (two stages ahead, through registers) and every wave applies
-//    it to its own group's 16 rows, so a shared page crosses the memory hierarchy once
-//    per workgroup instead of once per group.
+//    copied once from memory straight into an LDS ring (three stages ahead) and every
+//    wave applies it to its own group's 16 rows, so a shared page crosses the memory
+//    hierarchy once per workgroup instead of once per group.
 //
 // Per page and wave (all products on the matrix cores, fp32 accumulate):
 //   S^T  = K_base . Q^T                               16x16x32, all rows of the wave
@@ -33,6 +33,7 @@
 #include <type_traits>
 
 #include "internal.hpp"
+#include "lds_dma.hpp"
 #include "mfma.hpp"
 
 using namespace fkvk;
@@ -66,60 +67,9 @@ constexpr int cmax(int a, int b) { return a > b ? a : b; }
 
 // Base-page ring of the multi-group decode path: kRing stages of two pages (K and V
 // blocks of one head), written by direct memory-to-LDS copies.
-typedef __attribute__((address_space(3))) u32x4 LdsU32x4;
 constexpr int kRing = 4;
 constexpr int kStageBytes = 4 * kBlockBytes;
 
-// Copies from global memory straight into LDS (buffer_load ... lds).  The buffer
-// resource names one 4 KB block (its address is wave-uniform); lane i's 16 bytes at
-// block offset voff (its own) land at dst + 16 i.  The per-lane offset registers are
-// the same for every block, so no address register is rewritten while copies are in
-// flight.
-typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
-__device__ void raw_buffer_load_lds(i32x4 rsrc, __attribute__((address_space(3))) uint32_t *lds, int size, int voffset,
-                                    int soffset, int offset, int aux) __asm("llvm.amdgcn.raw.buffer.load.lds");
-__device__ __forceinline__ i32x4 block_rsrc(uint64_t base, int bytes = kBlockBytes) {
-    i32x4 r;
-    r.x = __builtin_amdgcn_readfirstlane((int)(uint32_t)base);
-    r.y = __builtin_amdgcn_readfirstlane((int)(uint32_t)(base >> 32));
-    r.z = bytes;       // bytes addressable through the resource
-    r.w = 0x00020000;  // raw 32-bit data format
-    return r;
-}
-// 16-byte buffer load into registers (the same per-lane offset register for every block,
-// a wave-uniform resource naming the block).
-__device__ i32x4 raw_buffer_load_b128(i32x4 rsrc, int voffset, int soffset, int aux) __asm("llvm.amdgcn.raw.buffer.load.v4i32");
-__device__ __forceinline__ u32x4 buf_load16(i32x4 rsrc, int voff) {
-    return __builtin_bit_cast(u32x4, raw_buffer_load_b128(rsrc, voff, 0, 0));
-}
-__device__ __forceinline__ void lds_dma16(i32x4 rsrc, int voff, LdsU32x4 *dst) {
-    raw_buffer_load_lds(rsrc, reinterpret_cast<__attribute__((address_space(3))) uint32_t *>(dst), 16, voff, 0, 0, 0);
-}
-
-// LDS byte address of a ring location.
-__device__ __forceinline__ uint32_t lds_addr(const LdsU32x4 *p) {
-    return (uint32_t)reinterpret_cast<uintptr_t>(p);
-}
-// Four 16-byte LDS reads at addr, addr + 1 KB, + 2 KB, + 3 KB (addr: this lane's byte
-// address), completed before the group ends.
-__device__ __forceinline__ void lds_read4(uint32_t addr, u32x4 (&out)[4]) {
-    asm volatile(
-        "ds_read_b128 %0, %4\n\t"
-        "ds_read_b128 %1, %4 offset:1024\n\t"
-        "ds_read_b128 %2, %4 offset:2048\n\t"
-        "ds_read_b128 %3, %4 offset:3072\n\t"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(out[0]), "=&v"(out[1]), "=&v"(out[2]), "=&v"(out[3])  // early clobber: the address stays intact
-        : "v"(addr)
-        : "memory");
-}
-
-// Wait until at most N vector-memory operations of this wave are outstanding.
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
 // Ring stage hand-over: this wave's copies older than its last N vector-memory operations
 // have landed in LDS (and its LDS reads of the previous stage completed inside their own
 // instruction groups), then all waves meet.  A plain barrier: the copies are ordered by
@@ -164,15 +114,6 @@ struct Rows {
         l = 0.f;
     }
 };
-
-// Zero tokens 4grp+i >= vis of a [.][token] fragment (bf16 pairs).
-__device__ __forceinline__ u32x2 mask4(u32x2 v, int vis, int grp) {
-    if (4 * grp + 0 >= vis) v.x &= 0xffff0000u;
-    if (4 * grp + 1 >= vis) v.x &= 0x0000ffffu;
-    if (4 * grp + 2 >= vis) v.y &= 0xffff0000u;
-    if (4 * grp + 3 >= vis) v.y &= 0x0000ffffu;
-    return v;
-}
 
 // Maximum over the four lane groups (lanes l, l^16, l^32, l^48) with the gfx950 lane
 // swaps (plain VALU, no LDS round trip).
@@ -670,7 +611,7 @@ __device__ __forceinline__ void split_body(const DecodeArgs &p) {
             const int npw = ngp == 4 ? 2 : 1;
             const int n_stages = (npg + 1) / 2;
             auto dma_stage = [&](int stage, LdsU32x4 *__restrict__ buf) __attribute__((always_inline)) {
-                const i32x4 rs = block_rsrc(base_addr(2 * stage + (wave >> 1)) + ((wave & 1) ? vbytes : 0));
+                const i32x4 rs = block_rsrc(base_addr(2 * stage + (wave >> 1)) + ((wave & 1) ? vbytes : 0), kBlockBytes);
                 LdsU32x4 *dst = buf + wave * (kBlockBytes / 16);
 #pragma unroll
                 for (int i = 0; i < 4; ++i) lds_dma16(rs, lane * 16 + i * 1024, dst + i * 64);
@@ -738,7 +679,7 @@ __device__ __forceinline__ void split_body(const DecodeArgs &p) {
         };
         auto load_page = [&](auto nsa_tag, int k, PageRegs &pr) __attribute__((always_inline)) {
             const uint64_t a = base_addr(k);
-            const i32x4 rk = block_rsrc(a), rv = block_rsrc(a + vbytes);
+            const i32x4 rk = block_rsrc(a, kBlockBytes), rv = block_rsrc(a + vbytes, kBlockBytes);
 #pragma unroll
             for (int i = 0; i < 4; ++i) pr.k[0][i] = buf_load16(rk, lane * 16 + i * 1024);
 #pragma unroll

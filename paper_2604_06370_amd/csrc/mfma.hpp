@@ -59,4 +59,13 @@ __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirs
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Zero tokens 4grp+i >= vis of a [.][token] fragment (bf16 pairs).
+__device__ __forceinline__ u32x2 mask4(u32x2 v, int vis, int grp) {
+    if (4 * grp + 0 >= vis) v.x &= 0xffff0000u;
+    if (4 * grp + 1 >= vis) v.x &= 0x0000ffffu;
+    if (4 * grp + 2 >= vis) v.y &= 0xffff0000u;
+    if (4 * grp + 3 >= vis) v.y &= 0x0000ffffu;
+    return v;
+}
+
 }  // namespace fkvk

@@ -25,6 +25,7 @@
 #include <string>
 
 #include "internal.hpp"
+#include "lds_dma.hpp"
 #include "mfma.hpp"
 
 using namespace fkvk;
@@ -422,6 +423,362 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// RoPE off: the key residual folds into the queries (S^T += C_K (B_K q)^T), so a tile
+// needs no rebuild and the stored blocks are used as they are.  Tiles then stream
+// through two LDS buffers by direct memory-to-LDS copies: while a tile is computed, wave
+// w copies page w of the next tile (its K and V blocks and, with an adapter, its rCache
+// page) into the other buffer.  One barrier per tile hands a buffer over: every wave has
+// waited for its own copies, and every wave has finished reading the buffer that the
+// copies issued after the barrier overwrite.
+//
+// Buffer layout (bytes): K blocks [page][4 KB], V blocks [page][4 KB], rCache pages as
+// [rank tile][page][1 KB] (four pages of one rank tile are 1 KB apart).  All are stored
+// verbatim: the K block's 16 bytes at k-step kk, lane l are the A fragment of the score
+// product, the V block's 16 bytes at chunk q2, lane l hold dims 32q2 + col (.xy) and
+// 32q2 + 16 + col (.zw) of tokens 4grp .. 4grp + 3, and the rCache fragment holds C_K
+// (.xy) and C_V (.zw) of the lane.
+template <int R>
+struct StreamShape {
+    static constexpr int RT = R == 0 ? 0 : (R + 15) / 16;
+    static constexpr int K_OFF = 0;
+    static constexpr int V_OFF = 4 * 4096;
+    static constexpr int C_OFF = 8 * 4096;
+    static constexpr int BUF_BYTES = C_OFF + 4 * RT * 1024;
+    static constexpr int SBV_BYTES = R > 0 ? R * D * 4 : 16;
+    static constexpr int SACC_BYTES = R > 0 ? ROWS_PER_WG * R * 4 : 16;
+    static constexpr int EPI_BYTES = SBV_BYTES + SACC_BYTES;
+    static constexpr int LDS_BYTES = (2 * BUF_BYTES > EPI_BYTES ? 2 * BUF_BYTES : EPI_BYTES);
+    static constexpr int OCC = 2 * LDS_BYTES <= 160 * 1024 ? 2 : 1;  // workgroups per CU
+};
+
+template <int R, int G>
+__global__ __launch_bounds__(256, StreamShape<R>::OCC) void prefill_stream_kernel(PrefillArgs p) {
+    using S = StreamShape<R>;
+    constexpr int RT = S::RT;
+    constexpr int RTX = RT > 0 ? RT : 1;
+    constexpr int TPW = ROWS_PER_WG / G;
+    __shared__ __attribute__((aligned(16))) u32x4 lds[S::LDS_BYTES / 16];
+    float *sBV = reinterpret_cast<float *>(lds);
+    float *sAcc = reinterpret_cast<float *>(reinterpret_cast<unsigned char *>(lds) + S::SBV_BYTES);
+
+    const int hkv = p.hkv;
+    const int bpa = p.blocks_per_agent_head;
+    const int xcd = blockIdx.x % kXcds, local = blockIdx.x / kXcds;
+    const int pair = (local / bpa) * kXcds + xcd;
+    const int qb = local - (local / bpa) * bpa;
+    if (pair >= p.n_agents * hkv) return;
+    const int a = pair / hkv;
+    const int h = pair - a * hkv;
+    const int q0 = p.q_indptr[a], nq = p.q_indptr[a + 1] - q0;
+    const int tok_begin = qb * TPW;
+    if (tok_begin >= nq) return;
+    const int L = p.seq_lens[a];
+    const int P0 = L - nq;  // position of the chunk's first query
+    const int ad = R > 0 ? p.adapter_idx[a] : -1;
+
+    const int lane = threadIdx.x & 63;
+    const int wave = uniform(threadIdx.x >> 6);
+    const int col = lane & 15, grp = lane >> 4;
+    const int64_t n = (int64_t)hkv * D;
+
+    const int n_pages = (L + PS - 1) / PS;
+    const int last_pos = P0 + (tok_begin + TPW < nq ? tok_begin + TPW : nq) - 1;
+    const int n_tiles = last_pos / TILE_KEYS + 1;
+    const int32_t *btb = p.base_bt + (int64_t)a * p.max_pages;
+    const int32_t *btr = R > 0 ? p.res_bt + (int64_t)a * p.max_pages : nullptr;
+    const bool use_res = R > 0 && ad >= 0;
+
+    // Page ids of this wave's pages (page 4 t + wave of tile t), 64 tiles per register:
+    // lane i holds the id for tile 64 c + i of chunk c (pages past the sequence repeat its
+    // last page, so every copy reads a real page; their keys are masked).
+    auto load_ids = [&](int c, int &idb, int &idr) __attribute__((always_inline)) {
+        const int pg = min((64 * c + lane) * 4 + wave, n_pages - 1);
+        idb = btb[pg];
+        idr = use_res ? btr[pg] : 0;
+    };
+    int idb_cur, idr_cur, idb_nxt, idr_nxt;
+    load_ids(0, idb_cur, idr_cur);
+    load_ids(1, idb_nxt, idr_nxt);
+
+    auto buf = [&](int tile) __attribute__((always_inline)) -> LdsU32x4 * {
+        return (LdsU32x4 *)(lds + (tile & 1) * (S::BUF_BYTES / 16));
+    };
+    // copies of tile `tile` (page 4 tile + wave): K block, V block, rCache page
+    auto copy_tile = [&](int tile, int idb, int idr) __attribute__((always_inline)) {
+        LdsU32x4 *b = buf(tile);
+        const uint64_t kaddr = reinterpret_cast<uint64_t>(p.base_kv + ((int64_t)idb * 2 * hkv + h) * (PS * D));
+        const i32x4 rk = block_rsrc(kaddr, 4096);
+        const i32x4 rv = block_rsrc(kaddr + (uint64_t)hkv * 4096, 4096);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) lds_dma16(rk, lane * 16 + i * 1024, b + (S::K_OFF + wave * 4096 + i * 1024) / 16);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) lds_dma16(rv, lane * 16 + i * 1024, b + (S::V_OFF + wave * 4096 + i * 1024) / 16);
+        if constexpr (R > 0) {
+            if (use_res) {
+                const i32x4 rc = block_rsrc(reinterpret_cast<uint64_t>(p.res_kv + (int64_t)idr * (RT * 512)), RT * 1024);
+#pragma unroll
+                for (int t = 0; t < RT; ++t) lds_dma16(rc, lane * 16 + t * 1024, b + (S::C_OFF + (t * 4 + wave) * 1024) / 16);
+            }
+        }
+    };
+
+    // queries of this lane's rows in the two 16-row tiles of the wave, in the contraction
+    // order of the stored K fragments
+    int row_tok[2], row_pos[2];
+    bool row_ok[2];
+    u32x4 qf[2][4];
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+        const int r = wave * ROWS_PER_WAVE + nt * 16 + col;
+        const int tk = tok_begin + r / G;
+        const int jj = r % G;
+        row_ok[nt] = tk < nq;
+        row_tok[nt] = tk;
+        row_pos[nt] = P0 + tk;
+        const uint16_t *qr = p.q + ((int64_t)(q0 + (row_ok[nt] ? tk : 0)) * p.hq + h * G + jj) * D;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+            u32x4 v = {0, 0, 0, 0};
+            if (row_ok[nt]) {
+                const u32x2 lo = ldg64(qr + 32 * kk + 4 * grp);
+                const u32x2 hi = ldg64(qr + 32 * kk + 16 + 4 * grp);
+                v = u32x4{lo.x, lo.y, hi.x, hi.y};
+            }
+            qf[nt][kk] = v;
+        }
+    }
+    // W^T = (B_K q)^T per row tile and rank tile: the residual key term of row j is
+    // (B_K q_j) . c_p, one extra contraction over the rank
+    u32x2 wq[2][RTX];
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+        for (int t = 0; t < RTX; ++t) wq[nt][t] = u32x2{0, 0};
+    if constexpr (R > 0) {
+        if (use_res) {
+#pragma unroll
+            for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+                for (int t = 0; t < RT; ++t) {
+                    f32x4 acc = {0, 0, 0, 0};
+                    const int rho = 16 * t + col;
+                    const uint16_t *bk = p.lora_b + (int64_t)ad * 2 * R * n + (int64_t)(rho < R ? rho : 0) * n + (int64_t)h * D;
+#pragma unroll
+                    for (int kk = 0; kk < 4; ++kk) {
+                        u32x4 av = {0, 0, 0, 0};
+                        if (rho < R) {
+                            const u32x2 lo = ldg64(bk + 32 * kk + 4 * grp);
+                            const u32x2 hi = ldg64(bk + 32 * kk + 16 + 4 * grp);
+                            av = u32x4{lo.x, lo.y, hi.x, hi.y};
+                        }
+                        acc = mfma32(av, qf[nt][kk], acc);
+                    }
+                    wq[nt][t] = pack4(acc);
+                }
+        }
+    }
+    // the page ids must be in registers before the first copy reads them
+    wait_vmcnt<0>();
+    copy_tile(0, __builtin_amdgcn_readlane(idb_cur, 0), __builtin_amdgcn_readlane(idr_cur, 0));
+
+    f32x4 oacc[8][2];
+#pragma unroll
+    for (int mt = 0; mt < 8; ++mt) oacc[mt][0] = oacc[mt][1] = f32x4{0, 0, 0, 0};
+    f32x4 racc[RTX][2];
+#pragma unroll
+    for (int t = 0; t < RTX; ++t) racc[t][0] = racc[t][1] = f32x4{0, 0, 0, 0};
+    float m_run[2] = {kNegInf, kNegInf}, l_run[2] = {0.f, 0.f};
+
+    for (int tile = 0; tile < n_tiles; ++tile) {
+        // tile's copies (and the page ids loaded with them) have landed; every wave is done
+        // with the previous tile, whose buffer the next copies overwrite
+        wait_vmcnt<0>();
+        __builtin_amdgcn_s_barrier();
+        const int tn = tile + 1;
+        if (tn < n_tiles) {
+            if ((tn & 63) == 0) {
+                idb_cur = idb_nxt;
+                idr_cur = idr_nxt;
+                load_ids((tn >> 6) + 1, idb_nxt, idr_nxt);
+            }
+            copy_tile(tn, __builtin_amdgcn_readlane(idb_cur, tn & 63), __builtin_amdgcn_readlane(idr_cur, tn & 63));
+        }
+        const uint32_t base = lds_addr(buf(tile)) + lane * 16;
+        // keys of the tile at or past the sequence end (the tile that holds it, or pages
+        // past it) may hold any bits in V and C_V: zero them
+        const bool ragged = (tile + 1) * TILE_KEYS > L;
+
+        // ---- scores for the 64 keys of the tile, 2 row tiles ----
+        f32x4 sacc[4][2];
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt) {
+            u32x4 kf[4];
+            lds_read4(base + S::K_OFF + kt * 4096, kf);
+            sacc[kt][0] = sacc[kt][1] = f32x4{0, 0, 0, 0};
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) {
+                sacc[kt][0] = mfma32(kf[kk], qf[0][kk], sacc[kt][0]);
+                sacc[kt][1] = mfma32(kf[kk], qf[1][kk], sacc[kt][1]);
+            }
+        }
+        if constexpr (R > 0) {
+            if (use_res) {
+#pragma unroll
+                for (int t = 0; t < RT; ++t) {
+                    // rCache fragments of the tile's four pages (C_K in .xy)
+                    u32x4 cf[4];
+                    lds_read4(base + S::C_OFF + t * 4096, cf);
+                    // C_K of rank rows 16t + 4grp .. +3 (rank 8: half a tile is padding)
+                    const bool kvalid = 16 * t + 4 * grp < R;
+#pragma unroll
+                    for (int kt = 0; kt < 4; ++kt) {
+                        const u32x4 ak = u32x4{kvalid ? cf[kt].x : 0u, kvalid ? cf[kt].y : 0u, 0u, 0u};
+                        // zero-padded 16x16x32 form: the chain stays on one instruction form
+                        sacc[kt][0] = mfma32(ak, u32x4{wq[0][t].x, wq[0][t].y, 0u, 0u}, sacc[kt][0]);
+                        sacc[kt][1] = mfma32(ak, u32x4{wq[1][t].x, wq[1][t].y, 0u, 0u}, sacc[kt][1]);
+                    }
+                }
+            }
+        }
+
+        // ---- causal mask + online softmax (rows live in lanes) ----
+        u32x2 pf[4][2];
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+            float sv[4][4];
+            float mx = kNegInf;
+#pragma unroll
+            for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int key = tile * TILE_KEYS + kt * PS + 4 * grp + i;
+                    sv[kt][i] = (row_ok[nt] && key <= row_pos[nt]) ? sacc[kt][nt][i] * p.scale_log2 : kNegInf;
+                    mx = fmaxf(mx, sv[kt][i]);
+                }
+            mx = fmaxf(mx, __shfl_xor(mx, 16));
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const float m_new = fmaxf(m_run[nt], mx);
+            const float m_use = m_new == kNegInf ? 0.f : m_new;
+            const float alpha = fast_exp2(m_run[nt] - m_use);
+            float ps = 0.f;
+#pragma unroll
+            for (int kt = 0; kt < 4; ++kt) {
+                f32x4 pv;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    pv[i] = fast_exp2(sv[kt][i] - m_use);
+                    ps += pv[i];
+                }
+                pf[kt][nt] = pack4(pv);
+            }
+            l_run[nt] = l_run[nt] * alpha + ps;
+            m_run[nt] = m_new;
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) oacc[mt][nt] *= alpha;
+#pragma unroll
+            for (int t = 0; t < RT; ++t) racc[t][nt] *= alpha;
+        }
+
+        // ---- O^T += V^T P^T and acc_r^T += C_V^T P^T over two 32-key halves ----
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            const u32x4 pb0 = u32x4{pf[2 * half][0].x, pf[2 * half][0].y, pf[2 * half + 1][0].x, pf[2 * half + 1][0].y};
+            const u32x4 pb1 = u32x4{pf[2 * half][1].x, pf[2 * half][1].y, pf[2 * half + 1][1].x, pf[2 * half + 1][1].y};
+            u32x4 v0[4], v1[4];
+            lds_read8(base + S::V_OFF + (2 * half) * 4096, base + S::V_OFF + (2 * half + 1) * 4096, v0, v1);
+            if (ragged) {
+                const int vis0 = L - (tile * 4 + 2 * half) * PS, vis1 = vis0 - PS;
+#pragma unroll
+                for (int q2 = 0; q2 < 4; ++q2) {
+                    const u32x2 a0 = mask4(u32x2{v0[q2].x, v0[q2].y}, vis0, grp), b0 = mask4(u32x2{v0[q2].z, v0[q2].w}, vis0, grp);
+                    const u32x2 a1 = mask4(u32x2{v1[q2].x, v1[q2].y}, vis1, grp), b1 = mask4(u32x2{v1[q2].z, v1[q2].w}, vis1, grp);
+                    v0[q2] = u32x4{a0.x, a0.y, b0.x, b0.y};
+                    v1[q2] = u32x4{a1.x, a1.y, b1.x, b1.y};
+                }
+            }
+#pragma unroll
+            for (int q2 = 0; q2 < 4; ++q2) {
+                const u32x4 va = u32x4{v0[q2].x, v0[q2].y, v1[q2].x, v1[q2].y};  // dim 32q2 + col
+                const u32x4 vb = u32x4{v0[q2].z, v0[q2].w, v1[q2].z, v1[q2].w};  // dim 32q2 + 16 + col
+                oacc[2 * q2][0] = mfma32(va, pb0, oacc[2 * q2][0]);
+                oacc[2 * q2][1] = mfma32(va, pb1, oacc[2 * q2][1]);
+                oacc[2 * q2 + 1][0] = mfma32(vb, pb0, oacc[2 * q2 + 1][0]);
+                oacc[2 * q2 + 1][1] = mfma32(vb, pb1, oacc[2 * q2 + 1][1]);
+            }
+            if constexpr (R > 0) {
+                if (use_res) {
+#pragma unroll
+                    for (int t = 0; t < RT; ++t) {
+                        // C_V of rank 16t + col, tokens 4grp .. +3 of the two pages (.zw)
+                        u32x4 cf[2];
+                        lds_read2(base + S::C_OFF + (t * 4 + 2 * half) * 1024, cf);
+                        u32x2 c0 = u32x2{cf[0].z, cf[0].w};
+                        u32x2 c1 = u32x2{cf[1].z, cf[1].w};
+                        if (ragged) {
+                            const int vis0 = L - (tile * 4 + 2 * half) * PS;
+                            c0 = mask4(c0, vis0, grp);
+                            c1 = mask4(c1, vis0 - PS, grp);
+                        }
+                        const bool vvalid = 16 * t + col < R;
+                        const u32x4 ca = vvalid ? u32x4{c0.x, c0.y, c1.x, c1.y} : u32x4{0, 0, 0, 0};
+                        racc[t][0] = mfma32(ca, pb0, racc[t][0]);
+                        racc[t][1] = mfma32(ca, pb1, racc[t][1]);
+                    }
+                }
+            }
+        }
+    }
+    wait_vmcnt<0>();
+    __syncthreads();  // the buffers are reused below
+
+    // ---- epilogue: O = (acc + acc_r . B_V[h]) / l ----
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+        l_run[nt] += __shfl_xor(l_run[nt], 16);
+        l_run[nt] += __shfl_xor(l_run[nt], 32);
+    }
+    if constexpr (R > 0) {
+        if (use_res) {
+            const uint16_t *bv = p.lora_b + ((int64_t)ad * 2 + 1) * R * n + (int64_t)h * D;
+            for (int e = threadIdx.x; e < R * D; e += 256) sBV[e] = bf16_to_f32(bv[(int64_t)(e / D) * n + (e % D)]);
+#pragma unroll
+            for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+                for (int t = 0; t < RT; ++t)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int rho = 16 * t + 4 * grp + i;
+                        if (rho < R) sAcc[(wave * ROWS_PER_WAVE + nt * 16 + col) * R + rho] = racc[t][nt][i];
+                    }
+            __syncthreads();
+#pragma unroll
+            for (int nt = 0; nt < 2; ++nt) {
+                const float *ar = sAcc + (wave * ROWS_PER_WAVE + nt * 16 + col) * R;
+                for (int rho = 0; rho < R; ++rho) {
+                    const float c = ar[rho];
+#pragma unroll
+                    for (int mt = 0; mt < 8; ++mt)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) oacc[mt][nt][i] += c * sBV[rho * D + 16 * mt + 4 * grp + i];
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+        if (!row_ok[nt]) continue;
+        const int r = wave * ROWS_PER_WAVE + nt * 16 + col;
+        const float inv = l_run[nt] > 0.f ? 1.f / l_run[nt] : 0.f;
+        uint16_t *orow = p.out + ((int64_t)(q0 + row_tok[nt]) * p.hq + h * G + r % G) * D;
+#pragma unroll
+        for (int mt = 0; mt < 8; ++mt) {
+            f32x4 o = oacc[mt][nt] * inv;
+            *reinterpret_cast<u32x2 *>(orow + 16 * mt + 4 * grp) = pack4(o);
+        }
+    }
+}
+
 template <int R, int G, bool ROPE>
 hipError_t launch_prefill(const PrefillArgs &pa, hipStream_t st, void *const *ev) {
     using S = PrefillShape<R, G, ROPE>;
@@ -430,7 +787,8 @@ hipError_t launch_prefill(const PrefillArgs &pa, hipStream_t st, void *const *ev
     const int pairs = (pa.n_agents * pa.hkv + kXcds - 1) / kXcds * kXcds;
     const int grid = pairs * pa.blocks_per_agent_head;
     (void)sizeof(S);
-    hipLaunchKernelGGL((prefill_kernel<R, G, ROPE>), dim3(grid), dim3(256), 0, st, pa);
+    if constexpr (ROPE) hipLaunchKernelGGL((prefill_kernel<R, G, ROPE>), dim3(grid), dim3(256), 0, st, pa);
+    else hipLaunchKernelGGL((prefill_stream_kernel<R, G>), dim3(grid), dim3(256), 0, st, pa);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[1]), st)) != hipSuccess) return e;
     return hipSuccess;
