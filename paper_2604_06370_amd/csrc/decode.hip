@@ -115,16 +115,6 @@ struct Rows {
     }
 };
 
-// Maximum over the four lane groups (lanes l, l^16, l^32, l^48) with the gfx950 lane
-// swaps (plain VALU, no LDS round trip).
-__device__ __forceinline__ float max_over_groups(float x) {
-    const uint32_t u = __float_as_uint(x);
-    const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-    const float y = fmaxf(x, __uint_as_float((threadIdx.x & 32) ? a[0] : a[1]));
-    const uint32_t v = __float_as_uint(y);
-    const auto b = __builtin_amdgcn_permlane16_swap(v, v, false, false);
-    return fmaxf(y, __uint_as_float((threadIdx.x & 16) ? b[0] : b[1]));
-}
 
 // Stage 2 on one page's S^T tile plus the value products.  Tokens tok0+4grp+i at or
 // past `len` (this lane's row's sequence length) or on an invalid page get zero weight;

@@ -68,4 +68,15 @@ __device__ __forceinline__ u32x2 mask4(u32x2 v, int vis, int grp) {
     return v;
 }
 
+// Maximum over the four lane groups (lanes l, l^16, l^32, l^48) with the gfx950 lane
+// swaps (plain VALU, no LDS round trip).
+__device__ __forceinline__ float max_over_groups(float x) {
+    const uint32_t u = __float_as_uint(x);
+    const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    const float y = fmaxf(x, __uint_as_float((threadIdx.x & 32) ? a[0] : a[1]));
+    const uint32_t v = __float_as_uint(y);
+    const auto b = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+    return fmaxf(y, __uint_as_float((threadIdx.x & 16) ? b[0] : b[1]));
+}
+
 }  // namespace fkvk

@@ -425,12 +425,14 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
 
 // ---------------------------------------------------------------------------
 // RoPE off: the key residual folds into the queries (S^T += C_K (B_K q)^T), so a tile
-// needs no rebuild and the stored blocks are used as they are.  Tiles then stream
-// through two LDS buffers by direct memory-to-LDS copies: while a tile is computed, wave
-// w copies page w of the next tile (its K and V blocks and, with an adapter, its rCache
-// page) into the other buffer.  One barrier per tile hands a buffer over: every wave has
-// waited for its own copies, and every wave has finished reading the buffer that the
-// copies issued after the barrier overwrite.
+// needs no rebuild and the stored blocks are used as they are.  A workgroup of eight
+// waves holds 256 query rows (twice the rows per key tile of the RoPE kernel, so half the
+// tile traffic per product), and tiles stream through a ring of three LDS buffers by
+// direct memory-to-LDS copies, two tiles ahead of the one being computed: wave w < 4
+// copies the K block (and, with an adapter, the rCache page) of page w of a tile, wave
+// 4 + w its V block.  One barrier per tile hands a buffer over: every wave has waited
+// (by count) for its copies of the tile, and every wave has finished reading the buffer
+// that the copies issued after the barrier overwrite.
 //
 // Buffer layout (bytes): K blocks [page][4 KB], V blocks [page][4 KB], rCache pages as
 // [rank tile][page][1 KB] (four pages of one rank tile are 1 KB apart).  All are stored
@@ -438,6 +440,12 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
 // product, the V block's 16 bytes at chunk q2, lane l hold dims 32q2 + col (.xy) and
 // 32q2 + 16 + col (.zw) of tokens 4grp .. 4grp + 3, and the rCache fragment holds C_K
 // (.xy) and C_V (.zw) of the lane.
+constexpr float kLazyRescale = 8.f;
+
+constexpr int kStreamWaves = 8;
+constexpr int kStreamRows = kStreamWaves * ROWS_PER_WAVE;
+constexpr int kStreamBufs = 3;
+
 template <int R>
 struct StreamShape {
     static constexpr int RT = R == 0 ? 0 : (R + 15) / 16;
@@ -446,18 +454,19 @@ struct StreamShape {
     static constexpr int C_OFF = 8 * 4096;
     static constexpr int BUF_BYTES = C_OFF + 4 * RT * 1024;
     static constexpr int SBV_BYTES = R > 0 ? R * D * 4 : 16;
-    static constexpr int SACC_BYTES = R > 0 ? ROWS_PER_WG * R * 4 : 16;
+    static constexpr int SACC_BYTES = R > 0 ? kStreamRows * R * 4 : 16;
     static constexpr int EPI_BYTES = SBV_BYTES + SACC_BYTES;
-    static constexpr int LDS_BYTES = (2 * BUF_BYTES > EPI_BYTES ? 2 * BUF_BYTES : EPI_BYTES);
-    static constexpr int OCC = 2 * LDS_BYTES <= 160 * 1024 ? 2 : 1;  // workgroups per CU
+    static constexpr int RING_BYTES = kStreamBufs * BUF_BYTES;
+    static constexpr int LDS_BYTES = RING_BYTES > EPI_BYTES ? RING_BYTES : EPI_BYTES;
+    static_assert(LDS_BYTES <= 160 * 1024, "LDS of one workgroup");
 };
 
 template <int R, int G>
-__global__ __launch_bounds__(256, StreamShape<R>::OCC) void prefill_stream_kernel(PrefillArgs p) {
+__global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(PrefillArgs p) {
     using S = StreamShape<R>;
     constexpr int RT = S::RT;
     constexpr int RTX = RT > 0 ? RT : 1;
-    constexpr int TPW = ROWS_PER_WG / G;
+    constexpr int TPW = kStreamRows / G;
     __shared__ __attribute__((aligned(16))) u32x4 lds[S::LDS_BYTES / 16];
     float *sBV = reinterpret_cast<float *>(lds);
     float *sAcc = reinterpret_cast<float *>(reinterpret_cast<unsigned char *>(lds) + S::SBV_BYTES);
@@ -489,36 +498,39 @@ __global__ __launch_bounds__(256, StreamShape<R>::OCC) void prefill_stream_kerne
     const int32_t *btr = R > 0 ? p.res_bt + (int64_t)a * p.max_pages : nullptr;
     const bool use_res = R > 0 && ad >= 0;
 
-    // Page ids of this wave's pages (page 4 t + wave of tile t), 64 tiles per register:
+    // This wave copies page pw of every tile: its K block and rCache page (waves 0..3) or
+    // its V block (waves 4..7).
+    const int pw = wave & 3;
+    const bool kwave = wave < 4;
+    const bool res_copy = use_res && kwave;
+    // Page ids of this wave's pages (page 4 t + pw of tile t), 64 tiles per register:
     // lane i holds the id for tile 64 c + i of chunk c (pages past the sequence repeat its
     // last page, so every copy reads a real page; their keys are masked).
     auto load_ids = [&](int c, int &idb, int &idr) __attribute__((always_inline)) {
-        const int pg = min((64 * c + lane) * 4 + wave, n_pages - 1);
+        const int pg = min((64 * c + lane) * 4 + pw, n_pages - 1);
         idb = btb[pg];
-        idr = use_res ? btr[pg] : 0;
+        idr = res_copy ? btr[pg] : 0;
     };
     int idb_cur, idr_cur, idb_nxt, idr_nxt;
     load_ids(0, idb_cur, idr_cur);
     load_ids(1, idb_nxt, idr_nxt);
 
     auto buf = [&](int tile) __attribute__((always_inline)) -> LdsU32x4 * {
-        return (LdsU32x4 *)(lds + (tile & 1) * (S::BUF_BYTES / 16));
+        return (LdsU32x4 *)(lds + (tile % kStreamBufs) * (S::BUF_BYTES / 16));
     };
-    // copies of tile `tile` (page 4 tile + wave): K block, V block, rCache page
+    // this wave's copies of tile `tile` (page 4 tile + pw)
     auto copy_tile = [&](int tile, int idb, int idr) __attribute__((always_inline)) {
         LdsU32x4 *b = buf(tile);
         const uint64_t kaddr = reinterpret_cast<uint64_t>(p.base_kv + ((int64_t)idb * 2 * hkv + h) * (PS * D));
-        const i32x4 rk = block_rsrc(kaddr, 4096);
-        const i32x4 rv = block_rsrc(kaddr + (uint64_t)hkv * 4096, 4096);
+        const i32x4 rs = block_rsrc(kwave ? kaddr : kaddr + (uint64_t)hkv * 4096, 4096);
+        LdsU32x4 *dst = b + ((kwave ? S::K_OFF : S::V_OFF) + pw * 4096) / 16;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) lds_dma16(rk, lane * 16 + i * 1024, b + (S::K_OFF + wave * 4096 + i * 1024) / 16);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) lds_dma16(rv, lane * 16 + i * 1024, b + (S::V_OFF + wave * 4096 + i * 1024) / 16);
+        for (int i = 0; i < 4; ++i) lds_dma16(rs, lane * 16 + i * 1024, dst + i * 64);
         if constexpr (R > 0) {
-            if (use_res) {
+            if (res_copy) {
                 const i32x4 rc = block_rsrc(reinterpret_cast<uint64_t>(p.res_kv + (int64_t)idr * (RT * 512)), RT * 1024);
 #pragma unroll
-                for (int t = 0; t < RT; ++t) lds_dma16(rc, lane * 16 + t * 1024, b + (S::C_OFF + (t * 4 + wave) * 1024) / 16);
+                for (int t = 0; t < RT; ++t) lds_dma16(rc, lane * 16 + t * 1024, b + (S::C_OFF + (t * 4 + pw) * 1024) / 16);
             }
         }
     };
@@ -578,9 +590,10 @@ __global__ __launch_bounds__(256, StreamShape<R>::OCC) void prefill_stream_kerne
                 }
         }
     }
-    // the page ids must be in registers before the first copy reads them
+    // the page ids must be in registers before the first copies read them
     wait_vmcnt<0>();
     copy_tile(0, __builtin_amdgcn_readlane(idb_cur, 0), __builtin_amdgcn_readlane(idr_cur, 0));
+    if (n_tiles > 1) copy_tile(1, __builtin_amdgcn_readlane(idb_cur, 1), __builtin_amdgcn_readlane(idr_cur, 1));
 
     f32x4 oacc[8][2];
 #pragma unroll
@@ -588,14 +601,23 @@ __global__ __launch_bounds__(256, StreamShape<R>::OCC) void prefill_stream_kerne
     f32x4 racc[RTX][2];
 #pragma unroll
     for (int t = 0; t < RTX; ++t) racc[t][0] = racc[t][1] = f32x4{0, 0, 0, 0};
-    float m_run[2] = {kNegInf, kNegInf}, l_run[2] = {0.f, 0.f};
+    f32x4 lacc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};  // row sums l
+    float m_run[2] = {kNegInf, kNegInf};
+    const float cl = p.scale_log2;
+    const u32x4 kOnes = u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u};  // bf16 1.0
 
     for (int tile = 0; tile < n_tiles; ++tile) {
-        // tile's copies (and the page ids loaded with them) have landed; every wave is done
-        // with the previous tile, whose buffer the next copies overwrite
-        wait_vmcnt<0>();
+        // this wave's copies of the tile have landed (only those of the next tile, issued
+        // after them, may still be in flight); after the barrier every wave's have, and
+        // every wave is done with the tile before, whose buffer the next copies overwrite
+        if (tile + 1 < n_tiles) {
+            if (res_copy) wait_vmcnt<4 + RT>();
+            else wait_vmcnt<4>();
+        } else {
+            wait_vmcnt<0>();
+        }
         __builtin_amdgcn_s_barrier();
-        const int tn = tile + 1;
+        const int tn = tile + 2;
         if (tn < n_tiles) {
             if ((tn & 63) == 0) {
                 idb_cur = idb_nxt;
@@ -643,41 +665,52 @@ __global__ __launch_bounds__(256, StreamShape<R>::OCC) void prefill_stream_kerne
         }
 
         // ---- causal mask + online softmax (rows live in lanes) ----
+        // A tile below every row's diagonal needs no mask.  The running maximum moves only
+        // when some row's scores exceed it by more than 2^kLazyRescale (then acc, acc_r and
+        // the row sums are rescaled); otherwise this tile's weights stay below 2^8.
+        const bool full = (tile + 1) * TILE_KEYS - 1 <= P0 + tok_begin;
         u32x2 pf[4][2];
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt) {
             float sv[4][4];
+            if (full) {
+#pragma unroll
+                for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) sv[kt][i] = sacc[kt][nt][i];
+            } else {
+#pragma unroll
+                for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int key = tile * TILE_KEYS + kt * PS + 4 * grp + i;
+                        sv[kt][i] = (row_ok[nt] && key <= row_pos[nt]) ? sacc[kt][nt][i] : kNegInf;
+                    }
+            }
             float mx = kNegInf;
 #pragma unroll
             for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int key = tile * TILE_KEYS + kt * PS + 4 * grp + i;
-                    sv[kt][i] = (row_ok[nt] && key <= row_pos[nt]) ? sacc[kt][nt][i] * p.scale_log2 : kNegInf;
-                    mx = fmaxf(mx, sv[kt][i]);
-                }
-            mx = fmaxf(mx, __shfl_xor(mx, 16));
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
-            const float m_new = fmaxf(m_run[nt], mx);
-            const float m_use = m_new == kNegInf ? 0.f : m_new;
-            const float alpha = fast_exp2(m_run[nt] - m_use);
-            float ps = 0.f;
+                for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sv[kt][i]);
+            mx = max_over_groups(mx) * cl;  // the scale is positive
+            if (__builtin_amdgcn_ballot_w64(mx > m_run[nt] + kLazyRescale) != 0) {
+                const float m_new = fmaxf(m_run[nt], mx);
+                const float alpha = fast_exp2(m_run[nt] - (m_new == kNegInf ? 0.f : m_new));
+#pragma unroll
+                for (int mt = 0; mt < 8; ++mt) oacc[mt][nt] *= alpha;
+#pragma unroll
+                for (int t = 0; t < RT; ++t) racc[t][nt] *= alpha;
+                lacc[nt] *= alpha;
+                m_run[nt] = m_new;
+            }
+            const float m_use = m_run[nt] == kNegInf ? 0.f : m_run[nt];
 #pragma unroll
             for (int kt = 0; kt < 4; ++kt) {
                 f32x4 pv;
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    pv[i] = fast_exp2(sv[kt][i] - m_use);
-                    ps += pv[i];
-                }
+                for (int i = 0; i < 4; ++i) pv[i] = fast_exp2(__builtin_fmaf(sv[kt][i], cl, -m_use));
                 pf[kt][nt] = pack4(pv);
             }
-            l_run[nt] = l_run[nt] * alpha + ps;
-            m_run[nt] = m_new;
-#pragma unroll
-            for (int mt = 0; mt < 8; ++mt) oacc[mt][nt] *= alpha;
-#pragma unroll
-            for (int t = 0; t < RT; ++t) racc[t][nt] *= alpha;
         }
 
         // ---- O^T += V^T P^T and acc_r^T += C_V^T P^T over two 32-key halves ----
@@ -706,6 +739,9 @@ __global__ __launch_bounds__(256, StreamShape<R>::OCC) void prefill_stream_kerne
                 oacc[2 * q2 + 1][0] = mfma32(vb, pb0, oacc[2 * q2 + 1][0]);
                 oacc[2 * q2 + 1][1] = mfma32(vb, pb1, oacc[2 * q2 + 1][1]);
             }
+            // row sums of the bf16 weights (every accumulator row holds the sum)
+            lacc[0] = mfma32(kOnes, pb0, lacc[0]);
+            lacc[1] = mfma32(kOnes, pb1, lacc[1]);
             if constexpr (R > 0) {
                 if (use_res) {
 #pragma unroll
@@ -733,15 +769,11 @@ __global__ __launch_bounds__(256, StreamShape<R>::OCC) void prefill_stream_kerne
     __syncthreads();  // the buffers are reused below
 
     // ---- epilogue: O = (acc + acc_r . B_V[h]) / l ----
-#pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
-        l_run[nt] += __shfl_xor(l_run[nt], 16);
-        l_run[nt] += __shfl_xor(l_run[nt], 32);
-    }
+    const float l_run[2] = {lacc[0][0], lacc[1][0]};
     if constexpr (R > 0) {
         if (use_res) {
             const uint16_t *bv = p.lora_b + ((int64_t)ad * 2 + 1) * R * n + (int64_t)h * D;
-            for (int e = threadIdx.x; e < R * D; e += 256) sBV[e] = bf16_to_f32(bv[(int64_t)(e / D) * n + (e % D)]);
+            for (int e = threadIdx.x; e < R * D; e += 64 * kStreamWaves) sBV[e] = bf16_to_f32(bv[(int64_t)(e / D) * n + (e % D)]);
 #pragma unroll
             for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
@@ -788,7 +820,7 @@ hipError_t launch_prefill(const PrefillArgs &pa, hipStream_t st, void *const *ev
     const int grid = pairs * pa.blocks_per_agent_head;
     (void)sizeof(S);
     if constexpr (ROPE) hipLaunchKernelGGL((prefill_kernel<R, G, ROPE>), dim3(grid), dim3(256), 0, st, pa);
-    else hipLaunchKernelGGL((prefill_stream_kernel<R, G>), dim3(grid), dim3(256), 0, st, pa);
+    else hipLaunchKernelGGL((prefill_stream_kernel<R, G>), dim3(grid), dim3(64 * kStreamWaves), 0, st, pa);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[1]), st)) != hipSuccess) return e;
     return hipSuccess;
@@ -842,12 +874,12 @@ extern "C" fkv_status fkv_residual_attention_prefill(const fkv_attn_args *a, voi
     pa.hkv = a->hkv;
     pa.max_pages = a->max_pages;
     // query blocks per (agent, KV head); blocks past an agent's own chunk exit at once
-    const int tok_per_wg = ROWS_PER_WG / g;
+    const bool rope = a->rope_cos != nullptr && a->r > 0;
+    const int tok_per_wg = (rope ? ROWS_PER_WG : kStreamRows) / g;
     const int maxq = a->max_q_per_agent > 0 ? a->max_q_per_agent : a->n_q;
     if (maxq > a->n_q) return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_prefill: max_q_per_agent > n_q");
     pa.blocks_per_agent_head = (maxq + tok_per_wg - 1) / tok_per_wg;
     pa.scale_log2 = a->scale * 1.4426950408889634f;
-    const bool rope = a->rope_cos != nullptr && a->r > 0;
     hipStream_t hs = static_cast<hipStream_t>(stream);
     hipError_t e = g == 4 ? dispatch_prefill<4>(a->r, rope, pa, hs, a->timing_events)
                           : dispatch_prefill<8>(a->r, rope, pa, hs, a->timing_events);
