@@ -167,7 +167,7 @@ def measure_prefill(args, dev, stream) -> dict:
         k_ms = float(ms.mean())
         tflops = fl["total"] / (k_ms * 1e-3) / 1e12
         res["rope_on" if rope else "rope_off"] = {
-            "kernel": "prefill_kernel" if rope else "prefill_stream_kernel", "kernel_ms": k_ms, "kernel_ms_p10_p50_p90": [float(np.percentile(ms, q)) for q in (10, 50, 90)],
+            "kernel": "prefill_kernel" if rope and wl.r > 32 else "prefill_stream_kernel", "kernel_ms": k_ms, "kernel_ms_p10_p50_p90": [float(np.percentile(ms, q)) for q in (10, 50, 90)],
             "tokens_per_s": fl["rows"] * n / (t1 - t0), "achieved": tflops, "frac": tflops / MFMA_BF16_PEAK_TFLOPS}
         lw.close()
         del lw

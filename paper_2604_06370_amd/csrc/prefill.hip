@@ -424,15 +424,19 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
 }
 
 // ---------------------------------------------------------------------------
-// RoPE off: the key residual folds into the queries (S^T += C_K (B_K q)^T), so a tile
-// needs no rebuild and the stored blocks are used as they are.  A workgroup of eight
-// waves holds 256 query rows (twice the rows per key tile of the RoPE kernel, so half the
-// tile traffic per product), and tiles stream through a ring of three LDS buffers by
-// direct memory-to-LDS copies, two tiles ahead of the one being computed: wave w < 4
-// copies the K block (and, with an adapter, the rCache page) of page w of a tile, wave
-// 4 + w its V block.  One barrier per tile hands a buffer over: every wave has waited
-// (by count) for its copies of the tile, and every wave has finished reading the buffer
-// that the copies issued after the barrier overwrite.
+// Streaming kernel.  A workgroup of eight waves holds 256 query rows (twice the rows per
+// key tile of the kernel above, so half the tile traffic per product), and 64-key tiles
+// stream through a ring of LDS buffers by direct memory-to-LDS copies: wave w < 4 copies
+// the K block (and, with an adapter, the rCache page) of page w of a tile, wave 4 + w its
+// V block.  One barrier per tile hands a buffer over: every wave has waited (by count)
+// for its copies of the tile, and every wave has finished reading the buffer that the
+// copies issued after the barrier overwrite.
+//  - RoPE off: the key residual folds into the queries (S^T += C_K (B_K q)^T), so the
+//    stored blocks are used as they are; three buffers, copies two tiles ahead.
+//  - RoPE on (rank up to 32): a tile also carries the table rows of its positions; two
+//    buffers, copies one tile ahead.  After a tile has landed each wave rebuilds a quarter
+//    of one page's keys in place (U^T = B_K^T C_K^T on the matrix cores, rotated, added to
+//    K_base) and a second barrier publishes the rebuilt tile.
 //
 // Buffer layout (bytes): K blocks [page][4 KB], V blocks [page][4 KB], rCache pages as
 // [rank tile][page][1 KB] (four pages of one rank tile are 1 KB apart).  All are stored
@@ -443,33 +447,41 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
 constexpr float kLazyRescale = 8.f;
 
 constexpr int kStreamWaves = 8;
+// RoPE on, the streaming kernel serves ranks up to 32 (its LDS ring and B_K^T fragments
+// fit one workgroup's LDS); rank 64 takes the kernel above
+constexpr bool stream_rope(int r) { return r <= 32; }
 constexpr int kStreamRows = kStreamWaves * ROWS_PER_WAVE;
-constexpr int kStreamBufs = 3;
 
-template <int R>
+template <int R, bool ROPE>
 struct StreamShape {
+    static constexpr int NBUF = ROPE ? 2 : 3;  // ring buffers (copies NBUF - 1 tiles ahead)
     static constexpr int RT = R == 0 ? 0 : (R + 15) / 16;
+    static constexpr int SBK_BYTES = ROPE ? RT * 8 * 64 * 8 : 0;  // B_K^T fragments (RoPE on)
     static constexpr int K_OFF = 0;
     static constexpr int V_OFF = 4 * 4096;
     static constexpr int C_OFF = 8 * 4096;
-    static constexpr int BUF_BYTES = C_OFF + 4 * RT * 1024;
+    // RoPE on: table rows [page][half][cos m, cos m + 1, sin m, sin m + 1][1 KB], m = 2 half
+    static constexpr int T_OFF = C_OFF + 4 * RT * 1024;
+    static constexpr int BUF_BYTES = T_OFF + (ROPE ? 4 * 2 * 4096 : 0);
     static constexpr int SBV_BYTES = R > 0 ? R * D * 4 : 16;
     static constexpr int SACC_BYTES = R > 0 ? kStreamRows * R * 4 : 16;
     static constexpr int EPI_BYTES = SBV_BYTES + SACC_BYTES;
-    static constexpr int RING_BYTES = kStreamBufs * BUF_BYTES;
-    static constexpr int LDS_BYTES = RING_BYTES > EPI_BYTES ? RING_BYTES : EPI_BYTES;
+    static constexpr int RING_BYTES = NBUF * BUF_BYTES;
+    static constexpr int MAIN_BYTES = RING_BYTES > EPI_BYTES ? RING_BYTES : EPI_BYTES;
+    static constexpr int LDS_BYTES = MAIN_BYTES + SBK_BYTES;
     static_assert(LDS_BYTES <= 160 * 1024, "LDS of one workgroup");
 };
 
-template <int R, int G>
+template <int R, int G, bool ROPE>
 __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(PrefillArgs p) {
-    using S = StreamShape<R>;
+    using S = StreamShape<R, ROPE>;
     constexpr int RT = S::RT;
     constexpr int RTX = RT > 0 ? RT : 1;
     constexpr int TPW = kStreamRows / G;
     __shared__ __attribute__((aligned(16))) u32x4 lds[S::LDS_BYTES / 16];
     float *sBV = reinterpret_cast<float *>(lds);
     float *sAcc = reinterpret_cast<float *>(reinterpret_cast<unsigned char *>(lds) + S::SBV_BYTES);
+    const u32x2 *sBK = reinterpret_cast<const u32x2 *>(reinterpret_cast<unsigned char *>(lds) + S::MAIN_BYTES);
 
     const int hkv = p.hkv;
     const int bpa = p.blocks_per_agent_head;
@@ -501,6 +513,7 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
     // This wave copies page pw of every tile: its K block and rCache page (waves 0..3) or
     // its V block (waves 4..7).
     const int pw = wave & 3;
+    const int half = wave >> 2;
     const bool kwave = wave < 4;
     const bool res_copy = use_res && kwave;
     // Page ids of this wave's pages (page 4 t + pw of tile t), 64 tiles per register:
@@ -516,7 +529,7 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
     load_ids(1, idb_nxt, idr_nxt);
 
     auto buf = [&](int tile) __attribute__((always_inline)) -> LdsU32x4 * {
-        return (LdsU32x4 *)(lds + (tile % kStreamBufs) * (S::BUF_BYTES / 16));
+        return (LdsU32x4 *)(lds + (tile % S::NBUF) * (S::BUF_BYTES / 16));
     };
     // this wave's copies of tile `tile` (page 4 tile + pw)
     auto copy_tile = [&](int tile, int idb, int idr) __attribute__((always_inline)) {
@@ -531,6 +544,21 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
                 const i32x4 rc = block_rsrc(reinterpret_cast<uint64_t>(p.res_kv + (int64_t)idr * (RT * 512)), RT * 1024);
 #pragma unroll
                 for (int t = 0; t < RT; ++t) lds_dma16(rc, lane * 16 + t * 1024, b + (S::C_OFF + (t * 4 + pw) * 1024) / 16);
+            }
+        }
+        if constexpr (ROPE && R > 0) {
+            if (use_res) {
+                // the table rows this wave's rebuild uses: frequency tiles 2 half, 2 half + 1
+                // of page pw (1 KB each, cos then sin)
+                const int64_t pg = min(tile * 4 + pw, n_pages - 1);
+                const uint64_t off = (uint64_t)(pg * (PS * D / 2) + 2 * half * 256) * 4;
+                const i32x4 tc = block_rsrc(reinterpret_cast<uint64_t>(p.rope_cos) + off, 2048);
+                const i32x4 ts = block_rsrc(reinterpret_cast<uint64_t>(p.rope_sin) + off, 2048);
+                LdsU32x4 *td = b + (S::T_OFF + (pw * 2 + half) * 4096) / 16;
+                lds_dma16(tc, lane * 16, td);
+                lds_dma16(tc, lane * 16 + 1024, td + 64);
+                lds_dma16(ts, lane * 16, td + 128);
+                lds_dma16(ts, lane * 16 + 1024, td + 192);
             }
         }
     };
@@ -567,7 +595,7 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
     for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
         for (int t = 0; t < RTX; ++t) wq[nt][t] = u32x2{0, 0};
-    if constexpr (R > 0) {
+    if constexpr (R > 0 && !ROPE) {
         if (use_res) {
 #pragma unroll
             for (int nt = 0; nt < 2; ++nt)
@@ -590,10 +618,35 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
                 }
         }
     }
+    // RoPE on: B_K^T fragments of the agent's adapter (lane holds B_K[16t + 4grp + i][h*D +
+    // 16mt + col]) in LDS for the whole launch; this wave rebuilds u tiles 2 half, 2 half + 1
+    // and their rotation partners + 4 of page pw, with the table rows of frequency tiles
+    // 2 half + j, loaded one tile ahead
+    if constexpr (ROPE && R > 0) {
+        if (use_res) {
+            u32x2 *bkt = const_cast<u32x2 *>(sBK);
+            const uint16_t *bk = p.lora_b + (int64_t)ad * 2 * R * n + (int64_t)h * D;
+            for (int idx = threadIdx.x; idx < RT * 8 * 64; idx += 64 * kStreamWaves) {
+                const int ln = idx & 63, rest = idx >> 6;
+                const int mt = rest & 7, t = rest >> 3;
+                const int c = ln & 15, gg = ln >> 4;
+                uint32_t w[2];
+#pragma unroll
+                for (int j = 0; j < 2; ++j) {
+                    const int r0 = 16 * t + 4 * gg + 2 * j;
+                    const uint16_t lo = r0 < R ? bk[(int64_t)r0 * n + 16 * mt + c] : (uint16_t)0;
+                    const uint16_t hi = r0 + 1 < R ? bk[(int64_t)(r0 + 1) * n + 16 * mt + c] : (uint16_t)0;
+                    w[j] = (uint32_t)lo | ((uint32_t)hi << 16);
+                }
+                bkt[idx] = u32x2{w[0], w[1]};
+            }
+            __syncthreads();  // B_K^T fragments written (no copy into LDS is in flight yet)
+        }
+    }
     // the page ids must be in registers before the first copies read them
     wait_vmcnt<0>();
     copy_tile(0, __builtin_amdgcn_readlane(idb_cur, 0), __builtin_amdgcn_readlane(idr_cur, 0));
-    if (n_tiles > 1) copy_tile(1, __builtin_amdgcn_readlane(idb_cur, 1), __builtin_amdgcn_readlane(idr_cur, 1));
+    if (S::NBUF == 3 && n_tiles > 1) copy_tile(1, __builtin_amdgcn_readlane(idb_cur, 1), __builtin_amdgcn_readlane(idr_cur, 1));
 
     f32x4 oacc[8][2];
 #pragma unroll
@@ -610,14 +663,15 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
         // this wave's copies of the tile have landed (only those of the next tile, issued
         // after them, may still be in flight); after the barrier every wave's have, and
         // every wave is done with the tile before, whose buffer the next copies overwrite
-        if (tile + 1 < n_tiles) {
+        // (two buffers: nothing else is in flight)
+        if (S::NBUF == 3 && tile + 1 < n_tiles) {
             if (res_copy) wait_vmcnt<4 + RT>();
             else wait_vmcnt<4>();
         } else {
             wait_vmcnt<0>();
         }
         __builtin_amdgcn_s_barrier();
-        const int tn = tile + 2;
+        const int tn = tile + S::NBUF - 1;
         if (tn < n_tiles) {
             if ((tn & 63) == 0) {
                 idb_cur = idb_nxt;
@@ -630,6 +684,58 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
         // keys of the tile at or past the sequence end (the tile that holds it, or pages
         // past it) may hold any bits in V and C_V: zero them
         const bool ragged = (tile + 1) * TILE_KEYS > L;
+        if constexpr (ROPE && R > 0) {
+            if (use_res) {
+                // Stage 1 for a quarter of page pw: U^T tiles, deferred RoPE, K = K_base +
+                // K_lora in place (keys past the sequence end are masked out of the scores)
+                u32x2 ck[RTX];
+#pragma unroll
+                for (int t = 0; t < RT; ++t) {
+                    const u32x4 c = lds_read1(base + S::C_OFF + (t * 4 + pw) * 1024);
+                    ck[t] = (16 * t + 4 * grp < R) ? u32x2{c.x, c.y} : u32x2{0, 0};
+                }
+                f32x4 u[4];  // u tiles 2 half, 2 half + 1, 2 half + 4, 2 half + 5
+#pragma unroll
+                for (int j = 0; j < 4; ++j) u[j] = f32x4{0, 0, 0, 0};
+#pragma unroll
+                for (int t = 0; t < RT; ++t) {
+                    // (explicit reads: the copies in flight write other LDS bytes)
+                    u32x2 bkf[4];
+                    lds_read4_b64_tiles(lds_addr((LdsU32x4 *)lds) + S::MAIN_BYTES + ((t * 8 + 2 * half) * 64 + lane) * 8, bkf);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) u[j] = mfma16(bkf[j], ck[t], u[j]);
+                }
+                // rotate-half pairs (tile m with m + 4) at the key's position
+                u32x4 rot[4];  // cos m, cos m + 1, sin m, sin m + 1 of this lane
+                lds_read4(base + S::T_OFF + (pw * 2 + half) * 4096, rot);
+#pragma unroll
+                for (int j = 0; j < 2; ++j) {
+                    const f32x4 c = __builtin_bit_cast(f32x4, rot[j]), s = __builtin_bit_cast(f32x4, rot[2 + j]);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float x = u[j][i], y = u[j + 2][i];
+                        u[j][i] = x * c[i] - y * s[i];
+                        u[j + 2][i] = y * c[i] + x * s[i];
+                    }
+                }
+                // K fragments half (u tiles 2 half, 2 half + 1) and half + 2 (tiles + 4)
+                const uint32_t ka = base + S::K_OFF + pw * 4096 + half * 1024;
+                const uint32_t kb = ka + 2 * 1024;
+                u32x4 kf[2];
+                lds_read2_2k(ka, kf);
+                u32x4 out[2];
+#pragma unroll
+                for (int j = 0; j < 2; ++j) {
+                    const u32x4 k = kf[j];
+                    const f32x4 lo = f32x4{bf16_lo(k.x), bf16_hi(k.x), bf16_lo(k.y), bf16_hi(k.y)} + u[2 * j];
+                    const f32x4 hi = f32x4{bf16_lo(k.z), bf16_hi(k.z), bf16_lo(k.w), bf16_hi(k.w)} + u[2 * j + 1];
+                    const u32x2 plo = pack4(lo), phi = pack4(hi);
+                    out[j] = u32x4{plo.x, plo.y, phi.x, phi.y};
+                }
+                lds_write2(ka, out[0], kb, out[1]);
+                __builtin_amdgcn_s_barrier();  // the rebuilt tile is complete
+            }
+        }
 
         // ---- scores for the 64 keys of the tile, 2 row tiles ----
         f32x4 sacc[4][2];
@@ -644,7 +750,7 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
                 sacc[kt][1] = mfma32(kf[kk], qf[1][kk], sacc[kt][1]);
             }
         }
-        if constexpr (R > 0) {
+        if constexpr (R > 0 && !ROPE) {
             if (use_res) {
 #pragma unroll
                 for (int t = 0; t < RT; ++t) {
@@ -819,8 +925,8 @@ hipError_t launch_prefill(const PrefillArgs &pa, hipStream_t st, void *const *ev
     const int pairs = (pa.n_agents * pa.hkv + kXcds - 1) / kXcds * kXcds;
     const int grid = pairs * pa.blocks_per_agent_head;
     (void)sizeof(S);
-    if constexpr (ROPE) hipLaunchKernelGGL((prefill_kernel<R, G, ROPE>), dim3(grid), dim3(256), 0, st, pa);
-    else hipLaunchKernelGGL((prefill_stream_kernel<R, G>), dim3(grid), dim3(64 * kStreamWaves), 0, st, pa);
+    if constexpr (ROPE && !stream_rope(R)) hipLaunchKernelGGL((prefill_kernel<R, G, ROPE>), dim3(grid), dim3(256), 0, st, pa);
+    else hipLaunchKernelGGL((prefill_stream_kernel<R, G, ROPE>), dim3(grid), dim3(64 * kStreamWaves), 0, st, pa);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[1]), st)) != hipSuccess) return e;
     return hipSuccess;
@@ -875,7 +981,7 @@ extern "C" fkv_status fkv_residual_attention_prefill(const fkv_attn_args *a, voi
     pa.max_pages = a->max_pages;
     // query blocks per (agent, KV head); blocks past an agent's own chunk exit at once
     const bool rope = a->rope_cos != nullptr && a->r > 0;
-    const int tok_per_wg = (rope ? ROWS_PER_WG : kStreamRows) / g;
+    const int tok_per_wg = ((rope && !stream_rope(a->r)) ? ROWS_PER_WG : kStreamRows) / g;
     const int maxq = a->max_q_per_agent > 0 ? a->max_q_per_agent : a->n_q;
     if (maxq > a->n_q) return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_prefill: max_q_per_agent > n_q");
     pa.blocks_per_agent_head = (maxq + tok_per_wg - 1) / tok_per_wg;

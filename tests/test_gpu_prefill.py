@@ -72,11 +72,12 @@ def test_prefill_70b_heads_rank64(rope):
     run_prefill(f"prefill-70b rope={rope}", wl, rope)
 
 
-@pytest.mark.parametrize("rank", [0, 32])
-def test_prefill_other_ranks(rank):
-    wl = W.fanout(f"pf-r{rank}", 53, n_agents=3, prefix=128, suffix_lo=1, suffix_hi=30, hq=32, hkv=8,
+@pytest.mark.parametrize("rope", [False, True])
+@pytest.mark.parametrize("rank,hq", [(0, 32), (8, 32), (32, 32), (16, 64)])
+def test_prefill_other_ranks(rank, hq, rope):
+    wl = W.fanout(f"pf-r{rank}-hq{hq}", 53, n_agents=3, prefix=128, suffix_lo=1, suffix_hi=30, hq=hq, hkv=8,
                   r=max(rank, 8), chunk=64, zero_residual=range(3) if rank == 0 else ())
-    run_prefill(f"prefill-r{rank}", wl, True)
+    run_prefill(f"prefill-r{rank}-hq{hq} rope={rope}", wl, rope)
 
 
 def test_copy_on_write_at_fork_and_append():
