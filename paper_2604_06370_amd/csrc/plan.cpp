@@ -169,18 +169,30 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
             }
             return end;
         };
-        // (the largest page count whose estimate is within 1% of the best: fewer items, fewer
-        // partial rows to merge)
+        // The largest page count whose estimate is within 5% of the best (fewer items, fewer
+        // partial rows to merge) among those that give every resident slot a workgroup; the
+        // simulation sees slots as independent, but a compute unit whose second slot idles
+        // streams less than one that runs two workgroups (measured: 448 workgroups of up to
+        // 128 pages at the 16-agent, 32K-prefix workload take 3 % longer than 512 of up to
+        // 112).  Without such a count, the largest within 1% of the best.
         const int32_t cands[] = {32, 40, 48, 56, 64, 80, 96, 112, 128};
         double est[9], best = 1e300;
+        int64_t units[9];
         for (int c = 0; c < 9; ++c) {
             const int32_t u = cands[c];
-            est[c] = sim([&](size_t i) { return is_multi(i) ? multi_pps : std::min(u, sc[i].cap); });
+            auto pages_of = [&](size_t i) { return is_multi(i) ? multi_pps : std::min(u, sc[i].cap); };
+            est[c] = sim(pages_of);
             best = std::min(best, est[c]);
+            units[c] = 0;
+            for (size_t i = 0; i < sc.size(); ++i)
+                units[c] += (int64_t)((sc[i].n + pages_of(i) - 1) / pages_of(i)) * (int64_t)chunk_sizes(segs[i].agents.size()).size();
         }
-        int32_t best_u = 64;
-        for (int c = 8; c >= 0; --c)
-            if (est[c] <= best * 1.01) { best_u = cands[c]; break; }
+        int32_t best_u = -1;
+        for (int c = 8; c >= 0 && best_u < 0; --c)
+            if (est[c] <= best * 1.05 && units[c] * nhb_units >= 2 * cus) best_u = cands[c];
+        for (int c = 8; c >= 0 && best_u < 0; --c)
+            if (est[c] <= best * 1.01) best_u = cands[c];
+        if (best_u < 0) best_u = 64;
         for (size_t i = 0; i < sc.size(); ++i) cand_pps[i] = is_multi(i) ? multi_pps : std::min(best_u, sc[i].cap);
         const int32_t rope_pps = (int32_t)std::max<int64_t>(
             4, std::min<int64_t>(fkv::kMaxPagesPerItem, [&] {
