@@ -282,7 +282,7 @@ def main():
         "metric": "decode attn tokens/s (+ achieved HBM GB/s), Llama-3-8B-shaped layer, 16 agents, 32K shared",
         "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16", "data": "synthetic (seeded, shapes of config %d)" % args.config,
+        "dtype": "bf16", "data": "synthetic (seeded, shapes and value distributions of %s)" % wl.name,
         "config": {"workload": wl.name, "agents": len(agents), "hq": wl.hq, "hkv": wl.hkv, "head_dim": wl.d,
                    "rank": wl.r, "page_size": wl.page_size, "rope": rope,
                    "seq_len_mean": float(np.mean(wl.seq_len[agents])), "pages_per_split": info["pages_per_split"],

@@ -84,7 +84,7 @@ def test_llama8b_shape_shortened(rope):
 
 @pytest.mark.parametrize("rope", [False, True])
 def test_tree_fork_rank32(rope):
-    # config-4 structure at reduced length: root, 4 sub-groups with a mid prefix, 64 agents
+    # long-context fan-out structure at reduced length: root, 4 sub-groups with a mid prefix, 64 agents
     wl = W.tree("tree-short", 22, node_parent=[-1, 0, 0, 0, 0], node_len=[1024, 128, 128, 128, 128],
                 agent_node=[1 + a // 16 for a in range(64)], suffix_lo=5, suffix_hi=90, hq=32, hkv=8, r=32)
     run_case(f"tree-r32 rope={rope}", wl, rope)
@@ -92,7 +92,7 @@ def test_tree_fork_rank32(rope):
 
 @pytest.mark.parametrize("rope", [False, True])
 def test_70b_shape_rank64_zero_residual_agents(rope):
-    # config-5 head layout (64 q / 8 kv heads, r 64), three fork trees, 10% of agents without residual
+    # 70B-shaped head layout (64 q / 8 kv heads, r 64), three fork trees, 10% of agents without residual
     wl = W.tree("70b-short", 23, node_parent=[-1, -1, -1], node_len=[256, 512, 1024],
                 agent_node=[a % 3 for a in range(32)], suffix_lo=1, suffix_hi=200, hq=64, hkv=8, r=64,
                 b_std=0.05, zero_residual=[9, 19, 29])
