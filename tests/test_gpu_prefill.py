@@ -80,6 +80,15 @@ def test_prefill_other_ranks(rank, hq, rope):
     run_prefill(f"prefill-r{rank}-hq{hq} rope={rope}", wl, rope)
 
 
+@pytest.mark.parametrize("rope", [False, True])
+def test_prefill_single_tile_and_one_token_chunks(rope):
+    """Sequences of one 64-key tile or less (no copy runs ahead) and chunks of one token."""
+    wl = W.fanout("pf-tiny", 56, n_agents=3, prefix=8, suffix_lo=0, suffix_hi=20, hq=32, hkv=8, r=16, chunk=30)
+    run_prefill(f"prefill-one-tile rope={rope}", wl, rope)
+    wl1 = W.fanout("pf-one", 57, n_agents=2, prefix=100, suffix_lo=0, suffix_hi=3, hq=32, hkv=8, r=16, chunk=1)
+    run_prefill(f"prefill-one-token rope={rope}", wl1, rope)
+
+
 def test_copy_on_write_at_fork_and_append():
     """Three agents fork the same 500-token context (the last page is partial and shared
     read-only), then each appends its own chunk: the first two appends copy the shared
