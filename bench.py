@@ -17,8 +17,8 @@ data the previous step left in the 256 MB last-level (MALL) cache.
 Roofline: the split kernel dominates.  Its algorithmic bytes per launch are the
 shared base pages counted once per segment, plus each agent's private base pages,
 rCache rows, adapter B matrices, queries, outputs, block tables and (RoPE on) the
-cos/sin rows read, and its duration is taken live from HIP events recorded around
-it on the launch stream.  "traffic" is the HBM bytes the hardware counters saw for
+cos/sin rows read, and its duration is taken live from HIP events that the library
+attaches to the kernel launch (the kernel's own start and end timestamps).  "traffic" is the HBM bytes the hardware counters saw for
 the same kernel (FETCH_SIZE + WRITE_SIZE, calibrated against a plain copy of known
 size), read from the committed counter summary when it was taken on the current
 kernel source, else null.
@@ -220,7 +220,7 @@ def main():
             lw.decode_setup(agents)
         info = lws[0]._decode["info"]
         byts = algorithmic_bytes(wl, lws[0], agents, rope)
-        # live per-kernel timing: events recorded by the library around its two launches
+        # live per-kernel timing: events the library attaches to its two launches
         ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
         for trio in ev:
             for e in trio:
@@ -228,9 +228,9 @@ def main():
         handles = [(ctypes.c_void_p * 3)(*[e.cuda_event for e in trio]) for trio in ev]
         for i in range(warmup):
             lws[i % len(lws)].decode()
-        # timed steps: the library records its HIP events around the split kernel of every
-        # `event_every`-th step (an event record costs GPU time of its own, so recording
-        # them on every step would slow the very steps being timed)
+        # timed steps: the library sets its HIP events on the split and merge launches of
+        # every `event_every`-th step (events cost GPU time of their own, so setting them
+        # on every step would slow the very steps being timed)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         timed = []

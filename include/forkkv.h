@@ -253,9 +253,10 @@ typedef struct {
     int32_t max_q_per_agent;    /* prefill: largest q_indptr[a+1] - q_indptr[a]; 0 = n_q.  Rows beyond
                                    it are not computed, so it must not be understated. */
     float scale;                /* softmax scale; typically 1/sqrt(d) */
-    void *const *timing_events; /* optional, host array of hipEvent_t: decode records [0] before its first
-                                   kernel, [1] after the split kernel and [2] after the merge kernel; prefill
-                                   records [0] and [1] around its kernel.  NULL = no events. */
+    void *const *timing_events; /* optional, host array of hipEvent_t (created with timing enabled), set by
+                                   the launches to the kernels' own execution timestamps: decode [0] start
+                                   and [1] end of the split kernel, [2] end of the merge kernel; prefill [0]
+                                   start and [1] end of its kernel.  NULL = no events. */
 } fkv_attn_args;
 
 /* Decode: one query row per agent attends to all seq_len keys of its agent

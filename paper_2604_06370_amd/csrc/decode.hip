@@ -26,6 +26,7 @@
 //   acc_r^T += C_V,s^T . P_s^T                         rank-space accumulator
 // The reconstructed K never leaves registers; the value residual stays in rank
 // space until the combine kernel applies B_V once (Eq. 4).
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -1074,14 +1075,15 @@ hipError_t launch_decode(const DecodeArgs &da_in, int n_blocks, int n_agents, in
     hipError_t e;
     DecodeArgs da = da_in;
     da.n_rows = n_agents * da.hq;
-    if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[0]), st)) != hipSuccess) return e;
-    if constexpr (ROPE) hipLaunchKernelGGL((decode_rope_kernel<R, G>), dim3(n_blocks), dim3(256), 0, st, da);
-    else hipLaunchKernelGGL((decode_split_kernel<R, G>), dim3(n_blocks), dim3(256), 0, st, da);
+    // timing events carry the kernels' own start and end timestamps (set by the launch)
+    hipEvent_t e0 = ev ? static_cast<hipEvent_t>(ev[0]) : nullptr;
+    hipEvent_t e1 = ev ? static_cast<hipEvent_t>(ev[1]) : nullptr;
+    hipEvent_t e2 = ev ? static_cast<hipEvent_t>(ev[2]) : nullptr;
+    if constexpr (ROPE) hipExtLaunchKernelGGL((decode_rope_kernel<R, G>), dim3(n_blocks), dim3(256), 0, st, e0, e1, 0, da);
+    else hipExtLaunchKernelGGL((decode_split_kernel<R, G>), dim3(n_blocks), dim3(256), 0, st, e0, e1, 0, da);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[1]), st)) != hipSuccess) return e;
-    hipLaunchKernelGGL((decode_combine_kernel<R, G>), dim3(da.n_rows), dim3(64 * CW), 0, st, da);
+    hipExtLaunchKernelGGL((decode_combine_kernel<R, G>), dim3(da.n_rows), dim3(64 * CW), 0, st, nullptr, e2, 0, da);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[2]), st)) != hipSuccess) return e;
     return hipSuccess;
 }
 

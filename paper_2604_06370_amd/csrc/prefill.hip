@@ -19,6 +19,7 @@
 // k-step kk, slot j of lane group grp is head-dim index 32kk + 16(j/4) + 4grp +
 // j%4 for the key products, and key 16(j/4) + 4grp + j%4 of a 32-key half for the
 // value products.  Queries and values are loaded in the same order.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -921,14 +922,17 @@ template <int R, int G, bool ROPE>
 hipError_t launch_prefill(const PrefillArgs &pa, hipStream_t st, void *const *ev) {
     using S = PrefillShape<R, G, ROPE>;
     hipError_t e;
-    if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[0]), st)) != hipSuccess) return e;
     const int pairs = (pa.n_agents * pa.hkv + kXcds - 1) / kXcds * kXcds;
     const int grid = pairs * pa.blocks_per_agent_head;
     (void)sizeof(S);
-    if constexpr (ROPE && !stream_rope(R)) hipLaunchKernelGGL((prefill_kernel<R, G, ROPE>), dim3(grid), dim3(256), 0, st, pa);
-    else hipLaunchKernelGGL((prefill_stream_kernel<R, G, ROPE>), dim3(grid), dim3(64 * kStreamWaves), 0, st, pa);
+    // timing events carry the kernel's own start and end timestamps (set by the launch)
+    hipEvent_t e0 = ev ? static_cast<hipEvent_t>(ev[0]) : nullptr;
+    hipEvent_t e1 = ev ? static_cast<hipEvent_t>(ev[1]) : nullptr;
+    if constexpr (ROPE && !stream_rope(R))
+        hipExtLaunchKernelGGL((prefill_kernel<R, G, ROPE>), dim3(grid), dim3(256), 0, st, e0, e1, 0, pa);
+    else
+        hipExtLaunchKernelGGL((prefill_stream_kernel<R, G, ROPE>), dim3(grid), dim3(64 * kStreamWaves), 0, st, e0, e1, 0, pa);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if (ev && (e = hipEventRecord(static_cast<hipEvent_t>(ev[1]), st)) != hipSuccess) return e;
     return hipSuccess;
 }
 
