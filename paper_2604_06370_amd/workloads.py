@@ -231,6 +231,20 @@ def tree(name: str, seed: int, *, node_parent: Sequence[int], node_len: Sequence
                   ch, set(zero_residual), b_std, q_std=q_std)
 
 
+def chain(name: str, seed: int, *, n_agents: int, root: int, step: int, suffix_lo: int, suffix_hi: int,
+          hq: int, hkv: int, d: int = 128, r: int, ps: int = 16, b_std: float = 0.02,
+          chunk: Sequence[int] = ()) -> Workload:
+    """ReAct-shaped sequential fork chain (Section 7's sequential agent workflows): agent 0
+    works on a shared root context; agent k forks the context of agent k - 1 extended by
+    `step` tokens (that agent's output and the tool result), so agent k shares root + k steps
+    with every later agent; each agent then has a private suffix."""
+    rng = np.random.default_rng(seed)
+    suffix = [int(x) for x in rng.integers(suffix_lo, suffix_hi + 1, size=n_agents)]
+    ch = list(chunk) if len(chunk) else [0] * n_agents
+    return _build(name, rng, hq, hkv, d, r, ps, [-1] + list(range(n_agents - 1)), [root] + [step] * (n_agents - 1),
+                  list(range(n_agents)), suffix, ch, set(), b_std)
+
+
 def config(cfg: int, seed: Optional[int] = None) -> Workload:
     """The five standard workloads (single attention layer, bf16)."""
     s = cfg if seed is None else seed
@@ -243,7 +257,7 @@ def config(cfg: int, seed: Optional[int] = None) -> Workload:
         return fanout("llama3-8b-16agents-32k-shared", s, n_agents=16, prefix=32768, suffix_lo=256,
                       suffix_hi=4096, hq=32, hkv=8, r=16)
     if cfg == 3:
-        # chunked prefill: as cfg 2, then each agent appends a 2048-token chunk whose rCache
+        # chunked prefill: the 16-agent workload above, then each agent appends a 2048-token chunk whose rCache
         # is x A with x ~ N(0,1) [2048 x 4096] and A ~ N(0, 1/4096).
         return fanout("llama3-8b-16agents-2048-chunk-prefill", s, n_agents=16, prefix=32768, suffix_lo=256,
                       suffix_hi=4096, hq=32, hkv=8, r=16, chunk=2048, chunk_c_from_hidden=True)

@@ -99,6 +99,25 @@ def test_release_returns_references_and_eviction_is_per_tree():
     assert s["base_evictions"] == 3 and s["res_evictions"] == 0 and s["res_pages_cached"] == 4
 
 
+def test_partial_hit_after_base_eviction_keeps_residual():
+    """Decoupled eviction (Section 5.2): once the base tree has evicted part of a released
+    context while the residual tree kept it, forking the same agent and tokens again
+    reports a residual hit over the whole context and a shorter base hit, so the caller
+    recomputes only the base K/V of [base_valid, seq_len)."""
+    t = rt.Tree(4, 6, 40)
+    t.fork(0, 1, np.arange(16))
+    t.release(0)
+    t.fork(1, 2, np.arange(100, 120))    # evicts 3 of the 4 cached base pages
+    t.release(1)
+    f = t.fork(2, 1, np.arange(16))
+    assert f.res_valid == 16
+    assert f.base_valid < 16 and f.base_valid % 4 == 0
+    s = t.pool_stats()
+    assert s["res_evictions"] == 0 and s["base_evictions"] >= 3
+    bb, rb, sl = t.block_tables([2], 4)
+    assert sl[0] == 16 and len(set(bb[0])) == 4 and len(set(rb[0])) == 4
+
+
 def test_failed_fork_leaves_tree_unchanged():
     t = rt.Tree(4, 5, 40)
     t.fork(0, 1, np.arange(16))

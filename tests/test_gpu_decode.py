@@ -210,3 +210,11 @@ def test_config4_full_size_sampled(config4, rope):
     ref = oracle_decode(wl, sample, rope)
     check_close(f"cfg4-full rope={rope}", out[[agents.index(a) for a in sample]], ref)
     lw.close()
+
+
+@pytest.mark.parametrize("rope", [False, True])
+def test_sequential_fork_chain(rope):
+    # ReAct-shaped chain: agent k forks agent k-1's context plus 100 tokens, so the shared
+    # segments hold 12, 11, ..., 1 agents (multi-group and single-group items, many splits)
+    wl = W.chain("chain-12", 24, n_agents=12, root=700, step=100, suffix_lo=3, suffix_hi=70, hq=32, hkv=8, r=16)
+    run_case(f"chain rope={rope}", wl, rope)
