@@ -309,6 +309,24 @@ fkv_status fkv_scatter_tokens(const int32_t *bt_base, const int32_t *bt_res, int
                               void *base_kv, void *res_kv, int32_t hkv, int32_t d, int32_t r,
                               int32_t page_size, void *stream);
 
+/* Producer: write n new tokens (positions pos0 .. pos0+n-1 of one sequence) into both pools,
+ * the cache-write step that precedes ResidualAttention (Section 5.2 stores the base and
+ * residual caches apart; Section 5.3 keeps the residual as the rank-r shrink of the hidden
+ * state, K = K_base + RoPE(C_K B_K) being rebuilt later):
+ *   base:  K = RoPE_pos(k_raw) (rotate-half pairs (i, i + d/2) with the fp32 tables of
+ *          fkv_rope_table; rope_cos = NULL stores k_raw as is) and V, k_raw/v [n][hkv][d] bf16;
+ *   res:   C_K = x . A_K^T and C_V = x . A_V^T, x [n][hidden] bf16, lora_a [2][r][hidden] bf16
+ *          (A_K then A_V of the sequence's adapter, rows of the shrink), fp32 accumulation,
+ *          rounded to bf16; lora_a = NULL (or r = 0) leaves the residual pool untouched.
+ * bt_base / bt_res: device block-table rows of the sequence (pages already allocated, e.g. by
+ * fkv_cow_append).  Requires d = 128, page_size = 16, r in {0, 8, 16, 32, 64}, hidden a
+ * multiple of 256, pos0 + n <= rope_max_pos with RoPE.  Device pointers; enqueued on
+ * `stream`; FKV_ERR_INVALID before any launch on bad arguments. */
+fkv_status fkv_produce_tokens(const int32_t *bt_base, const int32_t *bt_res, int64_t pos0, int64_t n, const void *x,
+                              int32_t hidden, const void *k_raw, const void *v, const void *lora_a,
+                              const float *rope_cos, const float *rope_sin, int64_t rope_max_pos, void *base_kv,
+                              void *res_kv, int32_t hkv, int32_t d, int32_t r, int32_t page_size, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

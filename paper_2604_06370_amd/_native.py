@@ -116,6 +116,9 @@ fkv_page_copy_launch = _sig("fkv_page_copy_launch", c_i32, [c_vp, c_i32, c_vp, c
 fkv_scatter_tokens = _sig("fkv_scatter_tokens", c_i32,
                           [c_vp, c_vp, c_i64, c_i64, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_i32, c_i32, c_i32, c_i32,
                            c_vp])
+fkv_produce_tokens = _sig("fkv_produce_tokens", c_i32,
+                          [c_vp, c_vp, c_i64, c_i64, c_vp, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, c_i64, c_vp, c_vp,
+                           c_i32, c_i32, c_i32, c_i32, c_vp])
 
 
 def check(status: int, what: str = "") -> None:

@@ -17,6 +17,7 @@
 #include <string>
 
 #include "internal.hpp"
+#include "mfma.hpp"
 
 namespace {
 
@@ -125,6 +126,108 @@ __global__ __launch_bounds__(256) void scatter_kernel(ScatterArgs a) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// Producer: the cache writes of new tokens (Section 5.2 / 5.3, the step before attention).
+// Per token at position pos: K = RoPE_pos(k_raw) (rotate-half pairs (i, i + d/2), angles from
+// the fp32 table) and V into the base pool; C_K = x A_K^T and C_V = x A_V^T (the LoRA shrink,
+// hidden -> r, fp32 accumulation on the matrix cores) into the residual pool.  Page size 16,
+// head dim 128 (the fragment layouts).  One workgroup per 64 tokens; wave w computes the
+// shrink for tokens 16w .. 16w + 15 with 16x16x32 products (A operand: 16 bytes of one
+// token's x row per lane; B operand: A^T rows staged in LDS in chunks of 256 hidden units,
+// shared by the four waves).
+struct ProduceArgs {
+    const int32_t *bt_base, *bt_res;
+    int64_t pos0;
+    int32_t n, hidden, hkv;
+    const uint16_t *x, *k_raw, *v, *lora_a;
+    const float *rope_cos, *rope_sin;
+    uint16_t *base_kv, *res_kv;
+};
+constexpr int kProdTok = 64;
+constexpr int kProdChunk = 256;
+
+template <int R>
+__global__ __launch_bounds__(256) void produce_kernel(ProduceArgs a) {
+    constexpr int PS = 16, D = 128, HALF = D / 2;
+    const int j0 = blockIdx.x * kProdTok;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int col = lane & 15, grp = lane >> 4;
+    if constexpr (R > 0) {
+        if (a.lora_a) {
+            constexpr int RT = (R + 15) / 16, NT = 2 * RT, KW = kProdChunk / 8;  // KW: 16-byte words per staged row
+            __shared__ fkvk::u32x4 sA[NT * 16 * KW];
+            fkvk::f32x4 acc[NT];
+#pragma unroll
+            for (int t = 0; t < NT; ++t) acc[t] = fkvk::f32x4{0, 0, 0, 0};
+            const int tok = j0 + 16 * wave + col;
+            const bool tok_ok = tok < a.n;
+            const uint16_t *xr = a.x + (int64_t)(tok_ok ? tok : 0) * a.hidden;
+            for (int kc = 0; kc < a.hidden; kc += kProdChunk) {
+                __syncthreads();  // the previous chunk is consumed
+                for (int e = threadIdx.x; e < NT * 16 * KW; e += 256) {
+                    const int row = e / KW, c8 = e - row * KW;
+                    const int kv = row / (RT * 16), rho = row - kv * (RT * 16);
+                    fkvk::u32x4 w = {0, 0, 0, 0};
+                    if (rho < R) w = fkvk::ldg128(a.lora_a + ((int64_t)(kv * R + rho) * a.hidden + kc + 8 * c8));
+                    sA[e] = w;
+                }
+                __syncthreads();
+#pragma unroll 4
+                for (int ks = 0; ks < kProdChunk / 32; ++ks) {
+                    const fkvk::u32x4 xa = tok_ok ? fkvk::ldg128(xr + kc + 32 * ks + 8 * grp) : fkvk::u32x4{0, 0, 0, 0};
+#pragma unroll
+                    for (int t = 0; t < NT; ++t) acc[t] = fkvk::mfma32(xa, sA[(t * 16 + col) * KW + 4 * ks + grp], acc[t]);
+                }
+            }
+            // acc[t] holds C[token 4grp + i][rank 16 (t % RT) + col] of shrink t / RT (K, then V)
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const int kv = t / RT, rho = 16 * (t % RT) + col;
+                if (rho >= R) continue;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int tj = j0 + 16 * wave + 4 * grp + i;
+                    if (tj >= a.n) continue;
+                    const int64_t pos = a.pos0 + tj;
+                    const int slot = (int)(pos % PS);
+                    uint16_t *pg = a.res_kv + (int64_t)a.bt_res[pos / PS] * res_page_elems(PS, R);
+                    const uint32_t h2 = fkvk::pack_bf16(acc[t][i], 0.f);
+                    pg[kv == 0 ? ck_off(slot, rho, PS, R) : cv_off(slot, rho, PS, R)] = (uint16_t)(h2 & 0xffffu);
+                }
+            }
+        }
+    }
+    // base K (rotated) and V: one (token, head, rotate-half pair) per item
+    const int items = kProdTok * a.hkv * HALF;
+    for (int e = threadIdx.x; e < items; e += 256) {
+        const int tl = e / (a.hkv * HALF);
+        const int rem = e - tl * (a.hkv * HALF);
+        const int hh = rem / HALF, f = rem - hh * HALF;
+        const int tj = j0 + tl;
+        if (tj >= a.n) continue;
+        const int64_t pos = a.pos0 + tj;
+        const int slot = (int)(pos % PS);
+        const int64_t src = ((int64_t)tj * a.hkv + hh) * D;
+        float x0 = fkvk::bf16_to_f32(a.k_raw[src + f]), x1 = fkvk::bf16_to_f32(a.k_raw[src + f + HALF]);
+        if (a.rope_cos) {
+            // table order [pos / 16][f / 16][pos % 16 + 16 ((f % 16) / 4)][f % 4]
+            const int64_t o = (pos / PS) * (PS * HALF) + (f / 16) * 256 + (slot + 16 * ((f % 16) / 4)) * 4 + f % 4;
+            const float c = a.rope_cos[o], s = a.rope_sin[o];
+            const float y0 = x0 * c - x1 * s, y1 = x1 * c + x0 * s;
+            x0 = y0;
+            x1 = y1;
+        }
+        constexpr int64_t blk = PS * D;
+        uint16_t *pg = a.base_kv + (int64_t)a.bt_base[pos / PS] * 2 * a.hkv * blk;
+        const uint32_t kk = fkvk::pack_bf16(x0, x1);
+        pg[hh * blk + k_off(slot, f, PS, D)] = (uint16_t)(kk & 0xffffu);
+        pg[hh * blk + k_off(slot, f + HALF, PS, D)] = (uint16_t)(kk >> 16);
+        pg[(a.hkv + hh) * blk + v_off(slot, f, PS, D)] = a.v[src + f];
+        pg[(a.hkv + hh) * blk + v_off(slot, f + HALF, PS, D)] = a.v[src + f + HALF];
+    }
+}
+
 }  // namespace
 
 extern "C" {
@@ -169,6 +272,41 @@ fkv_status fkv_scatter_tokens(const int32_t *bt_base, const int32_t *bt_res, int
     hipLaunchKernelGGL(scatter_kernel, dim3((unsigned)n), dim3(256), 0, static_cast<hipStream_t>(stream), a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fkv::fail(FKV_ERR_HIP, std::string("fkv_scatter_tokens: ") + hipGetErrorString(e));
+    return FKV_OK;
+}
+
+fkv_status fkv_produce_tokens(const int32_t *bt_base, const int32_t *bt_res, int64_t pos0, int64_t n, const void *x,
+                              int32_t hidden, const void *k_raw, const void *v, const void *lora_a,
+                              const float *rope_cos, const float *rope_sin, int64_t rope_max_pos, void *base_kv,
+                              void *res_kv, int32_t hkv, int32_t d, int32_t r, int32_t page_size, void *stream) {
+    fkv::clear_error();
+    if (pos0 < 0 || n < 0 || hkv < 1 || d != 128 || page_size != 16 || !(r == 0 || r == 8 || r == 16 || r == 32 || r == 64))
+        return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: needs d = 128, page_size = 16, r in {0, 8, 16, 32, 64}");
+    if (!bt_base || !base_kv || !k_raw || !v) return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: base table, pool, K or V missing");
+    if ((rope_cos == nullptr) != (rope_sin == nullptr))
+        return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: RoPE tables come in pairs");
+    if (rope_cos && pos0 + n > rope_max_pos) return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: RoPE table too short");
+    if (lora_a && r > 0) {
+        if (!x || hidden < kProdChunk || hidden % kProdChunk) return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: x and hidden (a multiple of 256) required with lora_a");
+        if (!bt_res || !res_kv) return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: residual table/pool missing");
+    }
+    if (n == 0) return FKV_OK;
+    if (n > INT32_MAX - kProdTok) return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: too many tokens in one call");
+    ProduceArgs a{bt_base, bt_res, pos0, (int32_t)n, hidden, hkv,
+                  static_cast<const uint16_t *>(x), static_cast<const uint16_t *>(k_raw), static_cast<const uint16_t *>(v),
+                  r > 0 ? static_cast<const uint16_t *>(lora_a) : nullptr, rope_cos, rope_sin,
+                  static_cast<uint16_t *>(base_kv), static_cast<uint16_t *>(res_kv)};
+    const dim3 grid((unsigned)((n + kProdTok - 1) / kProdTok));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    switch (r) {
+    case 0: hipLaunchKernelGGL(produce_kernel<0>, grid, dim3(256), 0, st, a); break;
+    case 8: hipLaunchKernelGGL(produce_kernel<8>, grid, dim3(256), 0, st, a); break;
+    case 16: hipLaunchKernelGGL(produce_kernel<16>, grid, dim3(256), 0, st, a); break;
+    case 32: hipLaunchKernelGGL(produce_kernel<32>, grid, dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL(produce_kernel<64>, grid, dim3(256), 0, st, a); break;
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fkv::fail(FKV_ERR_HIP, std::string("fkv_produce_tokens: ") + hipGetErrorString(e));
     return FKV_OK;
 }
 

@@ -231,6 +231,25 @@ def scatter_tokens(bt_base_row: Optional[torch.Tensor], bt_res_row: Optional[tor
           "fkv_scatter_tokens")
 
 
+def produce_tokens(bt_base_row: torch.Tensor, bt_res_row: Optional[torch.Tensor], pos0: int, x: Optional[torch.Tensor],
+                   k_raw: torch.Tensor, v: torch.Tensor, lora_a: Optional[torch.Tensor],
+                   rope: Optional[tuple], base_kv: torch.Tensor, res_kv: Optional[torch.Tensor],
+                   hkv: int, d: int, r: int, page_size: int, stream=None) -> None:
+    """fkv_produce_tokens: k_raw/v [n][hkv][d], x [n][hidden], lora_a [2][r][hidden] (bf16 device
+    tensors); rope = (cos, sin) fp32 tables from rope_tables, or None."""
+    n = k_raw.shape[0]
+    p = lambda t: t.data_ptr() if t is not None else None
+    for t in (x, k_raw, v, lora_a):
+        assert t is None or (t.is_contiguous() and t.dtype == torch.bfloat16)
+    hidden = x.shape[1] if x is not None else 0
+    cos, sin = (rope[0], rope[1]) if rope is not None else (None, None)
+    max_pos = cos.numel() // (d // 2) if cos is not None else 0
+    check(N.fkv_produce_tokens(p(bt_base_row), p(bt_res_row), pos0, n, p(x), hidden, p(k_raw), p(v), p(lora_a),
+                               p(cos), p(sin), max_pos, base_kv.data_ptr(), p(res_kv), hkv, d, r, page_size,
+                               _stream(stream)),
+          "fkv_produce_tokens")
+
+
 def make_args(*, q, base_kv, res_kv, lora_b, adapter_idx, base_bt, res_bt, seq_lens, out, hq, hkv, d, r,
               page_size, rope=None, plan_dev=None, q_indptr=None, workspace=None, n_q=0, max_q_per_agent=0,
               scale: Optional[float] = None) -> N.fkv_attn_args:
