@@ -130,6 +130,47 @@ def cpu_baseline(wl, agents, rope: bool, budget_s: float = 12.0) -> dict:
                       f"fp64 C oracle, {t_used:.1f} s of oracle time)"}
 
 
+def measure_producer(lw, wl, agents, dev, stream, steps: int = 5, hidden: int = 4096) -> dict:
+    """The cache-write producer on the prefill chunks: per agent one fkv_produce_tokens call
+    writing its chunk's RoPE'd K, V and C = x A^T (hidden 4096 -> rank r) into its pages.
+    Bound by HBM: bytes = x, K/V in, K/V pages out, C out, A, the RoPE rows."""
+    import torch
+    from paper_2604_06370_amd import runtime as rt
+    n = wl.n_queries(agents[0])
+    assert all(wl.n_queries(a) == n for a in agents)
+    na, hkv, d, r, ps = len(agents), wl.hkv, wl.d, wl.r, wl.page_size
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    x = torch.randn((na, n, hidden), device=dev, generator=g).to(torch.bfloat16)
+    k = torch.randn((na, n, hkv, d), device=dev, generator=g).to(torch.bfloat16)
+    v = torch.randn((na, n, hkv, d), device=dev, generator=g).to(torch.bfloat16)
+    a = (torch.randn((na, 2, r, hidden), device=dev, generator=g) * hidden ** -0.5).to(torch.bfloat16)
+    bb, rb, sl = lw.tree.block_tables(agents, lw.max_pages)
+    btb, btr = torch.from_numpy(bb).to(dev), torch.from_numpy(rb).to(dev)
+
+    def step():
+        for i in range(na):
+            rt.produce_tokens(btb[i], btr[i], int(sl[i]) - n, x[i], k[i], v[i], a[i], lw.rope_tab, lw.base_kv,
+                              lw.res_kv, hkv, d, r, ps, stream)
+
+    step()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for e0, e1 in ev:
+        e0.record(stream)
+        step()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev]))
+    per_tok = hidden * 2 + 4 * hkv * d * 2 + 2 * r * 2 + (d // 2 * 4 * 2 if lw.rope_tab is not None else 0)
+    byts = na * (n * per_tok + 2 * r * hidden * 2)
+    gbs = byts / (ms * 1e-3) / 1e9
+    del x, k, v, a
+    return {"workload": wl.name, "kernel": "produce_kernel", "tokens": na * n, "hidden": hidden, "rank": r,
+            "rope": lw.rope_tab is not None, "calls_per_step": na, "ms": ms, "algorithmic_bytes": byts,
+            "bound": "hbm", "achieved_GBps": gbs, "frac": gbs / HBM_PEAK_GBS}
+
+
 def measure_prefill(args, dev, stream) -> dict:
     """Chunked prefill on one workload (default: 16 agents append 2048-token chunks after a
     32768-token shared prefix), RoPE off and on; bound by the matrix cores."""
@@ -169,6 +210,8 @@ def measure_prefill(args, dev, stream) -> dict:
         res["rope_on" if rope else "rope_off"] = {
             "kernel": "prefill_kernel" if rope and wl.r > 32 else "prefill_stream_kernel", "kernel_ms": k_ms, "kernel_ms_p10_p50_p90": [float(np.percentile(ms, q)) for q in (10, 50, 90)],
             "tokens_per_s": fl["rows"] * n / (t1 - t0), "achieved": tflops, "frac": tflops / MFMA_BF16_PEAK_TFLOPS}
+        if rope:
+            res["producer"] = measure_producer(lw, wl, agents, dev, stream)
         lw.close()
         del lw
         torch.cuda.empty_cache()
@@ -309,6 +352,7 @@ def main():
             "traffic": counter_traffic(True, wl.name, q["info"]["pages_per_split"])}
     if not args.no_prefill:
         out["prefill"] = measure_prefill(args, dev, stream)
+        out["producer"] = out["prefill"].pop("producer")
     if not args.no_cpu_baseline:
         print("# timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wl, agents, rope)

@@ -320,7 +320,7 @@ fkv_status fkv_scatter_tokens(const int32_t *bt_base, const int32_t *bt_res, int
  *          rounded to bf16; lora_a = NULL (or r = 0) leaves the residual pool untouched.
  * bt_base / bt_res: device block-table rows of the sequence (pages already allocated, e.g. by
  * fkv_cow_append).  Requires d = 128, page_size = 16, r in {0, 8, 16, 32, 64}, hidden a
- * multiple of 256, pos0 + n <= rope_max_pos with RoPE.  Device pointers; enqueued on
+ * multiple of 1024, pos0 + n <= rope_max_pos with RoPE.  Device pointers; enqueued on
  * `stream`; FKV_ERR_INVALID before any launch on bad arguments. */
 fkv_status fkv_produce_tokens(const int32_t *bt_base, const int32_t *bt_res, int64_t pos0, int64_t n, const void *x,
                               int32_t hidden, const void *k_raw, const void *v, const void *lora_a,

@@ -131,79 +131,100 @@ __global__ __launch_bounds__(256) void scatter_kernel(ScatterArgs a) {
 // Per token at position pos: K = RoPE_pos(k_raw) (rotate-half pairs (i, i + d/2), angles from
 // the fp32 table) and V into the base pool; C_K = x A_K^T and C_V = x A_V^T (the LoRA shrink,
 // hidden -> r, fp32 accumulation on the matrix cores) into the residual pool.  Page size 16,
-// head dim 128 (the fragment layouts).  One workgroup per 64 tokens; wave w computes the
-// shrink for tokens 16w .. 16w + 15 with 16x16x32 products (A operand: 16 bytes of one
-// token's x row per lane; B operand: A^T rows staged in LDS in chunks of 256 hidden units,
-// shared by the four waves).
+// head dim 128 (the fragment layouts).  One launch, two kinds of workgroups:
+//  - shrink: 16 tokens; wave w covers a quarter of the hidden dimension with 16x16x32
+//    products (A operand: 16 bytes of one token's x row per lane; B operand: 16 bytes of one
+//    row of A, read straight from memory, L2-resident), eight k-steps of loads in flight;
+//    the four partial tiles are summed through LDS;
+//  - base: 64 tokens of one KV head, one (token, rotate-half pair) per item.
 struct ProduceArgs {
     const int32_t *bt_base, *bt_res;
     int64_t pos0;
-    int32_t n, hidden, hkv;
+    int32_t n, hidden, hkv, n_shrink_blocks;
     const uint16_t *x, *k_raw, *v, *lora_a;
     const float *rope_cos, *rope_sin;
     uint16_t *base_kv, *res_kv;
 };
-constexpr int kProdTok = 64;
-constexpr int kProdChunk = 256;
+constexpr int kShrinkTok = 16;
+constexpr int kBaseTok = 64;
+constexpr int kProdChunk = 1024;  // hidden is a multiple of this (four waves x 8 k-steps x 32)
 
 template <int R>
 __global__ __launch_bounds__(256) void produce_kernel(ProduceArgs a) {
     constexpr int PS = 16, D = 128, HALF = D / 2;
-    const int j0 = blockIdx.x * kProdTok;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int col = lane & 15, grp = lane >> 4;
-    if constexpr (R > 0) {
-        if (a.lora_a) {
-            constexpr int RT = (R + 15) / 16, NT = 2 * RT, KW = kProdChunk / 8;  // KW: 16-byte words per staged row
-            __shared__ fkvk::u32x4 sA[NT * 16 * KW];
+    if ((int)blockIdx.x < a.n_shrink_blocks) {
+        if constexpr (R > 0) {
+            constexpr int RT = (R + 15) / 16, NT = 2 * RT;
+            __shared__ fkvk::f32x4 s_part[3][NT][64];
+            const int j0 = blockIdx.x * kShrinkTok;
             fkvk::f32x4 acc[NT];
 #pragma unroll
             for (int t = 0; t < NT; ++t) acc[t] = fkvk::f32x4{0, 0, 0, 0};
-            const int tok = j0 + 16 * wave + col;
+            const int tok = j0 + col;
             const bool tok_ok = tok < a.n;
-            const uint16_t *xr = a.x + (int64_t)(tok_ok ? tok : 0) * a.hidden;
-            for (int kc = 0; kc < a.hidden; kc += kProdChunk) {
-                __syncthreads();  // the previous chunk is consumed
-                for (int e = threadIdx.x; e < NT * 16 * KW; e += 256) {
-                    const int row = e / KW, c8 = e - row * KW;
-                    const int kv = row / (RT * 16), rho = row - kv * (RT * 16);
-                    fkvk::u32x4 w = {0, 0, 0, 0};
-                    if (rho < R) w = fkvk::ldg128(a.lora_a + ((int64_t)(kv * R + rho) * a.hidden + kc + 8 * c8));
-                    sA[e] = w;
-                }
-                __syncthreads();
-#pragma unroll 4
-                for (int ks = 0; ks < kProdChunk / 32; ++ks) {
-                    const fkvk::u32x4 xa = tok_ok ? fkvk::ldg128(xr + kc + 32 * ks + 8 * grp) : fkvk::u32x4{0, 0, 0, 0};
-#pragma unroll
-                    for (int t = 0; t < NT; ++t) acc[t] = fkvk::mfma32(xa, sA[(t * 16 + col) * KW + 4 * ks + grp], acc[t]);
-                }
-            }
-            // acc[t] holds C[token 4grp + i][rank 16 (t % RT) + col] of shrink t / RT (K, then V)
+            const int quarter = a.hidden / 4;
+            const uint16_t *xr = a.x + (int64_t)(tok_ok ? tok : 0) * a.hidden + wave * quarter + 8 * grp;
+            // B operand rows: shrink t / RT (K, then V), rank 16 (t % RT) + col (rows past r read row 0, zeroed)
+            const uint16_t *ar[NT];
+            bool rok[NT];
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
-                const int kv = t / RT, rho = 16 * (t % RT) + col;
-                if (rho >= R) continue;
+                const int rho = 16 * (t % RT) + col;
+                rok[t] = rho < R;
+                ar[t] = a.lora_a + ((int64_t)((t / RT) * R + (rok[t] ? rho : 0)) * a.hidden + wave * quarter + 8 * grp);
+            }
+            for (int k0 = 0; k0 < quarter; k0 += 8 * 32) {
+                fkvk::u32x4 xa[8], bw[8][NT];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int tj = j0 + 16 * wave + 4 * grp + i;
-                    if (tj >= a.n) continue;
-                    const int64_t pos = a.pos0 + tj;
-                    const int slot = (int)(pos % PS);
-                    uint16_t *pg = a.res_kv + (int64_t)a.bt_res[pos / PS] * res_page_elems(PS, R);
-                    const uint32_t h2 = fkvk::pack_bf16(acc[t][i], 0.f);
-                    pg[kv == 0 ? ck_off(slot, rho, PS, R) : cv_off(slot, rho, PS, R)] = (uint16_t)(h2 & 0xffffu);
+                for (int ks = 0; ks < 8; ++ks) {
+                    xa[ks] = tok_ok ? fkvk::ldg128(xr + k0 + 32 * ks) : fkvk::u32x4{0, 0, 0, 0};
+#pragma unroll
+                    for (int t = 0; t < NT; ++t) bw[ks][t] = fkvk::ldg128(ar[t] + k0 + 32 * ks);
+                }
+#pragma unroll
+                for (int ks = 0; ks < 8; ++ks)
+#pragma unroll
+                    for (int t = 0; t < NT; ++t)
+                        acc[t] = fkvk::mfma32(xa[ks], rok[t] ? bw[ks][t] : fkvk::u32x4{0, 0, 0, 0}, acc[t]);
+            }
+            if (wave > 0) {
+#pragma unroll
+                for (int t = 0; t < NT; ++t) s_part[wave - 1][t][lane] = acc[t];
+            }
+            __syncthreads();
+            if (wave == 0) {
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
+                    fkvk::f32x4 c = acc[t];
+#pragma unroll
+                    for (int w = 0; w < 3; ++w) c += s_part[w][t][lane];
+                    // c holds C[token 4grp + i][rank 16 (t % RT) + col] of shrink t / RT
+                    const int kv = t / RT, rho = 16 * (t % RT) + col;
+                    if (rho >= R) continue;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int tj = j0 + 4 * grp + i;
+                        if (tj >= a.n) continue;
+                        const int64_t pos = a.pos0 + tj;
+                        const int slot = (int)(pos % PS);
+                        uint16_t *pg = a.res_kv + (int64_t)a.bt_res[pos / PS] * res_page_elems(PS, R);
+                        const uint32_t h2 = fkvk::pack_bf16(c[i], 0.f);
+                        pg[kv == 0 ? ck_off(slot, rho, PS, R) : cv_off(slot, rho, PS, R)] = (uint16_t)(h2 & 0xffffu);
+                    }
                 }
             }
         }
+        return;
     }
-    // base K (rotated) and V: one (token, head, rotate-half pair) per item
-    const int items = kProdTok * a.hkv * HALF;
-    for (int e = threadIdx.x; e < items; e += 256) {
-        const int tl = e / (a.hkv * HALF);
-        const int rem = e - tl * (a.hkv * HALF);
-        const int hh = rem / HALF, f = rem - hh * HALF;
+    // base K (rotated) and V of KV head hh for 64 tokens: one (token, rotate-half pair) per item
+    const int b = blockIdx.x - a.n_shrink_blocks;
+    const int hh = b % a.hkv;
+    const int j0 = (b / a.hkv) * kBaseTok;
+    for (int e = threadIdx.x; e < kBaseTok * HALF; e += 256) {
+        const int tl = e / HALF, f = e - tl * HALF;
         const int tj = j0 + tl;
         if (tj >= a.n) continue;
         const int64_t pos = a.pos0 + tj;
@@ -287,16 +308,19 @@ fkv_status fkv_produce_tokens(const int32_t *bt_base, const int32_t *bt_res, int
         return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: RoPE tables come in pairs");
     if (rope_cos && pos0 + n > rope_max_pos) return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: RoPE table too short");
     if (lora_a && r > 0) {
-        if (!x || hidden < kProdChunk || hidden % kProdChunk) return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: x and hidden (a multiple of 256) required with lora_a");
+        if (!x || hidden < kProdChunk || hidden % kProdChunk) return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: x and hidden (a multiple of 1024) required with lora_a");
         if (!bt_res || !res_kv) return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: residual table/pool missing");
     }
     if (n == 0) return FKV_OK;
-    if (n > INT32_MAX - kProdTok) return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: too many tokens in one call");
-    ProduceArgs a{bt_base, bt_res, pos0, (int32_t)n, hidden, hkv,
+    if (n > (int64_t)1 << 24) return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: too many tokens in one call");
+    const bool shrink = lora_a && r > 0;
+    const int32_t n_shrink = shrink ? (int32_t)((n + kShrinkTok - 1) / kShrinkTok) : 0;
+    const int64_t n_base = (n + kBaseTok - 1) / kBaseTok * hkv;
+    ProduceArgs a{bt_base, bt_res, pos0, (int32_t)n, hidden, hkv, n_shrink,
                   static_cast<const uint16_t *>(x), static_cast<const uint16_t *>(k_raw), static_cast<const uint16_t *>(v),
                   r > 0 ? static_cast<const uint16_t *>(lora_a) : nullptr, rope_cos, rope_sin,
                   static_cast<uint16_t *>(base_kv), static_cast<uint16_t *>(res_kv)};
-    const dim3 grid((unsigned)((n + kProdTok - 1) / kProdTok));
+    const dim3 grid((unsigned)(n_shrink + n_base));
     hipStream_t st = static_cast<hipStream_t>(stream);
     switch (r) {
     case 0: hipLaunchKernelGGL(produce_kernel<0>, grid, dim3(256), 0, st, a); break;

@@ -38,7 +38,7 @@ def _within_one_ulp(a16, b16, tag):
 @pytest.mark.parametrize("r", [8, 16, 64])
 @pytest.mark.parametrize("rope", [False, True])
 def test_producer_matches_oracle(r, rope):
-    hkv, d, ps, hidden, pos0, n = 8, 128, 16, 512, 37, 100
+    hkv, d, ps, hidden, pos0, n = 8, 128, 16, 1024, 37, 100
     print(f"case producer r={r} rope={rope} pos0={pos0} n={n}", flush=True)
     rng = np.random.default_rng(100 + r)
     tree = rt.Tree(ps, 64, 64)
