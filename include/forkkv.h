@@ -327,6 +327,28 @@ fkv_status fkv_produce_tokens(const int32_t *bt_base, const int32_t *bt_res, int
                               const float *rope_cos, const float *rope_sin, int64_t rope_max_pos, void *base_kv,
                               void *res_kv, int32_t hkv, int32_t d, int32_t r, int32_t page_size, void *stream);
 
+/* One sequence of a batched producer call (a host array of these; its pointers are device
+ * memory). */
+typedef struct {
+    const int32_t *bt_base;  /* the sequence's base block-table row */
+    const int32_t *bt_res;   /* its residual block-table row (may be NULL when lora_a is NULL) */
+    const void *lora_a;      /* its adapter's [2][r][hidden] bf16 shrink rows; NULL: base pool only */
+    int64_t pos0;            /* position of its first new token */
+    int64_t n;               /* its new tokens (0: nothing to do) */
+    int64_t row0;            /* row of its first new token in x, k_raw and v */
+} fkv_produce_seq;
+
+/* The producer over several sequences in one launch (same writes as fkv_produce_tokens for
+ * each sequence; up to 32 sequences per launch, more are enqueued in groups of 32).  x
+ * [rows][hidden], k_raw / v [rows][hkv][d] hold every sequence's new tokens, sequence i at
+ * rows row0 .. row0 + n - 1.  The sequences must write disjoint page slots (fkv_cow_append
+ * gives each appending sequence private pages); overlapping slots race.  Every sequence is
+ * checked before anything is launched: FKV_ERR_INVALID names the first bad one. */
+fkv_status fkv_produce_tokens_batch(const fkv_produce_seq *seqs, int32_t nseq, const void *x, int32_t hidden,
+                                    const void *k_raw, const void *v, const float *rope_cos, const float *rope_sin,
+                                    int64_t rope_max_pos, void *base_kv, void *res_kv, int32_t hkv, int32_t d,
+                                    int32_t r, int32_t page_size, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

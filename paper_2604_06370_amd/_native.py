@@ -121,6 +121,16 @@ fkv_produce_tokens = _sig("fkv_produce_tokens", c_i32,
                            c_i32, c_i32, c_i32, c_i32, c_vp])
 
 
+class fkv_produce_seq(ctypes.Structure):
+    _fields_ = [("bt_base", c_vp), ("bt_res", c_vp), ("lora_a", c_vp), ("pos0", c_i64), ("n", c_i64),
+                ("row0", c_i64)]
+
+
+fkv_produce_tokens_batch = _sig("fkv_produce_tokens_batch", c_i32,
+                                [ctypes.POINTER(fkv_produce_seq), c_i32, c_vp, c_i32, c_vp, c_vp, c_vp, c_vp, c_i64,
+                                 c_vp, c_vp, c_i32, c_i32, c_i32, c_i32, c_vp])
+
+
 def check(status: int, what: str = "") -> None:
     if status != FKV_OK:
         msg = fkv_last_error().decode(errors="replace")

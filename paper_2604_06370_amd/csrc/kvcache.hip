@@ -131,23 +131,36 @@ __global__ __launch_bounds__(256) void scatter_kernel(ScatterArgs a) {
 // Per token at position pos: K = RoPE_pos(k_raw) (rotate-half pairs (i, i + d/2), angles from
 // the fp32 table) and V into the base pool; C_K = x A_K^T and C_V = x A_V^T (the LoRA shrink,
 // hidden -> r, fp32 accumulation on the matrix cores) into the residual pool.  Page size 16,
-// head dim 128 (the fragment layouts).  One launch, two kinds of workgroups:
-//  - shrink: 16 tokens; wave w covers a quarter of the hidden dimension with 16x16x32
-//    products (A operand: 16 bytes of one token's x row per lane; B operand: 16 bytes of one
-//    row of A, read straight from memory, L2-resident), eight k-steps of loads in flight;
-//    the four partial tiles are summed through LDS;
-//  - base: 64 tokens of one KV head, one (token, rotate-half pair) per item.
-struct ProduceArgs {
+// head dim 128 (the fragment layouts).  Every workgroup covers one page of the call's
+// position range (slots outside [pos0, pos0 + n) are left as they are).  One launch, two
+// kinds of workgroups:
+//  - shrink (one per page): wave w covers a quarter of the hidden dimension with 16x16x32
+//    products (16 bytes of one token's x row and of one row of A per lane, A L2-resident),
+//    eight k-steps of loads in flight; the four partial tiles are summed through LDS.  C_K is
+//    computed transposed (A as the row operand), so each lane holds 4 ranks of one token
+//    and C_V 4 tokens of one rank: both are 8 contiguous bytes of the residual page;
+//  - base (one per page and group of four KV heads): the page's 16 token rows of K and V of
+//    each head come into LDS with 16-byte loads, all requested together; each thread then forms 16-byte chunks of the fragment-ordered blocks (K:
+//    one token's dims 32a + 16h + 4b + i and their rotate-half partners 64 further on, so
+//    the rotation needs nothing from other threads; V: 4 tokens x 2 dims) and stores them
+//    whole (V chunks that straddle the range end are written element by element).
+struct ProduceSeq {
     const int32_t *bt_base, *bt_res;
-    int64_t pos0;
-    int32_t n, hidden, hkv, n_shrink_blocks;
-    const uint16_t *x, *k_raw, *v, *lora_a;
+    const uint16_t *lora_a;     // null: no shrink for this sequence
+    int64_t pos0, row0;         // first new position; its row in x, k_raw and v
+    int32_t n, first_shrink;    // new tokens; its first shrink workgroup
+    int32_t first_base, pad;    // its first base workgroup
+};
+constexpr int kProdMaxSeqs = 32;  // sequences per launch (kernel-argument space)
+struct ProduceArgs {
+    ProduceSeq seq[kProdMaxSeqs];
+    int32_t nseq, n_shrink_blocks, hidden, hkv;
+    const uint16_t *x, *k_raw, *v;
     const float *rope_cos, *rope_sin;
     uint16_t *base_kv, *res_kv;
 };
-constexpr int kShrinkTok = 16;
-constexpr int kBaseTok = 64;
 constexpr int kProdChunk = 1024;  // hidden is a multiple of this (four waves x 8 k-steps x 32)
+constexpr int kProdHeads = 4;     // KV heads per base workgroup
 
 template <int R>
 __global__ __launch_bounds__(256) void produce_kernel(ProduceArgs a) {
@@ -155,40 +168,70 @@ __global__ __launch_bounds__(256) void produce_kernel(ProduceArgs a) {
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int col = lane & 15, grp = lane >> 4;
-    if ((int)blockIdx.x < a.n_shrink_blocks) {
+    // the sequence served: the last one whose first workgroup of this kind is at or below ours
+    const int bid = blockIdx.x;
+    const bool shrink_wg = bid < a.n_shrink_blocks;
+    int s = 0;
+    for (int j = 1; j < a.nseq; ++j)
+        if ((shrink_wg ? a.seq[j].first_shrink : a.seq[j].first_base) <= bid) s = j;
+    const ProduceSeq &q = a.seq[s];
+    const int lb = bid - (shrink_wg ? q.first_shrink : q.first_base);  // workgroup within the sequence
+    const int64_t pos0 = q.pos0, nq = q.n;
+    const int64_t page0 = pos0 / PS;
+    if (shrink_wg) {
         if constexpr (R > 0) {
             constexpr int RT = (R + 15) / 16, NT = 2 * RT;
             __shared__ fkvk::f32x4 s_part[3][NT][64];
-            const int j0 = blockIdx.x * kShrinkTok;
+            const int64_t pp = page0 + lb;
+            const int64_t tj0 = pp * PS - pos0;  // call index of slot 0 (negative on a first partial page)
             fkvk::f32x4 acc[NT];
 #pragma unroll
             for (int t = 0; t < NT; ++t) acc[t] = fkvk::f32x4{0, 0, 0, 0};
-            const int tok = j0 + col;
-            const bool tok_ok = tok < a.n;
+            const int64_t tok = tj0 + col;
+            const bool tok_ok = tok >= 0 && tok < nq;
             const int quarter = a.hidden / 4;
-            const uint16_t *xr = a.x + (int64_t)(tok_ok ? tok : 0) * a.hidden + wave * quarter + 8 * grp;
-            // B operand rows: shrink t / RT (K, then V), rank 16 (t % RT) + col (rows past r read row 0, zeroed)
+            const uint16_t *xr = a.x + q.row0 * a.hidden + (tok_ok ? tok : 0) * a.hidden + wave * quarter + 8 * grp;
+            // rows of A: shrink t / RT (K, then V), rank 16 (t % RT) + col (rows past r read row 0, zeroed)
             const uint16_t *ar[NT];
             bool rok[NT];
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
                 const int rho = 16 * (t % RT) + col;
                 rok[t] = rho < R;
-                ar[t] = a.lora_a + ((int64_t)((t / RT) * R + (rok[t] ? rho : 0)) * a.hidden + wave * quarter + 8 * grp);
+                ar[t] = q.lora_a + ((int64_t)((t / RT) * R + (rok[t] ? rho : 0)) * a.hidden + wave * quarter + 8 * grp);
             }
-            for (int k0 = 0; k0 < quarter; k0 += 8 * 32) {
-                fkvk::u32x4 xa[8], bw[8][NT];
+            // KS k-steps per round, two rounds in flight (the next round's loads are issued before
+            // the current round's products; the last round re-requests its own block so that
+            // every load is unconditional and the wait counts stay exact)
+            constexpr int KS = NT <= 2 ? 8 : (NT <= 4 ? 4 : 2);
+            constexpr int step = 32 * KS;
+            auto load = [&](int k0, fkvk::u32x4 (&xa)[KS], fkvk::u32x4 (&bw)[KS][NT]) __attribute__((always_inline)) {
 #pragma unroll
-                for (int ks = 0; ks < 8; ++ks) {
+                for (int ks = 0; ks < KS; ++ks) {
                     xa[ks] = tok_ok ? fkvk::ldg128(xr + k0 + 32 * ks) : fkvk::u32x4{0, 0, 0, 0};
 #pragma unroll
                     for (int t = 0; t < NT; ++t) bw[ks][t] = fkvk::ldg128(ar[t] + k0 + 32 * ks);
                 }
+            };
+            auto products = [&](const fkvk::u32x4 (&xa)[KS], const fkvk::u32x4 (&bw)[KS][NT]) __attribute__((always_inline)) {
 #pragma unroll
-                for (int ks = 0; ks < 8; ++ks)
+                for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-                    for (int t = 0; t < NT; ++t)
-                        acc[t] = fkvk::mfma32(xa[ks], rok[t] ? bw[ks][t] : fkvk::u32x4{0, 0, 0, 0}, acc[t]);
+                    for (int t = 0; t < NT; ++t) {
+                        const fkvk::u32x4 w = rok[t] ? bw[ks][t] : fkvk::u32x4{0, 0, 0, 0};
+                        // C_K^T (ranks in rows), C_V (tokens in rows)
+                        acc[t] = t < RT ? fkvk::mfma32(w, xa[ks], acc[t]) : fkvk::mfma32(xa[ks], w, acc[t]);
+                    }
+            };
+            fkvk::u32x4 xa0[KS], bw0[KS][NT], xa1[KS], bw1[KS][NT];
+            load(0, xa0, bw0);
+            for (int k0 = 0;;) {
+                load(min(k0 + step, quarter - step), xa1, bw1);
+                products(xa0, bw0);
+                if ((k0 += step) >= quarter) break;
+                load(min(k0 + step, quarter - step), xa0, bw0);
+                products(xa1, bw1);
+                if ((k0 += step) >= quarter) break;
             }
             if (wave > 0) {
 #pragma unroll
@@ -196,56 +239,132 @@ __global__ __launch_bounds__(256) void produce_kernel(ProduceArgs a) {
             }
             __syncthreads();
             if (wave == 0) {
+                uint16_t *pg = a.res_kv + (int64_t)q.bt_res[pp] * res_page_elems(PS, R);
 #pragma unroll
                 for (int t = 0; t < NT; ++t) {
                     fkvk::f32x4 c = acc[t];
 #pragma unroll
                     for (int w = 0; w < 3; ++w) c += s_part[w][t][lane];
-                    // c holds C[token 4grp + i][rank 16 (t % RT) + col] of shrink t / RT
-                    const int kv = t / RT, rho = 16 * (t % RT) + col;
-                    if (rho >= R) continue;
+                    const int kt = t % RT;
+                    const fkvk::u32x2 h4 = fkvk::u32x2{fkvk::pack_bf16(c[0], c[1]), fkvk::pack_bf16(c[2], c[3])};
+                    uint16_t *dst = pg + kt * 512 + (16 * grp + col) * 8;
+                    if (t < RT) {
+                        // C_K[token col][rank 16 kt + 4 grp + i] at dst[i]
+                        if (tok_ok && 16 * kt + 4 * grp < R) *reinterpret_cast<fkvk::u32x2 *>(dst) = h4;
+                    } else if (16 * kt + col < R) {
+                        // C_V[token 4 grp + i][rank 16 kt + col] at dst[4 + i]
+                        const int64_t tf = tj0 + 4 * grp;
+                        if (tf >= 0 && tf + 3 < nq) {
+                            *reinterpret_cast<fkvk::u32x2 *>(dst + 4) = h4;
+                        } else {
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const int tj = j0 + 4 * grp + i;
-                        if (tj >= a.n) continue;
-                        const int64_t pos = a.pos0 + tj;
-                        const int slot = (int)(pos % PS);
-                        uint16_t *pg = a.res_kv + (int64_t)a.bt_res[pos / PS] * res_page_elems(PS, R);
-                        const uint32_t h2 = fkvk::pack_bf16(c[i], 0.f);
-                        pg[kv == 0 ? ck_off(slot, rho, PS, R) : cv_off(slot, rho, PS, R)] = (uint16_t)(h2 & 0xffffu);
+                            for (int i = 0; i < 4; ++i)
+                                if (tf + i >= 0 && tf + i < nq)
+                                    dst[4 + i] = (uint16_t)((i & 1 ? h4[i >> 1] >> 16 : h4[i >> 1]) & 0xffffu);
+                        }
                     }
                 }
             }
         }
         return;
     }
-    // base K (rotated) and V of KV head hh for 64 tokens: one (token, rotate-half pair) per item
-    const int b = blockIdx.x - a.n_shrink_blocks;
-    const int hh = b % a.hkv;
-    const int j0 = (b / a.hkv) * kBaseTok;
-    for (int e = threadIdx.x; e < kBaseTok * HALF; e += 256) {
-        const int tl = e / HALF, f = e - tl * HALF;
-        const int tj = j0 + tl;
-        if (tj >= a.n) continue;
-        const int64_t pos = a.pos0 + tj;
-        const int slot = (int)(pos % PS);
-        const int64_t src = ((int64_t)tj * a.hkv + hh) * D;
-        float x0 = fkvk::bf16_to_f32(a.k_raw[src + f]), x1 = fkvk::bf16_to_f32(a.k_raw[src + f + HALF]);
+    // base K (rotated) and V of one page and up to kProdHeads KV heads: every head's token
+    // rows are requested before the first one is stored into LDS
+    __shared__ __attribute__((aligned(16))) uint16_t s_k[kProdHeads][PS * D], s_v[kProdHeads][PS * D];  // [slot][dim]
+    const int n_hg = (a.hkv + kProdHeads - 1) / kProdHeads;
+    const int b = lb;
+    const int h0 = (b % n_hg) * kProdHeads;
+    const int nh = min(kProdHeads, a.hkv - h0);
+    const int64_t pp = page0 + b / n_hg;
+    const int64_t tj0 = pp * PS - pos0;  // call index of slot 0 (negative on a first partial page)
+    {
+        const int t = threadIdx.x >> 4, c = threadIdx.x & 15;
+        const int64_t tj = tj0 + t;
+        const bool ok = tj >= 0 && tj < nq;
+        fkvk::u32x4 kx[kProdHeads], vx[kProdHeads];
+#pragma unroll
+        for (int i = 0; i < kProdHeads; ++i) {
+            kx[i] = vx[i] = fkvk::u32x4{0, 0, 0, 0};
+            if (ok && i < nh) {
+                const int64_t src = ((q.row0 + tj) * a.hkv + h0 + i) * D + 8 * c;
+                kx[i] = fkvk::ldg128(a.k_raw + src);
+                vx[i] = fkvk::ldg128(a.v + src);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < kProdHeads; ++i) {
+            *reinterpret_cast<fkvk::u32x4 *>(&s_k[i][t * D + 8 * c]) = kx[i];
+            *reinterpret_cast<fkvk::u32x4 *>(&s_v[i][t * D + 8 * c]) = vx[i];
+        }
+    }
+    __syncthreads();
+    constexpr int64_t blk = PS * D;
+    uint16_t *const pg = a.base_kv + (int64_t)q.bt_base[pp] * 2 * a.hkv * blk;
+    if (threadIdx.x < 128) {
+        // K chunks (a2, t, b4) and (a2 + 2, t, b4): element 4h + i is dim f = 32 a2 + 16 h + 4 b4 + i
+        // (the first member of a rotate-half pair) and f + 64 (its partner)
+        const int t = threadIdx.x & 15, b4 = (threadIdx.x >> 4) & 3, a2 = threadIdx.x >> 6;
+        const int64_t tj = tj0 + t;
+        if (tj < 0 || tj >= nq) return;
+        fkvk::f32x4 cs[2], sn[2];
         if (a.rope_cos) {
             // table order [pos / 16][f / 16][pos % 16 + 16 ((f % 16) / 4)][f % 4]
-            const int64_t o = (pos / PS) * (PS * HALF) + (f / 16) * 256 + (slot + 16 * ((f % 16) / 4)) * 4 + f % 4;
-            const float c = a.rope_cos[o], s = a.rope_sin[o];
-            const float y0 = x0 * c - x1 * s, y1 = x1 * c + x0 * s;
-            x0 = y0;
-            x1 = y1;
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int64_t o = pp * (PS * HALF) + (2 * a2 + h) * 256 + (t + 16 * b4) * 4;
+                cs[h] = *reinterpret_cast<const fkvk::f32x4 *>(a.rope_cos + o);
+                sn[h] = *reinterpret_cast<const fkvk::f32x4 *>(a.rope_sin + o);
+            }
         }
-        constexpr int64_t blk = PS * D;
-        uint16_t *pg = a.base_kv + (int64_t)a.bt_base[pos / PS] * 2 * a.hkv * blk;
-        const uint32_t kk = fkvk::pack_bf16(x0, x1);
-        pg[hh * blk + k_off(slot, f, PS, D)] = (uint16_t)(kk & 0xffffu);
-        pg[hh * blk + k_off(slot, f + HALF, PS, D)] = (uint16_t)(kk >> 16);
-        pg[(a.hkv + hh) * blk + v_off(slot, f, PS, D)] = a.v[src + f];
-        pg[(a.hkv + hh) * blk + v_off(slot, f + HALF, PS, D)] = a.v[src + f + HALF];
+        for (int hi = 0; hi < nh; ++hi) {
+            float x0[8], x1[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int f = 32 * a2 + 16 * (e >> 2) + 4 * b4 + (e & 3);
+                x0[e] = fkvk::bf16_to_f32(s_k[hi][t * D + f]);
+                x1[e] = fkvk::bf16_to_f32(s_k[hi][t * D + f + HALF]);
+            }
+            if (a.rope_cos) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float c = cs[e >> 2][e & 3], s = sn[e >> 2][e & 3];
+                    const float u = x0[e], w = x1[e];
+                    x0[e] = u * c - w * s;
+                    x1[e] = w * c + u * s;
+                }
+            }
+            uint16_t *kb = pg + (h0 + hi) * blk + (t + 16 * b4) * 8;
+            *reinterpret_cast<fkvk::u32x4 *>(kb + a2 * 512) =
+                fkvk::u32x4{fkvk::pack_bf16(x0[0], x0[1]), fkvk::pack_bf16(x0[2], x0[3]), fkvk::pack_bf16(x0[4], x0[5]),
+                            fkvk::pack_bf16(x0[6], x0[7])};
+            *reinterpret_cast<fkvk::u32x4 *>(kb + (a2 + 2) * 512) =
+                fkvk::u32x4{fkvk::pack_bf16(x1[0], x1[1]), fkvk::pack_bf16(x1[2], x1[3]), fkvk::pack_bf16(x1[4], x1[5]),
+                            fkvk::pack_bf16(x1[6], x1[7])};
+        }
+    } else {
+        // V chunks ci and ci + 128 (ci = 64 a + 16 q + c): element 4h + i is (dim 32a + 16h + c, token 4q + i)
+        for (int hi = 0; hi < nh; ++hi) {
+            uint16_t *vb = pg + (a.hkv + h0 + hi) * blk;
+#pragma unroll
+            for (int half = 0; half < 2; ++half) {
+                const int ci = (int)threadIdx.x - 128 + 128 * half;
+                const int av = ci >> 6, q = (ci >> 4) & 3, c = ci & 15;
+                uint16_t e8[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) e8[e] = s_v[hi][(4 * q + (e & 3)) * D + 32 * av + 16 * (e >> 2) + c];
+                const int64_t tf = tj0 + 4 * q;
+                if (tf >= 0 && tf + 3 < nq) {
+                    fkvk::u32x4 w;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) w[j] = (uint32_t)e8[2 * j] | ((uint32_t)e8[2 * j + 1] << 16);
+                    *reinterpret_cast<fkvk::u32x4 *>(vb + ci * 8) = w;
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (tf + (e & 3) >= 0 && tf + (e & 3) < nq) vb[ci * 8 + e] = e8[e];
+                }
+            }
+        }
     }
 }
 
@@ -296,42 +415,86 @@ fkv_status fkv_scatter_tokens(const int32_t *bt_base, const int32_t *bt_res, int
     return FKV_OK;
 }
 
+fkv_status fkv_produce_tokens_batch(const fkv_produce_seq *seqs, int32_t nseq, const void *x, int32_t hidden,
+                                    const void *k_raw, const void *v, const float *rope_cos, const float *rope_sin,
+                                    int64_t rope_max_pos, void *base_kv, void *res_kv, int32_t hkv, int32_t d,
+                                    int32_t r, int32_t page_size, void *stream) {
+    fkv::clear_error();
+    if (nseq < 0 || (nseq > 0 && !seqs) || hkv < 1 || d != 128 || page_size != 16 ||
+        !(r == 0 || r == 8 || r == 16 || r == 32 || r == 64))
+        return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: needs d = 128, page_size = 16, r in {0, 8, 16, 32, 64}");
+    if (!base_kv || !k_raw || !v) return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: pool, K or V missing");
+    if ((rope_cos == nullptr) != (rope_sin == nullptr))
+        return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: RoPE tables come in pairs");
+    // every sequence is checked before anything is launched
+    for (int32_t i = 0; i < nseq; ++i) {
+        const fkv_produce_seq &q = seqs[i];
+        const std::string who = "fkv_produce_tokens: sequence " + std::to_string(i) + ": ";
+        if (q.pos0 < 0 || q.n < 0 || q.row0 < 0) return fkv::fail(FKV_ERR_INVALID, who + "negative position, count or row");
+        if (q.n > (int64_t)1 << 24) return fkv::fail(FKV_ERR_INVALID, who + "too many tokens in one call");
+        if (q.n > 0 && !q.bt_base) return fkv::fail(FKV_ERR_INVALID, who + "base table missing");
+        if (rope_cos && q.pos0 + q.n > rope_max_pos) return fkv::fail(FKV_ERR_INVALID, who + "RoPE table too short");
+        if (q.lora_a && r > 0 && q.n > 0) {
+            if (!x || hidden < kProdChunk || hidden % kProdChunk)
+                return fkv::fail(FKV_ERR_INVALID, who + "x and hidden (a multiple of 1024) required with lora_a");
+            if (!q.bt_res || !res_kv) return fkv::fail(FKV_ERR_INVALID, who + "residual table/pool missing");
+        }
+    }
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const int64_t n_hg = (hkv + kProdHeads - 1) / kProdHeads;
+    for (int32_t c0 = 0; c0 < nseq; c0 += kProdMaxSeqs) {
+        ProduceArgs a{};
+        a.hidden = hidden;
+        a.hkv = hkv;
+        a.x = static_cast<const uint16_t *>(x);
+        a.k_raw = static_cast<const uint16_t *>(k_raw);
+        a.v = static_cast<const uint16_t *>(v);
+        a.rope_cos = rope_cos;
+        a.rope_sin = rope_sin;
+        a.base_kv = static_cast<uint16_t *>(base_kv);
+        a.res_kv = static_cast<uint16_t *>(res_kv);
+        int64_t n_shrink = 0, n_base = 0;
+        for (int32_t i = c0; i < nseq && i < c0 + kProdMaxSeqs; ++i) {
+            const fkv_produce_seq &q = seqs[i];
+            if (q.n == 0) continue;
+            const int64_t pages = (q.pos0 + q.n - 1) / page_size - q.pos0 / page_size + 1;  // pages the range touches
+            ProduceSeq &o = a.seq[a.nseq++];
+            o.bt_base = q.bt_base;
+            o.bt_res = q.bt_res;
+            o.lora_a = r > 0 ? static_cast<const uint16_t *>(q.lora_a) : nullptr;
+            o.pos0 = q.pos0;
+            o.row0 = q.row0;
+            o.n = (int32_t)q.n;
+            o.first_shrink = (int32_t)n_shrink;
+            o.first_base = (int32_t)n_base;  // offset by the shrink count below
+            if (o.lora_a) n_shrink += pages;
+            n_base += pages * n_hg;
+        }
+        if (a.nseq == 0) continue;
+        if (n_shrink + n_base > INT32_MAX) return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: batch too large");
+        for (int32_t j = 0; j < a.nseq; ++j) a.seq[j].first_base += (int32_t)n_shrink;
+        a.n_shrink_blocks = (int32_t)n_shrink;
+        const dim3 grid((unsigned)(n_shrink + n_base));
+        switch (r) {
+        case 0: hipLaunchKernelGGL(produce_kernel<0>, grid, dim3(256), 0, st, a); break;
+        case 8: hipLaunchKernelGGL(produce_kernel<8>, grid, dim3(256), 0, st, a); break;
+        case 16: hipLaunchKernelGGL(produce_kernel<16>, grid, dim3(256), 0, st, a); break;
+        case 32: hipLaunchKernelGGL(produce_kernel<32>, grid, dim3(256), 0, st, a); break;
+        default: hipLaunchKernelGGL(produce_kernel<64>, grid, dim3(256), 0, st, a); break;
+        }
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return fkv::fail(FKV_ERR_HIP, std::string("fkv_produce_tokens: ") + hipGetErrorString(e));
+    }
+    return FKV_OK;
+}
+
 fkv_status fkv_produce_tokens(const int32_t *bt_base, const int32_t *bt_res, int64_t pos0, int64_t n, const void *x,
                               int32_t hidden, const void *k_raw, const void *v, const void *lora_a,
                               const float *rope_cos, const float *rope_sin, int64_t rope_max_pos, void *base_kv,
                               void *res_kv, int32_t hkv, int32_t d, int32_t r, int32_t page_size, void *stream) {
-    fkv::clear_error();
-    if (pos0 < 0 || n < 0 || hkv < 1 || d != 128 || page_size != 16 || !(r == 0 || r == 8 || r == 16 || r == 32 || r == 64))
-        return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: needs d = 128, page_size = 16, r in {0, 8, 16, 32, 64}");
-    if (!bt_base || !base_kv || !k_raw || !v) return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: base table, pool, K or V missing");
-    if ((rope_cos == nullptr) != (rope_sin == nullptr))
-        return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: RoPE tables come in pairs");
-    if (rope_cos && pos0 + n > rope_max_pos) return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: RoPE table too short");
-    if (lora_a && r > 0) {
-        if (!x || hidden < kProdChunk || hidden % kProdChunk) return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: x and hidden (a multiple of 1024) required with lora_a");
-        if (!bt_res || !res_kv) return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: residual table/pool missing");
-    }
-    if (n == 0) return FKV_OK;
-    if (n > (int64_t)1 << 24) return fkv::fail(FKV_ERR_INVALID, "fkv_produce_tokens: too many tokens in one call");
-    const bool shrink = lora_a && r > 0;
-    const int32_t n_shrink = shrink ? (int32_t)((n + kShrinkTok - 1) / kShrinkTok) : 0;
-    const int64_t n_base = (n + kBaseTok - 1) / kBaseTok * hkv;
-    ProduceArgs a{bt_base, bt_res, pos0, (int32_t)n, hidden, hkv, n_shrink,
-                  static_cast<const uint16_t *>(x), static_cast<const uint16_t *>(k_raw), static_cast<const uint16_t *>(v),
-                  r > 0 ? static_cast<const uint16_t *>(lora_a) : nullptr, rope_cos, rope_sin,
-                  static_cast<uint16_t *>(base_kv), static_cast<uint16_t *>(res_kv)};
-    const dim3 grid((unsigned)(n_shrink + n_base));
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    switch (r) {
-    case 0: hipLaunchKernelGGL(produce_kernel<0>, grid, dim3(256), 0, st, a); break;
-    case 8: hipLaunchKernelGGL(produce_kernel<8>, grid, dim3(256), 0, st, a); break;
-    case 16: hipLaunchKernelGGL(produce_kernel<16>, grid, dim3(256), 0, st, a); break;
-    case 32: hipLaunchKernelGGL(produce_kernel<32>, grid, dim3(256), 0, st, a); break;
-    default: hipLaunchKernelGGL(produce_kernel<64>, grid, dim3(256), 0, st, a); break;
-    }
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return fkv::fail(FKV_ERR_HIP, std::string("fkv_produce_tokens: ") + hipGetErrorString(e));
-    return FKV_OK;
+    const fkv_produce_seq q{bt_base, bt_res, lora_a, pos0, n, 0};
+    return fkv_produce_tokens_batch(&q, 1, x, hidden, k_raw, v, rope_cos, rope_sin, rope_max_pos, base_kv, res_kv, hkv,
+                                    d, r, page_size, stream);
 }
 
 }  // extern "C"

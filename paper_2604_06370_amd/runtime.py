@@ -250,6 +250,26 @@ def produce_tokens(bt_base_row: torch.Tensor, bt_res_row: Optional[torch.Tensor]
           "fkv_produce_tokens")
 
 
+def produce_tokens_batch(seqs, x: Optional[torch.Tensor], k_raw: torch.Tensor, v: torch.Tensor,
+                         rope: Optional[tuple], base_kv: torch.Tensor, res_kv: Optional[torch.Tensor],
+                         hkv: int, d: int, r: int, page_size: int, stream=None) -> None:
+    """fkv_produce_tokens_batch: seqs = [(bt_base_row, bt_res_row, lora_a, pos0, n, row0), ...]
+    (device tensors or None for the first three); x [rows][hidden], k_raw/v [rows][hkv][d] bf16
+    hold every sequence's new tokens at rows row0 .. row0 + n - 1."""
+    p = lambda t: t.data_ptr() if t is not None else None
+    for t in [x, k_raw, v] + [s[2] for s in seqs]:
+        assert t is None or (t.is_contiguous() and t.dtype == torch.bfloat16)
+    arr = (N.fkv_produce_seq * max(1, len(seqs)))()
+    for i, (btb, btr, a, pos0, n, row0) in enumerate(seqs):
+        arr[i] = N.fkv_produce_seq(p(btb), p(btr), p(a), int(pos0), int(n), int(row0))
+    hidden = x.shape[1] if x is not None else 0
+    cos, sin = (rope[0], rope[1]) if rope is not None else (None, None)
+    max_pos = cos.numel() // (d // 2) if cos is not None else 0
+    check(N.fkv_produce_tokens_batch(arr, len(seqs), p(x), hidden, p(k_raw), p(v), p(cos), p(sin), max_pos,
+                                     base_kv.data_ptr(), p(res_kv), hkv, d, r, page_size, _stream(stream)),
+          "fkv_produce_tokens_batch")
+
+
 def make_args(*, q, base_kv, res_kv, lora_b, adapter_idx, base_bt, res_bt, seq_lens, out, hq, hkv, d, r,
               page_size, rope=None, plan_dev=None, q_indptr=None, workspace=None, n_q=0, max_q_per_agent=0,
               scale: Optional[float] = None) -> N.fkv_attn_args:

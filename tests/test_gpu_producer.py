@@ -23,7 +23,10 @@ def _bf16(a):
     return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda().view(torch.bfloat16)
 
 
-def _within_one_ulp(a16, b16, tag):
+def _within_one_ulp(a16, b16, tag, abs_slack=0.0):
+    """Equal within one bf16 unit in the last place of the larger value, plus abs_slack: the
+    absolute error of the kernel's fp32 arithmetic, which one unit does not cover where the
+    result is small after cancellation."""
     a = a16.view(torch.int16).cpu().numpy()
     b = b16.view(torch.int16).cpu().numpy()
     diff = a != b
@@ -31,7 +34,7 @@ def _within_one_ulp(a16, b16, tag):
         fa = W.bf16_bits_to_f64(a[diff].view(np.uint16))
         fb = W.bf16_bits_to_f64(b[diff].view(np.uint16))
         assert np.isfinite(fa).all() and np.isfinite(fb).all(), tag
-        assert (np.abs(fa - fb) <= 2.0 ** -7 * np.maximum(np.abs(fa), np.abs(fb)) + 1e-30).all(), tag
+        assert (np.abs(fa - fb) <= 2.0 ** -7 * np.maximum(np.abs(fa), np.abs(fb)) + abs_slack + 1e-30).all(), tag
     print(f"[{tag}] {int(diff.sum())} of {a.size} values differ by one unit in the last place", flush=True)
 
 
@@ -67,8 +70,8 @@ def test_producer_matches_oracle(r, rope):
                       hkv, d, r, ps)
     torch.cuda.synchronize()
     assert torch.equal(base_a[:, 1].view(torch.int16), base_b[:, 1].view(torch.int16)), "V"
-    _within_one_ulp(base_a[:, 0], base_b[:, 0], f"K r={r} rope={rope}")
-    _within_one_ulp(res_a, res_b, f"C r={r} rope={rope}")
+    _within_one_ulp(base_a[:, 0], base_b[:, 0], f"K r={r} rope={rope}", _rope_slack(kq) if rope else 0.0)
+    _within_one_ulp(res_a, res_b, f"C r={r} rope={rope}", _shrink_slack(xq, [akq, avq]))
 
 
 def test_producer_without_adapter_leaves_residual_pool():
@@ -85,3 +88,100 @@ def test_producer_without_adapter_leaves_residual_pool():
     torch.cuda.synchronize()
     assert torch.equal(res.view(torch.int16), res0.view(torch.int16))
     assert base.float().abs().sum() > 0
+
+
+def _rope_slack(k_raw):
+    """Absolute error bound of the kernel's fp32 rotation y = u c - w s (or w c + u s): the
+    fp32 table entries carry a relative error of 2^-24 each, the product and the sum round
+    once more, so |y_fp32 - y| <= (|u| + 2|w| + |y|) 2^-24 <= 4 max|k_raw| 2^-24."""
+    return 4.0 * 2.0 ** -24 * float(np.abs(k_raw).max())
+
+
+def _shrink_slack(x, a):
+    """Absolute error bound of the kernel's fp32 shrink C = x A^T: the bf16 x bf16 products
+    are exact in fp32 and at most `hidden` roundings of 2^-24 follow, so
+    |C_fp32 - C| <= hidden 2^-24 sum_i |x_i| |A_i|."""
+    hidden = x.shape[1]
+    return hidden * 2.0 ** -24 * float((np.abs(x) @ np.abs(np.concatenate(list(a), axis=0)).T).max())
+
+
+def _batch_case(specs, hkv, d, ps, r, hidden, seed, rope):
+    """Sequences (pos0, n, with_adapter) on disjoint page ranges; every input row stacked."""
+    rng = np.random.default_rng(seed)
+    max_pages = max((p0 + n + ps - 1) // ps for p0, n, _ in specs)
+    first, seqs_np = 0, []
+    for p0, n, ad in specs:
+        np_ = (p0 + n + ps - 1) // ps
+        seqs_np.append(np.arange(first, first + max_pages, dtype=np.int32))
+        first += np_
+    n_pool = first + max_pages  # rows past a sequence's own pages are never read
+    rows = sum(n for _, n, _ in specs)
+    x = W.bf16_bits_to_f64(W.f32_to_bf16_bits(rng.normal(size=(rows, hidden)).astype(np.float32)))
+    k = W.bf16_bits_to_f64(W.f32_to_bf16_bits(rng.normal(size=(rows, hkv, d)).astype(np.float32)))
+    v = W.bf16_bits_to_f64(W.f32_to_bf16_bits(rng.normal(size=(rows, hkv, d)).astype(np.float32)))
+    a = [W.bf16_bits_to_f64(W.f32_to_bf16_bits(rng.normal(scale=hidden ** -0.5, size=(2, r, hidden)).astype(np.float32)))
+         for _ in specs]
+    res_elems = int(rt.res_page_elems(ps, r))
+    base0 = torch.randint(-30000, 30000, (n_pool, 2, hkv, ps * d), dtype=torch.int16).cuda().view(torch.bfloat16)
+    res0 = torch.randint(-30000, 30000, (n_pool, res_elems), dtype=torch.int16).cuda().view(torch.bfloat16)
+    tables = rt.rope_tables(d, max_pages * ps, ROPE_BASE, "cuda") if rope else None
+    bts = [torch.from_numpy(s).cuda() for s in seqs_np]
+    return x, k, v, a, base0, res0, tables, bts
+
+
+@pytest.mark.parametrize("r", [16, 64])
+def test_producer_batch_matches_single_calls_and_oracle(r):
+    """One batched launch over ragged sequences (unaligned starts, a one-token sequence, one
+    without an adapter) writes exactly what per-sequence calls write, and matches the oracle."""
+    hkv, d, ps, hidden = 8, 128, 16, 1024
+    specs = [(37, 100, True), (0, 16, True), (5, 3, False), (64, 200, True), (15, 1, True)]
+    print(f"case producer batch r={r} specs={specs}", flush=True)
+    x, k, v, a, base0, res0, tables, bts = _batch_case(specs, hkv, d, ps, r, hidden, 300 + r, True)
+    xg, kg, vg = _bf16(x), _bf16(k), _bf16(v)
+    ag = [_bf16(ai) for ai in a]
+    base_batch, res_batch = base0.clone(), res0.clone()
+    base_one, res_one = base0.clone(), res0.clone()
+    base_ref, res_ref = base0.clone(), res0.clone()
+    seqs, row = [], 0
+    for (p0, n, ad), bt, ai in zip(specs, bts, ag):
+        seqs.append((bt, bt, ai if ad else None, p0, n, row))
+        row += n
+    rt.produce_tokens_batch(seqs, xg, kg, vg, tables, base_batch, res_batch, hkv, d, r, ps)
+    for (bt, btr, ai, p0, n, r0), (_, _, ad), a_np in zip(seqs, specs, a):
+        rt.produce_tokens(bt, btr, p0, xg[r0:r0 + n].contiguous(), kg[r0:r0 + n].contiguous(),
+                          vg[r0:r0 + n].contiguous(), ai, tables, base_one, res_one, hkv, d, r, ps)
+        kr, vr, ckr, cvr = oracle_produce(x[r0:r0 + n], k[r0:r0 + n], v[r0:r0 + n], a_np[0], a_np[1], p0, ROPE_BASE)
+        rt.scatter_tokens(bt, btr, p0, _bf16(kr), _bf16(vr), _bf16(ckr) if ad else None,
+                          _bf16(cvr) if ad else None, base_ref, res_ref, hkv, d, r, ps)
+    torch.cuda.synchronize()
+    assert torch.equal(base_batch.view(torch.int16), base_one.view(torch.int16)), "batch vs single calls: base"
+    assert torch.equal(res_batch.view(torch.int16), res_one.view(torch.int16)), "batch vs single calls: residual"
+    assert torch.equal(base_batch[:, 1].view(torch.int16), base_ref[:, 1].view(torch.int16)), "V"
+    _within_one_ulp(base_batch[:, 0], base_ref[:, 0], f"batch K r={r}", _rope_slack(k))
+    _within_one_ulp(res_batch, res_ref, f"batch C r={r}", max(_shrink_slack(x, ai) for ai in a))
+
+
+def test_producer_batch_over_32_sequences():
+    """40 short sequences: the batch goes out as launches of up to 32 sequences and still
+    writes exactly what per-sequence calls write."""
+    hkv, d, ps, r, hidden = 2, 128, 16, 16, 1024
+    rng = np.random.default_rng(41)
+    specs = [(int(rng.integers(0, 40)), int(rng.integers(1, 20)), bool(i % 7)) for i in range(40)]
+    print(f"case producer batch of {len(specs)} sequences", flush=True)
+    x, k, v, a, base0, res0, tables, bts = _batch_case(specs, hkv, d, ps, r, hidden, 42, True)
+    xg, kg, vg = _bf16(x), _bf16(k), _bf16(v)
+    ag = [_bf16(ai) for ai in a]
+    base_batch, res_batch = base0.clone(), res0.clone()
+    base_one, res_one = base0.clone(), res0.clone()
+    seqs, row = [], 0
+    for (p0, n, ad), bt, ai in zip(specs, bts, ag):
+        seqs.append((bt, bt, ai if ad else None, p0, n, row))
+        row += n
+    rt.produce_tokens_batch(seqs, xg, kg, vg, tables, base_batch, res_batch, hkv, d, r, ps)
+    for bt, btr, ai, p0, n, r0 in seqs:
+        rt.produce_tokens(bt, btr, p0, xg[r0:r0 + n].contiguous(), kg[r0:r0 + n].contiguous(),
+                          vg[r0:r0 + n].contiguous(), ai, tables, base_one, res_one, hkv, d, r, ps)
+    torch.cuda.synchronize()
+    assert torch.equal(base_batch.view(torch.int16), base_one.view(torch.int16))
+    assert torch.equal(res_batch.view(torch.int16), res_one.view(torch.int16))
+    assert not torch.equal(base_batch.view(torch.int16), base0.view(torch.int16))
