@@ -134,12 +134,12 @@ __global__ __launch_bounds__(256) void scatter_kernel(ScatterArgs a) {
 // head dim 128 (the fragment layouts).  Every workgroup covers one page of the call's
 // position range (slots outside [pos0, pos0 + n) are left as they are).  One launch, two
 // kinds of workgroups:
-//  - shrink (one per page): wave w covers a quarter of the hidden dimension with 16x16x32
+//  - shrink (one per page): wave w covers every fourth block of the hidden dimension with 16x16x32
 //    products (16 bytes of one token's x row and of one row of A per lane, A L2-resident),
 //    eight k-steps of loads in flight; the four partial tiles are summed through LDS.  C_K is
 //    computed transposed (A as the row operand), so each lane holds 4 ranks of one token
 //    and C_V 4 tokens of one rank: both are 8 contiguous bytes of the residual page;
-//  - base (one per page and group of four KV heads): the page's 16 token rows of K and V of
+//  - base (one per page and pair of KV heads): the page's 16 token rows of K and V of
 //    each head come into LDS with 16-byte loads, all requested together; each thread then forms 16-byte chunks of the fragment-ordered blocks (K:
 //    one token's dims 32a + 16h + 4b + i and their rotate-half partners 64 further on, so
 //    the rotation needs nothing from other threads; V: 4 tokens x 2 dims) and stores them
@@ -160,10 +160,10 @@ struct ProduceArgs {
     uint16_t *base_kv, *res_kv;
 };
 constexpr int kProdChunk = 1024;  // hidden is a multiple of this (four waves x 8 k-steps x 32)
-constexpr int kProdHeads = 4;     // KV heads per base workgroup
+constexpr int kProdHeads = 2;     // KV heads per base workgroup
 
 template <int R>
-__global__ __launch_bounds__(256) void produce_kernel(ProduceArgs a) {
+__global__ __launch_bounds__(256, 6) void produce_kernel(ProduceArgs a) {
     constexpr int PS = 16, D = 128, HALF = D / 2;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -190,7 +190,7 @@ __global__ __launch_bounds__(256) void produce_kernel(ProduceArgs a) {
             const int64_t tok = tj0 + col;
             const bool tok_ok = tok >= 0 && tok < nq;
             const int quarter = a.hidden / 4;
-            const uint16_t *xr = a.x + q.row0 * a.hidden + (tok_ok ? tok : 0) * a.hidden + wave * quarter + 8 * grp;
+            const uint16_t *xr = a.x + q.row0 * a.hidden + (tok_ok ? tok : 0) * a.hidden + 8 * grp;
             // rows of A: shrink t / RT (K, then V), rank 16 (t % RT) + col (rows past r read row 0, zeroed)
             const uint16_t *ar[NT];
             bool rok[NT];
@@ -198,19 +198,21 @@ __global__ __launch_bounds__(256) void produce_kernel(ProduceArgs a) {
             for (int t = 0; t < NT; ++t) {
                 const int rho = 16 * (t % RT) + col;
                 rok[t] = rho < R;
-                ar[t] = q.lora_a + ((int64_t)((t / RT) * R + (rok[t] ? rho : 0)) * a.hidden + wave * quarter + 8 * grp);
+                ar[t] = q.lora_a + ((int64_t)((t / RT) * R + (rok[t] ? rho : 0)) * a.hidden + 8 * grp);
             }
             // KS k-steps per round, two rounds in flight (the next round's loads are issued before
             // the current round's products; the last round re-requests its own block so that
-            // every load is unconditional and the wait counts stay exact)
-            constexpr int KS = NT <= 2 ? 8 : (NT <= 4 ? 4 : 2);
+            // every load is unconditional and the wait counts stay exact).  Round k0 of wave w
+            // covers hidden columns 4 k0 + w step .. + step - 1: the four waves' blocks of a round
+            // are adjacent, so each token row is read in runs of 4 step columns.
+            constexpr int KS = NT <= 2 ? 2 : 1;
             constexpr int step = 32 * KS;
             auto load = [&](int k0, fkvk::u32x4 (&xa)[KS], fkvk::u32x4 (&bw)[KS][NT]) __attribute__((always_inline)) {
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks) {
-                    xa[ks] = tok_ok ? fkvk::ldg128(xr + k0 + 32 * ks) : fkvk::u32x4{0, 0, 0, 0};
+                    xa[ks] = tok_ok ? fkvk::ldg128(xr + 4 * k0 + wave * step + 32 * ks) : fkvk::u32x4{0, 0, 0, 0};
 #pragma unroll
-                    for (int t = 0; t < NT; ++t) bw[ks][t] = fkvk::ldg128(ar[t] + k0 + 32 * ks);
+                    for (int t = 0; t < NT; ++t) bw[ks][t] = fkvk::ldg128(ar[t] + 4 * k0 + wave * step + 32 * ks);
                 }
             };
             auto products = [&](const fkvk::u32x4 (&xa)[KS], const fkvk::u32x4 (&bw)[KS][NT]) __attribute__((always_inline)) {
