@@ -134,7 +134,7 @@ __global__ __launch_bounds__(256) void scatter_kernel(ScatterArgs a) {
 // head dim 128 (the fragment layouts).  Every workgroup covers one page of the call's
 // position range (slots outside [pos0, pos0 + n) are left as they are).  One launch, two
 // kinds of workgroups:
-//  - shrink (one per page): wave w covers every fourth block of the hidden dimension with 16x16x32
+//  - shrink (one per four pages): wave w covers every fourth block of the hidden dimension with 16x16x32
 //    products (16 bytes of one token's x row and of one row of A per lane, A L2-resident),
 //    eight k-steps of loads in flight; the four partial tiles are summed through LDS.  C_K is
 //    computed transposed (A as the row operand), so each lane holds 4 ranks of one token
@@ -161,6 +161,7 @@ struct ProduceArgs {
 };
 constexpr int kProdChunk = 1024;  // hidden is a multiple of this (four waves x 8 k-steps x 32)
 constexpr int kProdHeads = 2;     // KV heads per base workgroup
+constexpr int kShrinkPages = 4;   // pages (16-token tiles) per shrink workgroup
 
 template <int R>
 __global__ __launch_bounds__(256, 6) void produce_kernel(ProduceArgs a) {
@@ -181,16 +182,22 @@ __global__ __launch_bounds__(256, 6) void produce_kernel(ProduceArgs a) {
     if (shrink_wg) {
         if constexpr (R > 0) {
             constexpr int RT = (R + 15) / 16, NT = 2 * RT;
-            __shared__ fkvk::f32x4 s_part[3][NT][64];
-            const int64_t pp = page0 + lb;
-            const int64_t tj0 = pp * PS - pos0;  // call index of slot 0 (negative on a first partial page)
-            fkvk::f32x4 acc[NT];
+            __shared__ fkvk::f32x4 s_part[3][NT][kShrinkPages][64];
+            // tile u: page page0 + kShrinkPages lb + u; token slot col of it is call index tj0[u] + col
+            int64_t tj0[kShrinkPages];
+            bool tok_ok[kShrinkPages];
+            const uint16_t *xr[kShrinkPages];
+            fkvk::f32x4 acc[NT][kShrinkPages];
 #pragma unroll
-            for (int t = 0; t < NT; ++t) acc[t] = fkvk::f32x4{0, 0, 0, 0};
-            const int64_t tok = tj0 + col;
-            const bool tok_ok = tok >= 0 && tok < nq;
+            for (int u = 0; u < kShrinkPages; ++u) {
+                tj0[u] = (page0 + (int64_t)kShrinkPages * lb + u) * PS - pos0;
+                const int64_t tok = tj0[u] + col;
+                tok_ok[u] = tok >= 0 && tok < nq;
+                xr[u] = a.x + q.row0 * a.hidden + (tok_ok[u] ? tok : 0) * a.hidden + 8 * grp;
+#pragma unroll
+                for (int t = 0; t < NT; ++t) acc[t][u] = fkvk::f32x4{0, 0, 0, 0};
+            }
             const int quarter = a.hidden / 4;
-            const uint16_t *xr = a.x + q.row0 * a.hidden + (tok_ok ? tok : 0) * a.hidden + 8 * grp;
             // rows of A: shrink t / RT (K, then V), rank 16 (t % RT) + col (rows past r read row 0, zeroed)
             const uint16_t *ar[NT];
             bool rok[NT];
@@ -204,28 +211,33 @@ __global__ __launch_bounds__(256, 6) void produce_kernel(ProduceArgs a) {
             // the current round's products; the last round re-requests its own block so that
             // every load is unconditional and the wait counts stay exact).  Round k0 of wave w
             // covers hidden columns 4 k0 + w step .. + step - 1: the four waves' blocks of a round
-            // are adjacent, so each token row is read in runs of 4 step columns.
+            // are adjacent, so each token row is read in runs of 4 step columns.  Every A
+            // fragment serves the kShrinkPages token tiles.
             constexpr int KS = NT <= 2 ? 2 : 1;
             constexpr int step = 32 * KS;
-            auto load = [&](int k0, fkvk::u32x4 (&xa)[KS], fkvk::u32x4 (&bw)[KS][NT]) __attribute__((always_inline)) {
+            auto load = [&](int k0, fkvk::u32x4 (&xa)[KS][kShrinkPages], fkvk::u32x4 (&bw)[KS][NT]) __attribute__((always_inline)) {
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks) {
-                    xa[ks] = tok_ok ? fkvk::ldg128(xr + 4 * k0 + wave * step + 32 * ks) : fkvk::u32x4{0, 0, 0, 0};
+                    const int off = 4 * k0 + wave * step + 32 * ks;
 #pragma unroll
-                    for (int t = 0; t < NT; ++t) bw[ks][t] = fkvk::ldg128(ar[t] + 4 * k0 + wave * step + 32 * ks);
+                    for (int u = 0; u < kShrinkPages; ++u)
+                        xa[ks][u] = tok_ok[u] ? fkvk::ldg128(xr[u] + off) : fkvk::u32x4{0, 0, 0, 0};
+#pragma unroll
+                    for (int t = 0; t < NT; ++t) bw[ks][t] = fkvk::ldg128(ar[t] + off);
                 }
             };
-            auto products = [&](const fkvk::u32x4 (&xa)[KS], const fkvk::u32x4 (&bw)[KS][NT]) __attribute__((always_inline)) {
+            auto products = [&](const fkvk::u32x4 (&xa)[KS][kShrinkPages], const fkvk::u32x4 (&bw)[KS][NT]) __attribute__((always_inline)) {
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
                     for (int t = 0; t < NT; ++t) {
                         const fkvk::u32x4 w = rok[t] ? bw[ks][t] : fkvk::u32x4{0, 0, 0, 0};
-                        // C_K^T (ranks in rows), C_V (tokens in rows)
-                        acc[t] = t < RT ? fkvk::mfma32(w, xa[ks], acc[t]) : fkvk::mfma32(xa[ks], w, acc[t]);
+#pragma unroll
+                        for (int u = 0; u < kShrinkPages; ++u)  // C_K^T (ranks in rows), C_V (tokens in rows)
+                            acc[t][u] = t < RT ? fkvk::mfma32(w, xa[ks][u], acc[t][u]) : fkvk::mfma32(xa[ks][u], w, acc[t][u]);
                     }
             };
-            fkvk::u32x4 xa0[KS], bw0[KS][NT], xa1[KS], bw1[KS][NT];
+            fkvk::u32x4 xa0[KS][kShrinkPages], bw0[KS][NT], xa1[KS][kShrinkPages], bw1[KS][NT];
             load(0, xa0, bw0);
             for (int k0 = 0;;) {
                 load(min(k0 + step, quarter - step), xa1, bw1);
@@ -237,32 +249,39 @@ __global__ __launch_bounds__(256, 6) void produce_kernel(ProduceArgs a) {
             }
             if (wave > 0) {
 #pragma unroll
-                for (int t = 0; t < NT; ++t) s_part[wave - 1][t][lane] = acc[t];
+                for (int t = 0; t < NT; ++t)
+#pragma unroll
+                    for (int u = 0; u < kShrinkPages; ++u) s_part[wave - 1][t][u][lane] = acc[t][u];
             }
             __syncthreads();
             if (wave == 0) {
-                uint16_t *pg = a.res_kv + (int64_t)q.bt_res[pp] * res_page_elems(PS, R);
 #pragma unroll
-                for (int t = 0; t < NT; ++t) {
-                    fkvk::f32x4 c = acc[t];
+                for (int u = 0; u < kShrinkPages; ++u) {
+                    if (tj0[u] >= nq) continue;  // page past the sequence's range: its table entry is not read
+                    const int64_t pp = page0 + (int64_t)kShrinkPages * lb + u;
+                    uint16_t *pg = a.res_kv + (int64_t)q.bt_res[pp] * res_page_elems(PS, R);
 #pragma unroll
-                    for (int w = 0; w < 3; ++w) c += s_part[w][t][lane];
-                    const int kt = t % RT;
-                    const fkvk::u32x2 h4 = fkvk::u32x2{fkvk::pack_bf16(c[0], c[1]), fkvk::pack_bf16(c[2], c[3])};
-                    uint16_t *dst = pg + kt * 512 + (16 * grp + col) * 8;
-                    if (t < RT) {
-                        // C_K[token col][rank 16 kt + 4 grp + i] at dst[i]
-                        if (tok_ok && 16 * kt + 4 * grp < R) *reinterpret_cast<fkvk::u32x2 *>(dst) = h4;
-                    } else if (16 * kt + col < R) {
-                        // C_V[token 4 grp + i][rank 16 kt + col] at dst[4 + i]
-                        const int64_t tf = tj0 + 4 * grp;
-                        if (tf >= 0 && tf + 3 < nq) {
-                            *reinterpret_cast<fkvk::u32x2 *>(dst + 4) = h4;
-                        } else {
+                    for (int t = 0; t < NT; ++t) {
+                        fkvk::f32x4 c = acc[t][u];
 #pragma unroll
-                            for (int i = 0; i < 4; ++i)
-                                if (tf + i >= 0 && tf + i < nq)
-                                    dst[4 + i] = (uint16_t)((i & 1 ? h4[i >> 1] >> 16 : h4[i >> 1]) & 0xffffu);
+                        for (int w = 0; w < 3; ++w) c += s_part[w][t][u][lane];
+                        const int kt = t % RT;
+                        const fkvk::u32x2 h4 = fkvk::u32x2{fkvk::pack_bf16(c[0], c[1]), fkvk::pack_bf16(c[2], c[3])};
+                        uint16_t *dst = pg + kt * 512 + (16 * grp + col) * 8;
+                        if (t < RT) {
+                            // C_K[token col][rank 16 kt + 4 grp + i] at dst[i]
+                            if (tok_ok[u] && 16 * kt + 4 * grp < R) *reinterpret_cast<fkvk::u32x2 *>(dst) = h4;
+                        } else if (16 * kt + col < R) {
+                            // C_V[token 4 grp + i][rank 16 kt + col] at dst[4 + i]
+                            const int64_t tf = tj0[u] + 4 * grp;
+                            if (tf >= 0 && tf + 3 < nq) {
+                                *reinterpret_cast<fkvk::u32x2 *>(dst + 4) = h4;
+                            } else {
+#pragma unroll
+                                for (int i = 0; i < 4; ++i)
+                                    if (tf + i >= 0 && tf + i < nq)
+                                        dst[4 + i] = (uint16_t)((i & 1 ? h4[i >> 1] >> 16 : h4[i >> 1]) & 0xffffu);
+                            }
                         }
                     }
                 }
@@ -469,7 +488,7 @@ fkv_status fkv_produce_tokens_batch(const fkv_produce_seq *seqs, int32_t nseq, c
             o.n = (int32_t)q.n;
             o.first_shrink = (int32_t)n_shrink;
             o.first_base = (int32_t)n_base;  // offset by the shrink count below
-            if (o.lora_a) n_shrink += pages;
+            if (o.lora_a) n_shrink += (pages + kShrinkPages - 1) / kShrinkPages;
             n_base += pages * n_hg;
         }
         if (a.nseq == 0) continue;
