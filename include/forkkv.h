@@ -85,6 +85,25 @@ const char *fkv_version(void);
 /* indexes rCache pages.  Both are radix trees with one page per edge.        */
 /* ------------------------------------------------------------------------ */
 
+/* Determinism contract (both trees; block tables are therefore reproducible bit for bit):
+ *   - Matching: a fork walks the tree one page-sized chunk of its tokens at a time; at each
+ *     step it takes, among the current page's children in creation order, the child whose
+ *     stored tokens match the longest prefix of the chunk (the first such child on ties; a
+ *     child matching the whole chunk ends the search).  A whole-chunk match is inherited (a
+ *     final chunk shorter than a page may inherit a page that holds more tokens, read-only);
+ *     a match of k > 0 tokens short of the chunk makes that page the copy-on-write source of
+ *     k tokens for the next new page; the walk stops at the first page it does not inherit.
+ *   - Allocation: a pool hands out its lowest free page id.
+ *   - Recency: each tree has a clock; a page is stamped with the next tick when it is
+ *     created and whenever a sequence starts or stops referencing it.  A fork references its
+ *     inherited pages in path order, then pins the copy-on-write source, evicts if needed,
+ *     creates its new pages in order and unpins the source (base tree first, then the
+ *     residual tree).  An append that writes into its exclusively owned last page stamps it
+ *     twice; one that copies it creates the copy, then drops the old page.  A release drops
+ *     the pages from last to first.
+ *   - Eviction: when a pool has fewer free pages than a call needs, cached pages (referenced
+ *     by no sequence) without children are evicted oldest stamp first (lower page id on
+ *     ties), a parent becoming a candidate when its last child is evicted. */
 typedef struct fkv_tree fkv_tree;
 
 typedef struct {

@@ -231,6 +231,17 @@ def tree(name: str, seed: int, *, node_parent: Sequence[int], node_len: Sequence
                   ch, set(zero_residual), b_std, q_std=q_std)
 
 
+def explicit(name: str, seed: int, *, node_parent: Sequence[int], node_len: Sequence[int],
+             agent_node: Sequence[int], suffix: Sequence[int], hq: int, hkv: int, d: int = 128, r: int,
+             ps: int = 16, b_std: float = 0.02, zero_residual: Sequence[int] = (), q_std: float = 1.0) -> Workload:
+    """Agents on a fork tree with the given private suffix lengths (0 allowed: the agent's
+    context is its node path).  Agents fork in list order, so an agent whose context is a
+    prefix of an earlier agent's shares that agent's partly filled last page read-only."""
+    return _build(name, np.random.default_rng(seed), hq, hkv, d, r, ps, list(node_parent), list(node_len),
+                  list(agent_node), [int(s) for s in suffix], [0] * len(agent_node), set(zero_residual), b_std,
+                  q_std=q_std)
+
+
 def chain(name: str, seed: int, *, n_agents: int, root: int, step: int, suffix_lo: int, suffix_hi: int,
           hq: int, hkv: int, d: int = 128, r: int, ps: int = 16, b_std: float = 0.02,
           chunk: Sequence[int] = ()) -> Workload:

@@ -218,3 +218,62 @@ def test_sequential_fork_chain(rope):
     # segments hold 12, 11, ..., 1 agents (multi-group and single-group items, many splits)
     wl = W.chain("chain-12", 24, n_agents=12, root=700, step=100, suffix_lo=3, suffix_hi=70, hq=32, hkv=8, r=16)
     run_case(f"chain rope={rope}", wl, rope)
+
+
+def _single_key_value(wl, a):
+    """Closed form for a sequence of one key: softmax over one key is 1, so every query head
+    of KV head h returns that key's rebuilt value V[0] = V_base[0] + C_V[0] B_V (Eq. 4)."""
+    vb = W.bf16_bits_to_f64(wl.base_v[wl.base_row[a][0]])               # [hkv, d]
+    if wl.has_residual[a]:
+        cv = W.bf16_bits_to_f64(wl.c_v[a][0])                             # [r]
+        bv = W.bf16_bits_to_f64(wl.b_v[a]).reshape(wl.r, wl.hkv, wl.d)    # [r, hkv, d]
+        vb = vb + np.einsum("r,rhd->hd", cv, bv)
+    return np.repeat(vb, wl.hq // wl.hkv, axis=0)                         # [hq, d]
+
+
+def _check_single_keys(tag, wl, g):
+    agents = wl.decode_agents()
+    for i, a in enumerate(agents):
+        if int(wl.seq_len[a]) == 1:
+            err = np.abs(g[i] - _single_key_value(wl, a)).max()
+            print(f"[{tag}] agent {a} L=1: max |O - V[0]| {err:.3e}", flush=True)
+            assert err <= TOL_MAX, f"{tag}: agent {a} with one key does not return its value"
+
+
+SHORT_LENGTHS = [1, 2, 15, 16, 17, 5, 31, 33]
+
+
+@pytest.mark.parametrize("rope", [False, True])
+@pytest.mark.parametrize("hq,r", [(32, 16), (64, 64), (32, 8)])
+def test_sequences_shorter_than_a_page(rope, hq, r):
+    """Private contexts of 1, 2, 15, 16, 17, 5, 31 and 33 tokens (first-page masking, one
+    key, page boundaries); agent 5 has no residual.  Amplified adapters (C B ~ N(0, 1)) so
+    that the residual moves the output visibly even at one key."""
+    L = SHORT_LENGTHS
+    wl = W.explicit(f"short-private-hq{hq}-r{r}", 61, node_parent=[-1], node_len=[0], agent_node=[0] * len(L),
+                    suffix=L, hq=hq, hkv=8, r=r, b_std=1.0 / np.sqrt(r), zero_residual=[5])
+    assert list(wl.seq_len) == L
+    g, _ = run_case(f"short-private hq={hq} r={r} rope={rope}", wl, rope)
+    _check_single_keys(f"short-private hq={hq} r={r} rope={rope}", wl, g)
+
+
+@pytest.mark.parametrize("rope", [False, True])
+@pytest.mark.parametrize("r,item_agents", [(16, 0), (16, 1), (16, 4), (32, 0)])
+def test_shared_partial_page_mixed_lengths(rope, r, item_agents):
+    """One partly filled base page read by agents of 15, 5 and 1 tokens (forked longest
+    first, so the shorter ones share it read-only), siblings that copy it on fork (16 and
+    17 tokens), one agent without residual, one longer agent: a shared work item whose rows
+    end inside its only page."""
+    # node 0: 1 token, node 1: +4 (5 tokens), node 2: +10 (15 tokens)
+    agent_node = [2, 1, 0, 2, 2, 2, 1, 0, 2, 2]
+    suffix = [0, 0, 0, 0, 1, 2, 0, 0, 0, 40]
+    wl = W.explicit(f"short-shared-r{r}", 62, node_parent=[-1, 0, 1], node_len=[1, 4, 10], agent_node=agent_node,
+                    suffix=suffix, hq=32, hkv=8, r=r, b_std=1.0 / np.sqrt(r), zero_residual=[3])
+    assert list(wl.seq_len) == [15, 5, 1, 15, 16, 17, 5, 1, 15, 55]
+    lw = LoadedWorkload(wl, rope=rope)
+    bb, _, _ = lw.tree.block_tables(list(range(wl.n_agents)), lw.max_pages)
+    shared = [a for a in range(wl.n_agents) if bb[a][0] == bb[0][0]]
+    assert shared == [0, 1, 2, 3, 6, 7, 8], shared   # the read-only sharers of agent 0's first page
+    lw.close()
+    g, _ = run_case(f"short-shared r={r} items={item_agents} rope={rope}", wl, rope, item_agents=item_agents)
+    _check_single_keys(f"short-shared r={r} rope={rope}", wl, g)
