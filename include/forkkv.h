@@ -292,6 +292,18 @@ typedef struct {
  * launch fails. */
 fkv_status fkv_residual_attention_decode(const fkv_attn_args *args, const fkv_plan *plan, void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, serving loops
+ * or harnesses that forbid allocation): the same decode as fkv_residual_attention_decode, with
+ * the partial rows kept in a static device array of FKV_NOALLOC_WORKSPACE_BYTES that the library
+ * holds on each GPU it runs on (from its first use there until the process ends) instead of
+ * args->workspace, which is ignored.  The call allocates and frees nothing; the caller still
+ * owns every input and output.  Every call on one GPU shares that GPU's array and nothing in
+ * it needs to start at zero (each call writes every partial row it reads); calls that overlap
+ * on one GPU (on different streams) race.  Errors as fkv_residual_attention_decode, plus
+ * FKV_ERR_INVALID when the plan's partial rows (fkv_plan_info.workspace_bytes) exceed the array. */
+#define FKV_NOALLOC_WORKSPACE_BYTES (64u << 20)
+fkv_status fkv_residual_attention_decode_noalloc(const fkv_attn_args *args, const fkv_plan *plan, void *stream);
+
 /* Chunked prefill: agent a's query rows q_indptr[a] .. q_indptr[a+1]-1 are the
  * last n_a = q_indptr[a+1]-q_indptr[a] tokens of its sequence (already in the
  * cache); row i sits at position seq_len[a] - n_a + i and attends causally to

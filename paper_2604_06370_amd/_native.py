@@ -108,6 +108,9 @@ fkv_decode_plan_serialize = _sig("fkv_decode_plan_serialize", c_i32, [c_vp, c_vp
 fkv_decode_plan_segments = _sig("fkv_decode_plan_segments", c_i32, [c_vp, c_vp, c_vp, c_vp, c_vp, c_i64])
 fkv_residual_attention_decode = _sig("fkv_residual_attention_decode", c_i32,
                                      [ctypes.POINTER(fkv_attn_args), c_vp, c_vp])
+fkv_residual_attention_decode_noalloc = _sig("fkv_residual_attention_decode_noalloc", c_i32,
+                                             [ctypes.POINTER(fkv_attn_args), c_vp, c_vp])
+FKV_NOALLOC_WORKSPACE_BYTES = 64 << 20
 fkv_residual_attention_prefill = _sig("fkv_residual_attention_prefill", c_i32,
                                       [ctypes.POINTER(fkv_attn_args), c_vp])
 fkv_rope_table = _sig("fkv_rope_table", c_i32, [c_i32, c_i32, c_f64, c_vp, c_vp])

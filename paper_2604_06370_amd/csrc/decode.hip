@@ -31,6 +31,8 @@
 
 #include <algorithm>
 #include <cmath>
+#include <mutex>
+#include <string>
 #include <type_traits>
 
 #include "internal.hpp"
@@ -1117,11 +1119,15 @@ fkv_status validate_attn_common(const fkv_attn_args *a, const char *who);
 int64_t plan_max_pages(const fkv_plan *plan);
 }  // namespace fkv
 
-extern "C" fkv_status fkv_residual_attention_decode(const fkv_attn_args *a, const fkv_plan *plan, void *stream) {
-    fkv::clear_error();
+namespace {
+
+// Both decode entry points: checks, then the split and merge launches with the partial rows
+// in `workspace` (`workspace_bytes` long).
+fkv_status decode_impl(const fkv_attn_args *a, const fkv_plan *plan, void *stream, void *workspace,
+                       size_t workspace_bytes) {
     fkv_status st = fkv::validate_attn_common(a, "fkv_residual_attention_decode");
     if (st != FKV_OK) return st;
-    if (!plan || !a->plan || !a->workspace)
+    if (!plan || !a->plan || !workspace)
         return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: plan (host and device copy) and workspace are required");
     const auto &w = plan->words;
     const int g = a->hq / a->hkv;
@@ -1129,7 +1135,7 @@ extern "C" fkv_status fkv_residual_attention_decode(const fkv_attn_args *a, cons
         return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: plan was built for other n_agents / heads");
     fkv_plan_info info;
     fkv_decode_plan_info(plan, a->d, a->r, &info);
-    if ((int64_t)a->workspace_bytes < info.workspace_bytes)
+    if ((int64_t)workspace_bytes < info.workspace_bytes)
         return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: workspace too small");
     if (a->rope_cos && (int64_t)a->rope_max_pos < fkv::plan_max_pages(plan) * a->page_size)
         return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: RoPE table shorter than the longest sequence");
@@ -1161,7 +1167,7 @@ extern "C" fkv_status fkv_residual_attention_decode(const fkv_attn_args *a, cons
     da.rope_cos = a->rope_cos;
     da.rope_sin = a->rope_sin;
     da.plan = a->plan;
-    da.ws = static_cast<float *>(a->workspace);
+    da.ws = static_cast<float *>(workspace);
     da.out = static_cast<uint16_t *>(a->out);
     da.hq = a->hq;
     da.hkv = a->hkv;
@@ -1173,7 +1179,6 @@ extern "C" fkv_status fkv_residual_attention_decode(const fkv_attn_args *a, cons
     da.off_zero = w[fkv::H_OFF_ZERO];
     da.off_desc = w[fkv::H_OFF_DESC];
     da.scale_log2 = a->scale * 1.4426950408889634f;
-    // grid-barrier words: the 256 bytes after the partial rows (see fkv_decode_plan_info)
     da.ws_bytes = fkv::decode_partials_bytes(plan, a->d, a->r);
     if (da.ws_bytes >= 0x7fffffff)
         return fkv::fail(FKV_ERR_UNSUPPORTED, "fkv_residual_attention_decode: partial rows above 2 GiB");
@@ -1186,4 +1191,59 @@ extern "C" fkv_status fkv_residual_attention_decode(const fkv_attn_args *a, cons
     if (e != hipSuccess)
         return fkv::fail(FKV_ERR_HIP, std::string("fkv_residual_attention_decode: launch failed: ") + hipGetErrorString(e));
     return FKV_OK;
+}
+
+// Partial rows of fkv_residual_attention_decode_noalloc: one array per GPU, held from the
+// library's first use on that GPU until the process ends.  Host code never passes the
+// array's name to a kernel (on the host it names a stand-in, not device memory): each
+// device's address comes from hipGetSymbolAddress with that device current.
+constexpr size_t kNoAllocBytes = FKV_NOALLOC_WORKSPACE_BYTES;
+__device__ __attribute__((aligned(256))) unsigned char scratch[kNoAllocBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_addr[kMaxDevices] = {};
+
+fkv_status scratch_address(void **out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return fkv::fail(FKV_ERR_HIP, std::string("fkv_residual_attention_decode_noalloc: hipGetDevice: ") + hipGetErrorString(e));
+    if (dev < 0 || dev >= kMaxDevices)
+        return fkv::fail(FKV_ERR_UNSUPPORTED, "fkv_residual_attention_decode_noalloc: device index above 63");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_addr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fkv::fail(FKV_ERR_HIP, std::string("fkv_residual_attention_decode_noalloc: hipGetSymbolAddress: ") +
+                                              hipGetErrorString(e));
+        g_scratch_addr[dev] = p;
+    }
+    *out = g_scratch_addr[dev];
+    return FKV_OK;
+}
+
+}  // namespace
+
+extern "C" fkv_status fkv_residual_attention_decode(const fkv_attn_args *a, const fkv_plan *plan, void *stream) {
+    fkv::clear_error();
+    if (!a) return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: null args");
+    return decode_impl(a, plan, stream, a->workspace, a->workspace_bytes);
+}
+
+extern "C" fkv_status fkv_residual_attention_decode_noalloc(const fkv_attn_args *a, const fkv_plan *plan, void *stream) {
+    fkv::clear_error();
+    if (!a || !plan) return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode_noalloc: null argument");
+    fkv_plan_info info;
+    fkv_status st = fkv_decode_plan_info(plan, a->d, a->r, &info);
+    if (st != FKV_OK) return st;
+    if (info.workspace_bytes > (int64_t)kNoAllocBytes)
+        return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode_noalloc: the plan's partial rows (" +
+                                              std::to_string(info.workspace_bytes) + " bytes) exceed the " +
+                                              std::to_string(kNoAllocBytes) + "-byte static workspace");
+    void *ws = nullptr;
+    st = scratch_address(&ws);
+    if (st != FKV_OK) return st;
+    return decode_impl(a, plan, stream, ws, kNoAllocBytes);
 }

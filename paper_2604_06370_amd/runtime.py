@@ -297,6 +297,12 @@ def residual_attention_decode(args: N.fkv_attn_args, plan: DecodePlan, stream=No
           "fkv_residual_attention_decode")
 
 
+def residual_attention_decode_noalloc(args: N.fkv_attn_args, plan: DecodePlan, stream=None) -> None:
+    """fkv_residual_attention_decode_noalloc: args.workspace is ignored (static per-GPU array)."""
+    check(N.fkv_residual_attention_decode_noalloc(ctypes.byref(args), plan.handle, _stream(stream)),
+          "fkv_residual_attention_decode_noalloc")
+
+
 def residual_attention_prefill(args: N.fkv_attn_args, stream=None) -> None:
     check(N.fkv_residual_attention_prefill(ctypes.byref(args), _stream(stream)), "fkv_residual_attention_prefill")
 

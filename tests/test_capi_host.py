@@ -364,3 +364,20 @@ def test_decode_plan_items_cover_every_agent_page_once(hq, hkv, r, rope, pps):
         partials = h["total_rows"] * hkv * ((128 + r + 2 + 3) // 4 * 4) * 4
         assert info["workspace_bytes"] == (partials + 255) // 256 * 256
         plan.close()
+
+
+def test_noalloc_decode_rejects_plans_beyond_its_static_workspace():
+    """Checked on the host before any device call: a plan whose partial rows exceed the
+    static array is refused with FKV_ERR_INVALID."""
+    A, mp, ps = 16, 320, 16
+    bb = np.arange(A * mp, dtype=np.int32).reshape(A, mp)      # nothing shared: private items only
+    sl = np.full(A, mp * ps, dtype=np.int32)
+    plan = rt.DecodePlan(bb, sl, 32, 8, ps, pages_per_split=4, r=16, rope=False, res_bt=bb,
+                         adapter_idx=np.arange(A, dtype=np.int32))
+    need = plan.info(128, 16)["workspace_bytes"]
+    assert need > N.FKV_NOALLOC_WORKSPACE_BYTES
+    args = N.fkv_attn_args()
+    args.n_agents, args.hq, args.hkv, args.d, args.r, args.page_size, args.max_pages = A, 32, 8, 128, 16, ps, mp
+    with pytest.raises(rt.FKVError) as e:
+        rt.residual_attention_decode_noalloc(args, plan, 0)
+    assert e.value.code == N.FKV_ERR_INVALID and "static workspace" in str(e.value)
