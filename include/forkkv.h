@@ -207,6 +207,9 @@ typedef struct {
                                  (fkv_decode_plan_default_agents); larger values are clamped */
     int32_t r;                /* residual rank the plan will be run with (0, 8, 16, 32, 64) */
     int32_t rope;             /* nonzero: the plan will be run with RoPE tables */
+    int32_t reserve_pages;    /* growth room of each agent, in pages past its current last page (as far
+                                 as max_pages allows): the plan stays valid while the agent's length
+                                 grows into it.  0 = 16 pages; negative = none */
 } fkv_decode_plan_params;
 
 typedef struct {
@@ -224,17 +227,30 @@ typedef struct {
  * head layout. */
 int32_t fkv_decode_plan_default_agents(int32_t hq, int32_t hkv, int32_t r, int32_t rope);
 
-/* Build a plan from host copies of the decode call's tables: base_bt and res_bt
- * [n_agents][max_pages], seq_lens and adapter_idx [n_agents] (res_bt and adapter_idx may be
- * NULL when r == 0 or RoPE is on).  Without RoPE the plan holds, per workgroup of the split
- * kernel, the page ids, sequence lengths and adapters it reads, so the plan must be rebuilt
- * whenever any of these tables changes (in a serving loop: every decode step).
- * Errors: FKV_ERR_INVALID for null or inconsistent arguments, FKV_ERR_UNSUPPORTED for
- * head layouts or ranks the kernels do not take. */
+/* Build a plan from host copies of the decode call's base block table base_bt
+ * [n_agents][max_pages] and seq_lens [n_agents] (res_bt and adapter_idx are not read and may
+ * be NULL).  The plan records which agents share which base pages (the segments) and how the
+ * work is cut into items and workgroups; it holds no page id, length or adapter: the kernels
+ * read those from the launch's block tables, seq_lens and adapter_idx.  So one plan serves
+ * consecutive decode steps while
+ *   - every agent's length stays within its capacity (fkv_decode_plan_covers checks this;
+ *     each agent's last item reads up to reserve_pages further pages as the agent grows), and
+ *   - the sharing structure is unchanged: no agent forked, released or replaced, and no
+ *     page of the agents' existing block-table entries replaced (a copy-on-write copy reported
+ *     by fkv_fork / fkv_cow_append for one of them; new entries past an agent's last page are
+ *     fine).
+ * Otherwise build a new plan.  Errors: FKV_ERR_INVALID for null or inconsistent arguments,
+ * FKV_ERR_UNSUPPORTED for head layouts or ranks the kernels do not take. */
 fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *params, const int32_t *base_bt,
                                   const int32_t *res_bt, const int32_t *seq_lens, const int32_t *adapter_idx,
                                   fkv_plan **out);
 void fkv_decode_plan_destroy(fkv_plan *plan);
+/* FKV_OK if host seq_lens [n_agents] (n_agents as at creation) are all >= 1 and within the
+ * plan's capacity; FKV_ERR_INVALID naming the first agent that outgrew it otherwise (build a
+ * new plan).  O(n_agents), allocates nothing. */
+fkv_status fkv_decode_plan_covers(const fkv_plan *plan, const int32_t *seq_lens, int32_t n_agents);
+/* Largest length agent a may reach under this plan (host output). */
+fkv_status fkv_decode_plan_capacity(const fkv_plan *plan, int32_t agent, int64_t *max_len);
 /* Sizes of the plan; workspace_bytes is computed for head dim d and rank r. */
 fkv_status fkv_decode_plan_info(const fkv_plan *plan, int32_t d, int32_t r, fkv_plan_info *out);
 /* Write the serialised plan (plan_words int32) to a host buffer; the caller copies
@@ -281,9 +297,11 @@ typedef struct {
 /* Decode: one query row per agent attends to all seq_len keys of its agent
  * (the current token's K/V/C is already in the cache).  Section 5.3,
  * Algorithm 1, split over the plan's work items with a log-sum-exp combine.
- * `plan` is the host plan whose serialised copy args->plan points to (grid size
- * and workspace size are taken from it); the block tables and sequence lengths
- * in args must be the ones the plan was built from.
+ * `plan` is the host plan whose serialised copy args->plan points to: the grid and workspace
+ * sizes come from it on the host, so the launch needs no read of device memory.  The block
+ * tables, seq_lens and adapter_idx in args are read by the kernels; they must keep the sharing
+ * structure the plan was built from and the lengths within its capacity (see
+ * fkv_decode_plan_create; a length past the capacity leaves those keys out of the result).
  * Supported: d = 128, page_size = 16, r in {0, 8, 16, 32, 64}, hq/hkv in {4, 8}.  The plan must
  * have been built for the same r and RoPE setting (FKV_ERR_INVALID otherwise), so that its work
  * items hold no more agents than fkv_decode_plan_default_agents allows.

@@ -63,7 +63,7 @@ class fkv_pool_stats(ctypes.Structure):
 class fkv_decode_plan_params(ctypes.Structure):
     _fields_ = [("n_agents", c_i32), ("hq", c_i32), ("hkv", c_i32), ("page_size", c_i32), ("max_pages", c_i32),
                 ("pages_per_split", c_i32), ("num_cus", c_i32), ("max_item_agents", c_i32), ("r", c_i32),
-                ("rope", c_i32)]
+                ("rope", c_i32), ("reserve_pages", c_i32)]
 
 
 class fkv_plan_info(ctypes.Structure):
@@ -103,6 +103,8 @@ fkv_decode_plan_create = _sig("fkv_decode_plan_create", c_i32,
                               [ctypes.POINTER(fkv_decode_plan_params), c_vp, c_vp, c_vp, c_vp, ctypes.POINTER(c_vp)])
 fkv_decode_plan_default_agents = _sig("fkv_decode_plan_default_agents", c_i32, [c_i32, c_i32, c_i32, c_i32])
 fkv_decode_plan_destroy = _sig("fkv_decode_plan_destroy", None, [c_vp])
+fkv_decode_plan_covers = _sig("fkv_decode_plan_covers", c_i32, [c_vp, c_vp, c_i32])
+fkv_decode_plan_capacity = _sig("fkv_decode_plan_capacity", c_i32, [c_vp, c_i32, ctypes.POINTER(c_i64)])
 fkv_decode_plan_info = _sig("fkv_decode_plan_info", c_i32, [c_vp, c_i32, c_i32, ctypes.POINTER(fkv_plan_info)])
 fkv_decode_plan_serialize = _sig("fkv_decode_plan_serialize", c_i32, [c_vp, c_vp, c_i64])
 fkv_decode_plan_segments = _sig("fkv_decode_plan_segments", c_i32, [c_vp, c_vp, c_vp, c_vp, c_vp, c_i64])

@@ -264,21 +264,19 @@ __device__ __forceinline__ void split_body(const DecodeArgs &p) {
     };
     __shared__ __attribute__((aligned(16))) u32x4 lds_ring[kRing * kStageBytes / 16];
 
-    // The block's descriptor holds everything the prologue needs (page range, head, every
-    // slot's agent, length, adapter and first partial, the base page ids and each slot's
-    // rCache page ids), at an address that depends on blockIdx only: one round of
-    // independent loads, after which the first base pages, rCache rows, queries and B_K
-    // slices are all requested together.
+    // The block's descriptor (at an address that depends on blockIdx only) names the item:
+    // page range start and capacity, KV head, the agent whose base block-table row names the
+    // item's pages, every slot's agent and first partial.  Page ids, sequence lengths and
+    // adapters come from the launch's own tables in the next round of loads, after which the
+    // first base pages, rCache rows, queries and B_K slices are all requested together.
     const int32_t *desc = p.plan + p.off_desc + (int64_t)blockIdx.x * fkv::kDescWords;
-    const int pg0 = desc[fkv::kDescPg0], pg1 = desc[fkv::kDescPg1], nag = desc[fkv::kDescNag];
-    const int h = desc[fkv::kDescHead];
-    const int item_max_len = desc[fkv::kDescMaxLen];
-    const int rstride = desc[fkv::kDescResStride];  // page ids per slot row of the residual table
-    const int npg = pg1 - pg0;
+    const int pg0 = desc[fkv::kDescPg0], pgcap = desc[fkv::kDescCap], nag = desc[fkv::kDescNag];
+    const int h = desc[fkv::kDescHead], leader = desc[fkv::kDescLeader];
+    const int npcap = pgcap - pg0;
     const int hkv = p.hkv;
     const int ng = (nag + AG - 1) / AG;
-    if (nag <= 0 || npg <= 0 || nag > S::MAX_SLOTS || (ng > 1 && !S::MULTI) || (ng == 1 && nag > NSW) ||
-        npg > (ng > 2 ? fkv::kMaxPagesMulti : fkv::kMaxPagesSingle) || (ng > 2 ? rstride != 64 : rstride != 128))
+    if (nag <= 0 || npcap <= 0 || nag > S::MAX_SLOTS || (ng > 1 && !S::MULTI) || (ng == 1 && nag > NSW) ||
+        npcap > (ng > 2 ? fkv::kMaxPagesMulti : fkv::kMaxPagesSingle))
         return;  // idle block, or rejected on the host
     const int ngp = ng == 1 ? 1 : (ng == 2 ? 2 : 4);   // groups rounded to a divisor of 4
 
@@ -293,24 +291,32 @@ __device__ __forceinline__ void split_body(const DecodeArgs &p) {
     const int qh = h * G + (col % G);
     const int64_t n = (int64_t)hkv * D;
 
-    // lane i < nag of every wave holds item slot i: agent, sequence length, adapter, first
-    // partial; lane i (and 64 + i) holds the base page id of item page i and, per slot s
-    // of this wave's group, that slot's rCache page id (-1: no adapter)
+    // lane i < nag of every wave holds item slot i: agent and first partial (plan), sequence
+    // length and adapter (launch arrays); lane i (and 64 + i) holds the base page id of item
+    // page i (the leader's row) and, per slot s of this wave's group, that slot's rCache page
+    // id (-1: no adapter).  Entries past the capacity repeat the last one.
     const bool lane_ag = lane < nag;
     const int l_agent = lane_ag ? desc[fkv::kDescAgent + lane] : 0;
-    const int l_len = lane_ag ? desc[fkv::kDescLen + lane] : 0;
-    const int l_ad = (R > 0 && lane_ag) ? desc[fkv::kDescAdapter + lane] : -1;
     const int l_part = lane_ag ? desc[fkv::kDescPart + lane] : 0;
-    const int bid0 = desc[fkv::kDescBase + min(lane, npg - 1)];
-    const int bid1 = desc[fkv::kDescBase + min(64 + lane, npg - 1)];
+    const int l_len = lane_ag ? p.seq_lens[l_agent] : 0;
+    const int l_ad = (R > 0 && lane_ag) ? p.adapter_idx[l_agent] : -1;
+    const int32_t *brow = p.base_bt + (int64_t)leader * p.max_pages + pg0;
+    const int bid0 = brow[min(lane, npcap - 1)];
+    const int bid1 = brow[min(64 + lane, npcap - 1)];
     int rid0[NSR], rid1[NSR];
 #pragma unroll
     for (int s = 0; s < NSR; ++s) {
         const bool ok = R > 0 && s < NSW && sb + s < nag;
-        const int32_t *row = desc + fkv::kDescRes + (ok ? sb + s : 0) * rstride;
-        rid0[s] = ok ? row[min(lane, npg - 1)] : -1;
-        rid1[s] = (ok && rstride > 64) ? row[min(64 + lane, npg - 1)] : -1;
+        const int ag_s = __builtin_amdgcn_readlane(l_agent, (sb + s) & 63);
+        const int32_t *row = p.res_bt + (int64_t)(ok ? ag_s : 0) * p.max_pages + pg0;
+        rid0[s] = ok ? row[min(lane, npcap - 1)] : -1;
+        rid1[s] = (ok && npcap > 64) ? row[min(64 + lane, npcap - 1)] : -1;
     }
+    // the item's longest sequence bounds the pages it reads (up to its capacity)
+    int item_max_len = 0;
+    for (int s = 0; s < nag; ++s) item_max_len = max(item_max_len, __builtin_amdgcn_readlane(l_len, s));
+    const int npg = min(pgcap, (item_max_len + PS - 1) / PS) - pg0;
+    const int pg1 = pg0 + max(npg, 0);
     // device address of the K block of (item page k, head h); V follows hkv blocks later.
     // Pages past the item repeat its last page, so loads issued ahead of the end stay valid.
     // (both table halves are read and the half is chosen on the scalar unit: no branch and
@@ -343,12 +349,20 @@ __device__ __forceinline__ void split_body(const DecodeArgs &p) {
         slot_len[s] = ok ? len : 0;
         if (ok) min_len = min(min_len, len);
         if (ok && slot_ad[s] >= 0) min_res = min(min_res, len);
+        if (slot_ad[s] < 0) rid0[s] = rid1[s] = -1;   // no adapter: the zero area
     }
     const int src_lane = (sb + my_slot) & 63;
     const int sh_agent = __shfl(l_agent, src_lane), sh_len = __shfl(l_len, src_lane);
     const int my_part = __shfl(l_part, src_lane) + copy;  // this lane's row's partial
     const int my_agent = row_active ? sh_agent : 0;
     const int my_len = row_active ? sh_len : 0;
+    const int64_t my_row = ((int64_t)my_part * G + col % G) * hkv + h;
+    if (npg <= 0) {  // the item's agents have not reached it yet: an empty partial (weight 0)
+        Rows<R> empty;
+        empty.init();
+        write_partial<R>(p, empty, row_active, my_row, grp);
+        return;
+    }
 
     // Query fragments and W = B_K q.  Their loads are issued after the first base pages
     // and rCache rows have been requested (each pipeline below calls this right after its
@@ -727,7 +741,7 @@ __device__ __forceinline__ void split_body(const DecodeArgs &p) {
         else run2(NSF{});
     }
 
-    write_partial<R>(p, st, row_active, ((int64_t)my_part * G + col % G) * hkv + h, grp);
+    write_partial<R>(p, st, row_active, my_row, grp);
 }
 
 template <int R, int G>
@@ -769,9 +783,10 @@ __global__ __launch_bounds__(256, 1) void decode_rope_kernel(DecodeArgs p) {
     const int item = blk / hkv;
     const int h = blk - item * hkv;
     const int32_t *rec = plan + p.off_items + item * fkv::kItemWords;
-    const int pg0 = rec[0], pg1 = rec[1], leader = rec[2], nag = rec[3];
-    const int32_t *item_agents = rec + 5;
-    if (nag > AG || pg1 - pg0 > kMaxPagesPerItem) return;  // rejected on the host
+    const int pg0 = rec[fkv::kItemP0], pgcap = rec[fkv::kItemCap], leader = rec[fkv::kItemLeader];
+    const int nag = rec[fkv::kItemNag];
+    const int32_t *item_agents = rec + fkv::kItemAgents;
+    if (nag > AG || pgcap - pg0 > kMaxPagesPerItem) return;  // rejected on the host
 
     const int lane = threadIdx.x & 63;
     const int wave = uniform(threadIdx.x >> 6);
@@ -779,9 +794,21 @@ __global__ __launch_bounds__(256, 1) void decode_rope_kernel(DecodeArgs p) {
     const int my_slot_l = col / G;
     const bool row_active = my_slot_l < nag;
     const int my_agent = row_active ? item_agents[my_slot_l] : 0;
-    const int my_part = row_active ? item_agents[fkv::kMaxItemAgents + my_slot_l] + wave : 0;  // wave = copy
+    const int my_part = row_active ? rec[fkv::kItemFirst + my_slot_l] + wave : 0;  // wave = copy
     const int qh = h * G + (col % G);
 
+    // lengths and adapters from the launch arrays; the longest sequence bounds the pages
+    int res_len[AG];
+    int max_len = 0;
+#pragma unroll
+    for (int s = 0; s < AG; ++s) {
+        const bool ok = s < nag;
+        const int ag_id = ok ? item_agents[s] : 0;
+        const int len = ok ? p.seq_lens[ag_id] : 0;
+        res_len[s] = (ok && p.adapter_idx[ag_id] >= 0) ? len : 0;
+        max_len = max(max_len, len);
+    }
+    const int pg1 = max(pg0, min(pgcap, (max_len + PS - 1) / PS));
     const int npg = pg1 - pg0;
     for (int idx = threadIdx.x; idx < (1 + nag) * npg; idx += 256) {
         const int t = idx / npg, i = idx - t * npg;
@@ -794,16 +821,6 @@ __global__ __launch_bounds__(256, 1) void decode_rope_kernel(DecodeArgs p) {
             v = p.adapter_idx[ag_id] >= 0 ? rp : 0;
         }
         s_tab[t * kMaxPagesPerItem + i] = v;
-    }
-    int res_len[AG];
-    int max_len = 0;
-#pragma unroll
-    for (int s = 0; s < AG; ++s) {
-        const bool ok = s < nag;
-        const int ag_id = ok ? item_agents[s] : 0;
-        const int len = ok ? p.seq_lens[ag_id] : 0;
-        res_len[s] = (ok && p.adapter_idx[ag_id] >= 0) ? len : 0;
-        max_len = max(max_len, len);
     }
     const int my_len = row_active ? p.seq_lens[my_agent] : 0;
     u32x4 qf[4];
@@ -1137,6 +1154,9 @@ fkv_status decode_impl(const fkv_attn_args *a, const fkv_plan *plan, void *strea
     fkv_decode_plan_info(plan, a->d, a->r, &info);
     if ((int64_t)workspace_bytes < info.workspace_bytes)
         return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: workspace too small");
+    if (a->max_pages < fkv::plan_max_pages(plan))
+        return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: block-table rows shorter than the plan's "
+                                          "page capacity");
     if (a->rope_cos && (int64_t)a->rope_max_pos < fkv::plan_max_pages(plan) * a->page_size)
         return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: RoPE table shorter than the longest sequence");
     if (g != 4 && g != 8)

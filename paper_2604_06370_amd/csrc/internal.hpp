@@ -15,8 +15,12 @@ void clear_error();
 
 // Decode plan, host side.  Serialised layout (all int32):
 //   header[kHeaderWords]
-//   items   [n_items][kItemWords]  {page_begin, page_end, leader, n_ag, copies, agent[16],
-//                                   partial[16]}  (partial[j] + c: partial of slot j, copy c)
+//   items   [n_items][kItemWords]  {page_begin, page_cap, leader, n_ag, copies, page_end_at_plan,
+//                                   agent[16], partial[16]}  (partial[j] + c: partial of slot j,
+//                                   copy c).  The item covers pages page_begin .. min(page_cap,
+//                                   ceil(longest length / ps)) - 1 of its agents, the length read
+//                                   from the device array at launch, so an item whose agent grows
+//                                   reads the new pages (up to page_cap) without a new plan.
 //   blocks  [n_blocks]             item * (hkv / H) + head block, or -1 for an idle block
 //                                  (H = heads per block, header word H_HEADS_PER_BLOCK)
 //   agent_ptr [n_agents+1]         agent a owns partials agent_ptr[a] .. agent_ptr[a+1]-1; query
@@ -25,40 +29,39 @@ void clear_error();
 //   (header word H_OFF_AGENT_SLOT is unused and equals H_OFF_ZERO)
 //   zero      [kZeroWords]         zeros, 16-byte aligned (read in place of the rCache of an
 //                                  agent without adapter or of an empty agent slot)
+//   descriptors [n_blocks][kDescWords]  (RoPE-off plans) see below
 // An item holds up to four agent groups; a group is the floor(16/g) agents whose
 // query heads of one KV head fill the 16 rows of one matrix-core tile.  An item of
 // ng groups runs on 4 / ngp wave copies (ngp = 1, 2, 4 for ng = 1, 2, 3..4); every
 // copy writes its own partial, so the item owns copies * n_ag partials (g rows each).
+// The plan holds no page id, sequence length or adapter: the kernels read them from the
+// block tables, seq_lens and adapter_idx of the launch.
 constexpr int kHeaderWords = 24;
 constexpr int kMaxRows = 16;        // query rows of one agent group (one wave's row tile)
 constexpr int kMaxGroups = 4;       // agent groups per item (one wave each)
 constexpr int kMaxItemAgents = 16;  // agents per item
-constexpr int kItemWords = 5 + 2 * kMaxItemAgents;
+enum ItemField { kItemP0 = 0, kItemCap, kItemLeader, kItemNag, kItemCopies, kItemEnd, kItemAgents };
+constexpr int kItemFirst = kItemAgents + kMaxItemAgents;
+constexpr int kItemWords = kItemFirst + kMaxItemAgents;
 constexpr int kMaxPagesPerItem = 64;  // upper bound of pages_per_split (block tables are staged in LDS)
 // RoPE-off plans: item page limits of the split kernel, whose page ids travel in lane
 // registers (two per table row: lanes 0..63 and 64..127)
 constexpr int kMaxPagesMulti = 64;    // items of three or four agent groups
 constexpr int kMaxPagesSingle = 128;  // items of one or two agent groups
+constexpr int kDefaultReservePages = 16;  // growth room of an agent's last item (decode steps)
 
 // Block descriptors (RoPE-off plans): block b of the split kernel reads the
 // kDescWords words at off_desc + b * kDescWords:
-//   [kDescPg0, kDescPg1)  item page range        kDescNag   agents in the item (0: idle block)
-//   kDescHead             KV head                kDescMaxLen longest sequence of the item
-//   kDescResStride        row stride of the rCache page-id table (64 for three or four
-//                         agent groups, else 128)
-//   kDescAgent/Len/Adapter/Part + slot   agent, sequence length, adapter (-1: none) and
-//                         first partial of each item slot
-//   kDescBase + i         base page id of item page i (the pages every agent shares)
-//   kDescRes + s * stride + i   rCache page id of slot s at item page i (-1: no adapter)
-enum DescField { kDescPg0 = 0, kDescPg1, kDescNag, kDescHead, kDescMaxLen, kDescResStride, kDescItem, kDescCopies };
+//   kDescPg0, kDescCap    item page range start and capacity end (pages read: up to
+//                         min(cap, ceil(longest length / ps)))
+//   kDescNag              agents in the item (0: idle block)    kDescHead  KV head
+//   kDescLeader           agent whose base block-table row names the item's pages
+//   kDescItem, kDescCopies
+//   kDescAgent + slot, kDescPart + slot   agent and first partial of each item slot
+enum DescField { kDescPg0 = 0, kDescCap, kDescNag, kDescHead, kDescLeader, kDescItem, kDescCopies };
 constexpr int kDescAgent = 8;
-constexpr int kDescLen = kDescAgent + kMaxItemAgents;
-constexpr int kDescAdapter = kDescLen + kMaxItemAgents;
-constexpr int kDescPart = kDescAdapter + kMaxItemAgents;
-constexpr int kDescBase = kDescPart + kMaxItemAgents;
-constexpr int kDescRes = kDescBase + kMaxPagesSingle;
-constexpr int kDescResWords = kMaxItemAgents * kMaxPagesMulti;  // = 8 slots x 128 pages as well
-constexpr int kDescWords = kDescRes + kDescResWords;
+constexpr int kDescPart = kDescAgent + kMaxItemAgents;
+constexpr int kDescWords = kDescPart + kMaxItemAgents;
 
 // Decode: one workgroup per (work item, KV head).  Without RoPE and with rank below 32 an
 // item holds up to four agent groups (their base pages are shared through LDS); with
@@ -104,6 +107,7 @@ int64_t decode_partials_bytes(const fkv_plan *plan, int32_t d, int32_t r);
 struct fkv_plan {
     std::vector<int32_t> words;
     std::vector<int32_t> seg_first_page, seg_n_pages, seg_agent_off, seg_agents;
-    int32_t hkv = 0, g = 0, n_agents = 0;
-    int32_t max_pages_used = 0;  // longest sequence, in pages
+    std::vector<int32_t> cap_pages;  // per agent: pages its items can read (length capacity / ps)
+    int32_t hkv = 0, g = 0, n_agents = 0, page_size = 0, max_pages = 0;
+    int32_t max_pages_used = 0;  // largest page capacity of any agent
 };

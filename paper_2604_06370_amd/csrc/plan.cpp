@@ -16,6 +16,7 @@
 #include <cmath>
 #include <functional>
 #include <queue>
+#include <string>
 #include <unordered_map>
 
 #include "internal.hpp"
@@ -35,9 +36,8 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
                                   fkv_plan **out) {
     fkv::clear_error();
     if (!prm || !base_bt || !seq_lens || !out) return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: null argument");
-    if (prm->r > 0 && prm->rope == 0 && (!res_bt || !adapter_idx))
-        return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: res_bt and adapter_idx are required for r > 0 "
-                                          "without RoPE");
+    (void)res_bt;  // page ids, lengths and adapters are read by the kernels at launch
+    (void)adapter_idx;
     const int32_t A = prm->n_agents, ps = prm->page_size, mp = prm->max_pages;
     if (A < 1 || prm->hkv < 1 || prm->hq < 1 || ps < 1 || mp < 1 || prm->pages_per_split < 0)
         return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: bad sizes");
@@ -218,7 +218,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     // 4. work items, clustered by (segment, split).  An item of ng agent groups runs its
     //    groups on 4 / ngp wave copies (ngp = ng rounded up to 1, 2 or 4), each writing its
     //    own partial rows: rows = copies * agents * g.
-    struct Item { int32_t p0, p1, copies; double cost; std::vector<int32_t> agents; };
+    struct Item { int32_t p0, p1, cap, copies; double cost; std::vector<int32_t> agents; };
     std::vector<Item> items;
     std::vector<std::pair<int32_t, int32_t>> clusters;  // [first item, item count)
     std::vector<double> cluster_cost;
@@ -237,7 +237,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
             for (size_t c : chunks) {
                 const int32_t ng = (int32_t)((c + ag - 1) / ag);
                 const int32_t ngp = ng == 1 ? 1 : (ng == 2 ? 2 : 4);
-                Item it{p0, p1, fkv::kMaxGroups / ngp, 0.0, {}};
+                Item it{p0, p1, p1, fkv::kMaxGroups / ngp, 0.0, {}};
                 for (size_t j = k; j < k + c; ++j) it.agents.push_back(s.agents[j]);
                 k += c;
                 total_rows += (int64_t)it.copies * (int64_t)c * g;
@@ -249,6 +249,35 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
             cluster_cost.push_back(cost);
         }
     }
+    // 4b. growth room for decode steps: each agent's last item may read up to `reserve` more
+    //     pages (as far as its block-table row reaches) when the agent's length grows, so the
+    //     plan stays valid while agents append tokens.  A last item that is the agent's alone
+    //     and has room under its page limit is extended; otherwise the agent gets a tail item
+    //     of its own that starts empty.
+    const int32_t reserve = prm->reserve_pages == 0 ? fkv::kDefaultReservePages : std::max<int32_t>(0, prm->reserve_pages);
+    std::vector<int32_t> last_item(A, -1);
+    for (size_t i = 0; i < items.size(); ++i)
+        for (int32_t a : items[i].agents)
+            if (items[i].p1 == npages[a]) last_item[a] = (int32_t)i;
+    std::vector<int32_t> cap_pages(npages);
+    for (int32_t a = 0; a < A; ++a) {
+        const int32_t room = std::min(reserve, mp - npages[a]);
+        if (room <= 0) continue;
+        Item &last = items[last_item[a]];
+        const int32_t limit = rope ? fkv::kMaxPagesPerItem : fkv::kMaxPagesSingle;
+        if (last.agents.size() == 1 && last.p1 - last.p0 + room <= limit) {
+            last.cap = last.p1 + room;
+        } else {
+            const int32_t first = (int32_t)items.size();
+            Item it{npages[a], npages[a], npages[a] + room, fkv::kMaxGroups, kItemOverhead, {a}};
+            total_rows += (int64_t)it.copies * g;
+            items.push_back(std::move(it));
+            clusters.push_back({first, 1});
+            cluster_cost.push_back(kItemOverhead);
+        }
+        cap_pages[a] = npages[a] + room;
+    }
+    for (const auto &it : items) pps_max = std::max(pps_max, it.cap - it.p0);
     if (total_rows * prm->hkv > INT32_MAX) return fkv::fail(FKV_ERR_UNSUPPORTED, "fkv_decode_plan_create: too many rows");
     const int32_t n_items = (int32_t)items.size();
     const int32_t hkv = prm->hkv;
@@ -295,7 +324,10 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     pl->hkv = hkv;
     pl->g = g;
     pl->n_agents = A;
-    pl->max_pages_used = P;
+    pl->page_size = ps;
+    pl->max_pages = mp;
+    pl->cap_pages = cap_pages;
+    pl->max_pages_used = *std::max_element(cap_pages.begin(), cap_pages.end());
     const int64_t off_items = fkv::kHeaderWords;
     const int64_t off_blocks = off_items + (int64_t)n_items * fkv::kItemWords;
     const int64_t off_ptr = off_blocks + n_blocks;
@@ -332,14 +364,16 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     w[fkv::H_OFF_DESC] = rope ? -1 : (int32_t)off_desc;
     for (int32_t i = 0; i < n_items; ++i) {
         int32_t *r = &w[off_items + (int64_t)i * fkv::kItemWords];
-        r[0] = items[i].p0;
-        r[1] = items[i].p1;
-        r[2] = items[i].agents[0];
-        r[3] = (int32_t)items[i].agents.size();
-        r[4] = items[i].copies;
+        const int32_t nag = (int32_t)items[i].agents.size();
+        r[fkv::kItemP0] = items[i].p0;
+        r[fkv::kItemCap] = items[i].cap;
+        r[fkv::kItemLeader] = items[i].agents[0];
+        r[fkv::kItemNag] = nag;
+        r[fkv::kItemCopies] = items[i].copies;
+        r[fkv::kItemEnd] = items[i].p1;
         for (int32_t j = 0; j < fkv::kMaxItemAgents; ++j) {
-            r[5 + j] = j < r[3] ? items[i].agents[j] : -1;
-            r[5 + fkv::kMaxItemAgents + j] = j < r[3] ? first[i][j] : -1;
+            r[fkv::kItemAgents + j] = j < nag ? items[i].agents[j] : -1;
+            r[fkv::kItemFirst + j] = j < nag ? first[i][j] : -1;
         }
     }
     for (int32_t b = 0; b < n_blocks; ++b) {
@@ -349,8 +383,8 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     }
     for (int32_t a = 0; a <= A; ++a) w[off_ptr + a] = ptr[a];
     if (!rope) {
-        // block descriptors: everything the split kernel's prologue reads, at an address
-        // that depends on the block index only
+        // block descriptors: the item a block serves, at an address that depends on the block
+        // index only (the kernel's first load)
         for (int32_t b = 0; b < n_blocks; ++b) {
             int32_t *d = &w[off_desc + (int64_t)b * fkv::kDescWords];
             const int32_t blk = w[off_blocks + b];
@@ -358,30 +392,16 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
             const int32_t i = blk / nhb;
             const Item &it = items[i];
             const int32_t nag = (int32_t)it.agents.size();
-            const int32_t ng = (nag + ag - 1) / ag;
-            const int32_t stride = ng > 2 ? fkv::kMaxPagesMulti : fkv::kMaxPagesSingle;
-            int32_t max_len = 0;
-            for (int32_t a : it.agents) max_len = std::max(max_len, seq_lens[a]);
             d[fkv::kDescPg0] = it.p0;
-            d[fkv::kDescPg1] = it.p1;
+            d[fkv::kDescCap] = it.cap;
             d[fkv::kDescNag] = nag;
             d[fkv::kDescHead] = (blk % nhb) * hpb;
-            d[fkv::kDescMaxLen] = max_len;
-            d[fkv::kDescResStride] = stride;
+            d[fkv::kDescLeader] = it.agents[0];
             d[fkv::kDescItem] = i;
             d[fkv::kDescCopies] = it.copies;
-            const int32_t leader = it.agents[0];
-            for (int32_t k = it.p0; k < it.p1; ++k)
-                d[fkv::kDescBase + (k - it.p0)] = base_bt[(int64_t)leader * mp + k];
             for (int32_t j = 0; j < nag; ++j) {
-                const int32_t a = it.agents[j];
-                const int32_t ad = prm->r > 0 ? adapter_idx[a] : -1;
-                d[fkv::kDescAgent + j] = a;
-                d[fkv::kDescLen + j] = seq_lens[a];
-                d[fkv::kDescAdapter + j] = ad;
+                d[fkv::kDescAgent + j] = it.agents[j];
                 d[fkv::kDescPart + j] = first[i][j];
-                for (int32_t k = it.p0; k < it.p1; ++k)
-                    d[fkv::kDescRes + j * stride + (k - it.p0)] = ad >= 0 ? res_bt[(int64_t)a * mp + k] : -1;
             }
         }
     }
@@ -396,6 +416,28 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
 }
 
 void fkv_decode_plan_destroy(fkv_plan *plan) { delete plan; }
+
+fkv_status fkv_decode_plan_covers(const fkv_plan *plan, const int32_t *seq_lens, int32_t n_agents) {
+    fkv::clear_error();
+    if (!plan || !seq_lens) return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_covers: null argument");
+    if (n_agents != plan->n_agents) return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_covers: agent count differs from the plan's");
+    for (int32_t a = 0; a < n_agents; ++a) {
+        const int64_t cap = (int64_t)plan->cap_pages[a] * plan->page_size;
+        if (seq_lens[a] < 1 || seq_lens[a] > cap)
+            return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_covers: agent " + std::to_string(a) + " has length " +
+                                                  std::to_string(seq_lens[a]) + ", the plan covers 1.." +
+                                                  std::to_string(cap) + ": build a new plan");
+    }
+    return FKV_OK;
+}
+
+fkv_status fkv_decode_plan_capacity(const fkv_plan *plan, int32_t agent, int64_t *max_len) {
+    fkv::clear_error();
+    if (!plan || !max_len || agent < 0 || agent >= plan->n_agents)
+        return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_capacity: bad argument");
+    *max_len = (int64_t)plan->cap_pages[agent] * plan->page_size;
+    return FKV_OK;
+}
 
 }  // extern "C"
 

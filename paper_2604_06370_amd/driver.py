@@ -27,15 +27,16 @@ def _bf16(a: np.ndarray, device) -> torch.Tensor:
 class LoadedWorkload:
     def __init__(self, wl: Workload, device="cuda", rope: bool = True, placement_seed: Optional[int] = None,
                  no_residual: bool = False, pages_per_split: int = 0, item_agents: int = 0, base_pages: Optional[int] = None,
-                 res_pages: Optional[int] = None):
+                 res_pages: Optional[int] = None, headroom_pages: int = 16):
         self.wl = wl
         self.device = torch.device(device)
         self.rope = rope and wl.r > 0
         ps, hkv, d, r = wl.page_size, wl.hkv, wl.d, wl.r
         A = wl.n_agents
         seq_len = wl.seq_len
-        need_res = int(sum((int(L) + ps - 1) // ps for L in seq_len))
-        need_base = int(wl.base_k.shape[0] // ps + 2 * A + 8)
+        # pools and block-table rows leave `headroom_pages` per agent for decode steps
+        need_res = int(sum((int(L) + ps - 1) // ps for L in seq_len)) + headroom_pages * A
+        need_base = int(wl.base_k.shape[0] // ps + 2 * A + 8) + headroom_pages * A
         nb = base_pages or need_base
         nr = res_pages or max(need_res + A, 1)
         self.tree = rt.Tree(ps, nb, nr)
@@ -56,7 +57,7 @@ class LoadedWorkload:
             # random subset before each fork so allocation lands on non-contiguous ids
             for pool, cap in ((0, nb), (1, nr)):
                 held[pool] = list(rng.permutation(self.tree.alloc_pages(pool, cap)))
-        max_pages = max(1, max((int(L) + ps - 1) // ps for L in seq_len))
+        max_pages = max(1, max((int(L) + ps - 1) // ps for L in seq_len)) + headroom_pages
         self.max_pages = max_pages
 
         def release_some(pool, k):
@@ -145,6 +146,34 @@ class LoadedWorkload:
             self.decode_setup()
         rt.residual_attention_decode(self._decode["args"], self._decode["plan"], stream)
         return self._decode["out"]
+
+    def append_token(self, a: int, rows: dict) -> rt.FillPlan:
+        """One decode step's cache write for agent a: fkv_cow_append of its new token, the
+        page copies it reports, then the token's base K/V and rCache rows (``rows`` as drawn by
+        workloads.append_decode_token) scattered into the slots the tree handed out."""
+        wl, dev = self.wl, self.device
+        ps, hkv, d, r = wl.page_size, wl.hkv, wl.d, wl.r
+        fp = self.tree.cow_append(a, [rows["token"]])
+        rt.page_copy(fp.copies, self.base_kv, self.res_kv, hkv, d, r, ps)
+        bt_b, bt_r, _ = self.tree.block_tables([a], self.max_pages)
+        pos = fp.seq_len - 1
+        rt.scatter_tokens(torch.from_numpy(bt_b[0]).to(dev), None, pos, _bf16(rows["k"], dev), _bf16(rows["v"], dev),
+                          None, None, self.base_kv, self.res_kv, hkv, d, r, ps)
+        if r > 0:
+            rt.scatter_tokens(None, torch.from_numpy(bt_r[0]).to(dev), pos, None, None, _bf16(rows["c_k"], dev),
+                              _bf16(rows["c_v"], dev), self.base_kv, self.res_kv, hkv, d, r, ps)
+        return fp
+
+    def refresh_decode_tables(self):
+        """Copy the tree's current block tables and lengths into the decode call's device
+        tables in place (the plan and the argument block keep pointing at them)."""
+        st = self._decode
+        bb, rb, sl = self.tree.block_tables(st["agents"], self.max_pages)
+        st["base_bt"].copy_(torch.from_numpy(bb))
+        st["res_bt"].copy_(torch.from_numpy(rb))
+        st["seq_lens"].copy_(torch.from_numpy(sl))
+        st["host_bt"] = (bb, rb, sl)
+        return sl
 
     # ---- chunked prefill over the agents that appended a chunk ----
     def prefill_setup(self, agents: Optional[Sequence[int]] = None):

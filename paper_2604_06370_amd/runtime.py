@@ -126,7 +126,7 @@ class DecodePlan:
     def __init__(self, base_bt: np.ndarray, seq_lens: np.ndarray, hq: int, hkv: int, page_size: int,
                  pages_per_split: int = 0, num_cus: int = 0, max_item_agents: int = 0, r: int = 0,
                  rope: bool = False, res_bt: Optional[np.ndarray] = None,
-                 adapter_idx: Optional[np.ndarray] = None):
+                 adapter_idx: Optional[np.ndarray] = None, reserve_pages: int = 0):
         bb = np.ascontiguousarray(base_bt, dtype=np.int32)
         sl = np.ascontiguousarray(seq_lens, dtype=np.int32)
         rb = np.ascontiguousarray(res_bt, dtype=np.int32) if res_bt is not None else None
@@ -136,7 +136,7 @@ class DecodePlan:
         if ad is not None and ad.shape != (bb.shape[0],):
             raise ValueError("adapter_idx must hold one entry per agent")
         prm = N.fkv_decode_plan_params(bb.shape[0], hq, hkv, page_size, bb.shape[1], pages_per_split, num_cus,
-                                       max_item_agents, r, int(bool(rope)))
+                                       max_item_agents, r, int(bool(rope)), reserve_pages)
         h = N.c_vp()
         check(N.fkv_decode_plan_create(ctypes.byref(prm), _ptr(bb), _ptr(rb) if rb is not None else None, _ptr(sl),
                                        _ptr(ad) if ad is not None else None, ctypes.byref(h)),
@@ -159,6 +159,17 @@ class DecodePlan:
     @property
     def handle(self):
         return self._h
+
+    def covers(self, seq_lens: np.ndarray) -> None:
+        """fkv_decode_plan_covers: raises FKVError when an agent has outgrown the plan."""
+        sl = np.ascontiguousarray(seq_lens, dtype=np.int32)
+        check(N.fkv_decode_plan_covers(self._h, _ptr(sl), len(sl)), "fkv_decode_plan_covers")
+
+    def capacity(self, agent: int) -> int:
+        """fkv_decode_plan_capacity: the longest length `agent` may reach under this plan."""
+        v = N.c_i64()
+        check(N.fkv_decode_plan_capacity(self._h, agent, ctypes.byref(v)), "fkv_decode_plan_capacity")
+        return v.value
 
     def info(self, d: int, r: int) -> dict:
         inf = N.fkv_plan_info()

@@ -292,6 +292,30 @@ def config(cfg: int, seed: Optional[int] = None) -> Workload:
     raise ValueError(f"unknown config {cfg}")
 
 
+def append_decode_token(wl: Workload, a: int, rng: np.random.Generator) -> dict:
+    """Draw one new token for decode agent ``a`` (its id, base K/V rows ~ N(0, 1), rCache rows
+    ~ N(0, 1), zero without residual) and extend the workload's logical arrays with it; the
+    agent's query now sits at the new last position.  Returns the drawn bf16 rows."""
+    hkv, d, r = wl.hkv, wl.d, wl.r
+    tok = int(rng.integers(0, VOCAB))
+    k = _normal_bf16(rng, (1, hkv, d))
+    v = _normal_bf16(rng, (1, hkv, d))
+    ck = _normal_bf16(rng, (1, r))
+    cv = _normal_bf16(rng, (1, r))
+    if not wl.has_residual[a]:
+        ck[:] = 0
+        cv[:] = 0
+    row = wl.base_k.shape[0]
+    wl.base_k = np.concatenate([wl.base_k, k])
+    wl.base_v = np.concatenate([wl.base_v, v])
+    wl.base_row[a] = np.append(wl.base_row[a], row)
+    wl.c_k[a] = np.concatenate([wl.c_k[a], ck])
+    wl.c_v[a] = np.concatenate([wl.c_v[a], cv])
+    wl.fork_tokens[a] = np.append(wl.fork_tokens[a], np.int32(tok)).astype(np.int32)
+    wl.q_pos[wl.q_offset[a]] = len(wl.fork_tokens[a]) - 1
+    return {"token": tok, "k": k, "v": v, "c_k": ck, "c_v": cv}
+
+
 def oracle_inputs(wl: Workload, agents: Optional[Sequence[int]] = None,
                   q_rows: Optional[dict] = None, rope: bool = True) -> dict:
     """Logical fp64 arrays for the oracle.  ``agents`` restricts the problem to a

@@ -237,21 +237,21 @@ def _parse_plan(words):
              total_rows=15, max_item_agents=16, heads_per_block=17, rank=18, rope=19, off_desc=21)
     h = {k: int(words[v]) for k, v in H.items()}
     items = []
-    iw = 5 + 2 * 16
+    iw = 6 + 2 * 16
     for i in range(h["n_items"]):
         r = words[h["off_items"] + iw * i: h["off_items"] + iw * (i + 1)]
         nag = int(r[3])
-        items.append(dict(p0=int(r[0]), p1=int(r[1]), leader=int(r[2]), nag=nag, copies=int(r[4]),
-                          agents=[int(x) for x in r[5:5 + nag]], pad=[int(x) for x in r[5 + nag:21]],
-                          first=[int(x) for x in r[21:21 + nag]], first_pad=[int(x) for x in r[21 + nag:37]]))
+        items.append(dict(p0=int(r[0]), cap=int(r[1]), leader=int(r[2]), nag=nag, copies=int(r[4]), end=int(r[5]),
+                          agents=[int(x) for x in r[6:6 + nag]], pad=[int(x) for x in r[6 + nag:22]],
+                          first=[int(x) for x in r[22:22 + nag]], first_pad=[int(x) for x in r[22 + nag:38]]))
     blocks = words[h["off_blocks"]: h["off_blocks"] + h["n_blocks"]]
     ptr = words[h["off_ptr"]: h["off_ptr"] + h["n_agents"] + 1]
     return h, items, blocks, ptr
 
 
-# block descriptor layout (RoPE-off plans): header words, then per-slot arrays, base ids, rCache ids
-DESC_AGENT, DESC_LEN, DESC_AD, DESC_PART, DESC_BASE, DESC_RES = 8, 24, 40, 56, 72, 200
-DESC_WORDS = DESC_RES + 16 * 64
+# block descriptor layout (RoPE-off plans): item fields, then per-slot agents and first partials
+DESC_AGENT, DESC_PART = 8, 24
+DESC_WORDS = DESC_PART + 16
 
 
 def _parse_desc(words, h):
@@ -259,10 +259,9 @@ def _parse_desc(words, h):
     for b in range(h["n_blocks"]):
         d = np.asarray(words[h["off_desc"] + b * DESC_WORDS: h["off_desc"] + (b + 1) * DESC_WORDS])
         nag = int(d[2])
-        out.append(dict(p0=int(d[0]), p1=int(d[1]), nag=nag, head=int(d[3]), max_len=int(d[4]), stride=int(d[5]),
-                        item=int(d[6]), copies=int(d[7]), agents=d[DESC_AGENT:DESC_AGENT + nag].tolist(),
-                        lens=d[DESC_LEN:DESC_LEN + nag].tolist(), ads=d[DESC_AD:DESC_AD + nag].tolist(),
-                        parts=d[DESC_PART:DESC_PART + nag].tolist(), base=d[DESC_BASE:DESC_RES], res=d[DESC_RES:]))
+        out.append(dict(p0=int(d[0]), cap=int(d[1]), nag=nag, head=int(d[3]), leader=int(d[4]), item=int(d[5]),
+                        copies=int(d[6]), agents=d[DESC_AGENT:DESC_AGENT + nag].tolist(),
+                        parts=d[DESC_PART:DESC_PART + nag].tolist()))
     return out
 
 
@@ -294,42 +293,46 @@ def _synthetic_tables(rng, n_agents, groups, prefix_pages, mid_pages, max_suffix
 @pytest.mark.parametrize("pps", [0, 4, 64])
 def test_decode_plan_items_cover_every_agent_page_once(hq, hkv, r, rope, pps):
     """Host-side invariants the decode kernels rely on for in-bounds access: every (agent,
-    page) in exactly one item, items within the page and agent limits, disjoint partial rows
-    (one set per wave copy of a group) and a CSR that points each agent's query heads at
-    exactly its rows."""
+    page) in exactly one item, every page of an agent's growth room in exactly one item (its
+    last item, or a tail item of its own), items within the page and agent limits, disjoint
+    partial rows (one set per wave copy of a group) and a CSR that points each agent's query
+    heads at exactly its rows."""
     rng = np.random.default_rng(hq + r + pps)
     g = hq // hkv
     for n_agents, groups, pre, mid, suf in [(16, 1, 300, 0, 40), (37, 3, 64, 9, 5), (5, 5, 0, 3, 2)]:
         bb, sl = _synthetic_tables(rng, n_agents, groups, pre, mid, suf)
-        rb = (bb + 7) * 3 + np.arange(bb.shape[1])[None, :]  # any distinct ids
-        ad = np.where(np.arange(n_agents) % 5 == 4, -1, (np.arange(n_agents) * 7) % 11).astype(np.int32)
+        extra = int(rng.integers(0, 24))  # room in the table rows for growth
+        bb = np.concatenate([bb, np.full((n_agents, extra), -1, np.int32)], axis=1)
+        mp = bb.shape[1]
         n_item = rt.decode_plan_default_agents(hq, hkv, r, rope)
-        plan = rt.DecodePlan(bb, sl, hq, hkv, 16, pps, r=r, rope=rope, res_bt=rb, adapter_idx=ad)
+        plan = rt.DecodePlan(bb, sl, hq, hkv, 16, pps, r=r, rope=rope)
         words = plan.serialize()
         h, items, blocks, ptr = _parse_plan(words)
         assert h["max_item_agents"] == n_item and (h["rank"], h["rope"]) == (r, int(rope))
         assert n_item <= (16 // g if rope else 16) and n_item <= 4 * (16 // g)
         hpb = h["heads_per_block"]
-        assert hpb in (1, 2, 4) and hkv % hpb == 0 and (hpb == 1 or not rope)
-        # with head blocks (the LDS-staged kernel) one page of an item fits its 48 KB stage
-        assert hpb == 1 or 8192 * hpb + n_item * 64 * r <= 48 * 1024
+        assert hpb == 1
+        npages = (sl + 15) // 16
         seen = np.zeros(bb.shape, np.int32)
         owned = [[] for _ in range(n_agents)]
         for it in items:
-            assert 0 <= it["p0"] < it["p1"] and it["p1"] - it["p0"] <= 256
+            assert 0 <= it["p0"] <= it["end"] <= it["cap"] <= mp
+            assert it["cap"] - it["p0"] <= (64 if rope else 128) and it["end"] - it["p0"] <= 128
             assert 1 <= it["nag"] <= h["max_item_agents"] and it["leader"] == it["agents"][0]
             assert all(x == -1 for x in it["pad"]) and all(x == -1 for x in it["first_pad"])
+            assert it["cap"] == it["end"] or (it["nag"] == 1 and it["end"] == npages[it["leader"]])
             for a in it["agents"]:
-                assert it["p1"] <= (sl[a] + 15) // 16
-                assert (bb[a, it["p0"]:it["p1"]] == bb[it["leader"], it["p0"]:it["p1"]]).all()
-                seen[a, it["p0"]:it["p1"]] += 1
+                assert it["end"] <= npages[a]
+                assert (bb[a, it["p0"]:it["end"]] == bb[it["leader"], it["p0"]:it["end"]]).all()
+                seen[a, it["p0"]:it["cap"]] += 1
             ng = -(-it["nag"] // (16 // g))
             assert it["copies"] == (4 if rope else 4 // (1 if ng == 1 else 2 if ng == 2 else 4))
             for j, a in enumerate(it["agents"]):
                 owned[a] += [it["first"][j] + c for c in range(it["copies"])]
         for a in range(n_agents):
-            npg = (sl[a] + 15) // 16
-            assert (seen[a, :npg] == 1).all() and (seen[a, npg:] == 0).all()
+            cap = min(npages[a] + 16, mp)
+            assert plan.capacity(a) == cap * 16
+            assert (seen[a, :cap] == 1).all() and (seen[a, cap:] == 0).all()
             # every partial of the agent is written by exactly one (item, slot, copy), and the
             # agent's partials are the contiguous range the CSR names
             assert sorted(owned[a]) == list(range(int(ptr[a]), int(ptr[a + 1])))
@@ -339,27 +342,22 @@ def test_decode_plan_items_cover_every_agent_page_once(hq, hkv, r, rope, pps):
         if rope:
             assert h["off_desc"] == -1
         else:
-            # each block's descriptor restates its item and head, the leader's base page ids
-            # and every slot's rCache page ids (-1 without adapter), within the page limits
+            # each block's descriptor restates its item and head
             for blk, dsc in zip(blocks, _parse_desc(words, h)):
                 if blk < 0:
                     assert dsc["nag"] == 0
                     continue
                 it = items[blk // hkv]
-                assert (dsc["p0"], dsc["p1"], dsc["nag"], dsc["head"], dsc["item"], dsc["copies"]) == \
-                    (it["p0"], it["p1"], it["nag"], blk % hkv, blk // hkv, it["copies"])
-                npg = it["p1"] - it["p0"]
-                ng = -(-it["nag"] // (16 // g))
-                assert dsc["stride"] == (64 if ng > 2 else 128) and npg <= dsc["stride"]
+                assert (dsc["p0"], dsc["cap"], dsc["nag"], dsc["head"], dsc["leader"], dsc["item"], dsc["copies"]) == \
+                    (it["p0"], it["cap"], it["nag"], blk % hkv, it["leader"], blk // hkv, it["copies"])
                 assert dsc["agents"] == it["agents"] and dsc["parts"] == it["first"]
-                assert dsc["lens"] == [int(sl[a]) for a in it["agents"]] and dsc["max_len"] == max(dsc["lens"])
-                exp_ad = [int(ad[a]) if r > 0 else -1 for a in it["agents"]]
-                assert dsc["ads"] == exp_ad
-                assert (dsc["base"][:npg] == bb[it["leader"], it["p0"]:it["p1"]]).all()
-                for j, a in enumerate(it["agents"]):
-                    row = dsc["res"][j * dsc["stride"]: j * dsc["stride"] + npg]
-                    exp = rb[a, it["p0"]:it["p1"]] if exp_ad[j] >= 0 else np.full(npg, -1)
-                    assert (row == exp).all()
+        # lengths within the capacity are covered; one token past it is not
+        plan.covers(np.minimum(sl + 5, [plan.capacity(a) for a in range(n_agents)]))
+        over = np.array([plan.capacity(a) for a in range(n_agents)], np.int32)
+        over[n_agents // 2] += 1
+        with pytest.raises(rt.FKVError) as e:
+            plan.covers(over)
+        assert e.value.code == N.FKV_ERR_INVALID and f"agent {n_agents // 2}" in str(e.value)
         info = plan.info(128, r)
         partials = h["total_rows"] * hkv * ((128 + r + 2 + 3) // 4 * 4) * 4
         assert info["workspace_bytes"] == (partials + 255) // 256 * 256

@@ -277,3 +277,32 @@ def test_shared_partial_page_mixed_lengths(rope, r, item_agents):
     lw.close()
     g, _ = run_case(f"short-shared r={r} items={item_agents} rope={rope}", wl, rope, item_agents=item_agents)
     _check_single_keys(f"short-shared r={r} rope={rope}", wl, g)
+
+
+@pytest.mark.parametrize("rope", [False, True])
+def test_one_plan_serves_consecutive_decode_steps(rope):
+    """A serving loop: 24 decode steps, each appending one token per agent (fkv_cow_append,
+    cache writes, block tables and lengths refreshed on the device in place) and decoding with
+    the plan built before the first step; every agent crosses at least one page boundary.
+    Each step's output is compared with the oracle on the grown contexts."""
+    wl = W.fanout("steps", 81, n_agents=8, prefix=500, suffix_lo=1, suffix_hi=60, hq=32, hkv=8, r=16,
+                  zero_residual=[6])
+    lw = LoadedWorkload(wl, rope=rope, headroom_pages=4)
+    st = lw.decode_setup()
+    plan, words0 = st["plan"], st["plan"].serialize()
+    agents = st["agents"]
+    rng = np.random.default_rng(9)
+    L0 = wl.seq_len.copy()
+    for step in range(24):
+        for a in agents:
+            fp = lw.append_token(a, W.append_decode_token(wl, a, rng))
+            assert fp.copies == [], "a private last page is written in place"
+        sl = lw.refresh_decode_tables()
+        plan.covers(sl)
+        out = lw.decode().clone()
+        torch.cuda.synchronize()
+        if step % 6 == 5 or step == 0:
+            check_close(f"step {step} rope={rope}", out, oracle_decode(wl, agents, rope))
+    assert all((L0[a] - 1) // 16 < (wl.seq_len[a] - 1) // 16 for a in agents)  # every agent took a new page
+    assert np.array_equal(plan.serialize(), words0) and lw._decode["plan"] is plan
+    lw.close()
