@@ -64,6 +64,7 @@ struct DecodeArgs {
     float scale_log2;  // softmax scale * log2(e)
     int64_t ws_bytes;  // bytes of the partial-row area of the workspace
     int32_t n_rows;    // query rows to merge: n_agents * hq
+    int32_t rope_max_pos;  // rows of the RoPE tables
 };
 
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
@@ -751,30 +752,38 @@ __global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(Deco
 
 
 // ---------------------------------------------------------------------------
-// RoPE on: one agent group per item; waves stride over the pages, registers
-// double-buffered.  The loop is specialised on the number NS of agent slots so that
-// every load it issues is consumed; all loads are unconditional and in a fixed order,
-// so the compiler can count them and the prefetched page stays in flight.
+// RoPE on (deferred RoPE of the rebuilt key, Section 5.3; Algorithm 1, stage 1).  One
+// workgroup per (work item, KV head h), four waves, two workgroups per compute unit.  An
+// item holds up to MS agents in up to four wave groups of NSW agents; wave w serves group
+// w % ngp as copy w / ngp and streams the item pages i with i % copies == copy straight
+// into registers (next page in flight), independently of the other waves: the rebuild is
+// vector-ALU bound, so no barrier ties the waves together.  The waves of one item read
+// each base page at about the same time, so it crosses HBM once per item and reaches the
+// other groups from the caches.  The B_K^T fragments of every slot of the item are built in
+// LDS once per workgroup.  Per page and slot s of the wave's group (matrix-core products,
+// fp32 accumulate):
+//   U^T   = B_K,s^T C_K,s^T                  16x16x16
+//   K_lr  = RoPE_p(U)                        rotate-half pairs (i, i + 64) in one lane, fp32
+//   S^T  += K_lr Q_s^T                       16x16x32, other slots' rows masked out of Q
 template <int R, int G>
 struct RopeShape {
-    static constexpr int AG = fkv::decode_rope_item_agents(G, R);  // agent slots of an item
-    static constexpr int RT = (R + 15) / 16;
-    static constexpr int BSTAGE_BYTES = AG * R * D * 2;     // row-major B_K slices
-    static constexpr int BKT_BYTES = AG * RT * 8 * 64 * 8;  // B_K^T fragments
-    static constexpr int TABLE_WORDS = (1 + AG) * kMaxPagesPerItem;
+    static constexpr int RT = (R + 15) / 16;                       // 16-wide rank tiles
+    static constexpr int NSW = fkv::decode_rope_wave_agents(G, R); // agent slots of a wave
+    static constexpr int MS = fkv::decode_rope_item_agents(G, R);  // agent slots of an item
+    static constexpr int BKT = MS * RT * 8 * 512;                  // (slot, tile, column tile) x 64 lanes x 8 B
+    static constexpr int BK_UNITS = MS * RT * 128;                 // (slot, rank pair, 8-dim chunk)
+    static_assert(BKT <= 64 * 1024, "two workgroups per compute unit");
+    static_assert(BK_UNITS % 256 == 0 && NSW * G <= ROWS, "shape");
 };
 
 template <int R, int G>
-__global__ __launch_bounds__(256, 1) void decode_rope_kernel(DecodeArgs p) {
+__global__ __launch_bounds__(256, 2) void decode_rope_kernel(DecodeArgs p) {
     static_assert(R > 0, "RoPE decode needs a residual");
     using S = RopeShape<R, G>;
     using RowsT = Rows<R>;
-    constexpr int AG = S::AG;
-    constexpr int RT = S::RT;
-    constexpr int RTX = RT;
-    __shared__ __attribute__((aligned(16))) uint16_t b_stage[S::BSTAGE_BYTES / 2];
-    __shared__ __attribute__((aligned(16))) uint32_t lds_bkt[S::BKT_BYTES / 4];
-    __shared__ int32_t s_tab[S::TABLE_WORDS];
+    constexpr int RT = S::RT, NSW = S::NSW, MS = S::MS;
+    constexpr int RTX = RowsT::RTX;
+    __shared__ __attribute__((aligned(16))) u32x2 bkt[S::BKT / 8];
 
     const int32_t *plan = p.plan;
     const int blk = plan[p.off_blocks + blockIdx.x];
@@ -785,206 +794,269 @@ __global__ __launch_bounds__(256, 1) void decode_rope_kernel(DecodeArgs p) {
     const int32_t *rec = plan + p.off_items + item * fkv::kItemWords;
     const int pg0 = rec[fkv::kItemP0], pgcap = rec[fkv::kItemCap], leader = rec[fkv::kItemLeader];
     const int nag = rec[fkv::kItemNag];
-    const int32_t *item_agents = rec + fkv::kItemAgents;
-    if (nag > AG || pgcap - pg0 > kMaxPagesPerItem) return;  // rejected on the host
+    const int npcap = pgcap - pg0;
+    if (nag < 1 || nag > MS || npcap < 1 || npcap > fkv::kMaxPagesSingle) return;  // rejected on the host
+    const int ng = (nag + NSW - 1) / NSW;
+    const int ngp = ng == 1 ? 1 : (ng == 2 ? 2 : 4);
+    const int copies = WAVES / ngp;
 
     const int lane = threadIdx.x & 63;
     const int wave = uniform(threadIdx.x >> 6);
     const int col = lane & 15, grp = lane >> 4;
-    const int my_slot_l = col / G;
-    const bool row_active = my_slot_l < nag;
-    const int my_agent = row_active ? item_agents[my_slot_l] : 0;
-    const int my_part = row_active ? rec[fkv::kItemFirst + my_slot_l] + wave : 0;  // wave = copy
+    const int my_group = wave % ngp, copy = wave / ngp;
+    const int sb = my_group * NSW;                   // first item slot of this wave's group
+    const int my_slot = col / G;                     // this lane's row: slot within the group
+    const bool row_active = my_slot < NSW && sb + my_slot < nag;
     const int qh = h * G + (col % G);
 
-    // lengths and adapters from the launch arrays; the longest sequence bounds the pages
-    int res_len[AG];
-    int max_len = 0;
+    // lane i < nag: slot i's agent and first partial (plan), length and adapter (launch
+    // arrays); lane i (and 64 + i): base page id of item page i (the leader's row) and, per
+    // slot of this wave's group, its rCache page id (-1: no adapter)
+    const bool lane_ag = lane < nag;
+    const int l_agent = lane_ag ? rec[fkv::kItemAgents + lane] : 0;
+    const int l_part = lane_ag ? rec[fkv::kItemFirst + lane] : 0;
+    const int l_len = lane_ag ? p.seq_lens[l_agent] : 0;
+    const int l_ad = lane_ag ? p.adapter_idx[l_agent] : -1;
+    const int32_t *brow = p.base_bt + (int64_t)leader * p.max_pages + pg0;
+    const int bid0 = brow[min(lane, npcap - 1)];
+    const int bid1 = brow[min(64 + lane, npcap - 1)];
+    int rid0[NSW], rid1[NSW];
 #pragma unroll
-    for (int s = 0; s < AG; ++s) {
-        const bool ok = s < nag;
-        const int ag_id = ok ? item_agents[s] : 0;
-        const int len = ok ? p.seq_lens[ag_id] : 0;
-        res_len[s] = (ok && p.adapter_idx[ag_id] >= 0) ? len : 0;
-        max_len = max(max_len, len);
+    for (int s = 0; s < NSW; ++s) {
+        const bool ok = sb + s < nag;
+        const int ag_s = __builtin_amdgcn_readlane(l_agent, (sb + s) & 63);
+        const int32_t *row = p.res_bt + (int64_t)(ok ? ag_s : 0) * p.max_pages + pg0;
+        rid0[s] = ok ? row[min(lane, npcap - 1)] : -1;
+        rid1[s] = (ok && npcap > 64) ? row[min(64 + lane, npcap - 1)] : -1;
     }
-    const int pg1 = max(pg0, min(pgcap, (max_len + PS - 1) / PS));
-    const int npg = pg1 - pg0;
-    for (int idx = threadIdx.x; idx < (1 + nag) * npg; idx += 256) {
-        const int t = idx / npg, i = idx - t * npg;
-        int32_t v;
-        if (t == 0) {
-            v = p.base_bt[(int64_t)leader * p.max_pages + pg0 + i];
-        } else {
-            const int ag_id = item_agents[t - 1];
-            const int32_t rp = p.res_bt[(int64_t)ag_id * p.max_pages + pg0 + i];
-            v = p.adapter_idx[ag_id] >= 0 ? rp : 0;
-        }
-        s_tab[t * kMaxPagesPerItem + i] = v;
-    }
-    const int my_len = row_active ? p.seq_lens[my_agent] : 0;
-    u32x4 qf[4];
-    load_q(p.q + ((int64_t)my_agent * p.hq + qh) * D, row_active, grp, qf);
-
-    // B_K^T fragments of the group's slots (lane holds B_K[16t + 4grp + i][16mt + col]),
-    // built from row-major B_K slices staged in LDS; zero for empty slots / no adapter
-    const int64_t n = (int64_t)hkv * D;
-    for (int idx = threadIdx.x; idx < AG * R * (D / 8); idx += 256) {
-        const int sl = idx / (R * (D / 8));
-        const int rem = idx - sl * (R * (D / 8));
-        const int rho = rem / (D / 8), c8 = rem - rho * (D / 8);
-        const int ad = sl < nag ? p.adapter_idx[item_agents[sl]] : -1;
-        u32x4 v = {0, 0, 0, 0};
-        if (ad >= 0) v = ldg128(p.lora_b + (int64_t)ad * 2 * R * n + (int64_t)rho * n + (int64_t)h * D + 8 * c8);
-        *reinterpret_cast<u32x4 *>(b_stage + (sl * R + rho) * D + 8 * c8) = v;
-    }
-    __syncthreads();
-    for (int idx = threadIdx.x; idx < AG * RT * 8 * 64; idx += 256) {
-        const int ln = idx & 63;
-        const int rest = idx >> 6;  // (sl*RT + t)*8 + mt
-        const int mt = rest & 7, sti = rest >> 3;
-        const int sl = sti / RTX, t = sti - sl * RTX;
-        const int c = ln & 15, gg = ln >> 4;
-        uint32_t w[2];
+    int item_max_len = 0;
+    for (int s = 0; s < nag; ++s) item_max_len = max(item_max_len, __builtin_amdgcn_readlane(l_len, s));
+    const int npg = min(pgcap, (item_max_len + PS - 1) / PS) - pg0;
+    // the wave's slots: keys that carry a residual (0 without adapter or past the item)
+    int res_len[NSW];
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int r0 = 16 * t + 4 * gg + 2 * j;
-            const uint16_t lo = r0 < R ? b_stage[(sl * R + r0) * D + 16 * mt + c] : (uint16_t)0;
-            const uint16_t hi = r0 + 1 < R ? b_stage[(sl * R + r0 + 1) * D + 16 * mt + c] : (uint16_t)0;
-            w[j] = (uint32_t)lo | ((uint32_t)hi << 16);
-        }
-        const int o = (((sl * RTX + t) * 8 + mt) * 64 + ln) * 2;
-        lds_bkt[o] = w[0];
-        lds_bkt[o + 1] = w[1];
+    for (int s = 0; s < NSW; ++s) {
+        const bool ok = sb + s < nag;
+        const int ad = __builtin_amdgcn_readlane(l_ad, (sb + s) & 63);
+        const int len = __builtin_amdgcn_readlane(l_len, (sb + s) & 63);
+        res_len[s] = (ok && ad >= 0) ? len : 0;
+        if (res_len[s] == 0) rid0[s] = rid1[s] = -1;
     }
-    __syncthreads();  // tables and B_K^T fragments ready
+    const int src_lane = (sb + my_slot) & 63;
+    const int sh_agent = __shfl(l_agent, src_lane), sh_len = __shfl(l_len, src_lane);
+    const int my_agent = row_active ? sh_agent : 0;
+    const int my_len = row_active ? sh_len : 0;
+    const int my_part = __shfl(l_part, src_lane) + copy;
+    const int64_t my_row = ((int64_t)my_part * G + col % G) * hkv + h;
 
-    const ResOffsets<R> ro(col, grp);
     RowsT st;
     st.init();
-    const int64_t res_page_halfs = RT * 512;
+    if (npg <= 0) {  // the item's agents have not reached it yet: an empty partial (weight 0)
+        write_partial<R>(p, st, row_active, my_row, grp);
+        return;
+    }
 
-    auto run_pages = [&](auto ns_tag) {
-        constexpr int NS = decltype(ns_tag)::value;
-        struct Frag {
-            f32x4 cs[4], sn[4];
-            u32x4 kf[4];
-            u32x2 vf[8];
-            u32x2 ck[NS][RTX];
-            u32x2 cv[NS][RTX];
-        };
-        auto load = [&](int pg, Frag &f) {
-            // RoPE rows first: they are consumed first
-            const float *cr = p.rope_cos + (int64_t)pg * (PS * D / 2);
-            const float *sr = p.rope_sin + (int64_t)pg * (PS * D / 2);
+    // B_K^T fragments of the item's slots for head h, built in LDS in rounds of four units: unit
+    // (slot, rank pair, 8-dim chunk) loads ranks 2q and 2q + 1 over 8 dims (ranks past R and
+    // slots without adapter: zero); lane (c, gg) of fragment (slot, tile t, column tile mt)
+    // holds B_K[16t + 4gg + j][16mt + c], j < 4, as two words of rank pairs
+    {
+        const int64_t n = (int64_t)hkv * D;
+        uint32_t *bw = reinterpret_cast<uint32_t *>(bkt);
+        constexpr int UPT = S::BK_UNITS / 256, ROUND = UPT < 4 ? UPT : 4;
+        for (int u0 = 0; u0 < UPT; u0 += ROUND) {
+            u32x4 bk_lo[ROUND], bk_hi[ROUND];
 #pragma unroll
-            for (int mt = 0; mt < 4; ++mt) {
-                f.cs[mt] = *reinterpret_cast<const f32x4 *>(cr + 256 * mt + lane * 4);
-                f.sn[mt] = *reinterpret_cast<const f32x4 *>(sr + 256 * mt + lane * 4);
-            }
-            const int bpage = uniform(s_tab[pg - pg0]);
-            const uint16_t *kblk = p.base_kv + ((int64_t)bpage * 2 * hkv + h) * kBlockHalfs;
-            const uint16_t *vblk = kblk + (int64_t)hkv * kBlockHalfs;
-#pragma unroll
-            for (int kk = 0; kk < 4; ++kk) f.kf[kk] = ldg128(kblk + kk * 512 + lane * 8);
-#pragma unroll
-            for (int q2 = 0; q2 < 4; ++q2) {
-                const u32x4 v = ldg128(vblk + q2 * 512 + lane * 8);
-                f.vf[2 * q2] = u32x2{v.x, v.y};
-                f.vf[2 * q2 + 1] = u32x2{v.z, v.w};
+            for (int u = 0; u < ROUND; ++u) {
+                const int idx = threadIdx.x + 256 * (u0 + u);
+                const int sl = idx / (RT * 128), rem = idx % (RT * 128);
+                const int rho = 2 * (rem / 16), c8 = rem % 16;
+                const int ad = __shfl(l_ad, sl & 63);
+                const bool ok = sl < nag && ad >= 0 && rho < R;
+                const uint16_t *src =
+                    p.lora_b + ((int64_t)(ok ? ad : 0) * 2 * R + (ok ? rho : 0)) * n + (int64_t)h * D + 8 * c8;
+                bk_lo[u] = ok ? ldg128(src) : u32x4{0, 0, 0, 0};
+                bk_hi[u] = (ok && rho + 1 < R) ? ldg128(src + n) : u32x4{0, 0, 0, 0};
             }
 #pragma unroll
-            for (int s = 0; s < NS; ++s) {
-                const int rpage = uniform(s_tab[(1 + s) * kMaxPagesPerItem + (pg - pg0)]);
-                const uint16_t *rb = p.res_kv + (int64_t)rpage * res_page_halfs;
+            for (int u = 0; u < ROUND; ++u) {
+                const int idx = threadIdx.x + 256 * (u0 + u);
+                const int sl = idx / (RT * 128), rem = idx % (RT * 128);
+                const int rho = 2 * (rem / 16), c8 = rem % 16;
+                const int t = rho / 16, gg = (rho % 16) / 4, j2 = (rho % 4) / 2;
+                const uint32_t lw[4] = {bk_lo[u].x, bk_lo[u].y, bk_lo[u].z, bk_lo[u].w};
+                const uint32_t hw[4] = {bk_hi[u].x, bk_hi[u].y, bk_hi[u].z, bk_hi[u].w};
 #pragma unroll
-                for (int t = 0; t < RT; ++t) {
-                    // two 8-byte loads: the single 16-byte form of this load gave wrong
-                    // results at rank 32 with this kernel's register allocation
-                    const u32x2 k = ldg64(rb + t * 512 + lane * 8);
-                    const u32x2 v = ldg64(rb + t * 512 + lane * 8 + 4);
-                    f.cv[s][t] = ro.cv_ok[t] ? v : u32x2{0, 0};
-                    f.ck[s][t] = ro.ck_ok[t] ? k : u32x2{0, 0};
+                for (int e = 0; e < 8; ++e) {
+                    const int i = 8 * c8 + e, mt = i / 16, c = i % 16;
+                    const uint32_t a = (e & 1) ? (lw[e >> 1] >> 16) : (lw[e >> 1] & 0xffffu);
+                    const uint32_t b = (e & 1) ? (hw[e >> 1] >> 16) : (hw[e >> 1] & 0xffffu);
+                    bw[((((sl * RT + t) * 8 + mt) * 64) + c + 16 * gg) * 2 + j2] = a | (b << 16);
                 }
-            }
-        };
-        auto compute = [&](int pg, Frag &f) {
-            const int tok0 = pg * PS;
-            const int vis = max_len - tok0;
-            if (vis < PS) {
-#pragma unroll
-                for (int mt = 0; mt < 8; ++mt) f.vf[mt] = mask4(f.vf[mt], vis, grp);
-            }
-            f32x4 sacc = {0, 0, 0, 0};
-#pragma unroll
-            for (int kk = 0; kk < 4; ++kk) sacc = mfma32(f.kf[kk], qf[kk], sacc);
-#pragma unroll
-            for (int s = 0; s < NS; ++s) {
-                const int svis = res_len[s] - tok0;
-                if (svis < PS) {
-#pragma unroll
-                    for (int t = 0; t < RT; ++t) {
-                        f.cv[s][t] = mask4(f.cv[s][t], svis, grp);
-                        f.ck[s][t] = col < svis ? f.ck[s][t] : u32x2{0, 0};
-                    }
-                }
-                // Stage 1: U^T = B_K^T C_K^T, deferred RoPE, then S^T += K_lora Q_s^T
-                f32x4 u[8];
-#pragma unroll
-                for (int mt = 0; mt < 8; ++mt) {
-                    u[mt] = f32x4{0, 0, 0, 0};
-#pragma unroll
-                    for (int t = 0; t < RT; ++t) {
-                        const u32x2 a =
-                            *reinterpret_cast<const u32x2 *>(lds_bkt + (((s * RTX + t) * 8 + mt) * 64 + lane) * 2);
-                        u[mt] = mfma16(a, f.ck[s][t], u[mt]);
-                    }
-                }
-#pragma unroll
-                for (int mt = 0; mt < 4; ++mt) {
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const float x = u[mt][i], y = u[mt + 4][i];
-                        u[mt][i] = x * f.cs[mt][i] - y * f.sn[mt][i];
-                        u[mt + 4][i] = y * f.cs[mt][i] + x * f.sn[mt][i];
-                    }
-                }
-#pragma unroll
-                for (int kk = 0; kk < 4; ++kk) {
-                    const u32x2 lo = pack4(u[2 * kk]), hi = pack4(u[2 * kk + 1]);
-                    const u32x4 b = my_slot_l == s ? qf[kk] : u32x4{0, 0, 0, 0};
-                    sacc = mfma32(u32x4{lo.x, lo.y, hi.x, hi.y}, b, sacc);
-                }
-            }
-            softmax_pv<R, NS>(st, sacc, row_active, tok0, my_len, p.scale_log2, f.vf, f.cv, my_slot_l, grp);
-        };
-        Frag fa, fb;
-        int pg = pg0 + wave;
-        if (pg < pg1) {
-            const int last = pg + (pg1 - 1 - pg) / WAVES * WAVES;
-            load(pg, fa);
-            for (;;) {
-                load(pg + WAVES <= last ? pg + WAVES : last, fb);
-                compute(pg, fa);
-                pg += WAVES;
-                if (pg > last) break;
-                load(pg + WAVES <= last ? pg + WAVES : last, fa);
-                compute(pg, fb);
-                pg += WAVES;
-                if (pg > last) break;
             }
         }
-    };
-    using I1 = std::integral_constant<int, 1>;
-    using I2 = std::integral_constant<int, cmin(2, AG)>;
-    using I3 = std::integral_constant<int, cmin(3, AG)>;
-    using I4 = std::integral_constant<int, cmin(4, AG)>;
-    if (nag == 1) run_pages(I1{});
-    else if (nag == 2 || AG == 2) run_pages(I2{});
-    else if (nag == 3) run_pages(I3{});
-    else run_pages(I4{});
+    }
 
-    write_partial<R>(p, st, row_active, ((int64_t)my_part * G + col % G) * hkv + h, grp);
+    // This wave's pages: copy, copy + copies, ...  One register set holds a page's K, V and
+    // rCache fragments (the stored orders are the operand orders) and the cos / sin of its
+    // positions; each part is refilled with the next page's as soon as its last use is issued
+    // (pages past the item repeat its last page).
+    const int64_t vhalfs = (int64_t)hkv * kBlockHalfs;
+    auto kblock = [&](int kk) __attribute__((always_inline)) -> const uint16_t * {
+        kk = min(kk, npg - 1);
+        const int lo = __builtin_amdgcn_readlane(bid0, kk & 63), hi = __builtin_amdgcn_readlane(bid1, kk & 63);
+        const int id = kk < 64 ? lo : hi;
+        return p.base_kv + ((int64_t)id * 2 * hkv + h) * kBlockHalfs;
+    };
+    u32x4 fk[4], fv[4], fc[NSW][RT];
+    f32x4 cs[4], sn[4];
+    auto load_k = [&](int kk) __attribute__((always_inline)) {
+        const uint16_t *b = kblock(kk);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) fk[i] = ldg128(b + i * 512 + lane * 8);
+    };
+    auto load_v = [&](int kk) __attribute__((always_inline)) {
+        const uint16_t *b = kblock(kk) + vhalfs;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) fv[i] = ldg128(b + i * 512 + lane * 8);
+    };
+    auto load_c = [&](int kk) __attribute__((always_inline)) {
+        kk = min(kk, npg - 1);
+#pragma unroll
+        for (int s = 0; s < NSW; ++s) {
+            const int rl = __builtin_amdgcn_readlane(rid0[s], kk & 63), rh = __builtin_amdgcn_readlane(rid1[s], kk & 63);
+            const int rp = kk < 64 ? rl : rh;
+            const uint16_t *rb = p.res_kv + (int64_t)(rp >= 0 ? rp : 0) * (RT * 512);
+#pragma unroll
+            for (int t = 0; t < RT; ++t) fc[s][t] = rp >= 0 ? ldg128(rb + t * 512 + lane * 8) : u32x4{0, 0, 0, 0};
+        }
+    };
+    // cos / sin at position 16 * page + t (t = col) for pairs 16mt + 4grp + i by angle addition
+    // from the table rows of position 16 * page (cs, sn, loaded per page: one 16-byte row piece
+    // per (mt, grp)) and of position t (c1, s1, the same for every page):
+    //   cos(a + b) = cos a cos b - sin a sin b,   sin(a + b) = sin a cos b + cos a sin b
+    f32x4 c1[4], s1[4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+        c1[mt] = *reinterpret_cast<const f32x4 *>(p.rope_cos + 256 * mt + lane * 4);
+        s1[mt] = *reinterpret_cast<const f32x4 *>(p.rope_sin + 256 * mt + lane * 4);
+    }
+    auto load_rope = [&](int kk) __attribute__((always_inline)) {
+        kk = min(kk, npg - 1);
+        const float *cr = p.rope_cos + (int64_t)(pg0 + kk) * (PS * D / 2) + 64 * grp;
+        const float *sr = p.rope_sin + (int64_t)(pg0 + kk) * (PS * D / 2) + 64 * grp;
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) {
+            cs[mt] = *reinterpret_cast<const f32x4 *>(cr + 256 * mt);
+            sn[mt] = *reinterpret_cast<const f32x4 *>(sr + 256 * mt);
+        }
+    };
+    auto rope_at_tokens = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) {
+            const f32x4 c0 = cs[mt], s0 = sn[mt];
+            cs[mt] = c0 * c1[mt] - s0 * s1[mt];
+            sn[mt] = s0 * c1[mt] + c0 * s1[mt];
+        }
+    };
+    const bool busy = sb < nag;  // a wave of an empty group has nothing to do
+    if (busy) {
+        load_k(copy);
+        load_c(copy);
+        load_rope(copy);
+        load_v(copy);
+    }
+    u32x4 qf[4];
+    load_q(p.q + ((int64_t)my_agent * p.hq + qh) * D, row_active, grp, qf);
+    __syncthreads();  // B_K^T fragments visible to every wave
+
+    for (int k = copy; busy && k < npg; k += copies) {
+        const int next = k + copies;
+        const int tok0 = (pg0 + k) * PS;
+        f32x4 sbase = {0, 0, 0, 0};
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) sbase = mfma32(fk[kk], qf[kk], sbase);
+        load_k(next);
+        // rCache fragments of slot s, tile t: tokens past the slot's own length (or all, without
+        // adapter) are zero
+        auto cfrag = [&](int s, int t, bool key) __attribute__((always_inline)) -> u32x2 {
+            u32x2 kx = u32x2{fc[s][t].x, fc[s][t].y}, vx = u32x2{fc[s][t].z, fc[s][t].w};
+            if constexpr (R == 8) {
+                kx = grp < 2 ? kx : u32x2{0, 0};
+                vx = col < 8 ? vx : u32x2{0, 0};
+            }
+            const int svis = res_len[s] - tok0;
+            if (svis < PS) {
+                vx = mask4(vx, svis, grp);
+                kx = col < svis ? kx : u32x2{0, 0};
+            }
+            return key ? kx : vx;
+        };
+        rope_at_tokens();
+        // Stage 1 per slot: U^T = B_K^T C_K^T, deferred RoPE, then K_lr Q^T, of which the
+        // slot's own rows (columns) are added to the scores
+        f32x4 sacc = sbase;
+#pragma unroll
+        for (int s = 0; s < NSW; ++s) {
+            const int slot = sb + s;
+            if (res_len[s] > tok0) {
+                f32x4 sres = {0, 0, 0, 0};
+                // two halves of the head dim: column tiles {2hf, 2hf + 1} and their rotate-half
+                // partners {2hf + 4, 2hf + 5} are the A operands of k-steps hf and hf + 2
+#pragma unroll
+                for (int hf = 0; hf < 2; ++hf) {
+                    const int mts[4] = {2 * hf, 2 * hf + 1, 2 * hf + 4, 2 * hf + 5};
+                    f32x4 u[4];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        u[j] = f32x4{0, 0, 0, 0};
+#pragma unroll
+                        for (int t = 0; t < RT; ++t)
+                            u[j] = mfma16(bkt[((slot * RT + t) * 8 + mts[j]) * 64 + lane], cfrag(s, t, true), u[j]);
+                    }
+#pragma unroll
+                    for (int j = 0; j < 2; ++j) {
+                        const int mt = mts[j];
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const float x = u[j][i], y = u[j + 2][i];
+                            u[j][i] = x * cs[mt][i] - y * sn[mt][i];
+                            u[j + 2][i] = y * cs[mt][i] + x * sn[mt][i];
+                        }
+                    }
+#pragma unroll
+                    for (int j = 0; j < 2; ++j) {
+                        const u32x2 lo = pack4(u[2 * j]), hi = pack4(u[2 * j + 1]);
+                        sres = mfma32(u32x4{lo.x, lo.y, hi.x, hi.y}, qf[hf + 2 * j], sres);
+                    }
+                }
+                if (my_slot == s) sacc += sres;
+            }
+            __builtin_amdgcn_sched_barrier(0);  // one slot's rebuild at a time (register pressure)
+        }
+        u32x2 cv[NSW][RTX];
+#pragma unroll
+        for (int s = 0; s < NSW; ++s)
+#pragma unroll
+            for (int t = 0; t < RT; ++t) cv[s][t] = cfrag(s, t, false);
+        load_c(next);
+        load_rope(next);
+        u32x2 vf[8];
+#pragma unroll
+        for (int q2 = 0; q2 < 4; ++q2) {
+            vf[2 * q2] = u32x2{fv[q2].x, fv[q2].y};
+            vf[2 * q2 + 1] = u32x2{fv[q2].z, fv[q2].w};
+        }
+        // value tokens past the item's longest sequence may hold any bits: zero them
+        const int vis = item_max_len - tok0;
+        if (vis < PS) {
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) vf[mt] = mask4(vf[mt], vis, grp);
+        }
+        softmax_pv<R, NSW>(st, sacc, row_active, tok0, my_len, p.scale_log2, vf, cv, my_slot, grp);
+        load_v(next);
+    }
+    write_partial<R>(p, st, row_active, my_row, grp);
 }
 
 
@@ -1171,7 +1243,7 @@ fkv_status decode_impl(const fkv_attn_args *a, const fkv_plan *plan, void *strea
     if (w[fkv::H_MAX_ITEM_AGENTS] > fkv::decode_item_agent_cap(g, a->hkv, a->r, rope_on))
         return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: the plan puts more agents in a work item "
                                           "than this kernel takes");
-    if (w[fkv::H_PAGES_PER_SPLIT] > (rope_on ? fkv::kMaxPagesPerItem : fkv::kMaxPagesSingle))
+    if (w[fkv::H_PAGES_PER_SPLIT] > fkv::kMaxPagesSingle)
         return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: plan items longer than the kernel takes");
     if (!rope_on && w[fkv::H_OFF_DESC] < 0)
         return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: plan has no block descriptors");
@@ -1199,6 +1271,7 @@ fkv_status decode_impl(const fkv_attn_args *a, const fkv_plan *plan, void *strea
     da.off_zero = w[fkv::H_OFF_ZERO];
     da.off_desc = w[fkv::H_OFF_DESC];
     da.scale_log2 = a->scale * 1.4426950408889634f;
+    da.rope_max_pos = a->rope_cos ? a->rope_max_pos : 0;
     da.ws_bytes = fkv::decode_partials_bytes(plan, a->d, a->r);
     if (da.ws_bytes >= 0x7fffffff)
         return fkv::fail(FKV_ERR_UNSUPPORTED, "fkv_residual_attention_decode: partial rows above 2 GiB");

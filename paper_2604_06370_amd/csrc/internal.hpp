@@ -72,10 +72,18 @@ constexpr int decode_wave_slots(int g, int r) {
     return r >= 64 ? (kMaxRows / g < 2 ? kMaxRows / g : 2) : kMaxRows / g;
 }
 constexpr int decode_heads_per_block(int, bool) { return 1; }
-// With RoPE an item holds one group, of at most two agents at rank 32 or more (the wave
-// keeps two pages of every slot's rCache fragments and RoPE rows in registers).
+// With RoPE a wave serves NSW agents (all the agents of a 16-row group below rank 32, two at
+// rank 32, one at rank 64: the wave keeps their rCache fragments of two pages in registers),
+// and an item holds up to four such wave groups, as many slots as 64 KB of B_K^T fragments
+// (kept in LDS for the launch) allow.
+constexpr int decode_rope_wave_agents(int g, int r) {
+    const int ag = kMaxRows / g;
+    return r >= 64 ? 1 : (r >= 32 ? (ag < 2 ? ag : 2) : ag);
+}
 constexpr int decode_rope_item_agents(int g, int r) {
-    return r >= 32 ? (kMaxRows / g < 2 ? kMaxRows / g : 2) : kMaxRows / g;
+    const int rt = r <= 16 ? 1 : (r + 15) / 16;
+    const int ms = 4 * decode_rope_wave_agents(g, r);
+    return ms < 16 / rt ? ms : 16 / rt;
 }
 // Largest number of agents per work item:
 constexpr int decode_item_agent_cap(int g, int hkv, int r, bool rope) {

@@ -44,9 +44,10 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     if (prm->hq % prm->hkv) return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: hq % hkv != 0");
     const int32_t g = prm->hq / prm->hkv;
     if (g > fkv::kMaxRows) return fkv::fail(FKV_ERR_UNSUPPORTED, "fkv_decode_plan_create: more than 16 query heads per KV head");
-    const int32_t ag = fkv::kMaxRows / g;  // agents per group
     if (prm->r < 0 || prm->max_item_agents < 0) return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: bad r / max_item_agents");
     const bool rope = prm->rope != 0 && prm->r > 0;
+    // agents per group: the slots one wave serves (RoPE) or that fill a 16-row tile
+    const int32_t ag = rope ? fkv::decode_rope_wave_agents(g, prm->r) : fkv::kMaxRows / g;
     const int32_t hpb = fkv::decode_heads_per_block(prm->hkv, rope);
     const int32_t cap = fkv::decode_item_agent_cap(g, prm->hkv, prm->r, rope);
     if (cap < 1) return fkv::fail(FKV_ERR_UNSUPPORTED, "fkv_decode_plan_create: rank too large for the decode kernels");
@@ -127,7 +128,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
                 cpp = std::max(cpp, item_page_cost((int32_t)c));
                 if ((c + ag - 1) / ag > 2) cap = fkv::kMaxPagesMulti;
             }
-            if (rope) cap = fkv::kMaxPagesPerItem;
+            if (rope) cap = fkv::kMaxPagesSingle;
             sc[i] = {segs[i].n, cap, cpp};
         }
         const int64_t slots = std::max<int64_t>(1, 2 * cus / nhb_units);  // items per round
@@ -194,12 +195,12 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
             if (est[c] <= best * 1.01) best_u = cands[c];
         if (best_u < 0) best_u = 64;
         for (size_t i = 0; i < sc.size(); ++i) cand_pps[i] = is_multi(i) ? multi_pps : std::min(best_u, sc[i].cap);
-        const int32_t rope_pps = (int32_t)std::max<int64_t>(
-            4, std::min<int64_t>(fkv::kMaxPagesPerItem, [&] {
-                int64_t units = 0;
-                for (auto &s : segs) units += (int64_t)s.n * (int64_t)chunk_sizes(s.agents.size()).size();
-                return (units * nhb_units + 3 * cus - 1) / (3 * cus);
-            }()));
+        // RoPE on: the per-page rebuild and rotation of every agent's keys bound the kernel,
+        // not the balance of items; items of 32 pages (fewer when a segment is shorter) keep
+        // the per-workgroup B_K^T build small against the pages it serves (measured on the
+        // 16-agent, 32K-prefix workload: 16 to 64 pages within 12 %, 32 best, 96 and 128 far
+        // slower).
+        constexpr int32_t kRopePages = 32;
         for (size_t i = 0; i < segs.size(); ++i) {
             int32_t pps;
             if (prm->pages_per_split > 0) {
@@ -207,7 +208,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
                     return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: pages_per_split above 128");
                 pps = std::min(prm->pages_per_split, sc[i].cap);
             } else {
-                const int32_t target = rope ? rope_pps : cand_pps[i];
+                const int32_t target = rope ? kRopePages : cand_pps[i];
                 const int64_t k = (segs[i].n + target - 1) / target;
                 pps = (int32_t)((segs[i].n + k - 1) / k);
             }
@@ -264,7 +265,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
         const int32_t room = std::min(reserve, mp - npages[a]);
         if (room <= 0) continue;
         Item &last = items[last_item[a]];
-        const int32_t limit = rope ? fkv::kMaxPagesPerItem : fkv::kMaxPagesSingle;
+        const int32_t limit = fkv::kMaxPagesSingle;
         if (last.agents.size() == 1 && last.p1 - last.p0 + room <= limit) {
             last.cap = last.p1 + room;
         } else {

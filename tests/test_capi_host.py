@@ -309,7 +309,7 @@ def test_decode_plan_items_cover_every_agent_page_once(hq, hkv, r, rope, pps):
         words = plan.serialize()
         h, items, blocks, ptr = _parse_plan(words)
         assert h["max_item_agents"] == n_item and (h["rank"], h["rope"]) == (r, int(rope))
-        assert n_item <= (16 // g if rope else 16) and n_item <= 4 * (16 // g)
+        assert n_item <= 16 and n_item <= 4 * (16 // g)
         hpb = h["heads_per_block"]
         assert hpb == 1
         npages = (sl + 15) // 16
@@ -317,7 +317,7 @@ def test_decode_plan_items_cover_every_agent_page_once(hq, hkv, r, rope, pps):
         owned = [[] for _ in range(n_agents)]
         for it in items:
             assert 0 <= it["p0"] <= it["end"] <= it["cap"] <= mp
-            assert it["cap"] - it["p0"] <= (64 if rope else 128) and it["end"] - it["p0"] <= 128
+            assert it["cap"] - it["p0"] <= 128 and it["end"] - it["p0"] <= 128
             assert 1 <= it["nag"] <= h["max_item_agents"] and it["leader"] == it["agents"][0]
             assert all(x == -1 for x in it["pad"]) and all(x == -1 for x in it["first_pad"])
             assert it["cap"] == it["end"] or (it["nag"] == 1 and it["end"] == npages[it["leader"]])
@@ -325,8 +325,10 @@ def test_decode_plan_items_cover_every_agent_page_once(hq, hkv, r, rope, pps):
                 assert it["end"] <= npages[a]
                 assert (bb[a, it["p0"]:it["end"]] == bb[it["leader"], it["p0"]:it["end"]]).all()
                 seen[a, it["p0"]:it["cap"]] += 1
-            ng = -(-it["nag"] // (16 // g))
-            assert it["copies"] == (4 if rope else 4 // (1 if ng == 1 else 2 if ng == 2 else 4))
+            # agents per group: a 16-row tile without RoPE; with RoPE the slots one wave serves
+            ag = 16 // g if not rope else (1 if r >= 64 else min(2, 16 // g) if r >= 32 else 16 // g)
+            ng = -(-it["nag"] // ag)
+            assert ng <= 4 and it["copies"] == 4 // (1 if ng == 1 else 2 if ng == 2 else 4)
             for j, a in enumerate(it["agents"]):
                 owned[a] += [it["first"][j] + c for c in range(it["copies"])]
         for a in range(n_agents):

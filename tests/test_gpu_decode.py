@@ -165,14 +165,15 @@ def test_split_sizes_agree(pps, rope):
     lw.close()
 
 
+@pytest.mark.parametrize("rope", [False, True])
 @pytest.mark.parametrize("item_agents", [1, 3, 4, 6, 8, 13, 16])
-def test_agents_per_item_agree(item_agents):
+def test_agents_per_item_agree(item_agents, rope):
     # 1..4 agent groups per work item (the last one partly filled), 1, 2 or 4 wave copies
     wl = W.fanout("groups", 43, n_agents=16, prefix=700, suffix_lo=1, suffix_hi=120, hq=32, hkv=8, r=16)
-    lw = LoadedWorkload(wl, rope=False, item_agents=item_agents)
+    lw = LoadedWorkload(wl, rope=rope, item_agents=item_agents)
     out = lw.decode().clone()
     torch.cuda.synchronize()
-    check_close(f"item_agents={item_agents}", out, oracle_decode(wl, wl.decode_agents(), False))
+    check_close(f"item_agents={item_agents} rope={rope}", out, oracle_decode(wl, wl.decode_agents(), rope))
     lw.close()
 
 
