@@ -245,10 +245,11 @@ struct SplitShape {
     static constexpr int AG = ROWS / G;                                         // agents per group
     static constexpr int RT = R == 0 ? 0 : (R + 15) / 16;                       // 16-wide rank tiles
     static constexpr int RTX = RT > 0 ? RT : 1;
-    static constexpr bool MULTI = R < 32;                                       // several groups per item
+    static constexpr int NG = fkv::decode_item_groups(G, R);                    // agent groups per item
+    static constexpr bool MULTI = NG > 1;                                       // several groups per item
     static constexpr int NSW = fkv::decode_wave_slots(G, R);                    // agent slots per wave
     static constexpr int NSR = R > 0 ? NSW : 1;
-    static constexpr int MAX_SLOTS = MULTI ? cmin(fkv::kMaxGroups * AG, fkv::kMaxItemAgents) : NSW;
+    static constexpr int MAX_SLOTS = MULTI ? cmin(NG * AG, fkv::kMaxItemAgents) : NSW;
     static constexpr int RES_PAGE = RT * 512;                                   // rCache page (halfs)
 };
 
@@ -674,8 +675,12 @@ __device__ __forceinline__ void split_body(const DecodeArgs &p) {
                 wait_vmcnt<0>();  // no copy into LDS outlives the block
             };
             (void)npw;
-            if (ngp == 4) run(NSF{}, I2{});
-            else run(NSF{}, I1{});
+            if constexpr (S::NG == 4) {
+                if (ngp == 4) run(NSF{}, I2{});
+                else run(NSF{}, I1{});
+            } else {
+                run(NSF{}, I1{});  // two groups at most: one page per wave and stage
+            }
         }
     } else {
         // One agent group: no page is shared between waves.  Wave w computes item pages
@@ -746,7 +751,7 @@ __device__ __forceinline__ void split_body(const DecodeArgs &p) {
 }
 
 template <int R, int G>
-__global__ __launch_bounds__(256, R >= 32 ? 1 : 2) void decode_split_kernel(DecodeArgs p) {
+__global__ __launch_bounds__(256, R >= 64 ? 1 : 2) void decode_split_kernel(DecodeArgs p) {
     split_body<R, G>(p);
 }
 

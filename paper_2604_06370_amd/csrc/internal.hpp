@@ -63,10 +63,10 @@ constexpr int kDescAgent = 8;
 constexpr int kDescPart = kDescAgent + kMaxItemAgents;
 constexpr int kDescWords = kDescPart + kMaxItemAgents;
 
-// Decode: one workgroup per (work item, KV head).  Without RoPE and with rank below 32 an
-// item holds up to four agent groups (their base pages are shared through LDS); with
-// rank 32 or more it holds one group, of at most two agents at rank 64 (the wave keeps
-// every slot's rCache fragments of a stage in registers).  With RoPE an item holds one
+// Decode: one workgroup per (work item, KV head).  Without RoPE an item holds up to four
+// agent groups below rank 32 and up to two at rank 32 (and at rank 64 with eight query heads
+// per KV head), their base pages shared through LDS; otherwise one group, of at most two
+// agents at rank 64 (the wave keeps every slot's rCache fragments of a stage in registers).  With RoPE an item holds one
 // group.  Agent slots one wave serves without RoPE:
 constexpr int decode_wave_slots(int g, int r) {
     return r >= 64 ? (kMaxRows / g < 2 ? kMaxRows / g : 2) : kMaxRows / g;
@@ -86,12 +86,19 @@ constexpr int decode_rope_item_agents(int g, int r) {
     return ms < 16 / rt ? ms : 16 / rt;
 }
 // Largest number of agents per work item:
+// Agent groups one RoPE-off work item may hold: four below rank 32; two at rank 32 and at
+// rank 64 when one wave serves a whole group (a stage's rCache fragments of a group then fit the
+// registers of four groups at rank 16); one otherwise.
+constexpr int decode_item_groups(int g, int r) {
+    return r < 32 ? kMaxGroups : (decode_wave_slots(g, r) >= kMaxRows / g ? 2 : 1);
+}
 constexpr int decode_item_agent_cap(int g, int hkv, int r, bool rope) {
     (void)hkv;
     const int ag = kMaxRows / g;
     if (rope && r > 0) return decode_rope_item_agents(g, r);
-    if (r >= 32) return decode_wave_slots(g, r);
-    return kMaxGroups * ag < kMaxItemAgents ? kMaxGroups * ag : kMaxItemAgents;
+    const int ng = decode_item_groups(g, r);
+    if (ng == 1) return decode_wave_slots(g, r);
+    return ng * ag < kMaxItemAgents ? ng * ag : kMaxItemAgents;
 }
 
 enum PlanHeader {
