@@ -309,6 +309,30 @@ def decode_entry(wl, dev, stream, rope: bool, steps: int, warmup: int, copies: i
             "partial_bytes": info["workspace_bytes"]}
 
 
+def graph_entry(wl, dev, rope: bool, steps: int) -> dict:
+    """Per-step wall time of the decode call issued eagerly and replayed from a HIP graph
+    captured once (small shapes are bound by launch overhead)."""
+    import torch
+    from paper_2604_06370_amd.driver import LoadedWorkload
+    lw = LoadedWorkload(wl, device=dev, rope=rope)
+    lw.decode_setup()
+    graph = lw.capture_decode_graph()
+    res = {"workload": wl.name, "rope": rope, "agents": len(wl.decode_agents()), "steps": steps}
+    for name, fn in (("eager", lambda: lw.decode()), ("graph", lambda: graph.replay())):
+        for _ in range(5):
+            fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            fn()
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / steps
+        res[name] = {"us_per_step": dt * 1e6, "tokens_per_s": len(wl.decode_agents()) / dt}
+    del graph
+    lw.close()
+    return res
+
+
 def plan_cost(wl, dev, rope: bool, reps: int = 5) -> dict:
     """Host cost of a decode plan for this workload (build + serialise, then the copy to the
     device), and how many decode steps it serves: it stays valid until an agent outgrows its
@@ -383,6 +407,8 @@ def suite(args, dev, stream) -> dict:
     w1 = W.config(1)
     run("tiny_4agents_rope_off", lambda: decode_entry(w1, dev, stream, False, st, 3, 3))
     run("tiny_4agents_rope_on", lambda: decode_entry(w1, dev, stream, True, st, 3, 3))
+    run("tiny_4agents_graph_rope_off", lambda: graph_entry(w1, dev, False, 200))
+    run("tiny_4agents_graph_rope_on", lambda: graph_entry(w1, dev, True, 200))
     w4 = W.config(4)
     run("fanout_64agents_128k_rope_off", lambda: decode_entry(w4, dev, stream, False, st, 2, 1))
     run("fanout_64agents_128k_rope_on", lambda: decode_entry(w4, dev, stream, True, st, 2, 1))

@@ -285,8 +285,9 @@ typedef struct {
     int32_t n_agents, hq, hkv, d, r, page_size, max_pages;
     int32_t rope_max_pos;       /* rows of the RoPE tables; every key position must be below it */
     int32_t n_q;                /* prefill: total query rows (= q_indptr[n_agents]) */
-    int32_t max_q_per_agent;    /* prefill: largest q_indptr[a+1] - q_indptr[a]; 0 = n_q.  Rows beyond
-                                   it are not computed, so it must not be understated. */
+    int32_t max_q_per_agent;    /* prefill: largest q_indptr[a+1] - q_indptr[a] (sizes the grid); 0 = n_q,
+                                   always enough.  If understated, the rows of an agent past it are
+                                   not computed and are written as NaN. */
     float scale;                /* softmax scale; typically 1/sqrt(d) */
     void *const *timing_events; /* optional, host array of hipEvent_t (created with timing enabled), set by
                                    the launches to the kernels' own execution timestamps: decode [0] start

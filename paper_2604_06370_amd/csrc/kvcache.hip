@@ -19,6 +19,8 @@
 #include "internal.hpp"
 #include "mfma.hpp"
 
+using namespace fkvk;
+
 namespace {
 
 // Offsets of (token t, dim dd) inside a K or V block (see the layout note above).
@@ -66,8 +68,34 @@ struct CopyArgs {
     int32_t hkv, d, r, ps;
 };
 
-// One workgroup per copy; each thread moves whole 16-bit elements whose token slot
-// is below n_valid.
+// One workgroup per copy.  Each thread moves 16-byte chunks: in both pools' layouts every
+// chunk of 8 values holds tokens of at most four consecutive slots, so a chunk whose slots are
+// all below n_valid is copied whole, one with none is skipped, and one that straddles n_valid
+// (a value chunk of four tokens, or an rCache chunk) is copied value by value.
+template <typename SlotOf>
+__device__ __forceinline__ void copy_chunks(const uint16_t *src, uint16_t *dst, int64_t elems, int n_valid,
+                                            SlotOf slot_of) {
+    const int64_t chunks = elems / 8;
+    for (int64_t c = threadIdx.x; c < chunks; c += blockDim.x) {
+        int lo = 1 << 30, hi = -1;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int sl = slot_of(8 * c + e);
+            lo = min(lo, sl);
+            hi = max(hi, sl);
+        }
+        if (hi < n_valid) {
+            reinterpret_cast<u32x4 *>(dst)[c] = reinterpret_cast<const u32x4 *>(src)[c];
+        } else if (lo < n_valid) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                if (slot_of(8 * c + e) < n_valid) dst[8 * c + e] = src[8 * c + e];
+        }
+    }
+    for (int64_t e = chunks * 8 + threadIdx.x; e < elems; e += blockDim.x)
+        if (slot_of(e) < n_valid) dst[e] = src[e];
+}
+
 __global__ __launch_bounds__(256) void page_copy_kernel(CopyArgs a) {
     const fkv_page_copy c = a.copies[blockIdx.x];
     const int n_valid = c.n_valid;
@@ -76,18 +104,31 @@ __global__ __launch_bounds__(256) void page_copy_kernel(CopyArgs a) {
         const int64_t page = 2 * a.hkv * blk;
         const uint16_t *src = a.base_kv + (int64_t)c.src * page;
         uint16_t *dst = a.base_kv + (int64_t)c.dst * page;
-        for (int64_t e = threadIdx.x; e < page; e += blockDim.x) {
-            const int64_t within = e % blk;
-            const bool is_v = (e / blk) >= a.hkv;
-            const int slot = is_v ? v_slot(within, a.ps, a.d) : k_slot(within, a.ps, a.d);
-            if (slot < n_valid) dst[e] = src[e];
+        const int hkv = a.hkv, ps = a.ps, d = a.d;
+        if (blk % 8 == 0) {
+            // chunks never straddle a block: K blocks first (hkv of them), then V blocks
+            copy_chunks(src, dst, page, n_valid, [=](int64_t e) {
+                const int64_t within = e % blk;
+                return (e / blk) >= hkv ? v_slot(within, ps, d) : k_slot(within, ps, d);
+            });
+        } else {
+            for (int64_t e = threadIdx.x; e < page; e += blockDim.x) {
+                const int64_t within = e % blk;
+                const int slot = (e / blk) >= hkv ? v_slot(within, ps, d) : k_slot(within, ps, d);
+                if (slot < n_valid) dst[e] = src[e];
+            }
         }
     } else {
         const int64_t page = res_page_elems(a.ps, a.r);
         const uint16_t *src = a.res_kv + (int64_t)c.src * page;
         uint16_t *dst = a.res_kv + (int64_t)c.dst * page;
-        for (int64_t e = threadIdx.x; e < page; e += blockDim.x)
-            if (c_slot(e, a.ps, a.r) < n_valid) dst[e] = src[e];
+        const int ps = a.ps, r = a.r;
+        if (ps == 16) {
+            copy_chunks(src, dst, page, n_valid, [=](int64_t e) { return c_slot(e, ps, r); });
+        } else {
+            for (int64_t e = threadIdx.x; e < page; e += blockDim.x)
+                if (c_slot(e, ps, r) < n_valid) dst[e] = src[e];
+        }
     }
 }
 
@@ -99,8 +140,95 @@ struct ScatterArgs {
     int32_t hkv, d, r, ps;
 };
 
-// Grid: one workgroup per token; threads cover (head, dim) for the base pool and
-// the rank for the residual pool.
+// Page size 16, head dim 128: one workgroup per page the range [pos0, pos0 + n) touches.  Every
+// 16-byte chunk of the fragment-ordered blocks is formed in registers from the source rows and
+// stored whole: a K chunk is 8 dims of one token (two 8-byte pieces of its row); a V chunk is 2
+// dims of four consecutive tokens and an rCache chunk 4 ranks of one token (C_K) and one rank of
+// four tokens (C_V), so chunks whose tokens are only partly in the range are written value by
+// value (slots outside the range, and the rank padding of r = 8, keep their bits).
+__global__ __launch_bounds__(256) void scatter_page_kernel(ScatterArgs a) {
+    constexpr int PS = 16, D = 128;
+    const int64_t first_page = a.pos0 / PS;
+    const int64_t lp = first_page + blockIdx.x;
+    const int64_t s0 = lp * PS;  // position of slot 0 of this page
+    const int t_lo = (int)max<int64_t>(0, a.pos0 - s0), t_hi = (int)min<int64_t>(PS, a.pos0 + a.n - s0);
+    auto row = [&](int t) { return s0 + t - a.pos0; };  // source row of slot t
+    const int hkv = a.hkv;
+    if (a.k_src) {
+        uint16_t *pg = a.base_kv + (int64_t)a.bt_base[lp] * 2 * hkv * PS * D;
+        // K: chunk (head, quarter q, lane L = t + 16 g) = dims 32q + 4g + 0..3 and 32q + 16 + 4g + 0..3 of token t
+        for (int c = threadIdx.x; c < hkv * 4 * 64; c += blockDim.x) {
+            const int hh = c / 256, q = (c / 64) % 4, L = c % 64;
+            const int t = L % 16, g = L / 16;
+            if (t < t_lo || t >= t_hi) continue;
+            const uint16_t *src = a.k_src + (row(t) * hkv + hh) * D + 32 * q + 4 * g;
+            const u32x2 lo = ldg64(src), hi = ldg64(src + 16);
+            *reinterpret_cast<u32x4 *>(pg + (int64_t)hh * PS * D + q * 512 + L * 8) = u32x4{lo.x, lo.y, hi.x, hi.y};
+        }
+        // V: chunk (head, quarter q, lane L = c + 16 tg) = dim 32q + c of tokens 4tg + 0..3, then dim 32q + 16 + c
+        uint16_t *pv = pg + (int64_t)hkv * PS * D;
+        for (int c = threadIdx.x; c < hkv * 4 * 64; c += blockDim.x) {
+            const int hh = c / 256, q = (c / 64) % 4, L = c % 64;
+            const int dc = L % 16, tg = L / 16;
+            const int ta = 4 * tg, tb = ta + 4;
+            if (tb <= t_lo || ta >= t_hi) continue;
+            uint16_t *dst = pv + (int64_t)hh * PS * D + q * 512 + L * 8;
+            if (ta >= t_lo && tb <= t_hi) {
+                uint16_t v[8];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const uint16_t *src = a.v_src + (row(ta + i) * hkv + hh) * D + 32 * q + dc;
+                    v[i] = src[0];
+                    v[4 + i] = src[16];
+                }
+                u32x4 w;
+                w.x = v[0] | ((uint32_t)v[1] << 16);
+                w.y = v[2] | ((uint32_t)v[3] << 16);
+                w.z = v[4] | ((uint32_t)v[5] << 16);
+                w.w = v[6] | ((uint32_t)v[7] << 16);
+                *reinterpret_cast<u32x4 *>(dst) = w;
+            } else {
+                for (int i = 0; i < 4; ++i) {
+                    const int t = ta + i;
+                    if (t < t_lo || t >= t_hi) continue;
+                    const uint16_t *src = a.v_src + (row(t) * hkv + hh) * D + 32 * q + dc;
+                    dst[i] = src[0];
+                    dst[4 + i] = src[16];
+                }
+            }
+        }
+    }
+    if (a.ck_src && a.r > 0) {
+        const int r = a.r, rt = (r + 15) / 16;
+        uint16_t *pg = a.res_kv + (int64_t)a.bt_res[lp] * rt * 512;
+        // tile k, lane L = c + 16 g: C_K[token c][16k + 4g + 0..3] at L*8, C_V[tokens 4g + 0..3][16k + c] at L*8 + 4
+        for (int c = threadIdx.x; c < rt * 64; c += blockDim.x) {
+            const int k = c / 64, L = c % 64;
+            const int tc = L % 16, g = L / 16;
+            uint16_t *dst = pg + k * 512 + L * 8;
+            if (tc >= t_lo && tc < t_hi && 16 * k + 4 * g < r) {
+                const uint16_t *src = a.ck_src + row(tc) * r + 16 * k + 4 * g;
+                if (r % 4 == 0) {
+                    *reinterpret_cast<u32x2 *>(dst) = ldg64(src);
+                } else {
+                    for (int i = 0; i < 4 && 16 * k + 4 * g + i < r; ++i) dst[i] = src[i];
+                }
+            }
+            const int rho = 16 * k + tc;
+            if (rho < r) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int t = 4 * g + i;
+                    if (t < t_lo || t >= t_hi) continue;
+                    dst[4 + i] = a.cv_src[row(t) * r + rho];
+                }
+            }
+        }
+    }
+}
+
+// Other shapes: one workgroup per token; threads cover (head, dim) for the base pool and the
+// rank for the residual pool.
 __global__ __launch_bounds__(256) void scatter_kernel(ScatterArgs a) {
     const int64_t j = blockIdx.x;
     const int64_t pos = a.pos0 + j;
@@ -430,7 +558,12 @@ fkv_status fkv_scatter_tokens(const int32_t *bt_base, const int32_t *bt_res, int
                   static_cast<const uint16_t *>(k_src), static_cast<const uint16_t *>(v_src),
                   static_cast<const uint16_t *>(ck_src), static_cast<const uint16_t *>(cv_src),
                   static_cast<uint16_t *>(base_kv), static_cast<uint16_t *>(res_kv), hkv, d, r, page_size};
-    hipLaunchKernelGGL(scatter_kernel, dim3((unsigned)n), dim3(256), 0, static_cast<hipStream_t>(stream), a);
+    if (page_size == 16 && d == 128) {
+        const int64_t pages = (pos0 + n - 1) / 16 - pos0 / 16 + 1;
+        hipLaunchKernelGGL(scatter_page_kernel, dim3((unsigned)pages), dim3(256), 0, static_cast<hipStream_t>(stream), a);
+    } else {
+        hipLaunchKernelGGL(scatter_kernel, dim3((unsigned)n), dim3(256), 0, static_cast<hipStream_t>(stream), a);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fkv::fail(FKV_ERR_HIP, std::string("fkv_scatter_tokens: ") + hipGetErrorString(e));
     return FKV_OK;

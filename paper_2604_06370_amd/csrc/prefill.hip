@@ -51,6 +51,20 @@ struct PrefillArgs {
     float scale_log2;
 };
 
+
+// Rows of an agent's chunk that its query blocks do not reach (a max_q_per_agent below the
+// agent's row count) are written as NaN by the agent's last block, so the shortfall shows in
+// the output instead of leaving stale memory there.
+__device__ __forceinline__ void poison_unreached_rows(const PrefillArgs &p, int q0, int nq, int h, int g, int reach) {
+    const uint32_t nan2 = 0x7fc07fc0u;  // two bf16 quiet NaNs
+    for (int64_t i = threadIdx.x; i < (int64_t)(nq - reach) * g * 32; i += blockDim.x) {
+        const int64_t row = i / 32, c = i % 32;
+        const int tok = reach + (int)(row / g), j = (int)(row % g);
+        uint16_t *orow = p.out + ((int64_t)(q0 + tok) * p.hq + h * g + j) * 128;
+        *reinterpret_cast<u32x2 *>(orow + 4 * c) = u32x2{nan2, nan2};
+    }
+}
+
 template <int R, int G, bool ROPE>
 struct PrefillShape {
     static constexpr int RT = R == 0 ? 0 : (R + 15) / 16;
@@ -92,6 +106,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
     const int h = pair - a * hkv;
     const int q0 = p.q_indptr[a], nq = p.q_indptr[a + 1] - q0;
     const int tok_begin = qb * TPW;
+    if (qb == bpa - 1 && nq > bpa * TPW) poison_unreached_rows(p, q0, nq, h, G, bpa * TPW);
     if (tok_begin >= nq) return;
     const int L = p.seq_lens[a];
     const int P0 = L - nq;  // position of the chunk's first query
@@ -494,6 +509,7 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
     const int h = pair - a * hkv;
     const int q0 = p.q_indptr[a], nq = p.q_indptr[a + 1] - q0;
     const int tok_begin = qb * TPW;
+    if (qb == bpa - 1 && nq > bpa * TPW) poison_unreached_rows(p, q0, nq, h, G, bpa * TPW);
     if (tok_begin >= nq) return;
     const int L = p.seq_lens[a];
     const int P0 = L - nq;  // position of the chunk's first query

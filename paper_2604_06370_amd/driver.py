@@ -164,6 +164,22 @@ class LoadedWorkload:
                               _bf16(rows["c_v"], dev), self.base_kv, self.res_kv, hkv, d, r, ps)
         return fp
 
+    def capture_decode_graph(self):
+        """Record one decode call (split and merge launches) into a HIP graph on a side stream;
+        replaying it re-runs the call on whatever the decode tables and caches then hold (the
+        plan, tables and workspace keep their addresses).  Returns the torch graph object."""
+        if self._decode is None:
+            self.decode_setup()
+        side = torch.cuda.Stream(device=self.device)
+        side.wait_stream(torch.cuda.current_stream(self.device))
+        with torch.cuda.stream(side):
+            self.decode(side)  # warm-up outside the capture
+        torch.cuda.current_stream(self.device).wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            self.decode()
+        return graph
+
     def refresh_decode_tables(self):
         """Copy the tree's current block tables and lengths into the decode call's device
         tables in place (the plan and the argument block keep pointing at them)."""

@@ -307,3 +307,36 @@ def test_one_plan_serves_consecutive_decode_steps(rope):
     assert all((L0[a] - 1) // 16 < (wl.seq_len[a] - 1) // 16 for a in agents)  # every agent took a new page
     assert np.array_equal(plan.serialize(), words0) and lw._decode["plan"] is plan
     lw.close()
+
+
+@pytest.mark.parametrize("rope", [False, True])
+def test_graph_replay_serves_decode_steps(rope):
+    """The decode call captured once in a HIP graph and replayed at every decode step (tables
+    and lengths refreshed in place between replays, eager work on the same stream between
+    them): each replay equals an eager call on the same state bit for bit and matches the
+    oracle."""
+    wl = W.config(1)
+    lw = LoadedWorkload(wl, rope=rope, headroom_pages=4)
+    st = lw.decode_setup()
+    graph = lw.capture_decode_graph()
+    agents = st["agents"]
+    rng = np.random.default_rng(3)
+    other = LoadedWorkload(W.fanout("graph-other", 90, n_agents=3, prefix=40, suffix_lo=1, suffix_hi=20, hq=8,
+                                    hkv=2, r=8), rope=rope)
+    for step in range(6):
+        if step:
+            for a in agents:
+                lw.append_token(a, W.append_decode_token(wl, a, rng))
+            st["plan"].covers(lw.refresh_decode_tables())
+        st["out"].fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        replayed = st["out"].clone()
+        other.decode()                     # eager work of the program between replays
+        eager = lw.decode().clone()
+        torch.cuda.synchronize()
+        assert torch.equal(replayed, eager), f"step {step}: graph replay differs from the eager call"
+        if step % 2 == 1:
+            check_close(f"graph step {step} rope={rope}", replayed, oracle_decode(wl, agents, rope))
+    other.close()
+    lw.close()

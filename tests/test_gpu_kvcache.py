@@ -1,0 +1,102 @@
+"""Cache writes on the GPU, bit for bit: fkv_scatter_tokens and fkv_page_copy_launch against the
+page layouts documented in include/forkkv.h, evaluated here in numpy (pools start as random
+bits; every slot a call must not touch keeps its bits).  Section 5.2: new tokens' bCache and
+rCache rows go into the page slots the tree hands out; a shared partial page is copied
+(its first n_valid slots) before it is written."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2604_06370_amd import runtime as rt
+
+pytestmark = pytest.mark.gpu
+
+PS, D = 16, 128
+
+
+def k_off(t, i):
+    return (i // 32) * 512 + (t + 16 * ((i % 16) // 4)) * 8 + 4 * ((i % 32) // 16) + i % 4
+
+
+def v_off(t, i):
+    return (i // 32) * 512 + (i % 16 + 16 * (t // 4)) * 8 + 4 * ((i // 16) % 2) + t % 4
+
+
+def ck_off(t, rho):
+    return (rho // 16) * 512 + (16 * ((rho % 16) // 4) + t) * 8 + rho % 4
+
+
+def cv_off(t, rho):
+    return (rho // 16) * 512 + (16 * (t // 4) + rho % 16) * 8 + 4 + t % 4
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda()
+
+
+def _host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy().view(np.uint16)
+
+
+@pytest.mark.parametrize("hkv,r,pos0,n", [(8, 16, 0, 1), (8, 16, 5, 37), (2, 8, 13, 70), (8, 32, 31, 2),
+                                          (4, 64, 16, 16), (8, 16, 3, 2048)])
+def test_scatter_matches_the_documented_layout(hkv, r, pos0, n):
+    rng = np.random.default_rng(pos0 * 7 + n)
+    rt_tiles = (r + 15) // 16
+    npages = (pos0 + n + PS - 1) // PS + 3
+    base = rng.integers(0, 1 << 16, size=(npages, 2, hkv, PS * D), dtype=np.uint16)
+    res = rng.integers(0, 1 << 16, size=(npages, rt_tiles * 512), dtype=np.uint16)
+    bt_b = rng.permutation(npages).astype(np.int32)
+    bt_r = rng.permutation(npages).astype(np.int32)
+    k = rng.integers(0, 1 << 16, size=(n, hkv, D), dtype=np.uint16)
+    v = rng.integers(0, 1 << 16, size=(n, hkv, D), dtype=np.uint16)
+    ck = rng.integers(0, 1 << 16, size=(n, r), dtype=np.uint16)
+    cv = rng.integers(0, 1 << 16, size=(n, r), dtype=np.uint16)
+    exp_b, exp_r = base.copy(), res.copy()
+    ti = np.arange(D)
+    for j in range(n):
+        p = pos0 + j
+        pb, pr, t = bt_b[p // PS], bt_r[p // PS], p % PS
+        for h in range(hkv):
+            exp_b[pb, 0, h, k_off(t, ti)] = k[j, h]
+            exp_b[pb, 1, h, v_off(t, ti)] = v[j, h]
+        for rho in range(r):               # rank padding (r = 8) keeps its bits
+            exp_r[pr, ck_off(t, rho)] = ck[j, rho]
+            exp_r[pr, cv_off(t, rho)] = cv[j, rho]
+    base_d, res_d = _dev(base), _dev(res)
+    print(f"case scatter hkv={hkv} r={r} pos0={pos0} n={n}", flush=True)
+    rt.scatter_tokens(_dev(bt_b), _dev(bt_r), pos0, _dev(k).view(torch.bfloat16), _dev(v).view(torch.bfloat16),
+                      _dev(ck).view(torch.bfloat16), _dev(cv).view(torch.bfloat16), base_d, res_d, hkv, D, r, PS)
+    assert np.array_equal(_host(base_d), exp_b)
+    assert np.array_equal(_host(res_d), exp_r)
+
+
+@pytest.mark.parametrize("hkv,r", [(8, 16), (2, 8), (8, 64)])
+def test_page_copies_move_exactly_the_valid_slots(hkv, r):
+    rng = np.random.default_rng(hkv + r)
+    rt_tiles = (r + 15) // 16
+    npages = 40
+    base = rng.integers(0, 1 << 16, size=(npages, 2, hkv, PS * D), dtype=np.uint16)
+    res = rng.integers(0, 1 << 16, size=(npages, rt_tiles * 512), dtype=np.uint16)
+    copies = []
+    valid = [1, 2, 3, 4, 5, 7, 8, 11, 15, 16]
+    for i, nv in enumerate(valid):
+        copies.append((0, 2 * i, 2 * i + 1, nv))        # base pool: page 2i -> 2i + 1
+        copies.append((1, 2 * i + 1, 2 * i, nv))        # residual pool: page 2i + 1 -> 2i
+    exp_b, exp_r = base.copy(), res.copy()
+    ti = np.arange(D)
+    for pool, src, dst, nv in copies:
+        for t in range(nv):
+            if pool == 0:
+                for h in range(hkv):
+                    for kv, off in ((0, k_off(t, ti)), (1, v_off(t, ti))):
+                        exp_b[dst, kv, h, off] = base[src, kv, h, off]
+            else:
+                for rho in range(16 * rt_tiles):
+                    for off in (ck_off(t, rho), cv_off(t, rho)):
+                        exp_r[dst, off] = res[src, off]
+    base_d, res_d = _dev(base), _dev(res)
+    rt.page_copy(copies, base_d, res_d, hkv, D, r, PS)
+    assert np.array_equal(_host(base_d), exp_b)
+    assert np.array_equal(_host(res_d), exp_r)

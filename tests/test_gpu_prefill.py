@@ -155,3 +155,25 @@ def test_config5_mixed_full_size_sampled(rope):
     pos = {int(x): i for i, x in enumerate(st["rows"])}
     check_close(f"cfg5-prefill rope={rope}", out_p[[pos[int(x)] for x in p["q_index"]]], ref)
     lw.close()
+
+
+def test_understated_row_count_shows_as_nan_rows():
+    """max_q_per_agent sizes the grid; rows of an agent beyond what it covers are not computed
+    and must come out as NaN (never stale memory), while the covered rows stay correct."""
+    wl = W.fanout("pf-maxq", 54, n_agents=2, prefix=64, suffix_lo=1, suffix_hi=10, hq=32, hkv=8, r=16, chunk=100)
+    lw = LoadedWorkload(wl, rope=False)
+    st = lw.prefill_setup()
+    st["args"].max_q_per_agent = 10          # one block of 64 tokens per agent (4 query heads per KV head)
+    st["out"].zero_()
+    out = lw.prefill().clone()
+    torch.cuda.synchronize()
+    o = out.float().cpu().numpy()
+    rows = st["rows"]
+    for i, a in enumerate(st["agents"]):
+        mine = o[i * 100:(i + 1) * 100]
+        assert np.isfinite(mine[:64]).all() and np.isnan(mine[64:]).all()
+    p = W.oracle_inputs(wl, agents=st["agents"], q_rows={a: np.arange(64) for a in st["agents"]}, rope=False)
+    ref = oracle.residual_attention(p)
+    pos = {int(x): i for i, x in enumerate(rows)}
+    check_close("maxq covered rows", out[[pos[int(x)] for x in p["q_index"]]], ref)
+    lw.close()
