@@ -185,6 +185,17 @@ fkv_status fkv_get_block_tables(const fkv_tree *tree, const int32_t *seq_ids, in
 
 fkv_status fkv_get_pool_stats(const fkv_tree *tree, fkv_pool_stats *out);
 
+/* Debug check (host copies) of the tables an attention call will read, for callers that build
+ * or edit tables themselves (the kernels trust every page id they are given): for each agent a,
+ * seq_lens[a] is in 1 .. max_pages * page_size, the first ceil(seq_lens[a] / page_size) entries
+ * of base_bt row a are in [0, num_base_pages), and, when adapter_idx[a] >= 0, those of res_bt
+ * row a are in [0, num_res_pages) (res_bt and adapter_idx may be NULL for r = 0).  Tables are
+ * [n_agents][max_pages].  FKV_ERR_INVALID names the first bad agent, page and id.  The Python
+ * binding runs it before every launch when the environment variable FKV_DEBUG is set. */
+fkv_status fkv_validate_tables(const int32_t *base_bt, const int32_t *res_bt, const int32_t *seq_lens,
+                               const int32_t *adapter_idx, int32_t n_agents, int32_t max_pages, int32_t page_size,
+                               int32_t num_base_pages, int32_t num_res_pages);
+
 /* ------------------------------------------------------------------------ */
 /* Decode plan (host).  Agents whose base block tables name the same physical */
 /* pages over a range of logical pages form a segment; each segment is split */

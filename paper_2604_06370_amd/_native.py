@@ -98,6 +98,7 @@ fkv_cow_append = _sig("fkv_cow_append", c_i32, [c_vp, c_i32, c_vp, c_i64, ctypes
 fkv_release = _sig("fkv_release", c_i32, [c_vp, c_i32])
 fkv_seq_info = _sig("fkv_seq_info", c_i32, [c_vp, c_i32, ctypes.POINTER(c_i64), P_i32])
 fkv_get_block_tables = _sig("fkv_get_block_tables", c_i32, [c_vp, c_vp, c_i32, c_i32, c_vp, c_vp, c_vp])
+fkv_validate_tables = _sig("fkv_validate_tables", c_i32, [c_vp, c_vp, c_vp, c_vp, c_i32, c_i32, c_i32, c_i32, c_i32])
 fkv_get_pool_stats = _sig("fkv_get_pool_stats", c_i32, [c_vp, ctypes.POINTER(fkv_pool_stats)])
 fkv_decode_plan_create = _sig("fkv_decode_plan_create", c_i32,
                               [ctypes.POINTER(fkv_decode_plan_params), c_vp, c_vp, c_vp, c_vp, ctypes.POINTER(c_vp)])

@@ -48,7 +48,36 @@ extern "C" {
 
 const char *fkv_last_error(void) { return g_last_error.c_str(); }
 
-const char *fkv_version(void) { return "forkkv-mi355x 0.1 (gfx950)"; }
+const char *fkv_version(void) { return "forkkv-mi355x 0.2 (gfx950)"; }
+
+fkv_status fkv_validate_tables(const int32_t *base_bt, const int32_t *res_bt, const int32_t *seq_lens,
+                               const int32_t *adapter_idx, int32_t n_agents, int32_t max_pages, int32_t page_size,
+                               int32_t num_base_pages, int32_t num_res_pages) {
+    fkv::clear_error();
+    if (!base_bt || !seq_lens || n_agents < 1 || max_pages < 1 || page_size < 1 || num_base_pages < 1)
+        return fkv::fail(FKV_ERR_INVALID, "fkv_validate_tables: bad argument");
+    for (int32_t a = 0; a < n_agents; ++a) {
+        const int64_t L = seq_lens[a];
+        if (L < 1 || L > (int64_t)max_pages * page_size)
+            return fkv::fail(FKV_ERR_INVALID, "fkv_validate_tables: agent " + std::to_string(a) + " has length " +
+                                                  std::to_string(L));
+        const int32_t np = (int32_t)((L + page_size - 1) / page_size);
+        const bool res = res_bt && adapter_idx && adapter_idx[a] >= 0;
+        for (int32_t i = 0; i < np; ++i) {
+            const int32_t b = base_bt[(int64_t)a * max_pages + i];
+            if (b < 0 || b >= num_base_pages)
+                return fkv::fail(FKV_ERR_INVALID, "fkv_validate_tables: agent " + std::to_string(a) + " page " +
+                                                      std::to_string(i) + " names base page " + std::to_string(b));
+            if (res) {
+                const int32_t r = res_bt[(int64_t)a * max_pages + i];
+                if (r < 0 || r >= num_res_pages)
+                    return fkv::fail(FKV_ERR_INVALID, "fkv_validate_tables: agent " + std::to_string(a) + " page " +
+                                                          std::to_string(i) + " names residual page " + std::to_string(r));
+            }
+        }
+    }
+    return FKV_OK;
+}
 
 fkv_status fkv_rope_table(int32_t d, int32_t max_pos, double base, float *cos_out, float *sin_out) {
     fkv::clear_error();

@@ -119,6 +119,7 @@ class LoadedWorkload:
                              max_item_agents=self.item_agents, r=wl.r, rope=self.rope, res_bt=rb,
                              adapter_idx=self.adapter_idx_host[agents])
         info = plan.info(wl.d, wl.r)
+        self._debug_check(bb, rb, sl, self.adapter_idx_host[agents])
         dev = self.device
         q_rows = torch.tensor([int(wl.q_offset[a]) for a in agents], device=dev)
         st = {
@@ -140,6 +141,11 @@ class LoadedWorkload:
                                   workspace=st["ws"])
         self._decode = st
         return st
+
+    def _debug_check(self, bb, rb, sl, ad):
+        if rt.debug_enabled():
+            rt.validate_tables(bb, rb if self.wl.r > 0 else None, sl, ad if self.wl.r > 0 else None,
+                               self.wl.page_size, self.base_kv.shape[0], self.res_kv.shape[0])
 
     def decode(self, stream=None) -> torch.Tensor:
         if self._decode is None:
@@ -189,6 +195,7 @@ class LoadedWorkload:
         st["res_bt"].copy_(torch.from_numpy(rb))
         st["seq_lens"].copy_(torch.from_numpy(sl))
         st["host_bt"] = (bb, rb, sl)
+        self._debug_check(bb, rb, sl, self.adapter_idx_host[st["agents"]])
         return sl
 
     # ---- chunked prefill over the agents that appended a chunk ----
@@ -196,6 +203,7 @@ class LoadedWorkload:
         wl = self.wl
         agents = list(wl.prefill_agents() if agents is None else agents)
         bb, rb, sl = self.tree.block_tables(agents, self.max_pages)
+        self._debug_check(bb, rb, sl, self.adapter_idx_host[agents])
         dev = self.device
         counts = [wl.n_queries(a) for a in agents]
         indptr = np.zeros(len(agents) + 1, dtype=np.int32)

@@ -7,6 +7,7 @@ opaque C handles.
 from __future__ import annotations
 
 import ctypes
+import os
 from dataclasses import dataclass
 from typing import List, Optional, Sequence, Tuple
 
@@ -109,6 +110,23 @@ class Tree:
         s = N.fkv_pool_stats()
         check(N.fkv_get_pool_stats(self._h, ctypes.byref(s)), "fkv_get_pool_stats")
         return {f: getattr(s, f) for f, _ in s._fields_}
+
+
+def validate_tables(base_bt: np.ndarray, res_bt: Optional[np.ndarray], seq_lens: np.ndarray,
+                    adapter_idx: Optional[np.ndarray], page_size: int, num_base_pages: int, num_res_pages: int) -> None:
+    """fkv_validate_tables on host copies; raises FKVError naming the first bad entry."""
+    bb = np.ascontiguousarray(base_bt, dtype=np.int32)
+    rb = np.ascontiguousarray(res_bt, dtype=np.int32) if res_bt is not None else None
+    sl = np.ascontiguousarray(seq_lens, dtype=np.int32)
+    ad = np.ascontiguousarray(adapter_idx, dtype=np.int32) if adapter_idx is not None else None
+    check(N.fkv_validate_tables(_ptr(bb), _ptr(rb) if rb is not None else None, _ptr(sl),
+                                _ptr(ad) if ad is not None else None, bb.shape[0], bb.shape[1], page_size,
+                                num_base_pages, num_res_pages), "fkv_validate_tables")
+
+
+def debug_enabled() -> bool:
+    """FKV_DEBUG set (to anything but 0): table checks before every launch."""
+    return os.environ.get("FKV_DEBUG", "0") not in ("", "0")
 
 
 def decode_plan_default_agents(hq: int, hkv: int, r: int, rope: bool) -> int:

@@ -381,3 +381,27 @@ def test_noalloc_decode_rejects_plans_beyond_its_static_workspace():
     with pytest.raises(rt.FKVError) as e:
         rt.residual_attention_decode_noalloc(args, plan, 0)
     assert e.value.code == N.FKV_ERR_INVALID and "static workspace" in str(e.value)
+
+
+def test_table_validation_names_the_first_bad_entry():
+    bb = np.array([[0, 1, 2, 0], [3, 4, 0, 0]], np.int32)
+    rb = np.array([[5, 6, 7, 0], [8, 9, 0, 0]], np.int32)
+    sl = np.array([40, 20], np.int32)
+    ad = np.array([0, -1], np.int32)
+    rt.validate_tables(bb, rb, sl, ad, 16, 5, 10)
+    rt.validate_tables(bb, None, sl, None, 16, 5, 0)
+    bad = bb.copy()
+    bad[1, 1] = 5                      # past the base pool
+    with pytest.raises(rt.FKVError) as e:
+        rt.validate_tables(bad, rb, sl, ad, 16, 5, 10)
+    assert "agent 1 page 1 names base page 5" in str(e.value)
+    badr = rb.copy()
+    badr[0, 2] = -1
+    with pytest.raises(rt.FKVError) as e:
+        rt.validate_tables(bb, badr, sl, ad, 16, 5, 10)
+    assert "residual page -1" in str(e.value)
+    badr[1, 0] = 99                    # agent 1 has no adapter: its residual row is not read
+    badr[0, 2] = 7
+    rt.validate_tables(bb, badr, sl, ad, 16, 5, 10)
+    with pytest.raises(rt.FKVError):
+        rt.validate_tables(bb, rb, np.array([40, 65], np.int32), ad, 16, 5, 10)   # longer than the rows
