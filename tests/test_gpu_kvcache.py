@@ -9,25 +9,11 @@ import torch
 
 from paper_2604_06370_amd import runtime as rt
 
+from layouts import ck_off, cv_off, k_off, v_off
+
 pytestmark = pytest.mark.gpu
 
 PS, D = 16, 128
-
-
-def k_off(t, i):
-    return (i // 32) * 512 + (t + 16 * ((i % 16) // 4)) * 8 + 4 * ((i % 32) // 16) + i % 4
-
-
-def v_off(t, i):
-    return (i // 32) * 512 + (i % 16 + 16 * (t // 4)) * 8 + 4 * ((i // 16) % 2) + t % 4
-
-
-def ck_off(t, rho):
-    return (rho // 16) * 512 + (16 * ((rho % 16) // 4) + t) * 8 + rho % 4
-
-
-def cv_off(t, rho):
-    return (rho // 16) * 512 + (16 * (t // 4) + rho % 16) * 8 + 4 + t % 4
 
 
 def _dev(a):
