@@ -333,6 +333,40 @@ def graph_entry(wl, dev, rope: bool, steps: int) -> dict:
     return res
 
 
+def mixed_entry(wl, dev, rope: bool, steps: int) -> dict:
+    """One step of a ragged mixed batch (decode rows and prefill chunks): the two calls one after
+    the other on one stream, the two on concurrent streams, and one HIP graph holding both as
+    concurrent branches; wall time per step."""
+    import torch
+    from paper_2604_06370_amd.driver import LoadedWorkload
+    print(f"# mixed batch {wl.name} rope={rope}", file=sys.stderr, flush=True)
+    lw = LoadedWorkload(wl, device=dev, rope=rope)
+    lw.decode_setup()
+    lw.prefill_setup()
+    graph = lw.capture_mixed_graph()
+    side = torch.cuda.Stream(device=dev)
+    res = {"workload": wl.name, "rope": rope, "decode_agents": len(wl.decode_agents()),
+           "prefill_rows": int(sum(wl.n_queries(a) for a in wl.prefill_agents())), "steps": steps}
+
+    def sequential():
+        lw.decode()
+        lw.prefill()
+
+    for name, fn in (("sequential", sequential), ("two_streams", lambda: lw.mixed(side)),
+                     ("graph", lambda: graph.replay()), ("decode_only", lambda: lw.decode()),
+                     ("prefill_only", lambda: lw.prefill())):
+        fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            fn()
+        torch.cuda.synchronize()
+        res[name + "_ms"] = (time.perf_counter() - t0) * 1e3 / steps
+    del graph
+    lw.close()
+    return res
+
+
 def plan_cost(wl, dev, rope: bool, reps: int = 5) -> dict:
     """Host cost of a decode plan for this workload (build + serialise, then the copy to the
     device), and how many decode steps it serves: it stays valid until an agent outgrows its
@@ -417,7 +451,15 @@ def suite(args, dev, stream) -> dict:
     run("70b_mixed_decode_rope_off", lambda: decode_entry(w5, dev, stream, False, st, 2, 2))
     run("70b_mixed_decode_rope_on", lambda: decode_entry(w5, dev, stream, True, st, 2, 2))
     run("70b_mixed_prefill", lambda: measure_prefill_wl(w5, dev, stream, max(2, st // 4)))
+    run("70b_mixed_one_step", lambda: mixed_entry(w5, dev, False, max(2, st // 4)))
     del w5
+    # a decode-heavy mixed step at the 8B shape: 12 agents decode, 4 prefill 256-token chunks
+    wm = W.tree("llama3-8b-16agents-32k-mixed-12decode-4x256prefill", 2, node_parent=[-1], node_len=[32768],
+                agent_node=[0] * 16, suffix_lo=256, suffix_hi=4096, hq=32, hkv=8, r=16,
+                chunk=[256 if a % 4 == 3 else 0 for a in range(16)])
+    run("8b_mixed_one_step_rope_off", lambda: mixed_entry(wm, dev, False, st))
+    run("8b_mixed_one_step_rope_on", lambda: mixed_entry(wm, dev, True, st))
+    del wm
     # one GPU's share of a tensor-parallel degree-8 deployment of the 16-agent 32K workload
     tp = W.fanout("llama3-8b-16agents-32k-shared-tp8-share", 2, n_agents=16, prefix=32768, suffix_lo=256,
                   suffix_hi=4096, hq=4, hkv=1, r=16)

@@ -186,6 +186,40 @@ class LoadedWorkload:
             self.decode()
         return graph
 
+    def mixed(self, side=None):
+        """The ragged mixed batch of one step: the decode rows (split and merge kernels) on the
+        current stream and the prefill chunks on `side`, forked from and joined back to it, so
+        the HBM-bound decode and the matrix-core-bound prefill run at the same time."""
+        if self._decode is None:
+            self.decode_setup()
+        if self._prefill is None:
+            self.prefill_setup()
+        main = torch.cuda.current_stream(self.device)
+        side = side or torch.cuda.Stream(device=self.device)
+        side.wait_stream(main)                     # fork
+        with torch.cuda.stream(side):
+            self.prefill(side)
+        self.decode(main)
+        main.wait_stream(side)                     # join
+        return self._decode["out"], self._prefill["out"]
+
+    def capture_mixed_graph(self):
+        """One HIP graph for the mixed batch: the decode and prefill launches as two concurrent
+        branches (fork and join inside the capture); a replay issues the whole step at once."""
+        if self._decode is None:
+            self.decode_setup()
+        if self._prefill is None:
+            self.prefill_setup()
+        cap, side = torch.cuda.Stream(device=self.device), torch.cuda.Stream(device=self.device)
+        cap.wait_stream(torch.cuda.current_stream(self.device))
+        with torch.cuda.stream(cap):
+            self.mixed(side)  # warm-up outside the capture
+        torch.cuda.current_stream(self.device).wait_stream(cap)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=cap):
+            self.mixed(side)
+        return graph
+
     def refresh_decode_tables(self):
         """Copy the tree's current block tables and lengths into the decode call's device
         tables in place (the plan and the argument block keep pointing at them)."""
