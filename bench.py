@@ -545,7 +545,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (the kernel would shard by KV "
-              "head with no exchange; see DESIGN.md). Run with --gpus 1.", file=sys.stderr)
+              "head with no exchange). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -231,15 +231,15 @@ struct ResOffsets {
 
 // ---------------------------------------------------------------------------
 // RoPE off.  One workgroup per (work item, KV head), four waves; wave w serves agent
-// group w % ngp as copy w / ngp.  The item's base pages stream through a two-buffer LDS
-// ring in stages of SP pages (SP = 2 when the item has four groups, else 4); every wave
-// loads two 4 KB blocks per load round into registers, one or two stages ahead, and
-// stores them into the ring once the stage before has been consumed.  A wave computes
-// its share of a stage as one step of two pages (four groups: the whole stage; two
-// groups: pages 2c, 2c+1 for copy c) or of one page (one group: page c), so one wave
-// instruction of the 16x16x32 form covers 32 keys of the value products.  Its agents'
-// rCache fragments come straight from memory one stage ahead (one 16-byte load per
-// slot, page and rank tile).
+// group w % ngp as copy w / ngp.  Items of several groups (shared prefixes) stream their
+// base pages through an LDS ring of kRing stages of two pages, written by direct
+// memory-to-LDS copies kRing - 1 stages ahead (each wave copies one 4 KB block per
+// stage); a wave computes its share of a stage as one step of two pages (four groups:
+// the whole stage, so one 16x16x32 instruction covers 32 keys of the value products) or
+// of one page (two groups: page `copy`).  Items of one group stride over their pages
+// straight from memory into registers, one or two pages ahead.  Every wave's rCache
+// fragments come straight from memory (one 16-byte load per slot, page and rank tile),
+// two stages ahead on the ring path.
 template <int R, int G>
 struct SplitShape {
     static constexpr int AG = ROWS / G;                                         // agents per group

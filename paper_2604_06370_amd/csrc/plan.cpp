@@ -112,8 +112,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     //    matrix-core work per base byte; about 2.5x a single agent's page at 16 agents, as
     //    measured), and every item pays a fixed prologue worth about 24 pages (see below
     //    for how the split sizes are chosen).  Splits of a segment are equal.
-    //    RoPE on: about three (item, head block) workgroups per compute unit, 64 pages at
-    //    most per item.
+    //    RoPE on: items of 32 pages (see below).
     const int64_t cus = prm->num_cus > 0 ? prm->num_cus : 256;
     const int32_t nhb_units = prm->hkv / hpb;
     std::vector<int32_t> seg_pps(segs.size());
@@ -472,7 +471,8 @@ int32_t fkv_decode_plan_default_agents(int32_t hq, int32_t hkv, int32_t r, int32
     // Without RoPE the residual key term is one small product per page and agent, so a
     // workgroup serves up to four groups from each staged base page (as many agents as
     // fit one LDS stage).  With RoPE the per-page rebuild (Stage 1 plus the rotation)
-    // dominates; one group per workgroup keeps the four waves independent.
+    // dominates: each wave serves the agents whose rebuilt keys fit its registers, and an
+    // item holds as many such wave groups as 64 KB of B_K^T fragments in LDS allow.
     if (r < 0) return 0;
     return fkv::decode_item_agent_cap(g, hkv, r, rope != 0 && r > 0);
 }
