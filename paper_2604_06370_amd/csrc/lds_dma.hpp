@@ -81,6 +81,18 @@ __device__ __forceinline__ u32x4 lds_read1(uint32_t addr) {
         : "memory");
     return out;
 }
+// Four 16-byte LDS reads at addr, addr + 64, + 128, + 192 bytes.
+__device__ __forceinline__ void lds_read4_64(uint32_t addr, u32x4 (&out)[4]) {
+    asm volatile(
+        "ds_read_b128 %0, %4\n\t"
+        "ds_read_b128 %1, %4 offset:64\n\t"
+        "ds_read_b128 %2, %4 offset:128\n\t"
+        "ds_read_b128 %3, %4 offset:192\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(out[0]), "=&v"(out[1]), "=&v"(out[2]), "=&v"(out[3])
+        : "v"(addr)
+        : "memory");
+}
 // Two 16-byte LDS reads at addr and addr + 2 KB.
 __device__ __forceinline__ void lds_read2_2k(uint32_t addr, u32x4 (&out)[2]) {
     asm volatile(

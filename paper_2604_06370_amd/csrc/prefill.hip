@@ -1,17 +1,16 @@
 // ResidualAttention chunked prefill for gfx950 (Section 6 prefill kernel,
 // Algorithm 1 with a block of query rows).
 //
-// One workgroup = (agent a, KV head h, block of query tokens); its 128 rows are
-// (query token, query head of h).  Every row of the block belongs to the same
-// agent, so the agent's keys are rebuilt once per 64-key tile and shared by all
-// rows through LDS:
-//   wave w rebuilds page w of the tile:  U^T = B_K^T C_K^T  (MFMA),
-//                                        K_lora = RoPE_p(U) (rotate-half, fp32),
-//                                        K = K_base + K_lora -> bf16 -> LDS
-//   then every wave, for its 32 rows:    S^T = K Q^T        (16x16x32 MFMA)
-//                                        causal mask + online softmax
-//                                        O^T   += V^T P^T   (16x16x32 MFMA)
-//                                        acc_r^T += C_V^T P^T
+// One workgroup of eight waves = (agent a, KV head h, block of 256 query rows); its rows
+// are (query token, query head of h), all of the same agent, so every 64-key tile of the
+// agent's keys is staged once in LDS and applied to all 256 rows:
+//   RoPE on, per tile: U^T = B_K^T C_K^T (MFMA), K_lora = RoPE_p(U) (rotate-half, fp32),
+//                      K = K_base + K_lora -> bf16, in place in LDS
+//   every wave, for its 32 rows:  S^T = K Q^T              (16x16x32 MFMA)
+//                                 RoPE off: S^T += C_K (B_K q)^T
+//                                 causal mask + online softmax
+//                                 O^T   += V^T P^T          (16x16x32 MFMA)
+//                                 acc_r^T += C_V^T P^T
 // and at the end O = (O + acc_r . B_V[h]) / l (Eq. 4) is written in bf16.
 //
 // The contraction index of the 16x16x32 products is permuted so that the
@@ -35,10 +34,8 @@ namespace {
 
 constexpr int D = 128;
 constexpr int PS = 16;
-constexpr int WAVES = 4;
 constexpr int ROWS_PER_WAVE = 32;          // two 16-row tiles
-constexpr int ROWS_PER_WG = WAVES * ROWS_PER_WAVE;
-constexpr int TILE_KEYS = 64;              // four pages, one per wave
+constexpr int TILE_KEYS = 64;              // four pages
 constexpr int kXcds = 8;
 constexpr float kNegInf = -INFINITY;
 
@@ -49,6 +46,7 @@ struct PrefillArgs {
     uint16_t *out;
     int32_t n_agents, hq, hkv, max_pages, blocks_per_agent_head;
     float scale_log2;
+    int32_t rope_rows;  // positions the RoPE tables hold
 };
 
 
@@ -65,383 +63,8 @@ __device__ __forceinline__ void poison_unreached_rows(const PrefillArgs &p, int 
     }
 }
 
-template <int R, int G, bool ROPE>
-struct PrefillShape {
-    static constexpr int RT = R == 0 ? 0 : (R + 15) / 16;
-    static constexpr int TOK_PER_WG = ROWS_PER_WG / G;
-    static constexpr int RES_PAGE = RT * 512;                  // residual page (fragment order)
-    static constexpr int SK_BYTES = 4 * 4 * 64 * 16;          // [page][kk][lane] 16 B
-    static constexpr int SV_BYTES = 4 * PS * D * 2;             // [page][d][16] bf16
-    static constexpr int SCV_BYTES = R > 0 ? 4 * R * PS * 2 : 16;  // [page][rho][16] bf16
-    static constexpr int SBK_BYTES = (R > 0 && ROPE) ? RT * 8 * 64 * 8 : 16;  // B_K^T fragments
-    static constexpr int SBV_BYTES = R > 0 ? R * D * 4 : 16;    // B_V[h] slice, fp32
-    static constexpr int SACC_BYTES = R > 0 ? ROWS_PER_WG * R * 4 : 16;  // acc_r rows for the epilogue
-    static constexpr int EPI_BYTES = SBV_BYTES + SACC_BYTES;
-    static constexpr int MAIN_BYTES = SK_BYTES + SV_BYTES + SCV_BYTES;
-    static constexpr int LDS_BYTES = (MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES) + SBK_BYTES;
-};
-
-template <int R, int G, bool ROPE>
-__global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
-    using S = PrefillShape<R, G, ROPE>;
-    constexpr int RT = S::RT;
-    constexpr int TPW = S::TOK_PER_WG;
-    __shared__ __attribute__((aligned(16))) unsigned char lds[S::LDS_BYTES];
-    u32x4 *sK = reinterpret_cast<u32x4 *>(lds);
-    uint16_t *sV = reinterpret_cast<uint16_t *>(lds + S::SK_BYTES);
-    uint16_t *sCV = reinterpret_cast<uint16_t *>(lds + S::SK_BYTES + S::SV_BYTES);
-    u32x2 *sBK = reinterpret_cast<u32x2 *>(lds + (S::MAIN_BYTES > S::EPI_BYTES ? S::MAIN_BYTES : S::EPI_BYTES));
-    float *sBV = reinterpret_cast<float *>(lds);
-    float *sAcc = reinterpret_cast<float *>(lds + S::SBV_BYTES);
-
-    // Consecutive workgroup ids go round-robin to the 8 XCDs: keep all query blocks of one
-    // (agent, KV head) on one XCD so the key/value tiles they all stream hit that XCD's L2.
-    const int hkv = p.hkv;
-    const int bpa = p.blocks_per_agent_head;
-    const int xcd = blockIdx.x % kXcds, local = blockIdx.x / kXcds;
-    const int pair = (local / bpa) * kXcds + xcd;
-    const int qb = local - (local / bpa) * bpa;
-    if (pair >= p.n_agents * hkv) return;
-    const int a = pair / hkv;
-    const int h = pair - a * hkv;
-    const int q0 = p.q_indptr[a], nq = p.q_indptr[a + 1] - q0;
-    const int tok_begin = qb * TPW;
-    if (qb == bpa - 1 && nq > bpa * TPW) poison_unreached_rows(p, q0, nq, h, G, bpa * TPW);
-    if (tok_begin >= nq) return;
-    const int L = p.seq_lens[a];
-    const int P0 = L - nq;  // position of the chunk's first query
-    const int ad = R > 0 ? p.adapter_idx[a] : -1;
-
-    const int lane = threadIdx.x & 63;
-    const int wave = uniform(threadIdx.x >> 6);
-    const int col = lane & 15, grp = lane >> 4;
-    const int64_t n = (int64_t)hkv * D;
-
-    // rows of this lane in the two 16-row tiles of the wave
-    int row_tok[2], row_pos[2];
-    bool row_ok[2];
-    u32x4 qf[2][4];
-#pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
-        const int r = wave * ROWS_PER_WAVE + nt * 16 + col;
-        const int t = tok_begin + r / G;
-        const int jj = r % G;
-        row_ok[nt] = t < nq;
-        row_tok[nt] = t;
-        row_pos[nt] = P0 + t;
-        const uint16_t *qr = p.q + ((int64_t)(q0 + (row_ok[nt] ? t : 0)) * p.hq + h * G + jj) * D;
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-            u32x4 v = {0, 0, 0, 0};
-            if (row_ok[nt]) {
-                const u32x2 lo = ldg64(qr + 32 * kk + 4 * grp);
-                const u32x2 hi = ldg64(qr + 32 * kk + 16 + 4 * grp);
-                v = u32x4{lo.x, lo.y, hi.x, hi.y};
-            }
-            qf[nt][kk] = v;
-        }
-    }
-
-    // B_K^T fragments for the rebuild: lane holds B_K[16t + 4grp + i][h*D + 16mt + col]
-    if constexpr (R > 0 && ROPE) {
-        if (ad >= 0) {
-            const uint16_t *bk = p.lora_b + (int64_t)ad * 2 * R * n + (int64_t)h * D;
-            for (int idx = threadIdx.x; idx < RT * 8 * 64; idx += 256) {
-                const int ln = idx & 63, rest = idx >> 6;
-                const int mt = rest & 7, t = rest >> 3;
-                const int c = ln & 15, gg = ln >> 4;
-                uint32_t w[2];
-#pragma unroll
-                for (int j = 0; j < 2; ++j) {
-                    const int r0 = 16 * t + 4 * gg + 2 * j;
-                    const uint16_t lo = r0 < R ? bk[(int64_t)r0 * n + 16 * mt + c] : (uint16_t)0;
-                    const uint16_t hi = r0 + 1 < R ? bk[(int64_t)(r0 + 1) * n + 16 * mt + c] : (uint16_t)0;
-                    w[j] = (uint32_t)lo | ((uint32_t)hi << 16);
-                }
-                sBK[idx] = u32x2{w[0], w[1]};
-            }
-        }
-    }
-    // RoPE off: the residual key term of row j is (B_K q_j) . c_p; fold it as an extra
-    // contraction over the rank: S^T += C_K (B_K q)^T.
-    u32x2 wq[2][RT > 0 ? RT : 1];
-    if constexpr (R > 0 && !ROPE) {
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-            for (int t = 0; t < RT; ++t) {
-                f32x4 acc = {0, 0, 0, 0};
-                if (ad >= 0) {
-                    const int rho = 16 * t + col;
-                    const uint16_t *bk = p.lora_b + (int64_t)ad * 2 * R * n + (int64_t)rho * n + (int64_t)h * D;
-#pragma unroll
-                    for (int kk = 0; kk < 4; ++kk) {
-                        u32x4 av = {0, 0, 0, 0};
-                        if (rho < R) {
-                            const u32x2 lo = ldg64(bk + 32 * kk + 4 * grp);
-                            const u32x2 hi = ldg64(bk + 32 * kk + 16 + 4 * grp);
-                            av = u32x4{lo.x, lo.y, hi.x, hi.y};
-                        }
-                        acc = mfma32(av, qf[nt][kk], acc);  // W^T[rho][row]
-                    }
-                }
-                wq[nt][t] = pack4(acc);
-            }
-    }
-    __syncthreads();
-
-    f32x4 oacc[8][2];
-#pragma unroll
-    for (int mt = 0; mt < 8; ++mt) oacc[mt][0] = oacc[mt][1] = f32x4{0, 0, 0, 0};
-    f32x4 racc[RT > 0 ? RT : 1][2];
-#pragma unroll
-    for (int t = 0; t < (RT > 0 ? RT : 1); ++t) racc[t][0] = racc[t][1] = f32x4{0, 0, 0, 0};
-    float m_run[2] = {kNegInf, kNegInf}, l_run[2] = {0.f, 0.f};
-
-    const int n_pages = (L + PS - 1) / PS;
-    const int last_pos = P0 + (tok_begin + TPW < nq ? tok_begin + TPW : nq) - 1;
-    const int n_tiles = last_pos / TILE_KEYS + 1;
-    const int32_t *btb = p.base_bt + (int64_t)a * p.max_pages;
-    const int32_t *btr = R > 0 ? p.res_bt + (int64_t)a * p.max_pages : nullptr;
-    const int64_t kv_block = (int64_t)PS * D;
-
-    for (int tile = 0; tile < n_tiles; ++tile) {
-        // ---- stage: wave w rebuilds page w of the tile into LDS ----
-        {
-            const int pg = tile * 4 + wave;
-            const int tok0 = pg * PS;
-            const bool have = pg < n_pages;
-            const int bpage = have ? btb[pg] : 0;
-            const uint16_t *kblk = p.base_kv + ((int64_t)bpage * 2 * hkv + h) * kv_block;
-            const uint16_t *vblk = kblk + (int64_t)hkv * kv_block;
-            const int vis = L - tok0;  // valid keys in this page
-            // K_base, stored in the permuted 16x16x32 A layout: one 16-byte load per k-step
-            f32x4 kacc[8];
-#pragma unroll
-            for (int kk = 0; kk < 4; ++kk) {
-                const u32x4 kb = have ? ldg128(kblk + kk * 512 + lane * 8) : u32x4{0, 0, 0, 0};
-                kacc[2 * kk] = f32x4{bf16_lo(kb.x), bf16_hi(kb.x), bf16_lo(kb.y), bf16_hi(kb.y)};
-                kacc[2 * kk + 1] = f32x4{bf16_lo(kb.z), bf16_hi(kb.z), bf16_lo(kb.w), bf16_hi(kb.w)};
-            }
-            const uint16_t *rb = nullptr;
-            if constexpr (R > 0) {
-                if (ad >= 0 && have) rb = p.res_kv + (int64_t)btr[pg] * S::RES_PAGE;
-            }
-            if constexpr (R > 0 && ROPE) {
-                if (rb) {
-                    f32x4 u[8];
-#pragma unroll
-                    for (int mt = 0; mt < 8; ++mt) u[mt] = f32x4{0, 0, 0, 0};
-#pragma unroll
-                    for (int t = 0; t < RT; ++t) {
-                        const u32x2 c = ldg64(rb + t * 512 + lane * 8);
-                        const u32x2 ck = (16 * t + 4 * grp < R) ? c : u32x2{0, 0};
-#pragma unroll
-                        for (int mt = 0; mt < 8; ++mt) u[mt] = mfma16(sBK[(t * 8 + mt) * 64 + lane], ck, u[mt]);
-                    }
-                    const float *cr = p.rope_cos + (int64_t)pg * (PS * D / 2) + lane * 4;
-                    const float *sr = p.rope_sin + (int64_t)pg * (PS * D / 2) + lane * 4;
-#pragma unroll
-                    for (int mt = 0; mt < 4; ++mt) {
-                        const f32x4 cs = *reinterpret_cast<const f32x4 *>(cr + 256 * mt);
-                        const f32x4 sn = *reinterpret_cast<const f32x4 *>(sr + 256 * mt);
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) {
-                            const float x = u[mt][i], y = u[mt + 4][i];
-                            kacc[mt][i] += x * cs[i] - y * sn[i];
-                            kacc[mt + 4][i] += y * cs[i] + x * sn[i];
-                        }
-                    }
-                }
-            }
-#pragma unroll
-            for (int kk = 0; kk < 4; ++kk) {
-                const u32x2 lo = pack4(kacc[2 * kk]), hi = pack4(kacc[2 * kk + 1]);
-                sK[(wave * 4 + kk) * 64 + lane] = u32x4{lo.x, lo.y, hi.x, hi.y};
-            }
-            // V page as stored ([d][16 keys]); keys past the sequence end are zeroed
-            for (int e = lane; e < D * PS / 4; e += 64) {
-                u32x2 v = have ? ldg64(vblk + 4 * e) : u32x2{0, 0};
-                const int k0 = 4 * ((((4 * e) & 511) >> 3) >> 4);  // tokens k0..k0+3 (fragment order)
-                if (k0 + 0 >= vis) v.x &= 0xffff0000u;
-                if (k0 + 1 >= vis) v.x &= 0x0000ffffu;
-                if (k0 + 2 >= vis) v.y &= 0xffff0000u;
-                if (k0 + 3 >= vis) v.y &= 0x0000ffffu;
-                *reinterpret_cast<u32x2 *>(sV + wave * D * PS + 4 * e) = v;
-            }
-            if constexpr (R > 0) {
-                // C_V^T rows of the page: lane (c, g) of tile t holds C_V[4g .. 4g+3][16t + c]
-#pragma unroll
-                for (int t = 0; t < RT; ++t) {
-                    const int rho = 16 * t + col;
-                    u32x2 v = {0, 0};
-                    if (rb) v = ldg64(rb + t * 512 + lane * 8 + 4);
-                    const int k0 = 4 * grp;
-                    if (k0 + 0 >= vis) v.x &= 0xffff0000u;
-                    if (k0 + 1 >= vis) v.x &= 0x0000ffffu;
-                    if (k0 + 2 >= vis) v.y &= 0xffff0000u;
-                    if (k0 + 3 >= vis) v.y &= 0x0000ffffu;
-                    if (rho < R) *reinterpret_cast<u32x2 *>(sCV + wave * R * PS + rho * PS + 4 * grp) = v;
-                }
-            }
-        }
-        __syncthreads();
-
-        // ---- scores for the 64 keys of the tile, 2 row tiles ----
-        f32x4 sacc[4][2];
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt) {
-            sacc[kt][0] = sacc[kt][1] = f32x4{0, 0, 0, 0};
-#pragma unroll
-            for (int kk = 0; kk < 4; ++kk) {
-                const u32x4 kf = sK[(kt * 4 + kk) * 64 + lane];
-                sacc[kt][0] = mfma32(kf, qf[0][kk], sacc[kt][0]);
-                sacc[kt][1] = mfma32(kf, qf[1][kk], sacc[kt][1]);
-            }
-        }
-        if constexpr (R > 0 && !ROPE) {
-            if (ad >= 0) {
-#pragma unroll
-                for (int kt = 0; kt < 4; ++kt) {
-                    const int pg = tile * 4 + kt;
-                    if (pg >= n_pages) continue;
-                    const uint16_t *rb = p.res_kv + (int64_t)btr[pg] * S::RES_PAGE;
-#pragma unroll
-                    for (int t = 0; t < RT; ++t) {
-                        const u32x2 c = ldg64(rb + t * 512 + lane * 8);
-                        const u32x2 ck = (16 * t + 4 * grp < R) ? c : u32x2{0, 0};
-                        // zero-padded 16x16x32 form: the accumulator chain stays on one
-                        // instruction form (see the decode kernel)
-                        const u32x4 a = u32x4{ck.x, ck.y, 0u, 0u};
-                        sacc[kt][0] = mfma32(a, u32x4{wq[0][t].x, wq[0][t].y, 0u, 0u}, sacc[kt][0]);
-                        sacc[kt][1] = mfma32(a, u32x4{wq[1][t].x, wq[1][t].y, 0u, 0u}, sacc[kt][1]);
-                    }
-                }
-            }
-        }
-
-        // ---- causal mask + online softmax (rows live in lanes) ----
-        u32x2 pf[4][2];
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt) {
-            float sv[4][4];
-            float mx = kNegInf;
-#pragma unroll
-            for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int key = tile * TILE_KEYS + kt * PS + 4 * grp + i;
-                    sv[kt][i] = (row_ok[nt] && key <= row_pos[nt]) ? sacc[kt][nt][i] * p.scale_log2 : kNegInf;
-                    mx = fmaxf(mx, sv[kt][i]);
-                }
-            mx = fmaxf(mx, __shfl_xor(mx, 16));
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
-            const float m_new = fmaxf(m_run[nt], mx);
-            const float m_use = m_new == kNegInf ? 0.f : m_new;
-            const float alpha = fast_exp2(m_run[nt] - m_use);
-            float ps = 0.f;
-#pragma unroll
-            for (int kt = 0; kt < 4; ++kt) {
-                f32x4 pv;
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    pv[i] = fast_exp2(sv[kt][i] - m_use);
-                    ps += pv[i];
-                }
-                pf[kt][nt] = pack4(pv);
-            }
-            l_run[nt] = l_run[nt] * alpha + ps;
-            m_run[nt] = m_new;
-#pragma unroll
-            for (int mt = 0; mt < 8; ++mt) oacc[mt][nt] *= alpha;
-#pragma unroll
-            for (int t = 0; t < RT; ++t) racc[t][nt] *= alpha;
-        }
-
-        // ---- O^T += V^T P^T and acc_r^T += C_V^T P^T over two 32-key halves ----
-#pragma unroll
-        for (int half = 0; half < 2; ++half) {
-            const u32x4 pb0 = u32x4{pf[2 * half][0].x, pf[2 * half][0].y, pf[2 * half + 1][0].x, pf[2 * half + 1][0].y};
-            const u32x4 pb1 = u32x4{pf[2 * half][1].x, pf[2 * half][1].y, pf[2 * half + 1][1].x, pf[2 * half + 1][1].y};
-#pragma unroll
-            for (int mt = 0; mt < 8; ++mt) {
-                const int voff = (mt >> 1) * 512 + lane * 8 + 4 * (mt & 1);
-                const u32x2 lo = *reinterpret_cast<const u32x2 *>(sV + (2 * half) * D * PS + voff);
-                const u32x2 hi = *reinterpret_cast<const u32x2 *>(sV + (2 * half + 1) * D * PS + voff);
-                const u32x4 va = u32x4{lo.x, lo.y, hi.x, hi.y};
-                oacc[mt][0] = mfma32(va, pb0, oacc[mt][0]);
-                oacc[mt][1] = mfma32(va, pb1, oacc[mt][1]);
-            }
-            if constexpr (R > 0) {
-                if (ad >= 0) {
-#pragma unroll
-                    for (int t = 0; t < RT; ++t) {
-                        const int rho = 16 * t + col;
-                        u32x4 ca = {0, 0, 0, 0};
-                        if (rho < R) {
-                            const u32x2 lo = *reinterpret_cast<const u32x2 *>(sCV + (2 * half) * R * PS + rho * PS + 4 * grp);
-                            const u32x2 hi = *reinterpret_cast<const u32x2 *>(sCV + (2 * half + 1) * R * PS + rho * PS + 4 * grp);
-                            ca = u32x4{lo.x, lo.y, hi.x, hi.y};
-                        }
-                        racc[t][0] = mfma32(ca, pb0, racc[t][0]);
-                        racc[t][1] = mfma32(ca, pb1, racc[t][1]);
-                    }
-                }
-            }
-        }
-        __syncthreads();
-    }
-
-    // ---- epilogue: O = (acc + acc_r . B_V[h]) / l ----
-#pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
-        l_run[nt] += __shfl_xor(l_run[nt], 16);
-        l_run[nt] += __shfl_xor(l_run[nt], 32);
-    }
-    if constexpr (R > 0) {
-        if (ad >= 0) {
-            const uint16_t *bv = p.lora_b + ((int64_t)ad * 2 + 1) * R * n + (int64_t)h * D;
-            for (int e = threadIdx.x; e < R * D; e += 256) sBV[e] = bf16_to_f32(bv[(int64_t)(e / D) * n + (e % D)]);
-#pragma unroll
-            for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-                for (int t = 0; t < RT; ++t)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const int rho = 16 * t + 4 * grp + i;
-                        if (rho < R) sAcc[(wave * ROWS_PER_WAVE + nt * 16 + col) * R + rho] = racc[t][nt][i];
-                    }
-            __syncthreads();
-#pragma unroll
-            for (int nt = 0; nt < 2; ++nt) {
-                const float *ar = sAcc + (wave * ROWS_PER_WAVE + nt * 16 + col) * R;
-                for (int rho = 0; rho < R; ++rho) {
-                    const float c = ar[rho];
-#pragma unroll
-                    for (int mt = 0; mt < 8; ++mt)
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) oacc[mt][nt][i] += c * sBV[rho * D + 16 * mt + 4 * grp + i];
-                }
-            }
-        }
-    }
-#pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
-        if (!row_ok[nt]) continue;
-        const int r = wave * ROWS_PER_WAVE + nt * 16 + col;
-        const float inv = l_run[nt] > 0.f ? 1.f / l_run[nt] : 0.f;
-        uint16_t *orow = p.out + ((int64_t)(q0 + row_tok[nt]) * p.hq + h * G + r % G) * D;
-#pragma unroll
-        for (int mt = 0; mt < 8; ++mt) {
-            f32x4 o = oacc[mt][nt] * inv;
-            *reinterpret_cast<u32x2 *>(orow + 16 * mt + 4 * grp) = pack4(o);
-        }
-    }
-}
-
 // ---------------------------------------------------------------------------
-// Streaming kernel.  A workgroup of eight waves holds 256 query rows (twice the rows per
-// key tile of the kernel above, so half the tile traffic per product), and 64-key tiles
+// Streaming kernel.  A workgroup of eight waves holds 256 query rows, and 64-key tiles
 // stream through a ring of LDS buffers by direct memory-to-LDS copies: wave w < 4 copies
 // the K block (and, with an adapter, the rCache page) of page w of a tile, wave 4 + w its
 // V block.  One barrier per tile hands a buffer over: every wave has waited (by count)
@@ -449,10 +72,13 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
 // copies issued after the barrier overwrite.
 //  - RoPE off: the key residual folds into the queries (S^T += C_K (B_K q)^T), so the
 //    stored blocks are used as they are; three buffers, copies two tiles ahead.
-//  - RoPE on (rank up to 32): a tile also carries the table rows of its positions; two
-//    buffers, copies one tile ahead.  After a tile has landed each wave rebuilds a quarter
-//    of one page's keys in place (U^T = B_K^T C_K^T on the matrix cores, rotated, added to
-//    K_base) and a second barrier publishes the rebuilt tile.
+//  - RoPE on: a tile also carries the cos/sin rows of its pages' first positions (each
+//    wave copies the 8 + 8 values per lane group that its rebuild uses); the rotation
+//    angle of token t of a page starting at p0 comes from those rows and the rows of
+//    positions 0..15 (kept in LDS for the launch) by angle addition.  Three buffers up to
+//    rank 32, two at rank 64 (copies one tile ahead).  After a tile has landed each wave rebuilds half of one page's keys
+//    in place (U^T = B_K^T C_K^T on the matrix cores, rotated, added to K_base) and a
+//    second barrier publishes the rebuilt tile.
 //
 // Buffer layout (bytes): K blocks [page][4 KB], V blocks [page][4 KB], rCache pages as
 // [rank tile][page][1 KB] (four pages of one rank tile are 1 KB apart).  All are stored
@@ -463,14 +89,11 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs p) {
 constexpr float kLazyRescale = 8.f;
 
 constexpr int kStreamWaves = 8;
-// RoPE on, the streaming kernel serves ranks up to 32 (its LDS ring and B_K^T fragments
-// fit one workgroup's LDS); rank 64 takes the kernel above
-constexpr bool stream_rope(int r) { return r <= 32; }
 constexpr int kStreamRows = kStreamWaves * ROWS_PER_WAVE;
 
 template <int R, bool ROPE>
 struct StreamShape {
-    static constexpr int NBUF = ROPE ? 2 : 3;  // ring buffers (copies NBUF - 1 tiles ahead)
+    static constexpr int NBUF = (ROPE && R > 32) ? 2 : 3;  // ring buffers (copies NBUF - 1 tiles ahead)
     static constexpr int RT = R == 0 ? 0 : (R + 15) / 16;
     static constexpr int SBK_BYTES = ROPE ? RT * 8 * 64 * 8 : 0;  // B_K^T fragments (RoPE on)
     static constexpr int K_OFF = 0;
@@ -478,13 +101,16 @@ struct StreamShape {
     static constexpr int C_OFF = 8 * 4096;
     // RoPE on: table rows [page][half][cos m, cos m + 1, sin m, sin m + 1][1 KB], m = 2 half
     static constexpr int T_OFF = C_OFF + 4 * RT * 1024;
-    static constexpr int BUF_BYTES = T_OFF + (ROPE ? 4 * 2 * 4096 : 0);
+    // RoPE on: [page pw][half][cos, sin][frequency tile j][lane group] 16 B
+    static constexpr int BUF_BYTES = T_OFF + (ROPE ? 4 * 2 * 256 : 0);
     static constexpr int SBV_BYTES = R > 0 ? R * D * 4 : 16;
     static constexpr int SACC_BYTES = R > 0 ? kStreamRows * R * 4 : 16;
     static constexpr int EPI_BYTES = SBV_BYTES + SACC_BYTES;
     static constexpr int RING_BYTES = NBUF * BUF_BYTES;
     static constexpr int MAIN_BYTES = RING_BYTES > EPI_BYTES ? RING_BYTES : EPI_BYTES;
-    static constexpr int LDS_BYTES = MAIN_BYTES + SBK_BYTES;
+    // RoPE on: cos then sin of positions 0..15 in the table's own order ([tile m][lane] 16 B)
+    static constexpr int COLT_BYTES = ROPE ? 2 * 4096 : 0;
+    static constexpr int LDS_BYTES = MAIN_BYTES + SBK_BYTES + COLT_BYTES;
     static_assert(LDS_BYTES <= 160 * 1024, "LDS of one workgroup");
 };
 
@@ -548,6 +174,10 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
     auto buf = [&](int tile) __attribute__((always_inline)) -> LdsU32x4 * {
         return (LdsU32x4 *)(lds + (tile % S::NBUF) * (S::BUF_BYTES / 16));
     };
+    // RoPE tables (rope_rows positions of D / 2 floats each)
+    const int rope_bytes = ROPE ? p.rope_rows * (D / 2) * 4 : 0;
+    const i32x4 rope_rc = block_rsrc(reinterpret_cast<uint64_t>(p.rope_cos), rope_bytes);
+    const i32x4 rope_rs = block_rsrc(reinterpret_cast<uint64_t>(p.rope_sin), rope_bytes);
     // this wave's copies of tile `tile` (page 4 tile + pw)
     auto copy_tile = [&](int tile, int idb, int idr) __attribute__((always_inline)) {
         LdsU32x4 *b = buf(tile);
@@ -565,17 +195,16 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
         }
         if constexpr (ROPE && R > 0) {
             if (use_res) {
-                // the table rows this wave's rebuild uses: frequency tiles 2 half, 2 half + 1
-                // of page pw (1 KB each, cos then sin)
-                const int64_t pg = min(tile * 4 + pw, n_pages - 1);
-                const uint64_t off = (uint64_t)(pg * (PS * D / 2) + 2 * half * 256) * 4;
-                const i32x4 tc = block_rsrc(reinterpret_cast<uint64_t>(p.rope_cos) + off, 2048);
-                const i32x4 ts = block_rsrc(reinterpret_cast<uint64_t>(p.rope_sin) + off, 2048);
-                LdsU32x4 *td = b + (S::T_OFF + (pw * 2 + half) * 4096) / 16;
-                lds_dma16(tc, lane * 16, td);
-                lds_dma16(tc, lane * 16 + 1024, td + 64);
-                lds_dma16(ts, lane * 16, td + 128);
-                lds_dma16(ts, lane * 16 + 1024, td + 192);
+                // cos and sin at the first position of page pw for the frequencies this wave's
+                // rebuild uses: lane 4j + g (< 8) copies the 16 bytes that lane group g holds in
+                // frequency tile 2 half + j of the page's first table row
+                const int pg = min(tile * 4 + pw, n_pages - 1);
+                const int voff = ((pg * (PS * D / 2) + (2 * half + (lane >> 2)) * 256) + 64 * (lane & 3)) * 4;
+                LdsU32x4 *td = b + (S::T_OFF + (pw * 2 + half) * 256) / 16;
+                if (lane < 8) {
+                    lds_dma16(rope_rc, voff, td);
+                    lds_dma16(rope_rs, voff, td + 8);
+                }
             }
         }
     };
@@ -658,6 +287,10 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
                 bkt[idx] = u32x2{w[0], w[1]};
             }
             __syncthreads();  // B_K^T fragments written (no copy into LDS is in flight yet)
+            // cos and sin of positions 0..15 (the first 4 KB of each table): wave w copies
+            // kilobyte w % 4 of cos (w < 4) or sin; they land before the first tile's barrier
+            LdsU32x4 *colt = (LdsU32x4 *)(lds + (S::MAIN_BYTES + S::SBK_BYTES) / 16);
+            lds_dma16(wave < 4 ? rope_rc : rope_rs, lane * 16 + (wave & 3) * 1024, colt + wave * 64);
         }
     }
     // the page ids must be in registers before the first copies read them
@@ -680,9 +313,13 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
         // this wave's copies of the tile have landed (only those of the next tile, issued
         // after them, may still be in flight); after the barrier every wave's have, and
         // every wave is done with the tile before, whose buffer the next copies overwrite
-        // (two buffers: nothing else is in flight)
+        // (last tile, or two buffers: nothing else is in flight)
         if (S::NBUF == 3 && tile + 1 < n_tiles) {
-            if (res_copy) wait_vmcnt<4 + RT>();
+            // per tile a wave copies 4 blocks, plus its rCache page (K waves, with an adapter)
+            // and, RoPE on with an adapter, two table rows
+            constexpr int kTab = (ROPE && R > 0) ? 2 : 0;
+            if (res_copy) wait_vmcnt<4 + RT + kTab>();
+            else if (use_res) wait_vmcnt<4 + kTab>();
             else wait_vmcnt<4>();
         } else {
             wait_vmcnt<0>();
@@ -722,17 +359,25 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
 #pragma unroll
                     for (int j = 0; j < 4; ++j) u[j] = mfma16(bkf[j], ck[t], u[j]);
                 }
-                // rotate-half pairs (tile m with m + 4) at the key's position
-                u32x4 rot[4];  // cos m, cos m + 1, sin m, sin m + 1 of this lane
-                lds_read4(base + S::T_OFF + (pw * 2 + half) * 4096, rot);
+                // rotate-half pairs (tile m with m + 4) at the key's position p0 + col: the
+                // angle of page start p0 plus the angle of offset col (angle addition)
+                u32x4 rot0[4];  // cos m, cos m + 1, sin m, sin m + 1 at p0 (this lane group)
+                lds_read4_64(lds_addr(buf(tile)) + S::T_OFF + (pw * 2 + half) * 256 + grp * 16, rot0);
+                u32x4 rotc[2], rots[2];  // cos, sin of tiles m, m + 1 at position col
+                const uint32_t colt = lds_addr((LdsU32x4 *)lds) + S::MAIN_BYTES + S::SBK_BYTES + 2 * half * 1024 + lane * 16;
+                lds_read2(colt, rotc);
+                lds_read2(colt + 4096, rots);
 #pragma unroll
                 for (int j = 0; j < 2; ++j) {
-                    const f32x4 c = __builtin_bit_cast(f32x4, rot[j]), s = __builtin_bit_cast(f32x4, rot[2 + j]);
+                    const f32x4 c0 = __builtin_bit_cast(f32x4, rot0[j]), s0 = __builtin_bit_cast(f32x4, rot0[2 + j]);
+                    const f32x4 ct = __builtin_bit_cast(f32x4, rotc[j]), st = __builtin_bit_cast(f32x4, rots[j]);
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
+                        const float c = c0[i] * ct[i] - s0[i] * st[i];
+                        const float s = s0[i] * ct[i] + c0[i] * st[i];
                         const float x = u[j][i], y = u[j + 2][i];
-                        u[j][i] = x * c[i] - y * s[i];
-                        u[j + 2][i] = y * c[i] + x * s[i];
+                        u[j][i] = x * c - y * s;
+                        u[j + 2][i] = y * c + x * s;
                     }
                 }
                 // K fragments half (u tiles 2 half, 2 half + 1) and half + 2 (tiles + 4)
@@ -910,6 +555,7 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
 #pragma unroll
             for (int nt = 0; nt < 2; ++nt) {
                 const float *ar = sAcc + (wave * ROWS_PER_WAVE + nt * 16 + col) * R;
+#pragma unroll 4
                 for (int rho = 0; rho < R; ++rho) {
                     const float c = ar[rho];
 #pragma unroll
@@ -936,18 +582,13 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
 
 template <int R, int G, bool ROPE>
 hipError_t launch_prefill(const PrefillArgs &pa, hipStream_t st, void *const *ev) {
-    using S = PrefillShape<R, G, ROPE>;
     hipError_t e;
     const int pairs = (pa.n_agents * pa.hkv + kXcds - 1) / kXcds * kXcds;
     const int grid = pairs * pa.blocks_per_agent_head;
-    (void)sizeof(S);
     // timing events carry the kernel's own start and end timestamps (set by the launch)
     hipEvent_t e0 = ev ? static_cast<hipEvent_t>(ev[0]) : nullptr;
     hipEvent_t e1 = ev ? static_cast<hipEvent_t>(ev[1]) : nullptr;
-    if constexpr (ROPE && !stream_rope(R))
-        hipExtLaunchKernelGGL((prefill_kernel<R, G, ROPE>), dim3(grid), dim3(256), 0, st, e0, e1, 0, pa);
-    else
-        hipExtLaunchKernelGGL((prefill_stream_kernel<R, G, ROPE>), dim3(grid), dim3(64 * kStreamWaves), 0, st, e0, e1, 0, pa);
+    hipExtLaunchKernelGGL((prefill_stream_kernel<R, G, ROPE>), dim3(grid), dim3(64 * kStreamWaves), 0, st, e0, e1, 0, pa);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return hipSuccess;
 }
@@ -999,9 +640,10 @@ extern "C" fkv_status fkv_residual_attention_prefill(const fkv_attn_args *a, voi
     pa.hq = a->hq;
     pa.hkv = a->hkv;
     pa.max_pages = a->max_pages;
+    pa.rope_rows = a->rope_cos ? a->rope_max_pos : 0;
     // query blocks per (agent, KV head); blocks past an agent's own chunk exit at once
     const bool rope = a->rope_cos != nullptr && a->r > 0;
-    const int tok_per_wg = ((rope && !stream_rope(a->r)) ? ROWS_PER_WG : kStreamRows) / g;
+    const int tok_per_wg = kStreamRows / g;
     const int maxq = a->max_q_per_agent > 0 ? a->max_q_per_agent : a->n_q;
     if (maxq > a->n_q) return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_prefill: max_q_per_agent > n_q");
     pa.blocks_per_agent_head = (maxq + tok_per_wg - 1) / tok_per_wg;
