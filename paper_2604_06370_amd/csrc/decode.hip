@@ -89,10 +89,10 @@ constexpr int cmin(int a, int b) { return a < b ? a : b; }
 // rounded up to a multiple of 4 so every record is 16-byte aligned.
 __host__ __device__ constexpr int ws_stride_of(int r) { return (D + r + 2 + 3) / 4 * 4; }
 
-// Partial rows travel between workgroups of one launch (the merged launch) and between
-// launches.  They are written and read at device scope (cache policy sc1: coherent
-// across the XCDs' L2 caches, no cache write-back or invalidation needed), 16 bytes per
-// lane, through a buffer resource over the workspace (byte offsets below 4 GiB).
+// Partial rows travel from the split kernel to the merge kernel.  They are written and read
+// at device scope (cache policy sc1: coherent across the XCDs' L2 caches, no cache
+// write-back or invalidation needed), 16 bytes per lane, through a buffer resource over the
+// workspace (byte offsets below 4 GiB).
 __device__ void raw_buffer_store_v4f32(f32x4 data, i32x4 rsrc, int voffset, int soffset, int aux) __asm("llvm.amdgcn.raw.buffer.store.v4f32");
 __device__ f32x4 raw_buffer_load_v4f32(i32x4 rsrc, int voffset, int soffset, int aux) __asm("llvm.amdgcn.raw.buffer.load.v4f32");
 constexpr int kDeviceCoherent = 16;  // cache-policy operand: sc1
@@ -418,18 +418,21 @@ __device__ __forceinline__ void split_body(const DecodeArgs &p) {
 
     // rCache fragments of the wave's slots (NSA: 1 or NSR) for NP item pages from k0: one
     // 16-byte load per (page, slot, rank tile), at the address the descriptor names
-    auto load_c = [&](auto nsa_tag, auto np_tag, int k0, CFrag &c) __attribute__((always_inline)) {
-        constexpr int NSA = decltype(nsa_tag)::value, NP = decltype(np_tag)::value;
+    auto load_c_page = [&](auto nsa_tag, int j, int k, CFrag &c) __attribute__((always_inline)) {
+        constexpr int NSA = decltype(nsa_tag)::value;
         if constexpr (R > 0) {
 #pragma unroll
-            for (int j = 0; j < NP; ++j)
+            for (int s = 0; s < NSA; ++s) {
+                const i32x4 rs = block_rsrc(res_addr(k, s), RT * 1024);
 #pragma unroll
-                for (int s = 0; s < NSA; ++s) {
-                    const i32x4 rs = block_rsrc(res_addr(k0 + j, s), RT * 1024);
-#pragma unroll
-                    for (int t = 0; t < RT; ++t) c.kv[j][s][t] = buf_load16(rs, lane * 16 + t * 1024);
-                }
+                for (int t = 0; t < RT; ++t) c.kv[j][s][t] = buf_load16(rs, lane * 16 + t * 1024);
+            }
         }
+    };
+    auto load_c = [&](auto nsa_tag, auto np_tag, int k0, CFrag &c) __attribute__((always_inline)) {
+        constexpr int NP = decltype(np_tag)::value;
+#pragma unroll
+        for (int j = 0; j < NP; ++j) load_c_page(nsa_tag, j, k0 + j, c);
     };
 
     // ---- Stages 1-2 for NP item pages from k0, fragments in registers ----
@@ -437,7 +440,10 @@ __device__ __forceinline__ void split_body(const DecodeArgs &p) {
     // vf[j][q2]: the page's value chunk q2 in its stored order, dims 32q2 + col (.xy) and
     // 32q2 + 16 + col (.zw) of tokens 4grp .. 4grp + 3.  For two pages the value product
     // takes 32 keys: the pair's two 8-byte halves form one 16x16x32 operand.
-    auto compute = [&](auto nsa_tag, auto np_tag, int k0, auto &&get_k, auto &&get_v, CFrag &c)
+    // `hook(0)` runs after the score products, `hook(1)` before the value products: the ring
+    // path issues the next stages' rCache loads there, so that the texture path works while
+    // the wave computes instead of all four waves issuing together after the barrier.
+    auto compute = [&](auto nsa_tag, auto np_tag, int k0, auto &&get_k, auto &&get_v, CFrag &c, auto &&hook)
         __attribute__((always_inline)) {
         constexpr int NSA = decltype(nsa_tag)::value;
         constexpr int NP = decltype(np_tag)::value;
@@ -504,6 +510,9 @@ __device__ __forceinline__ void split_body(const DecodeArgs &p) {
                 }
             }
         }
+        __builtin_amdgcn_sched_barrier(0);
+        hook(0);
+        __builtin_amdgcn_sched_barrier(0);
         // Stage 2: online softmax over the step's keys (rows in lanes, keys in lane groups).
         // Keys 4grp + i of page j are visible to this lane's row when i < kv; a step inside
         // every row's sequence skips the test.
@@ -551,6 +560,9 @@ __device__ __forceinline__ void split_body(const DecodeArgs &p) {
             pf[j] = pack4(pv);
         }
         st.l += psum;
+        __builtin_amdgcn_sched_barrier(0);
+        hook(1);
+        __builtin_amdgcn_sched_barrier(0);
         u32x4 vf[NP][4];
         get_v(vf);
         // value tokens past the item's longest sequence (or on a padding page) may hold any
@@ -633,10 +645,17 @@ __device__ __forceinline__ void split_body(const DecodeArgs &p) {
             // reads whose wait is part of the same instruction group: the compiler sees no
             // LDS load that it would have to order after the copies still in flight, which
             // are waited for (by count) before the barrier that precedes each stage.
+            // The copies go first, the rCache loads of stage s + 2 one page each after the score
+            // and before the value products of stage s (a stage's copies are then followed by
+            // at least (kRing - 2) * (4 + NC) vector-memory operations before it is computed,
+            // the count each stage waits for).
             auto iterate = [&](auto nsa_tag, auto np_tag, int s, CFrag &c_now, CFrag &c_next2) __attribute__((always_inline)) {
                 constexpr int NP = decltype(np_tag)::value;
-                load_c(nsa_tag, np_tag, 2 * (s + 2) + (NP == 2 ? 0 : copy), c_next2);
                 dma_stage(s + kRing - 1, ring_buf(s + kRing - 1));
+                const int kc = 2 * (s + 2) + (NP == 2 ? 0 : copy);
+                auto hook = [&](int ph) __attribute__((always_inline)) {
+                    if (ph < NP) load_c_page(nsa_tag, ph, kc + ph, c_next2);
+                };
                 const uint32_t cur = lds_addr(ring_buf(s)) + lane * 16;
                 auto get_k = [&](u32x4 (&kf)[NP][4]) __attribute__((always_inline)) {
 #pragma unroll
@@ -646,7 +665,7 @@ __device__ __forceinline__ void split_body(const DecodeArgs &p) {
 #pragma unroll
                     for (int j = 0; j < NP; ++j) lds_read4(cur + (NP == 2 ? j : copy) * 2 * kBlockBytes + kBlockBytes, vf[j]);
                 };
-                compute(nsa_tag, np_tag, 2 * s + (NP == 2 ? 0 : copy), get_k, get_v, c_now);
+                compute(nsa_tag, np_tag, 2 * s + (NP == 2 ? 0 : copy), get_k, get_v, c_now, hook);
             };
             auto run = [&](auto nsa_tag, auto np_tag) __attribute__((always_inline)) {
                 constexpr int NP = decltype(np_tag)::value;
@@ -699,6 +718,7 @@ __device__ __forceinline__ void split_body(const DecodeArgs &p) {
             for (int i = 0; i < 4; ++i) pr.v[0][i] = buf_load16(rv, lane * 16 + i * 1024);
             load_c(nsa_tag, I1{}, k, pr.c);
         };
+        auto no_hook = [](int) {};
         auto regs_k = [](PageRegs &pr) {
             return [&pr](u32x4 (&kf)[1][4]) __attribute__((always_inline)) {
 #pragma unroll
@@ -719,10 +739,10 @@ __device__ __forceinline__ void split_body(const DecodeArgs &p) {
             prologue_products();
             for (int i = 0; i < n_my;) {
                 load_page(nsa_tag, wave + WAVES * (i + 1), pb);
-                compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pa), regs_v(pa), pa.c);
+                compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pa), regs_v(pa), pa.c, no_hook);
                 if (++i >= n_my) break;
                 load_page(nsa_tag, wave + WAVES * (i + 1), pa);
-                compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pb), regs_v(pb), pb.c);
+                compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pb), regs_v(pb), pb.c, no_hook);
                 if (++i >= n_my) break;
             }
         };
@@ -733,13 +753,13 @@ __device__ __forceinline__ void split_body(const DecodeArgs &p) {
             prologue_products();
             for (int i = 0; i < n_my;) {
                 load_page(nsa_tag, wave + WAVES * (i + 2), pc);
-                compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pa), regs_v(pa), pa.c);
+                compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pa), regs_v(pa), pa.c, no_hook);
                 if (++i >= n_my) break;
                 load_page(nsa_tag, wave + WAVES * (i + 2), pa);
-                compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pb), regs_v(pb), pb.c);
+                compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pb), regs_v(pb), pb.c, no_hook);
                 if (++i >= n_my) break;
                 load_page(nsa_tag, wave + WAVES * (i + 2), pb);
-                compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pc), regs_v(pc), pc.c);
+                compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pc), regs_v(pc), pc.c, no_hook);
                 if (++i >= n_my) break;
             }
         };
