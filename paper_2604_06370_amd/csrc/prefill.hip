@@ -400,16 +400,23 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
         }
 
         // ---- scores for the 64 keys of the tile, 2 row tiles ----
+        // (below rank 64 two pages' K fragments are read per wait, so each wait on the LDS
+        // is followed by 16 products instead of 8)
         f32x4 sacc[4][2];
+        constexpr int KPW = R < 64 ? 2 : 1;  // pages read per LDS wait
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt) {
-            u32x4 kf[4];
-            lds_read4(base + S::K_OFF + kt * 4096, kf);
-            sacc[kt][0] = sacc[kt][1] = f32x4{0, 0, 0, 0};
+        for (int kt = 0; kt < 4; kt += KPW) {
+            u32x4 kf[KPW][4];
+            if constexpr (KPW == 2) lds_read8(base + S::K_OFF + kt * 4096, base + S::K_OFF + (kt + 1) * 4096, kf[0], kf[1]);
+            else lds_read4(base + S::K_OFF + kt * 4096, kf[0]);
 #pragma unroll
-            for (int kk = 0; kk < 4; ++kk) {
-                sacc[kt][0] = mfma32(kf[kk], qf[0][kk], sacc[kt][0]);
-                sacc[kt][1] = mfma32(kf[kk], qf[1][kk], sacc[kt][1]);
+            for (int j = 0; j < KPW; ++j) {
+                sacc[kt + j][0] = sacc[kt + j][1] = f32x4{0, 0, 0, 0};
+#pragma unroll
+                for (int kk = 0; kk < 4; ++kk) {
+                    sacc[kt + j][0] = mfma32(kf[j][kk], qf[0][kk], sacc[kt + j][0]);
+                    sacc[kt + j][1] = mfma32(kf[j][kk], qf[1][kk], sacc[kt + j][1]);
+                }
             }
         }
         if constexpr (R > 0 && !ROPE) {
