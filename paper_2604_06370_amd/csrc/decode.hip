@@ -193,6 +193,46 @@ __device__ __forceinline__ void write_partial(const DecodeArgs &p, Rows<R> &st, 
     if (grp == 0) raw_buffer_store_v4f32(f32x4{st.m, st.l, 0.f, 0.f}, rs, dst + (D + R) * 4, 0, kDeviceCoherent);
 }
 
+// The wave copies of one agent group (waves my_group + ngp c, c < copies) each hold a partial
+// of the same 16 rows over their share of the pages.  Copies c > 0 leave theirs in LDS (`buf`,
+// at least 4 x (9 + RT) x 1 KB) and copy 0 merges them into its own (the weights 2^(m_c - M)
+// of a log-sum-exp merge; acc, acc_r and l of a copy always refer to its m), so the group
+// writes one partial.  Every wave of the block calls this; the LDS the block used before is
+// free once all waves have arrived.
+template <int R>
+__device__ __forceinline__ void merge_wave_copies(Rows<R> &st, int wave, int copy, int my_group, int ngp, int copies,
+                                                  f32x4 *buf) {
+    constexpr int RTX = Rows<R>::RTX;
+    constexpr int NF4 = 8 + RTX + 1;  // oacc, racc, (m, l) of a lane, in float4 units
+    const int lane = threadIdx.x & 63;
+    __syncthreads();
+    if (copy > 0) {
+        f32x4 *dst = buf + wave * NF4 * 64 + lane;
+#pragma unroll
+        for (int mt = 0; mt < 8; ++mt) dst[mt * 64] = st.oacc[mt];
+#pragma unroll
+        for (int t = 0; t < RTX; ++t) dst[(8 + t) * 64] = st.racc[t];
+        dst[(8 + RTX) * 64] = f32x4{st.m, st.l, 0.f, 0.f};
+    }
+    __syncthreads();
+    if (copy == 0) {
+        for (int c = 1; c < copies; ++c) {
+            const f32x4 *src = buf + (my_group + ngp * c) * NF4 * 64 + lane;
+            const f32x4 ml = src[(8 + RTX) * 64];
+            const float M = fmaxf(st.m, ml.x);
+            const float Mu = M == kNegInf ? 0.f : M;
+            const float w0 = fast_exp2(st.m - Mu), w1 = fast_exp2(ml.x - Mu);
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) st.oacc[mt] = st.oacc[mt] * w0 + src[mt * 64] * w1;
+#pragma unroll
+            for (int t = 0; t < RTX; ++t) st.racc[t] = st.racc[t] * w0 + src[(8 + t) * 64] * w1;
+            st.l = st.l * w0 + ml.y * w1;
+            st.m = M;
+        }
+    }
+}
+constexpr int merge_lds_bytes(int r) { return 4 * (8 + (r > 0 ? (r + 15) / 16 : 1) + 1) * 64 * 16; }
+
 // Q^T as the B operand of the 16x16x32 products.  The head-dim index of slot j in
 // k-step kk is 32kk + 16(j/4) + 4grp + j%4 for this lane group: the order in which
 // a rebuilt key tile leaves the 16x16x16 accumulators and in which K blocks are
@@ -355,14 +395,14 @@ __device__ __forceinline__ void split_body(const DecodeArgs &p) {
     }
     const int src_lane = (sb + my_slot) & 63;
     const int sh_agent = __shfl(l_agent, src_lane), sh_len = __shfl(l_len, src_lane);
-    const int my_part = __shfl(l_part, src_lane) + copy;  // this lane's row's partial
+    const int my_part = __shfl(l_part, src_lane);  // this lane's row's partial
     const int my_agent = row_active ? sh_agent : 0;
     const int my_len = row_active ? sh_len : 0;
     const int64_t my_row = ((int64_t)my_part * G + col % G) * hkv + h;
     if (npg <= 0) {  // the item's agents have not reached it yet: an empty partial (weight 0)
         Rows<R> empty;
         empty.init();
-        write_partial<R>(p, empty, row_active, my_row, grp);
+        if (copy == 0) write_partial<R>(p, empty, row_active, my_row, grp);
         return;
     }
 
@@ -767,7 +807,9 @@ __device__ __forceinline__ void split_body(const DecodeArgs &p) {
         else run2(NSF{});
     }
 
-    write_partial<R>(p, st, row_active, my_row, grp);
+    static_assert(merge_lds_bytes(R) <= kRing * kStageBytes, "merge area inside the ring");
+    merge_wave_copies<R>(st, wave, copy, my_group, ngp, WAVES / ngp, reinterpret_cast<f32x4 *>(lds_ring));
+    if (copy == 0) write_partial<R>(p, st, row_active, my_row, grp);
 }
 
 template <int R, int G>
@@ -808,7 +850,8 @@ __global__ __launch_bounds__(256, 2) void decode_rope_kernel(DecodeArgs p) {
     using RowsT = Rows<R>;
     constexpr int RT = S::RT, NSW = S::NSW, MS = S::MS;
     constexpr int RTX = RowsT::RTX;
-    __shared__ __attribute__((aligned(16))) u32x2 bkt[S::BKT / 8];
+    // B_K^T fragments for the launch; at the end the merge area of the wave copies
+    __shared__ __attribute__((aligned(16))) u32x2 bkt[cmax(S::BKT, merge_lds_bytes(R)) / 8];
 
     const int32_t *plan = p.plan;
     const int blk = plan[p.off_blocks + blockIdx.x];
@@ -871,13 +914,13 @@ __global__ __launch_bounds__(256, 2) void decode_rope_kernel(DecodeArgs p) {
     const int sh_agent = __shfl(l_agent, src_lane), sh_len = __shfl(l_len, src_lane);
     const int my_agent = row_active ? sh_agent : 0;
     const int my_len = row_active ? sh_len : 0;
-    const int my_part = __shfl(l_part, src_lane) + copy;
+    const int my_part = __shfl(l_part, src_lane);
     const int64_t my_row = ((int64_t)my_part * G + col % G) * hkv + h;
 
     RowsT st;
     st.init();
     if (npg <= 0) {  // the item's agents have not reached it yet: an empty partial (weight 0)
-        write_partial<R>(p, st, row_active, my_row, grp);
+        if (copy == 0) write_partial<R>(p, st, row_active, my_row, grp);
         return;
     }
 
@@ -1081,7 +1124,8 @@ __global__ __launch_bounds__(256, 2) void decode_rope_kernel(DecodeArgs p) {
         softmax_pv<R, NSW>(st, sacc, row_active, tok0, my_len, p.scale_log2, vf, cv, my_slot, grp);
         load_v(next);
     }
-    write_partial<R>(p, st, row_active, my_row, grp);
+    merge_wave_copies<R>(st, wave, copy, my_group, ngp, copies, reinterpret_cast<f32x4 *>(bkt));
+    if (copy == 0) write_partial<R>(p, st, row_active, my_row, grp);
 }
 
 

@@ -15,9 +15,8 @@ void clear_error();
 
 // Decode plan, host side.  Serialised layout (all int32):
 //   header[kHeaderWords]
-//   items   [n_items][kItemWords]  {page_begin, page_cap, leader, n_ag, copies, page_end_at_plan,
-//                                   agent[16], partial[16]}  (partial[j] + c: partial of slot j,
-//                                   copy c).  The item covers pages page_begin .. min(page_cap,
+//   items   [n_items][kItemWords]  {page_begin, page_cap, leader, n_ag, copies (1), page_end_at_plan,
+//                                   agent[16], partial[16]}  (partial[j]: partial of slot j).  The item covers pages page_begin .. min(page_cap,
 //                                   ceil(longest length / ps)) - 1 of its agents, the length read
 //                                   from the device array at launch, so an item whose agent grows
 //                                   reads the new pages (up to page_cap) without a new plan.
@@ -32,8 +31,9 @@ void clear_error();
 //   descriptors [n_blocks][kDescWords]  (RoPE-off plans) see below
 // An item holds up to four agent groups; a group is the floor(16/g) agents whose
 // query heads of one KV head fill the 16 rows of one matrix-core tile.  An item of
-// ng groups runs on 4 / ngp wave copies (ngp = 1, 2, 4 for ng = 1, 2, 3..4); every
-// copy writes its own partial, so the item owns copies * n_ag partials (g rows each).
+// ng groups runs on 4 / ngp wave copies (ngp = 1, 2, 4 for ng = 1, 2, 3..4); the copies
+// of a group merge their partials in LDS, so the item owns n_ag partials (g rows each) and
+// its `copies` field (partials per slot) is 1.
 // The plan holds no page id, sequence length or adapter: the kernels read them from the
 // block tables, seq_lens and adapter_idx of the launch.
 constexpr int kHeaderWords = 24;

@@ -216,8 +216,9 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     }
 
     // 4. work items, clustered by (segment, split).  An item of ng agent groups runs its
-    //    groups on 4 / ngp wave copies (ngp = ng rounded up to 1, 2 or 4), each writing its
-    //    own partial rows: rows = copies * agents * g.
+    //    groups on 4 / ngp wave copies (ngp = ng rounded up to 1, 2 or 4); the copies of a
+    //    group merge their partial rows inside the workgroup, so every slot owns one partial
+    //    (the `copies` field of an item: partials per slot, 1): rows = agents * g.
     struct Item { int32_t p0, p1, cap, copies; double cost; std::vector<int32_t> agents; };
     std::vector<Item> items;
     std::vector<std::pair<int32_t, int32_t>> clusters;  // [first item, item count)
@@ -235,9 +236,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
             double cost = 0;
             size_t k = 0;
             for (size_t c : chunks) {
-                const int32_t ng = (int32_t)((c + ag - 1) / ag);
-                const int32_t ngp = ng == 1 ? 1 : (ng == 2 ? 2 : 4);
-                Item it{p0, p1, p1, fkv::kMaxGroups / ngp, 0.0, {}};
+                Item it{p0, p1, p1, 1, 0.0, {}};
                 for (size_t j = k; j < k + c; ++j) it.agents.push_back(s.agents[j]);
                 k += c;
                 total_rows += (int64_t)it.copies * (int64_t)c * g;
@@ -269,7 +268,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
             last.cap = last.p1 + room;
         } else {
             const int32_t first = (int32_t)items.size();
-            Item it{npages[a], npages[a], npages[a] + room, fkv::kMaxGroups, kItemOverhead, {a}};
+            Item it{npages[a], npages[a], npages[a] + room, 1, kItemOverhead, {a}};
             total_rows += (int64_t)it.copies * g;
             items.push_back(std::move(it));
             clusters.push_back({first, 1});
@@ -306,7 +305,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     const int32_t n_blocks = (int32_t)(depth * kNumXcd);
 
     // 6. partials, contiguous per agent (CSR): agent a owns [ptr[a], ptr[a+1]); slot j of an
-    //    item writes its copies c to partials first[j] + c
+    //    item writes partial first[j]
     std::vector<int32_t> ptr(A + 1, 0);
     for (const auto &it : items)
         for (int32_t a : it.agents) ptr[a + 1] += it.copies;

@@ -328,7 +328,7 @@ def test_decode_plan_items_cover_every_agent_page_once(hq, hkv, r, rope, pps):
             # agents per group: a 16-row tile without RoPE; with RoPE the slots one wave serves
             ag = 16 // g if not rope else (1 if r >= 64 else min(2, 16 // g) if r >= 32 else 16 // g)
             ng = -(-it["nag"] // ag)
-            assert ng <= 4 and it["copies"] == 4 // (1 if ng == 1 else 2 if ng == 2 else 4)
+            assert ng <= 4 and it["copies"] == 1  # the wave copies of a group merge in the workgroup
             for j, a in enumerate(it["agents"]):
                 owned[a] += [it["first"][j] + c for c in range(it["copies"])]
         for a in range(n_agents):
@@ -369,7 +369,7 @@ def test_decode_plan_items_cover_every_agent_page_once(hq, hkv, r, rope, pps):
 def test_noalloc_decode_rejects_plans_beyond_its_static_workspace():
     """Checked on the host before any device call: a plan whose partial rows exceed the
     static array is refused with FKV_ERR_INVALID."""
-    A, mp, ps = 16, 320, 16
+    A, mp, ps = 48, 320, 16
     bb = np.arange(A * mp, dtype=np.int32).reshape(A, mp)      # nothing shared: private items only
     sl = np.full(A, mp * ps, dtype=np.int32)
     plan = rt.DecodePlan(bb, sl, 32, 8, ps, pages_per_split=4, r=16, rope=False, res_bt=bb,

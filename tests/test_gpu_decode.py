@@ -170,10 +170,10 @@ def test_one_kv_head_many_partials(rope):
     """One GPU's share of a tensor-parallel deployment (one KV head, four query heads): 16 rows
     with over 128 partials each, merged by sixteen waves per row.  The split sizes make the
     partials many; the result must not depend on how they are merged."""
-    wl = W.fanout("tp-share", 47, n_agents=4, prefix=4096, suffix_lo=5, suffix_hi=200, hq=4, hkv=1, r=16)
+    wl = W.fanout("tp-share", 47, n_agents=4, prefix=8192, suffix_lo=5, suffix_hi=200, hq=4, hkv=1, r=16)
     lw = LoadedWorkload(wl, rope=rope, pages_per_split=4)
     info = lw.decode_setup()["info"]
-    assert info["workspace_bytes"] > 4 * 4 * 128 * (128 + 16 + 2) * 4  # > 128 partial rows per query row
+    assert info["workspace_bytes"] > 4 * 4 * 128 * (128 + 16 + 4) * 4  # > 128 partial rows per query row
     out = lw.decode().clone()
     torch.cuda.synchronize()
     check_close(f"one-kv-head rope={rope}", out, oracle_decode(wl, wl.decode_agents(), rope))
