@@ -232,10 +232,12 @@ typedef struct {
     int32_t pages_per_split;
 } fkv_plan_info;
 
-/* Most agents one decode work item can hold for (hq, hkv, r, rope): with RoPE one group
- * of floor(16/g) agents; without RoPE up to four groups, as many as fit one LDS stage
- * together with a page of four KV heads' base blocks.  Returns 0 for an unsupported
- * head layout. */
+/* Most agents one decode work item can hold for (hq, hkv, r, rope).  A group is the
+ * floor(16/g) agents whose query heads of one KV head fill a 16-row matrix tile.  Without
+ * RoPE: four groups below rank 32, two at rank 32, one (of at most two agents) at rank 64.
+ * With RoPE: up to four wave groups of the agents one wave rebuilds (a whole group below
+ * rank 32, two agents at rank 32, one at rank 64), at most 16 / ceil(r/16) agents (their
+ * B_K^T fragments fill 64 KB of LDS).  Returns 0 for an unsupported head layout. */
 int32_t fkv_decode_plan_default_agents(int32_t hq, int32_t hkv, int32_t r, int32_t rope);
 
 /* Build a plan from host copies of the decode call's base block table base_bt

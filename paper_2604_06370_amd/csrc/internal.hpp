@@ -66,8 +66,8 @@ constexpr int kDescWords = kDescPart + kMaxItemAgents;
 // Decode: one workgroup per (work item, KV head).  Without RoPE an item holds up to four
 // agent groups below rank 32 and up to two at rank 32 (and at rank 64 with eight query heads
 // per KV head), their base pages shared through LDS; otherwise one group, of at most two
-// agents at rank 64 (the wave keeps every slot's rCache fragments of a stage in registers).  With RoPE an item holds one
-// group.  Agent slots one wave serves without RoPE:
+// agents at rank 64 (the wave keeps every slot's rCache fragments of a stage in registers).
+// With RoPE see decode_rope_wave_agents below.  Agent slots one wave serves without RoPE:
 constexpr int decode_wave_slots(int g, int r) {
     return r >= 64 ? (kMaxRows / g < 2 ? kMaxRows / g : 2) : kMaxRows / g;
 }
@@ -85,7 +85,6 @@ constexpr int decode_rope_item_agents(int g, int r) {
     const int ms = 4 * decode_rope_wave_agents(g, r);
     return ms < 16 / rt ? ms : 16 / rt;
 }
-// Largest number of agents per work item:
 // Agent groups one RoPE-off work item may hold: four below rank 32; two at rank 32 and at
 // rank 64 when one wave serves a whole group (a stage's rCache fragments of a group then fit the
 // registers of four groups at rank 16); one otherwise.
