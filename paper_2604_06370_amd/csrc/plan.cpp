@@ -195,11 +195,24 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
         if (best_u < 0) best_u = 64;
         for (size_t i = 0; i < sc.size(); ++i) cand_pps[i] = is_multi(i) ? multi_pps : std::min(best_u, sc[i].cap);
         // RoPE on: the per-page rebuild and rotation of every agent's keys bound the kernel,
-        // not the balance of items; items of 32 pages (fewer when a segment is shorter) keep
-        // the per-workgroup B_K^T build small against the pages it serves (measured on the
-        // 16-agent, 32K-prefix workload: 16 to 64 pages within 12 %, 32 best, 96 and 128 far
-        // slower).
-        constexpr int32_t kRopePages = 32;
+        // not the balance of items.  Items of 32 pages (fewer when a segment is shorter) when
+        // that gives the two resident workgroups per compute unit few rounds (16 agents over
+        // a 32K prefix: 1152 workgroups; 16 to 64 pages within 12 %, 32 best); on larger
+        // workloads items of 64 or 128 pages, the largest that still leave at least 2.5
+        // workgroups per resident slot: fewer B_K^T builds and partial rows per page (64
+        // agents over a 128K tree: 2978 -> 2743 us per step at 128 pages; 70B heads, 24
+        // agents: 727 -> 637 us).
+        int32_t rope_pages = 32;
+        if (rope) {
+            auto rope_blocks = [&](int32_t pages) {
+                int64_t b = 0;
+                for (size_t i = 0; i < segs.size(); ++i)
+                    b += (int64_t)((segs[i].n + pages - 1) / pages) * (int64_t)chunk_sizes(segs[i].agents.size()).size();
+                return b * nhb_units;
+            };
+            for (int32_t pages : {64, 128})
+                if (rope_blocks(pages) * 2 >= 5 * slots * nhb_units) rope_pages = pages;
+        }
         for (size_t i = 0; i < segs.size(); ++i) {
             int32_t pps;
             if (prm->pages_per_split > 0) {
@@ -207,7 +220,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
                     return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: pages_per_split above 128");
                 pps = std::min(prm->pages_per_split, sc[i].cap);
             } else {
-                const int32_t target = rope ? kRopePages : cand_pps[i];
+                const int32_t target = rope ? rope_pages : cand_pps[i];
                 const int64_t k = (segs[i].n + target - 1) / target;
                 pps = (int32_t)((segs[i].n + k - 1) / k);
             }
