@@ -2,17 +2,20 @@
 //
 // One workgroup = one (work item, KV head h), four waves.  A work item is a page range
 // of a segment together with the agents that read the same base pages there, in groups
-// of floor(16/g) agents whose g query heads of KV head h fill the 16 rows of one
-// matrix-core tile.  An item of ng groups runs on the four waves as ng groups x 4/ngp
-// copies (ngp = ng rounded up to 1, 2 or 4); each copy covers its share of the pages
-// and writes its own partial rows (acc, acc_r, m, l) straight from registers.  A second
-// kernel merges an agent's partials (log-sum-exp combine) and applies Stage 3.
-//  - single-group items (private suffixes; every item with RoPE or rank >= 32): the
-//    waves stride over the pages with a register-double-buffered pipeline;
-//  - multi-group items (shared prefixes): stages of two pages; each base K/V block is
-//    copied once from memory straight into an LDS ring (three stages ahead) and every
-//    wave applies it to its own group's 16 rows, so a shared page crosses the memory
-//    hierarchy once per workgroup instead of once per group.
+// of agents whose query heads of KV head h fill the 16 rows of one matrix-core tile.  An
+// item of ng groups runs on the four waves as ng groups x 4/ngp copies (ngp = ng rounded
+// up to 1, 2 or 4); each copy covers its share of the pages, the copies of a group merge
+// their partial rows (acc, acc_r, m, l) in LDS, and the group writes one partial per
+// agent.  A second kernel merges an agent's partials (log-sum-exp combine) and applies
+// Stage 3.  Without RoPE (decode_split_kernel):
+//  - items of one group (private suffixes): the waves stride over the pages with a
+//    register-double-buffered pipeline;
+//  - items of two to four groups (shared prefixes): each base K/V block is copied once
+//    from memory straight into an LDS ring (three stages ahead) and every wave applies it
+//    to its own group's 16 rows, so a shared page crosses the memory hierarchy once per
+//    workgroup instead of once per group.
+// With RoPE (decode_rope_kernel) every wave streams its pages straight into registers and
+// rebuilds its agents' keys (see there).
 //
 // Per page and wave (all products on the matrix cores, fp32 accumulate):
 //   S^T  = K_base . Q^T                               16x16x32, all rows of the wave
