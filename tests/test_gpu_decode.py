@@ -107,6 +107,17 @@ def test_rank8_and_no_residual_pool():
     run_case("all agents base-only", wl0, True, residual_delta=False)
 
 
+@pytest.mark.parametrize("rope", [False, True])
+@pytest.mark.parametrize("hq,hkv,r,n_agents", [(12, 3, 16, 10), (16, 2, 16, 7), (40, 5, 8, 12)])
+def test_other_head_layouts(rope, hq, hkv, r, n_agents):
+    """KV-head counts other than 8 (odd ones included) and eight query heads per KV head below
+    rank 32, with items of three or four agent groups over the shared prefix.  Amplified
+    adapters, so that a head or adapter slice taken from the wrong place shows."""
+    wl = W.fanout(f"heads-hq{hq}-hkv{hkv}-r{r}", 58, n_agents=n_agents, prefix=900, suffix_lo=1, suffix_hi=90,
+                  hq=hq, hkv=hkv, r=r, b_std=1.0 / np.sqrt(r))
+    run_case(f"heads hq={hq} hkv={hkv} r={r} rope={rope}", wl, rope)
+
+
 @pytest.mark.parametrize("variant", ["amplified", "sharp", "needle"])
 def test_stress_variants(variant):
     kw = dict(n_agents=16, prefix=1024, suffix_lo=3, suffix_hi=200, hq=32, hkv=8, r=16)

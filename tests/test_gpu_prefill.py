@@ -65,6 +65,15 @@ def test_prefill_small_ragged(rope):
 
 
 @pytest.mark.parametrize("rope", [False, True])
+@pytest.mark.parametrize("hq,hkv", [(12, 3), (16, 2)])
+def test_prefill_other_head_layouts(rope, hq, hkv):
+    """KV-head counts other than 8 (an odd one included) and eight query heads per KV head."""
+    wl = W.fanout(f"pf-hq{hq}-hkv{hkv}", 59, n_agents=3, prefix=200, suffix_lo=1, suffix_hi=40, hq=hq, hkv=hkv,
+                  r=16, chunk=90, b_std=0.25)
+    run_prefill(f"prefill hq={hq} hkv={hkv} rope={rope}", wl, rope)
+
+
+@pytest.mark.parametrize("rope", [False, True])
 def test_prefill_70b_heads_rank64(rope):
     wl = W.tree("pf-70b", 52, node_parent=[-1, -1], node_len=[300, 700], agent_node=[0, 1, 0, 1],
                 suffix_lo=1, suffix_hi=60, hq=64, hkv=8, r=64, b_std=0.05, chunk=[70, 33, 1, 129],
