@@ -1178,14 +1178,22 @@ __global__ __launch_bounds__(64 * CW) void decode_combine_kernel(DecodeArgs p) {
     const int rec0 = (int)(((int64_t)k0 * G * p.hkv + jj * p.hkv + h) * stride * 4) + (lane <= NV ? 16 * lane : 0);
     const int kstride = G * p.hkv * stride * 4;
 
-    // B_V[rho][h*D + 4 lane .. +3] for the output dims of lanes 0..31 (wave 0)
-    u32x2 bv[RB];
-    if constexpr (R > 0) {
+    // B_V[rho][h*D + 4 lane .. +3] for the output dims of lanes 0..31 of wave 0, requested at
+    // the start: in registers of wave 0 for the four-wave merge; for the sixteen-wave one (at
+    // most 128 registers per lane) in LDS, each wave copying a share of it.
+    constexpr bool kBvRegs = CW == kCombineWaves;
+    __shared__ u32x2 s_bv[(R > 0 && !kBvRegs) ? R * (D / 4) : 1];
+    const uint16_t *bv_row = p.lora_b + ((int64_t)(ad >= 0 ? ad : 0) * 2 + 1) * R * p.hkv * D + (int64_t)h * D;
+    u32x2 bv[kBvRegs ? RB : 1];
+    if constexpr (R > 0 && kBvRegs) {
         if (wave == 0) {
-            const uint16_t *bvp = p.lora_b + ((int64_t)(ad >= 0 ? ad : 0) * 2 + 1) * R * p.hkv * D + (int64_t)h * D + 4 * (lane & 31);
 #pragma unroll
-            for (int rho = 0; rho < R; ++rho) bv[rho] = ad >= 0 ? ldg64(bvp + (int64_t)rho * p.hkv * D) : u32x2{0, 0};
+            for (int rho = 0; rho < R; ++rho)
+                bv[rho] = ad >= 0 ? ldg64(bv_row + (int64_t)rho * p.hkv * D + 4 * (lane & 31)) : u32x2{0, 0};
         }
+    } else if constexpr (R > 0) {
+        for (int i = threadIdx.x; i < R * (D / 4); i += 64 * CW)
+            s_bv[i] = ad >= 0 ? ldg64(bv_row + (int64_t)(i / (D / 4)) * p.hkv * D + 4 * (i % (D / 4))) : u32x2{0, 0};
     }
 
     f32x4 acc = {0, 0, 0, 0};
@@ -1209,7 +1217,7 @@ __global__ __launch_bounds__(64 * CW) void decode_combine_kernel(DecodeArgs p) {
         if (wave > 0 && lane <= NV) s_acc[wave - 1][lane] = lane == NV ? f32x4{M, L, 0.f, 0.f} : acc;
         __syncthreads();
         if (wave > 0) return;
-#pragma unroll
+#pragma unroll 3
         for (int w = 0; w < CW - 1; ++w) {
             const f32x4 v = lane <= NV ? s_acc[w][lane] : f32x4{0, 0, 0, 0};
             lse_merge(M, L, acc, __shfl(v.x, NV), __shfl(v.y, NV), lane < NV ? v : f32x4{0, 0, 0, 0});
@@ -1217,14 +1225,21 @@ __global__ __launch_bounds__(64 * CW) void decode_combine_kernel(DecodeArgs p) {
     }
     // Stage 3 (Eq. 4): lanes 0..31 own output dims 4 lane .. +3; acc_r sits in lanes 32..
     f32x4 o = acc;
-    if constexpr (R > 0) {
+    auto apply_bv = [&](int rho, u32x2 b) __attribute__((always_inline)) {
+        const float ar = __shfl(acc[rho % 4], D / 4 + rho / 4);
+        o[0] += ar * bf16_lo(b.x);
+        o[1] += ar * bf16_hi(b.x);
+        o[2] += ar * bf16_lo(b.y);
+        o[3] += ar * bf16_hi(b.y);
+    };
+    if constexpr (R > 0 && kBvRegs) {
 #pragma unroll
-        for (int rho = 0; rho < R; ++rho) {
-            const float ar = __shfl(acc[rho % 4], D / 4 + rho / 4);
-            o[0] += ar * bf16_lo(bv[rho].x);
-            o[1] += ar * bf16_hi(bv[rho].x);
-            o[2] += ar * bf16_lo(bv[rho].y);
-            o[3] += ar * bf16_hi(bv[rho].y);
+        for (int rho = 0; rho < R; ++rho) apply_bv(rho, bv[rho]);
+    } else if constexpr (R > 0) {
+        // eight ranks per LDS wait keeps the sixteen-wave merge within its registers
+        for (int r0 = 0; r0 < R; r0 += 8) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) apply_bv(r0 + i, s_bv[(r0 + i) * (D / 4) + (lane & 31)]);
         }
     }
     const float inv = L > 0.f ? 1.f / L : 0.f;
