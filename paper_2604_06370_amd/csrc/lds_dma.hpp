@@ -144,6 +144,51 @@ __device__ __forceinline__ void lds_write2(uint32_t addr0, const u32x4 &v0, uint
         : "memory");
 }
 
+// Compiler-visible forms of the reads above (same addresses and results): the compiler
+// schedules these loads and their waits among the surrounding products.  Only for LDS that
+// no copy in flight writes, read between barriers that LDS accesses cannot cross
+// (lds_fence_barrier).  CV selects them, else the explicit reads.
+__device__ __forceinline__ u32x4 lds_load(uint32_t addr) {
+    return *reinterpret_cast<const __attribute__((address_space(3))) u32x4 *>((uintptr_t)addr);
+}
+template <bool CV>
+__device__ __forceinline__ void lds_get2(uint32_t addr, u32x4 (&out)[2]) {
+    if constexpr (CV) {
+        out[0] = lds_load(addr);
+        out[1] = lds_load(addr + 1024);
+    } else {
+        lds_read2(addr, out);
+    }
+}
+template <bool CV>
+__device__ __forceinline__ void lds_get4(uint32_t addr, u32x4 (&out)[4]) {
+    if constexpr (CV) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) out[i] = lds_load(addr + 1024 * i);
+    } else {
+        lds_read4(addr, out);
+    }
+}
+template <bool CV>
+__device__ __forceinline__ void lds_get8(uint32_t addr0, uint32_t addr1, u32x4 (&o0)[4], u32x4 (&o1)[4]) {
+    if constexpr (CV) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            o0[i] = lds_load(addr0 + 1024 * i);
+            o1[i] = lds_load(addr1 + 1024 * i);
+        }
+    } else {
+        lds_read8(addr0, addr1, o0, o1);
+    }
+}
+// Workgroup barrier after this wave's LDS accesses have completed; the compiler moves no
+// memory access across it.
+__device__ __forceinline__ void lds_fence_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
 // Wait until at most N vector-memory operations of this wave are outstanding.
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {

@@ -94,6 +94,10 @@ constexpr int kStreamRows = kStreamWaves * ROWS_PER_WAVE;
 template <int R, bool ROPE>
 struct StreamShape {
     static constexpr int NBUF = (ROPE && R > 32) ? 2 : 3;  // ring buffers (copies NBUF - 1 tiles ahead)
+    // Tile reads the compiler schedules (rank 64: 15.6 instead of 16.6 ms at 70B heads,
+    // 8 x 1024 rows) or explicit ones that wait for themselves (below: no gain, 22.6 vs
+    // 23.0 ms at 16 x 2048 rows, 8B heads)
+    static constexpr bool CV = R >= 64;
     static constexpr int RT = R == 0 ? 0 : (R + 15) / 16;
     static constexpr int SBK_BYTES = ROPE ? RT * 8 * 64 * 8 : 0;  // B_K^T fragments (RoPE on)
     static constexpr int K_OFF = 0;
@@ -324,7 +328,8 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
         } else {
             wait_vmcnt<0>();
         }
-        __builtin_amdgcn_s_barrier();
+        if constexpr (S::CV) lds_fence_barrier();
+        else __builtin_amdgcn_s_barrier();
         const int tn = tile + S::NBUF - 1;
         if (tn < n_tiles) {
             if ((tn & 63) == 0) {
@@ -395,7 +400,9 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
                     out[j] = u32x4{plo.x, plo.y, phi.x, phi.y};
                 }
                 lds_write2(ka, out[0], kb, out[1]);
-                __builtin_amdgcn_s_barrier();  // the rebuilt tile is complete
+                // the rebuilt tile is complete
+                if constexpr (S::CV) lds_fence_barrier();
+                else __builtin_amdgcn_s_barrier();
             }
         }
 
@@ -407,8 +414,8 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
 #pragma unroll
         for (int kt = 0; kt < 4; kt += KPW) {
             u32x4 kf[KPW][4];
-            if constexpr (KPW == 2) lds_read8(base + S::K_OFF + kt * 4096, base + S::K_OFF + (kt + 1) * 4096, kf[0], kf[1]);
-            else lds_read4(base + S::K_OFF + kt * 4096, kf[0]);
+            if constexpr (KPW == 2) lds_get8<S::CV>(base + S::K_OFF + kt * 4096, base + S::K_OFF + (kt + 1) * 4096, kf[0], kf[1]);
+            else lds_get4<S::CV>(base + S::K_OFF + kt * 4096, kf[0]);
 #pragma unroll
             for (int j = 0; j < KPW; ++j) {
                 sacc[kt + j][0] = sacc[kt + j][1] = f32x4{0, 0, 0, 0};
@@ -425,7 +432,7 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
                 for (int t = 0; t < RT; ++t) {
                     // rCache fragments of the tile's four pages (C_K in .xy)
                     u32x4 cf[4];
-                    lds_read4(base + S::C_OFF + t * 4096, cf);
+                    lds_get4<S::CV>(base + S::C_OFF + t * 4096, cf);
                     // C_K of rank rows 16t + 4grp .. +3 (rank 8: half a tile is padding)
                     const bool kvalid = 16 * t + 4 * grp < R;
 #pragma unroll
@@ -494,7 +501,7 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
             const u32x4 pb0 = u32x4{pf[2 * half][0].x, pf[2 * half][0].y, pf[2 * half + 1][0].x, pf[2 * half + 1][0].y};
             const u32x4 pb1 = u32x4{pf[2 * half][1].x, pf[2 * half][1].y, pf[2 * half + 1][1].x, pf[2 * half + 1][1].y};
             u32x4 v0[4], v1[4];
-            lds_read8(base + S::V_OFF + (2 * half) * 4096, base + S::V_OFF + (2 * half + 1) * 4096, v0, v1);
+            lds_get8<S::CV>(base + S::V_OFF + (2 * half) * 4096, base + S::V_OFF + (2 * half + 1) * 4096, v0, v1);
             if (ragged) {
                 const int vis0 = L - (tile * 4 + 2 * half) * PS, vis1 = vis0 - PS;
 #pragma unroll
@@ -523,7 +530,7 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
                     for (int t = 0; t < RT; ++t) {
                         // C_V of rank 16t + col, tokens 4grp .. +3 of the two pages (.zw)
                         u32x4 cf[2];
-                        lds_read2(base + S::C_OFF + (t * 4 + 2 * half) * 1024, cf);
+                        lds_get2<S::CV>(base + S::C_OFF + (t * 4 + 2 * half) * 1024, cf);
                         u32x2 c0 = u32x2{cf[0].z, cf[0].w};
                         u32x2 c1 = u32x2{cf[1].z, cf[1].w};
                         if (ragged) {
