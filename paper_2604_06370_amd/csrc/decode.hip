@@ -663,152 +663,160 @@ __device__ __forceinline__ void split_body(const DecodeArgs &p) {
     using I2 = std::integral_constant<int, 2>;
     using NSF = std::integral_constant<int, NSR>;
 
-    if (ngp > 1) {
-        if constexpr (S::MULTI) {
-            // Several agent groups share each base page through an LDS ring of kRing stages
-            // of two pages ([K p0 | V p0 | K p1 | V p1], 4 KB each).  Memory writes a stage
-            // straight into LDS (global_load_lds, no registers): wave w copies block w of
-            // stage s + kRing - 1 while stage s is computed.  Four groups: every wave computes
-            // both pages for its group; two groups: wave (group, copy) computes page `copy`.
-            // rCache fragments go to registers two stages ahead.
-            constexpr int NPW_MAX = 2;
-            const int npw = ngp == 4 ? 2 : 1;
-            const int n_stages = (npg + 1) / 2;
-            auto dma_stage = [&](int stage, LdsU32x4 *__restrict__ buf) __attribute__((always_inline)) {
-                const i32x4 rs = block_rsrc(base_addr(2 * stage + (wave >> 1)) + ((wave & 1) ? vbytes : 0), kBlockBytes);
-                LdsU32x4 *dst = buf + wave * (kBlockBytes / 16);
+    // Base pages that no other item reads are loaded as data read once (kDescStream), so
+    // that they displace less of the rCache rows the item's other KV heads re-read from L2.
+    auto paths = [&](auto policy_tag) __attribute__((always_inline)) {
+        constexpr int POL = decltype(policy_tag)::value;
+        if (ngp > 1) {
+            if constexpr (S::MULTI) {
+                // Several agent groups share each base page through an LDS ring of kRing stages
+                // of two pages ([K p0 | V p0 | K p1 | V p1], 4 KB each).  Memory writes a stage
+                // straight into LDS (global_load_lds, no registers): wave w copies block w of
+                // stage s + kRing - 1 while stage s is computed.  Four groups: every wave computes
+                // both pages for its group; two groups: wave (group, copy) computes page `copy`.
+                // rCache fragments go to registers two stages ahead.
+                constexpr int NPW_MAX = 2;
+                const int npw = ngp == 4 ? 2 : 1;
+                const int n_stages = (npg + 1) / 2;
+                auto dma_stage = [&](int stage, LdsU32x4 *__restrict__ buf) __attribute__((always_inline)) {
+                    const i32x4 rs = block_rsrc(base_addr(2 * stage + (wave >> 1)) + ((wave & 1) ? vbytes : 0), kBlockBytes);
+                    LdsU32x4 *dst = buf + wave * (kBlockBytes / 16);
 #pragma unroll
-                for (int i = 0; i < 4; ++i) lds_dma16(rs, lane * 16 + i * 1024, dst + i * 64);
-            };
-            auto ring_buf = [&](int stage) __attribute__((always_inline)) -> LdsU32x4 * {
-                return (LdsU32x4 *)(lds_ring + (stage % kRing) * (kStageBytes / 16));
-            };
-            // One iteration: request the rCache rows of stage s + 2, copy stage s + kRing - 1
-            // into its ring buffer, compute stage s.  The ring is read with explicit LDS
-            // reads whose wait is part of the same instruction group: the compiler sees no
-            // LDS load that it would have to order after the copies still in flight, which
-            // are waited for (by count) before the barrier that precedes each stage.
-            // The copies go first, the rCache loads of stage s + 2 one page each after the score
-            // and before the value products of stage s (a stage's copies are then followed by
-            // at least (kRing - 2) * (4 + NC) vector-memory operations before it is computed,
-            // the count each stage waits for).
-            auto iterate = [&](auto nsa_tag, auto np_tag, int s, CFrag &c_now, CFrag &c_next2) __attribute__((always_inline)) {
-                constexpr int NP = decltype(np_tag)::value;
-                dma_stage(s + kRing - 1, ring_buf(s + kRing - 1));
-                const int kc = 2 * (s + 2) + (NP == 2 ? 0 : copy);
-                auto hook = [&](int ph) __attribute__((always_inline)) {
-                    if (ph < NP) load_c_page(nsa_tag, ph, kc + ph, c_next2);
+                    for (int i = 0; i < 4; ++i) lds_dma16<POL>(rs, lane * 16 + i * 1024, dst + i * 64);
                 };
-                const uint32_t cur = lds_addr(ring_buf(s)) + lane * 16;
-                auto get_k = [&](u32x4 (&kf)[NP][4]) __attribute__((always_inline)) {
-#pragma unroll
-                    for (int j = 0; j < NP; ++j) lds_read4(cur + (NP == 2 ? j : copy) * 2 * kBlockBytes, kf[j]);
+                auto ring_buf = [&](int stage) __attribute__((always_inline)) -> LdsU32x4 * {
+                    return (LdsU32x4 *)(lds_ring + (stage % kRing) * (kStageBytes / 16));
                 };
-                auto get_v = [&](u32x4 (&vf)[NP][4]) __attribute__((always_inline)) {
+                // One iteration: request the rCache rows of stage s + 2, copy stage s + kRing - 1
+                // into its ring buffer, compute stage s.  The ring is read with explicit LDS
+                // reads whose wait is part of the same instruction group: the compiler sees no
+                // LDS load that it would have to order after the copies still in flight, which
+                // are waited for (by count) before the barrier that precedes each stage.
+                // The copies go first, the rCache loads of stage s + 2 one page each after the score
+                // and before the value products of stage s (a stage's copies are then followed by
+                // at least (kRing - 2) * (4 + NC) vector-memory operations before it is computed,
+                // the count each stage waits for).
+                auto iterate = [&](auto nsa_tag, auto np_tag, int s, CFrag &c_now, CFrag &c_next2) __attribute__((always_inline)) {
+                    constexpr int NP = decltype(np_tag)::value;
+                    dma_stage(s + kRing - 1, ring_buf(s + kRing - 1));
+                    const int kc = 2 * (s + 2) + (NP == 2 ? 0 : copy);
+                    auto hook = [&](int ph) __attribute__((always_inline)) {
+                        if (ph < NP) load_c_page(nsa_tag, ph, kc + ph, c_next2);
+                    };
+                    const uint32_t cur = lds_addr(ring_buf(s)) + lane * 16;
+                    auto get_k = [&](u32x4 (&kf)[NP][4]) __attribute__((always_inline)) {
 #pragma unroll
-                    for (int j = 0; j < NP; ++j) lds_read4(cur + (NP == 2 ? j : copy) * 2 * kBlockBytes + kBlockBytes, vf[j]);
+                        for (int j = 0; j < NP; ++j) lds_read4(cur + (NP == 2 ? j : copy) * 2 * kBlockBytes, kf[j]);
+                    };
+                    auto get_v = [&](u32x4 (&vf)[NP][4]) __attribute__((always_inline)) {
+#pragma unroll
+                        for (int j = 0; j < NP; ++j) lds_read4(cur + (NP == 2 ? j : copy) * 2 * kBlockBytes + kBlockBytes, vf[j]);
+                    };
+                    compute(nsa_tag, np_tag, 2 * s + (NP == 2 ? 0 : copy), get_k, get_v, c_now, hook);
                 };
-                compute(nsa_tag, np_tag, 2 * s + (NP == 2 ? 0 : copy), get_k, get_v, c_now, hook);
-            };
-            auto run = [&](auto nsa_tag, auto np_tag) __attribute__((always_inline)) {
-                constexpr int NP = decltype(np_tag)::value;
-                constexpr int NC = R > 0 ? decltype(nsa_tag)::value * NP * RT : 0;  // rCache loads per iteration
-                // vm operations issued after a stage's copies until that stage is computed:
-                // kRing - 2 further iterations
-                constexpr int kWait = (kRing - 2) * (4 + NC);
-                static_assert(kWait < 64, "vmcnt range");
-                CFrag c0, c1, c2;
-                load_c(nsa_tag, np_tag, NP == 2 ? 0 : copy, c0);
-                load_c(nsa_tag, np_tag, 2 + (NP == 2 ? 0 : copy), c1);
+                auto run = [&](auto nsa_tag, auto np_tag) __attribute__((always_inline)) {
+                    constexpr int NP = decltype(np_tag)::value;
+                    constexpr int NC = R > 0 ? decltype(nsa_tag)::value * NP * RT : 0;  // rCache loads per iteration
+                    // vm operations issued after a stage's copies until that stage is computed:
+                    // kRing - 2 further iterations
+                    constexpr int kWait = (kRing - 2) * (4 + NC);
+                    static_assert(kWait < 64, "vmcnt range");
+                    CFrag c0, c1, c2;
+                    load_c(nsa_tag, np_tag, NP == 2 ? 0 : copy, c0);
+                    load_c(nsa_tag, np_tag, 2 + (NP == 2 ? 0 : copy), c1);
 #pragma unroll
-                for (int k = 0; k < kRing - 1; ++k) dma_stage(k, ring_buf(k));
-                prologue_products();
-                for (int s = 0;;) {
-                    stage_barrier<kWait>();
-                    iterate(nsa_tag, np_tag, s, c0, c2);
-                    if (++s >= n_stages) break;
-                    stage_barrier<kWait>();
-                    iterate(nsa_tag, np_tag, s, c1, c0);
-                    if (++s >= n_stages) break;
-                    stage_barrier<kWait>();
-                    iterate(nsa_tag, np_tag, s, c2, c1);
-                    if (++s >= n_stages) break;
+                    for (int k = 0; k < kRing - 1; ++k) dma_stage(k, ring_buf(k));
+                    prologue_products();
+                    for (int s = 0;;) {
+                        stage_barrier<kWait>();
+                        iterate(nsa_tag, np_tag, s, c0, c2);
+                        if (++s >= n_stages) break;
+                        stage_barrier<kWait>();
+                        iterate(nsa_tag, np_tag, s, c1, c0);
+                        if (++s >= n_stages) break;
+                        stage_barrier<kWait>();
+                        iterate(nsa_tag, np_tag, s, c2, c1);
+                        if (++s >= n_stages) break;
+                    }
+                    wait_vmcnt<0>();  // no copy into LDS outlives the block
+                };
+                (void)npw;
+                if constexpr (S::NG == 4) {
+                    if (ngp == 4) run(NSF{}, I2{});
+                    else run(NSF{}, I1{});
+                } else {
+                    run(NSF{}, I1{});  // two groups at most: one page per wave and stage
                 }
-                wait_vmcnt<0>();  // no copy into LDS outlives the block
-            };
-            (void)npw;
-            if constexpr (S::NG == 4) {
-                if (ngp == 4) run(NSF{}, I2{});
-                else run(NSF{}, I1{});
-            } else {
-                run(NSF{}, I1{});  // two groups at most: one page per wave and stage
             }
+        } else {
+            // One agent group: no page is shared between waves.  Wave w computes item pages
+            // w, w + 4, ... straight from registers (the stored fragment order is the operand
+            // order), with the next two pages and their rCache rows in flight.
+            struct PageRegs {
+                u32x4 k[1][4], v[1][4];
+                CFrag c;
+            };
+            auto load_page = [&](auto nsa_tag, int k, PageRegs &pr) __attribute__((always_inline)) {
+                const uint64_t a = base_addr(k);
+                const i32x4 rk = block_rsrc(a, kBlockBytes), rv = block_rsrc(a + vbytes, kBlockBytes);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) pr.k[0][i] = buf_load16<POL>(rk, lane * 16 + i * 1024);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) pr.v[0][i] = buf_load16<POL>(rv, lane * 16 + i * 1024);
+                load_c(nsa_tag, I1{}, k, pr.c);
+            };
+            auto no_hook = [](int) {};
+            auto regs_k = [](PageRegs &pr) {
+                return [&pr](u32x4 (&kf)[1][4]) __attribute__((always_inline)) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) kf[0][i] = pr.k[0][i];
+                };
+            };
+            auto regs_v = [](PageRegs &pr) {
+                return [&pr](u32x4 (&vf)[1][4]) __attribute__((always_inline)) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) vf[0][i] = pr.v[0][i];
+                };
+            };
+            const int n_my = wave < npg ? (npg - wave + WAVES - 1) / WAVES : 0;
+            // one agent: two pages in flight; several agents (more rCache rows per page): one
+            auto run2 = [&](auto nsa_tag) __attribute__((always_inline)) {
+                PageRegs pa, pb;
+                load_page(nsa_tag, wave, pa);
+                prologue_products();
+                for (int i = 0; i < n_my;) {
+                    load_page(nsa_tag, wave + WAVES * (i + 1), pb);
+                    compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pa), regs_v(pa), pa.c, no_hook);
+                    if (++i >= n_my) break;
+                    load_page(nsa_tag, wave + WAVES * (i + 1), pa);
+                    compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pb), regs_v(pb), pb.c, no_hook);
+                    if (++i >= n_my) break;
+                }
+            };
+            auto run1 = [&](auto nsa_tag) __attribute__((always_inline)) {
+                PageRegs pa, pb, pc;
+                load_page(nsa_tag, wave, pa);
+                load_page(nsa_tag, wave + WAVES, pb);
+                prologue_products();
+                for (int i = 0; i < n_my;) {
+                    load_page(nsa_tag, wave + WAVES * (i + 2), pc);
+                    compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pa), regs_v(pa), pa.c, no_hook);
+                    if (++i >= n_my) break;
+                    load_page(nsa_tag, wave + WAVES * (i + 2), pa);
+                    compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pb), regs_v(pb), pb.c, no_hook);
+                    if (++i >= n_my) break;
+                    load_page(nsa_tag, wave + WAVES * (i + 2), pb);
+                    compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pc), regs_v(pc), pc.c, no_hook);
+                    if (++i >= n_my) break;
+                }
+            };
+            if (R == 0 || nag == 1) run1(I1{});
+            else run2(NSF{});
         }
-    } else {
-        // One agent group: no page is shared between waves.  Wave w computes item pages
-        // w, w + 4, ... straight from registers (the stored fragment order is the operand
-        // order), with the next two pages and their rCache rows in flight.
-        struct PageRegs {
-            u32x4 k[1][4], v[1][4];
-            CFrag c;
-        };
-        auto load_page = [&](auto nsa_tag, int k, PageRegs &pr) __attribute__((always_inline)) {
-            const uint64_t a = base_addr(k);
-            const i32x4 rk = block_rsrc(a, kBlockBytes), rv = block_rsrc(a + vbytes, kBlockBytes);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) pr.k[0][i] = buf_load16(rk, lane * 16 + i * 1024);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) pr.v[0][i] = buf_load16(rv, lane * 16 + i * 1024);
-            load_c(nsa_tag, I1{}, k, pr.c);
-        };
-        auto no_hook = [](int) {};
-        auto regs_k = [](PageRegs &pr) {
-            return [&pr](u32x4 (&kf)[1][4]) __attribute__((always_inline)) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) kf[0][i] = pr.k[0][i];
-            };
-        };
-        auto regs_v = [](PageRegs &pr) {
-            return [&pr](u32x4 (&vf)[1][4]) __attribute__((always_inline)) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) vf[0][i] = pr.v[0][i];
-            };
-        };
-        const int n_my = wave < npg ? (npg - wave + WAVES - 1) / WAVES : 0;
-        // one agent: two pages in flight; several agents (more rCache rows per page): one
-        auto run2 = [&](auto nsa_tag) __attribute__((always_inline)) {
-            PageRegs pa, pb;
-            load_page(nsa_tag, wave, pa);
-            prologue_products();
-            for (int i = 0; i < n_my;) {
-                load_page(nsa_tag, wave + WAVES * (i + 1), pb);
-                compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pa), regs_v(pa), pa.c, no_hook);
-                if (++i >= n_my) break;
-                load_page(nsa_tag, wave + WAVES * (i + 1), pa);
-                compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pb), regs_v(pb), pb.c, no_hook);
-                if (++i >= n_my) break;
-            }
-        };
-        auto run1 = [&](auto nsa_tag) __attribute__((always_inline)) {
-            PageRegs pa, pb, pc;
-            load_page(nsa_tag, wave, pa);
-            load_page(nsa_tag, wave + WAVES, pb);
-            prologue_products();
-            for (int i = 0; i < n_my;) {
-                load_page(nsa_tag, wave + WAVES * (i + 2), pc);
-                compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pa), regs_v(pa), pa.c, no_hook);
-                if (++i >= n_my) break;
-                load_page(nsa_tag, wave + WAVES * (i + 2), pa);
-                compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pb), regs_v(pb), pb.c, no_hook);
-                if (++i >= n_my) break;
-                load_page(nsa_tag, wave + WAVES * (i + 2), pb);
-                compute(nsa_tag, I1{}, wave + WAVES * i, regs_k(pc), regs_v(pc), pc.c, no_hook);
-                if (++i >= n_my) break;
-            }
-        };
-        if (R == 0 || nag == 1) run1(I1{});
-        else run2(NSF{});
-    }
+    };
+    // (not at rank 32, where the second instance would not fit the registers without scratch)
+    if (R != 32 && desc[fkv::kDescStream] != 0) paths(std::integral_constant<int, R != 32 ? kCacheStream : kCacheDefault>{});
+    else paths(std::integral_constant<int, kCacheDefault>{});
 
     static_assert(merge_lds_bytes(R) <= kRing * kStageBytes, "merge area inside the ring");
     merge_wave_copies<R>(st, wave, copy, my_group, ngp, WAVES / ngp, reinterpret_cast<f32x4 *>(lds_ring));

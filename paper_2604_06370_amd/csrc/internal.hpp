@@ -57,8 +57,10 @@ constexpr int kDefaultReservePages = 16;  // growth room of an agent's last item
 //   kDescNag              agents in the item (0: idle block)    kDescHead  KV head
 //   kDescLeader           agent whose base block-table row names the item's pages
 //   kDescItem, kDescCopies
+//   kDescStream           1: no other item reads this item's base pages (the kernel loads
+//                         them as data read once); 0: other items of the segment do
 //   kDescAgent + slot, kDescPart + slot   agent and first partial of each item slot
-enum DescField { kDescPg0 = 0, kDescCap, kDescNag, kDescHead, kDescLeader, kDescItem, kDescCopies };
+enum DescField { kDescPg0 = 0, kDescCap, kDescNag, kDescHead, kDescLeader, kDescItem, kDescCopies, kDescStream };
 constexpr int kDescAgent = 8;
 constexpr int kDescPart = kDescAgent + kMaxItemAgents;
 constexpr int kDescWords = kDescPart + kMaxItemAgents;

@@ -32,15 +32,20 @@ __device__ __forceinline__ i32x4 block_rsrc(uint64_t base, int bytes) {
     r.w = 0x00020000;  // raw 32-bit data format
     return r;
 }
+// Cache policy of a load (the instruction's cache-policy bits): kCacheStream marks data read
+// once (non-temporal), so that it displaces less of what other workgroups re-read.
+constexpr int kCacheDefault = 0, kCacheStream = 2;
 // 16-byte buffer load into registers.
 __device__ i32x4 raw_buffer_load_b128(i32x4 rsrc, int voffset, int soffset, int aux) __asm("llvm.amdgcn.raw.buffer.load.v4i32");
+template <int POLICY = kCacheDefault>
 __device__ __forceinline__ u32x4 buf_load16(i32x4 rsrc, int voff) {
-    return __builtin_bit_cast(u32x4, raw_buffer_load_b128(rsrc, voff, 0, 0));
+    return __builtin_bit_cast(u32x4, raw_buffer_load_b128(rsrc, voff, 0, POLICY));
 }
 // Copy: lane i's 16 bytes at byte offset voff of the resource land at dst + 16 i.  The
 // instruction's immediate offset stays 0 (it would shift the LDS destination as well).
+template <int POLICY = kCacheDefault>
 __device__ __forceinline__ void lds_dma16(i32x4 rsrc, int voff, LdsU32x4 *dst) {
-    raw_buffer_load_lds(rsrc, reinterpret_cast<__attribute__((address_space(3))) uint32_t *>(dst), 16, voff, 0, 0, 0);
+    raw_buffer_load_lds(rsrc, reinterpret_cast<__attribute__((address_space(3))) uint32_t *>(dst), 16, voff, 0, 0, POLICY);
 }
 
 // LDS byte address of an LDS location.

@@ -232,7 +232,12 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     //    groups on 4 / ngp wave copies (ngp = ng rounded up to 1, 2 or 4); the copies of a
     //    group merge their partial rows inside the workgroup, so every slot owns one partial
     //    (the `copies` field of an item: partials per slot, 1): rows = agents * g.
-    struct Item { int32_t p0, p1, cap, copies; double cost; std::vector<int32_t> agents; };
+    struct Item {
+        int32_t p0, p1, cap, copies;
+        double cost;
+        std::vector<int32_t> agents;
+        bool solo;  // no other item reads its base pages (one item per split of its segment)
+    };
     std::vector<Item> items;
     std::vector<std::pair<int32_t, int32_t>> clusters;  // [first item, item count)
     std::vector<double> cluster_cost;
@@ -249,7 +254,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
             double cost = 0;
             size_t k = 0;
             for (size_t c : chunks) {
-                Item it{p0, p1, p1, 1, 0.0, {}};
+                Item it{p0, p1, p1, 1, 0.0, {}, chunks.size() == 1};
                 for (size_t j = k; j < k + c; ++j) it.agents.push_back(s.agents[j]);
                 k += c;
                 total_rows += (int64_t)it.copies * (int64_t)c * g;
@@ -281,7 +286,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
             last.cap = last.p1 + room;
         } else {
             const int32_t first = (int32_t)items.size();
-            Item it{npages[a], npages[a], npages[a] + room, 1, kItemOverhead, {a}};
+            Item it{npages[a], npages[a], npages[a] + room, 1, kItemOverhead, {a}, true};
             total_rows += (int64_t)it.copies * g;
             items.push_back(std::move(it));
             clusters.push_back({first, 1});
@@ -411,6 +416,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
             d[fkv::kDescLeader] = it.agents[0];
             d[fkv::kDescItem] = i;
             d[fkv::kDescCopies] = it.copies;
+            d[fkv::kDescStream] = it.solo ? 1 : 0;
             for (int32_t j = 0; j < nag; ++j) {
                 d[fkv::kDescAgent + j] = it.agents[j];
                 d[fkv::kDescPart + j] = first[i][j];
