@@ -461,10 +461,12 @@ def suite(args, dev, stream) -> dict:
     run("8b_mixed_one_step_rope_on", lambda: mixed_entry(wm, dev, True, st))
     del wm
     # one GPU's share of a tensor-parallel degree-8 deployment of the 16-agent 32K workload
+    # (71 MB per step: eight cache copies, so that the copies together exceed twice the 256 MB
+    # MALL and no step finds its pages there; with three, part of each step came from the MALL)
     tp = W.fanout("llama3-8b-16agents-32k-shared-tp8-share", 2, n_agents=16, prefix=32768, suffix_lo=256,
                   suffix_hi=4096, hq=4, hkv=1, r=16)
-    run("tp8_share_hkv1_rope_off", lambda: decode_entry(tp, dev, stream, False, st, 3, 3))
-    run("tp8_share_hkv1_rope_on", lambda: decode_entry(tp, dev, stream, True, st, 3, 3))
+    run("tp8_share_hkv1_rope_off", lambda: decode_entry(tp, dev, stream, False, st, 3, 8))
+    run("tp8_share_hkv1_rope_on", lambda: decode_entry(tp, dev, stream, True, st, 3, 8))
     del tp
     # LoRA rank sweep at the 16-agent 32K shape
     for r in (8, 16, 32):
