@@ -124,7 +124,8 @@ struct Rows {
 
 
 // Stage 2 on one page's S^T tile plus the value products.  Tokens tok0+4grp+i at or
-// past `len` (this lane's row's sequence length) or on an invalid page get zero weight;
+// past `len` (this lane's row's sequence length; only tested with LEN_MASK, which a caller
+// may leave off for a page inside every row's sequence) or on an invalid page get zero weight;
 // vf must already be zero for tokens past every row's length, cv for tokens past its
 // slot's residual length.
 //
@@ -134,7 +135,7 @@ struct Rows {
 // partial is exact whichever m it ends with.
 constexpr float kLazyRescale = 8.f;
 
-template <int R, int NS>
+template <int R, int NS, bool LEN_MASK = true>
 __device__ __forceinline__ void softmax_pv(Rows<R> &st, f32x4 sacc, bool valid, int tok0, int len, float scale_log2,
                                            const u32x2 *vf, const u32x2 (*cv)[Rows<R>::RTX], int my_slot_l,
                                            int grp) {
@@ -143,7 +144,7 @@ __device__ __forceinline__ void softmax_pv(Rows<R> &st, f32x4 sacc, bool valid, 
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int tok = tok0 + 4 * grp + i;
-        sv[i] = (valid && tok < len) ? sacc[i] * scale_log2 : kNegInf;
+        sv[i] = (valid && (!LEN_MASK || tok < len)) ? sacc[i] * scale_log2 : kNegInf;
         mx = fmaxf(mx, sv[i]);
     }
     mx = max_over_groups(mx);
@@ -911,8 +912,11 @@ __global__ __launch_bounds__(256, 2) void decode_rope_kernel(DecodeArgs p) {
     int item_max_len = 0;
     for (int s = 0; s < nag; ++s) item_max_len = max(item_max_len, __builtin_amdgcn_readlane(l_len, s));
     const int npg = min(pgcap, (item_max_len + PS - 1) / PS) - pg0;
-    // the wave's slots: keys that carry a residual (0 without adapter or past the item)
+    // the wave's slots: keys that carry a residual (0 without adapter or past the item), and
+    // the shortest sequence among them: pages that end at or before it hold written keys,
+    // values and rCache rows for every row of the wave, so they need no length masks
     int res_len[NSW];
+    int wave_min_len = item_max_len;
 #pragma unroll
     for (int s = 0; s < NSW; ++s) {
         const bool ok = sb + s < nag;
@@ -920,6 +924,7 @@ __global__ __launch_bounds__(256, 2) void decode_rope_kernel(DecodeArgs p) {
         const int len = __builtin_amdgcn_readlane(l_len, (sb + s) & 63);
         res_len[s] = (ok && ad >= 0) ? len : 0;
         if (res_len[s] == 0) rid0[s] = rid1[s] = -1;
+        if (ok) wave_min_len = min(wave_min_len, len);
     }
     const int src_lane = (sb + my_slot) & 63;
     const int sh_agent = __shfl(l_agent, src_lane), sh_len = __shfl(l_len, src_lane);
@@ -1049,7 +1054,10 @@ __global__ __launch_bounds__(256, 2) void decode_rope_kernel(DecodeArgs p) {
     load_q(p.q + ((int64_t)my_agent * p.hq + qh) * D, row_active, grp, qf);
     __syncthreads();  // B_K^T fragments visible to every wave
 
-    for (int k = copy; busy && k < npg; k += copies) {
+    // One page of the wave's loop.  EDGE: the page may reach past a row's sequence, so rCache
+    // rows, value tokens and scores are masked by length; interior pages skip those masks.
+    auto page = [&](auto edge_tag, int k) __attribute__((always_inline)) {
+        constexpr bool EDGE = decltype(edge_tag)::value;
         const int next = k + copies;
         const int tok0 = (pg0 + k) * PS;
         f32x4 sbase = {0, 0, 0, 0};
@@ -1064,10 +1072,12 @@ __global__ __launch_bounds__(256, 2) void decode_rope_kernel(DecodeArgs p) {
                 kx = grp < 2 ? kx : u32x2{0, 0};
                 vx = col < 8 ? vx : u32x2{0, 0};
             }
-            const int svis = res_len[s] - tok0;
-            if (svis < PS) {
-                vx = mask4(vx, svis, grp);
-                kx = col < svis ? kx : u32x2{0, 0};
+            if constexpr (EDGE) {
+                const int svis = res_len[s] - tok0;
+                if (svis < PS) {
+                    vx = mask4(vx, svis, grp);
+                    kx = col < svis ? kx : u32x2{0, 0};
+                }
             }
             return key ? kx : vx;
         };
@@ -1127,14 +1137,20 @@ __global__ __launch_bounds__(256, 2) void decode_rope_kernel(DecodeArgs p) {
             vf[2 * q2 + 1] = u32x2{fv[q2].z, fv[q2].w};
         }
         // value tokens past the item's longest sequence may hold any bits: zero them
-        const int vis = item_max_len - tok0;
-        if (vis < PS) {
+        if constexpr (EDGE) {
+            const int vis = item_max_len - tok0;
+            if (vis < PS) {
 #pragma unroll
-            for (int mt = 0; mt < 8; ++mt) vf[mt] = mask4(vf[mt], vis, grp);
+                for (int mt = 0; mt < 8; ++mt) vf[mt] = mask4(vf[mt], vis, grp);
+            }
         }
-        softmax_pv<R, NSW>(st, sacc, row_active, tok0, my_len, p.scale_log2, vf, cv, my_slot, grp);
+        softmax_pv<R, NSW, EDGE>(st, sacc, row_active, tok0, my_len, p.scale_log2, vf, cv, my_slot, grp);
         load_v(next);
-    }
+    };
+    // interior pages first (a prefix of the wave's pages), then the rest
+    int k = copy;
+    for (; busy && k < npg && (pg0 + k + 1) * PS <= wave_min_len; k += copies) page(std::false_type{}, k);
+    for (; busy && k < npg; k += copies) page(std::true_type{}, k);
     merge_wave_copies<R>(st, wave, copy, my_group, ngp, copies, reinterpret_cast<f32x4 *>(bkt));
     if (copy == 0) write_partial<R>(p, st, row_active, my_row, grp);
 }
