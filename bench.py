@@ -67,8 +67,9 @@ def counter_traffic(rope: bool, workload: str, pages_per_split: int):
 def algorithmic_bytes(wl, lw, agents, rope: bool) -> dict:
     """Bytes one decode step must move at least once: each shared base page once, every agent's
     private pages and rCache rows, adapters, queries, outputs, block tables and (RoPE on) the
-    RoPE rows the kernel reads (cos and sin of each page's first position, 512 B per page, plus
-    the 16 in-page offsets)."""
+    smallest table that gives every position's cos and sin: each page's first position, 512 B
+    per page, plus the 16 in-page offsets (angle addition does the rest).  The RoPE kernel reads
+    every position's row instead (8 KB per page); the counter traffic includes those bytes."""
     ps, hkv, d, r = wl.page_size, wl.hkv, wl.d, wl.r
     bb, rb, sl = lw._decode["host_bt"]
     # distinct physical base pages and the most tokens any agent reads from each
