@@ -844,7 +844,7 @@ __global__ __launch_bounds__(256, R >= 64 ? 1 : 2) void decode_split_kernel(Deco
 // fp32 accumulate):
 //   U^T   = B_K,s^T C_K,s^T                  16x16x16
 //   K_lr  = RoPE_p(U)                        rotate-half pairs (i, i + 64) in one lane, fp32
-//   S^T  += K_lr Q_s^T                       16x16x32, other slots' rows masked out of Q
+//   S^T  += K_lr Q^T                         16x16x32, kept for the slot's own rows (columns)
 template <int R, int G>
 struct RopeShape {
     static constexpr int RT = (R + 15) / 16;                       // 16-wide rank tiles
