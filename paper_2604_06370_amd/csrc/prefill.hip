@@ -348,30 +348,128 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
                 // Stage 1 for a quarter of page pw: U^T tiles, deferred RoPE, K = K_base +
                 // K_lora in place (keys past the sequence end are masked out of the scores)
                 u32x2 ck[RTX];
-#pragma unroll
-                for (int t = 0; t < RT; ++t) {
-                    const u32x4 c = lds_read1(base + S::C_OFF + (t * 4 + pw) * 1024);
-                    ck[t] = (16 * t + 4 * grp < R) ? u32x2{c.x, c.y} : u32x2{0, 0};
-                }
                 f32x4 u[4];  // u tiles 2 half, 2 half + 1, 2 half + 4, 2 half + 5
 #pragma unroll
                 for (int j = 0; j < 4; ++j) u[j] = f32x4{0, 0, 0, 0};
-#pragma unroll
-                for (int t = 0; t < RT; ++t) {
-                    // (explicit reads: the copies in flight write other LDS bytes)
+                u32x4 rot0[4];  // cos m, cos m + 1, sin m, sin m + 1 at p0 (this lane group)
+                u32x4 rotc[2], rots[2];  // cos, sin of tiles m, m + 1 at position col
+                const uint32_t colt = lds_addr((LdsU32x4 *)lds) + S::MAIN_BYTES + S::SBK_BYTES + 2 * half * 1024 + lane * 16;
+                const uint32_t ka = base + S::K_OFF + pw * 4096 + half * 1024;
+                const uint32_t kb = ka + 2 * 1024;
+                u32x4 kf[2];
+                if constexpr (RT == 1) {
+                    // every LDS read of the rebuild under one wait (rCache fragment, B_K^T tiles,
+                    // cos/sin pieces, K fragments): 16 agents x 2048-token chunks, 28.0 -> 26.9 ms
+                    u32x4 c;
                     u32x2 bkf[4];
-                    lds_read4_b64_tiles(lds_addr((LdsU32x4 *)lds) + S::MAIN_BYTES + ((t * 8 + 2 * half) * 64 + lane) * 8, bkf);
+                    asm volatile(
+                        "ds_read_b128 %0, %15\n\t"
+                        "ds_read_b64 %1, %16\n\t"
+                        "ds_read_b64 %2, %16 offset:512\n\t"
+                        "ds_read_b64 %3, %16 offset:2048\n\t"
+                        "ds_read_b64 %4, %16 offset:2560\n\t"
+                        "ds_read_b128 %5, %17\n\t"
+                        "ds_read_b128 %6, %17 offset:64\n\t"
+                        "ds_read_b128 %7, %17 offset:128\n\t"
+                        "ds_read_b128 %8, %17 offset:192\n\t"
+                        "ds_read_b128 %9, %18\n\t"
+                        "ds_read_b128 %10, %18 offset:1024\n\t"
+                        "ds_read_b128 %11, %18 offset:4096\n\t"
+                        "ds_read_b128 %12, %18 offset:5120\n\t"
+                        "ds_read_b128 %13, %19\n\t"
+                        "ds_read_b128 %14, %19 offset:2048\n\t"
+                        "s_waitcnt lgkmcnt(0)"
+                        : "=&v"(c), "=&v"(bkf[0]), "=&v"(bkf[1]), "=&v"(bkf[2]), "=&v"(bkf[3]), "=&v"(rot0[0]), "=&v"(rot0[1]),
+                          "=&v"(rot0[2]), "=&v"(rot0[3]), "=&v"(rotc[0]), "=&v"(rotc[1]), "=&v"(rots[0]), "=&v"(rots[1]),
+                          "=&v"(kf[0]), "=&v"(kf[1])
+                        : "v"(base + S::C_OFF + pw * 1024),
+                          "v"(lds_addr((LdsU32x4 *)lds) + S::MAIN_BYTES + ((2 * half) * 64 + lane) * 8),
+                          "v"(lds_addr(buf(tile)) + S::T_OFF + (pw * 2 + half) * 256 + grp * 16), "v"(colt), "v"(ka)
+                        : "memory");
+                    ck[0] = (4 * grp < R) ? u32x2{c.x, c.y} : u32x2{0, 0};
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) u[j] = mfma16(bkf[j], ck[t], u[j]);
+                    for (int j = 0; j < 4; ++j) u[j] = mfma16(bkf[j], ck[0], u[j]);
+                } else {
+                    // two groups under one wait each: the rCache fragments and B_K^T tiles of every
+                    // rank tile (rank tile t is 4 KB further in both), then cos/sin and K
+                    u32x4 c[RT];
+                    u32x2 bkf[RT][4];
+                    const uint32_t ca = base + S::C_OFF + pw * 1024;
+                    const uint32_t ba = lds_addr((LdsU32x4 *)lds) + S::MAIN_BYTES + ((2 * half) * 64 + lane) * 8;
+                    static_assert(RT == 2 || RT == 4, "rank tiles");
+                    if constexpr (RT == 2) {
+                        asm volatile(
+                            "ds_read_b128 %0, %10\n\t"
+                            "ds_read_b128 %1, %10 offset:4096\n\t"
+                            "ds_read_b64 %2, %11\n\t"
+                            "ds_read_b64 %3, %11 offset:512\n\t"
+                            "ds_read_b64 %4, %11 offset:2048\n\t"
+                            "ds_read_b64 %5, %11 offset:2560\n\t"
+                            "ds_read_b64 %6, %11 offset:4096\n\t"
+                            "ds_read_b64 %7, %11 offset:4608\n\t"
+                            "ds_read_b64 %8, %11 offset:6144\n\t"
+                            "ds_read_b64 %9, %11 offset:6656\n\t"
+                            "s_waitcnt lgkmcnt(0)"
+                            : "=&v"(c[0]), "=&v"(c[1]), "=&v"(bkf[0][0]), "=&v"(bkf[0][1]), "=&v"(bkf[0][2]),
+                              "=&v"(bkf[0][3]), "=&v"(bkf[1][0]), "=&v"(bkf[1][1]), "=&v"(bkf[1][2]), "=&v"(bkf[1][3])
+                            : "v"(ca), "v"(ba)
+                            : "memory");
+                    } else {
+                        asm volatile(
+                            "ds_read_b128 %0, %20\n\t"
+                            "ds_read_b128 %1, %20 offset:4096\n\t"
+                            "ds_read_b128 %2, %20 offset:8192\n\t"
+                            "ds_read_b128 %3, %20 offset:12288\n\t"
+                            "ds_read_b64 %4, %21\n\t"
+                            "ds_read_b64 %5, %21 offset:512\n\t"
+                            "ds_read_b64 %6, %21 offset:2048\n\t"
+                            "ds_read_b64 %7, %21 offset:2560\n\t"
+                            "ds_read_b64 %8, %21 offset:4096\n\t"
+                            "ds_read_b64 %9, %21 offset:4608\n\t"
+                            "ds_read_b64 %10, %21 offset:6144\n\t"
+                            "ds_read_b64 %11, %21 offset:6656\n\t"
+                            "ds_read_b64 %12, %21 offset:8192\n\t"
+                            "ds_read_b64 %13, %21 offset:8704\n\t"
+                            "ds_read_b64 %14, %21 offset:10240\n\t"
+                            "ds_read_b64 %15, %21 offset:10752\n\t"
+                            "ds_read_b64 %16, %21 offset:12288\n\t"
+                            "ds_read_b64 %17, %21 offset:12800\n\t"
+                            "ds_read_b64 %18, %21 offset:14336\n\t"
+                            "ds_read_b64 %19, %21 offset:14848\n\t"
+                            "s_waitcnt lgkmcnt(0)"
+                            : "=&v"(c[0]), "=&v"(c[1]), "=&v"(c[2]), "=&v"(c[3]), "=&v"(bkf[0][0]), "=&v"(bkf[0][1]),
+                              "=&v"(bkf[0][2]), "=&v"(bkf[0][3]), "=&v"(bkf[1][0]), "=&v"(bkf[1][1]),
+                              "=&v"(bkf[1][2]), "=&v"(bkf[1][3]), "=&v"(bkf[2][0]), "=&v"(bkf[2][1]),
+                              "=&v"(bkf[2][2]), "=&v"(bkf[2][3]), "=&v"(bkf[3][0]), "=&v"(bkf[3][1]),
+                              "=&v"(bkf[3][2]), "=&v"(bkf[3][3])
+                            : "v"(ca), "v"(ba)
+                            : "memory");
+                    }
+#pragma unroll
+                    for (int t = 0; t < RT; ++t) {
+                        ck[t] = (16 * t + 4 * grp < R) ? u32x2{c[t].x, c[t].y} : u32x2{0, 0};
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) u[j] = mfma16(bkf[t][j], ck[t], u[j]);
+                    }
+                    asm volatile(
+                        "ds_read_b128 %0, %10\n\t"
+                        "ds_read_b128 %1, %10 offset:64\n\t"
+                        "ds_read_b128 %2, %10 offset:128\n\t"
+                        "ds_read_b128 %3, %10 offset:192\n\t"
+                        "ds_read_b128 %4, %11\n\t"
+                        "ds_read_b128 %5, %11 offset:1024\n\t"
+                        "ds_read_b128 %6, %11 offset:4096\n\t"
+                        "ds_read_b128 %7, %11 offset:5120\n\t"
+                        "ds_read_b128 %8, %12\n\t"
+                        "ds_read_b128 %9, %12 offset:2048\n\t"
+                        "s_waitcnt lgkmcnt(0)"
+                        : "=&v"(rot0[0]), "=&v"(rot0[1]), "=&v"(rot0[2]), "=&v"(rot0[3]), "=&v"(rotc[0]), "=&v"(rotc[1]),
+                          "=&v"(rots[0]), "=&v"(rots[1]), "=&v"(kf[0]), "=&v"(kf[1])
+                        : "v"(lds_addr(buf(tile)) + S::T_OFF + (pw * 2 + half) * 256 + grp * 16), "v"(colt), "v"(ka)
+                        : "memory");
                 }
                 // rotate-half pairs (tile m with m + 4) at the key's position p0 + col: the
                 // angle of page start p0 plus the angle of offset col (angle addition)
-                u32x4 rot0[4];  // cos m, cos m + 1, sin m, sin m + 1 at p0 (this lane group)
-                lds_read4_64(lds_addr(buf(tile)) + S::T_OFF + (pw * 2 + half) * 256 + grp * 16, rot0);
-                u32x4 rotc[2], rots[2];  // cos, sin of tiles m, m + 1 at position col
-                const uint32_t colt = lds_addr((LdsU32x4 *)lds) + S::MAIN_BYTES + S::SBK_BYTES + 2 * half * 1024 + lane * 16;
-                lds_read2(colt, rotc);
-                lds_read2(colt + 4096, rots);
 #pragma unroll
                 for (int j = 0; j < 2; ++j) {
                     const f32x4 c0 = __builtin_bit_cast(f32x4, rot0[j]), s0 = __builtin_bit_cast(f32x4, rot0[2 + j]);
@@ -385,11 +483,7 @@ __global__ __launch_bounds__(64 * kStreamWaves, 1) void prefill_stream_kernel(Pr
                         u[j + 2][i] = y * c + x * s;
                     }
                 }
-                // K fragments half (u tiles 2 half, 2 half + 1) and half + 2 (tiles + 4)
-                const uint32_t ka = base + S::K_OFF + pw * 4096 + half * 1024;
-                const uint32_t kb = ka + 2 * 1024;
-                u32x4 kf[2];
-                lds_read2_2k(ka, kf);
+                // K fragments half (u tiles 2 half, 2 half + 1) and half + 2 (tiles + 4), read above
                 u32x4 out[2];
 #pragma unroll
                 for (int j = 0; j < 2; ++j) {
