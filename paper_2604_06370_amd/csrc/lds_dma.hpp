@@ -75,52 +75,6 @@ __device__ __forceinline__ void lds_read2(uint32_t addr, u32x4 (&out)[2]) {
         : "v"(addr)
         : "memory");
 }
-// One 16-byte LDS read.
-__device__ __forceinline__ u32x4 lds_read1(uint32_t addr) {
-    u32x4 out;
-    asm volatile(
-        "ds_read_b128 %0, %1\n\t"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(out)
-        : "v"(addr)
-        : "memory");
-    return out;
-}
-// Four 16-byte LDS reads at addr, addr + 64, + 128, + 192 bytes.
-__device__ __forceinline__ void lds_read4_64(uint32_t addr, u32x4 (&out)[4]) {
-    asm volatile(
-        "ds_read_b128 %0, %4\n\t"
-        "ds_read_b128 %1, %4 offset:64\n\t"
-        "ds_read_b128 %2, %4 offset:128\n\t"
-        "ds_read_b128 %3, %4 offset:192\n\t"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(out[0]), "=&v"(out[1]), "=&v"(out[2]), "=&v"(out[3])
-        : "v"(addr)
-        : "memory");
-}
-// Two 16-byte LDS reads at addr and addr + 2 KB.
-__device__ __forceinline__ void lds_read2_2k(uint32_t addr, u32x4 (&out)[2]) {
-    asm volatile(
-        "ds_read_b128 %0, %2\n\t"
-        "ds_read_b128 %1, %2 offset:2048\n\t"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(out[0]), "=&v"(out[1])
-        : "v"(addr)
-        : "memory");
-}
-// Four 8-byte LDS reads at addr + 0, 512, 2048 and 2560 bytes (the B_K^T fragments of
-// tiles m, m + 1, m + 4, m + 5 when one tile of 64 lanes is 512 bytes).
-__device__ __forceinline__ void lds_read4_b64_tiles(uint32_t addr, u32x2 (&out)[4]) {
-    asm volatile(
-        "ds_read_b64 %0, %4\n\t"
-        "ds_read_b64 %1, %4 offset:512\n\t"
-        "ds_read_b64 %2, %4 offset:2048\n\t"
-        "ds_read_b64 %3, %4 offset:2560\n\t"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(out[0]), "=&v"(out[1]), "=&v"(out[2]), "=&v"(out[3])
-        : "v"(addr)
-        : "memory");
-}
 // Eight 16-byte LDS reads: four at addr0 + 0/1/2/3 KB, four at addr1 + 0/1/2/3 KB.
 __device__ __forceinline__ void lds_read8(uint32_t addr0, uint32_t addr1, u32x4 (&o0)[4], u32x4 (&o1)[4]) {
     asm volatile(
