@@ -866,15 +866,12 @@ __global__ __launch_bounds__(256, 2) void decode_rope_kernel(DecodeArgs p) {
     // B_K^T fragments for the launch; at the end the merge area of the wave copies
     __shared__ __attribute__((aligned(16))) u32x2 bkt[cmax(S::BKT, merge_lds_bytes(R)) / 8];
 
-    const int32_t *plan = p.plan;
-    const int blk = plan[p.off_blocks + blockIdx.x];
-    if (blk < 0) return;
+    // the block's descriptor (at an address that depends on blockIdx only) names the item
+    const int32_t *desc = p.plan + p.off_desc + (int64_t)blockIdx.x * fkv::kDescWords;
+    const int pg0 = desc[fkv::kDescPg0], pgcap = desc[fkv::kDescCap], nag = desc[fkv::kDescNag];
+    if (nag <= 0) return;  // idle block
     const int hkv = p.hkv;
-    const int item = blk / hkv;
-    const int h = blk - item * hkv;
-    const int32_t *rec = plan + p.off_items + item * fkv::kItemWords;
-    const int pg0 = rec[fkv::kItemP0], pgcap = rec[fkv::kItemCap], leader = rec[fkv::kItemLeader];
-    const int nag = rec[fkv::kItemNag];
+    const int h = desc[fkv::kDescHead], leader = desc[fkv::kDescLeader];
     const int npcap = pgcap - pg0;
     if (nag < 1 || nag > MS || npcap < 1 || npcap > fkv::kMaxPagesSingle) return;  // rejected on the host
     const int ng = (nag + NSW - 1) / NSW;
@@ -894,8 +891,8 @@ __global__ __launch_bounds__(256, 2) void decode_rope_kernel(DecodeArgs p) {
     // arrays); lane i (and 64 + i): base page id of item page i (the leader's row) and, per
     // slot of this wave's group, its rCache page id (-1: no adapter)
     const bool lane_ag = lane < nag;
-    const int l_agent = lane_ag ? rec[fkv::kItemAgents + lane] : 0;
-    const int l_part = lane_ag ? rec[fkv::kItemFirst + lane] : 0;
+    const int l_agent = lane_ag ? desc[fkv::kDescAgent + lane] : 0;
+    const int l_part = lane_ag ? desc[fkv::kDescPart + lane] : 0;
     const int l_len = lane_ag ? p.seq_lens[l_agent] : 0;
     const int l_ad = lane_ag ? p.adapter_idx[l_agent] : -1;
     const int32_t *brow = p.base_bt + (int64_t)leader * p.max_pages + pg0;
@@ -950,6 +947,7 @@ __global__ __launch_bounds__(256, 2) void decode_rope_kernel(DecodeArgs p) {
         uint32_t *bw = reinterpret_cast<uint32_t *>(bkt);
         constexpr int UPT = S::BK_UNITS / 256, ROUND = UPT < 4 ? UPT : 4;
         for (int u0 = 0; u0 < UPT; u0 += ROUND) {
+            if (256 * u0 / (RT * 128) >= nag) break;  // slots past the item's agents are never read
             u32x4 bk_lo[ROUND], bk_hi[ROUND];
 #pragma unroll
             for (int u = 0; u < ROUND; ++u) {
@@ -969,6 +967,7 @@ __global__ __launch_bounds__(256, 2) void decode_rope_kernel(DecodeArgs p) {
                 const int sl = idx / (RT * 128), rem = idx % (RT * 128);
                 const int rho = 2 * (rem / 16), c8 = rem % 16;
                 const int t = rho / 16, gg = (rho % 16) / 4, j2 = (rho % 4) / 2;
+                if (sl >= nag) continue;
                 const uint32_t lw[4] = {bk_lo[u].x, bk_lo[u].y, bk_lo[u].z, bk_lo[u].w};
                 const uint32_t hw[4] = {bk_hi[u].x, bk_hi[u].y, bk_hi[u].z, bk_hi[u].w};
 #pragma unroll
@@ -1351,7 +1350,7 @@ fkv_status decode_impl(const fkv_attn_args *a, const fkv_plan *plan, void *strea
                                           "than this kernel takes");
     if (w[fkv::H_PAGES_PER_SPLIT] > fkv::kMaxPagesSingle)
         return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: plan items longer than the kernel takes");
-    if (!rope_on && w[fkv::H_OFF_DESC] < 0)
+    if (w[fkv::H_OFF_DESC] < 0)
         return fkv::fail(FKV_ERR_INVALID, "fkv_residual_attention_decode: plan has no block descriptors");
     DecodeArgs da;
     da.q = static_cast<const uint16_t *>(a->q);

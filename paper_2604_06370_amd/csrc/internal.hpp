@@ -28,7 +28,7 @@ void clear_error();
 //   (header word H_OFF_AGENT_SLOT is unused and equals H_OFF_ZERO)
 //   zero      [kZeroWords]         zeros, 16-byte aligned (read in place of the rCache of an
 //                                  agent without adapter or of an empty agent slot)
-//   descriptors [n_blocks][kDescWords]  (RoPE-off plans) see below
+//   descriptors [n_blocks][kDescWords]  see below
 // An item holds up to four agent groups; a group is the floor(16/g) agents whose
 // query heads of one KV head fill the 16 rows of one matrix-core tile.  An item of
 // ng groups runs on 4 / ngp wave copies (ngp = 1, 2, 4 for ng = 1, 2, 3..4); the copies
@@ -50,8 +50,8 @@ constexpr int kMaxPagesMulti = 64;    // items of three or four agent groups
 constexpr int kMaxPagesSingle = 128;  // items of one or two agent groups
 constexpr int kDefaultReservePages = 16;  // growth room of an agent's last item (decode steps)
 
-// Block descriptors (RoPE-off plans): block b of the split kernel reads the
-// kDescWords words at off_desc + b * kDescWords:
+// Block descriptors: block b of the decode kernel (either form) reads the kDescWords words at
+// off_desc + b * kDescWords:
 //   kDescPg0, kDescCap    item page range start and capacity end (pages read: up to
 //                         min(cap, ceil(longest length / ps)))
 //   kDescNag              agents in the item (0: idle block)    kDescHead  KV head

@@ -350,7 +350,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     const int64_t off_ptr = off_blocks + n_blocks;
     const int64_t off_zero = (off_ptr + A + 1 + 3) / 4 * 4;
     const int64_t off_desc = off_zero + fkv::kZeroWords;
-    const int64_t total = off_desc + (rope ? 0 : (int64_t)n_blocks * fkv::kDescWords);
+    const int64_t total = off_desc + (int64_t)n_blocks * fkv::kDescWords;
     if (total > INT32_MAX) {
         delete pl;
         return fkv::fail(FKV_ERR_UNSUPPORTED, "fkv_decode_plan_create: plan too large");
@@ -378,7 +378,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
     w[fkv::H_RANK] = prm->r;
     w[fkv::H_ROPE] = rope ? 1 : 0;
     w[fkv::H_OFF_ZERO] = (int32_t)off_zero;
-    w[fkv::H_OFF_DESC] = rope ? -1 : (int32_t)off_desc;
+    w[fkv::H_OFF_DESC] = (int32_t)off_desc;
     for (int32_t i = 0; i < n_items; ++i) {
         int32_t *r = &w[off_items + (int64_t)i * fkv::kItemWords];
         const int32_t nag = (int32_t)items[i].agents.size();
@@ -399,7 +399,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
         w[off_blocks + b] = k < lst.size() ? lst[k] : -1;
     }
     for (int32_t a = 0; a <= A; ++a) w[off_ptr + a] = ptr[a];
-    if (!rope) {
+    {
         // block descriptors: the item a block serves, at an address that depends on the block
         // index only (the kernel's first load)
         for (int32_t b = 0; b < n_blocks; ++b) {

@@ -341,18 +341,16 @@ def test_decode_plan_items_cover_every_agent_page_once(hq, hkv, r, rope, pps):
         assert int(ptr[0]) == 0 and h["total_rows"] == int(ptr[-1]) * g
         ids = [b for b in blocks if b >= 0]
         assert sorted(ids) == list(range(len(items) * (hkv // hpb))) and len(blocks) % 8 == 0
-        if rope:
-            assert h["off_desc"] == -1
-        else:
-            # each block's descriptor restates its item and head
-            for blk, dsc in zip(blocks, _parse_desc(words, h)):
-                if blk < 0:
-                    assert dsc["nag"] == 0
-                    continue
-                it = items[blk // hkv]
-                assert (dsc["p0"], dsc["cap"], dsc["nag"], dsc["head"], dsc["leader"], dsc["item"], dsc["copies"]) == \
-                    (it["p0"], it["cap"], it["nag"], blk % hkv, it["leader"], blk // hkv, it["copies"])
-                assert dsc["agents"] == it["agents"] and dsc["parts"] == it["first"]
+        # each block's descriptor (RoPE-on and RoPE-off plans) restates its item and head
+        assert h["off_desc"] >= 0
+        for blk, dsc in zip(blocks, _parse_desc(words, h)):
+            if blk < 0:
+                assert dsc["nag"] == 0
+                continue
+            it = items[blk // hkv]
+            assert (dsc["p0"], dsc["cap"], dsc["nag"], dsc["head"], dsc["leader"], dsc["item"], dsc["copies"]) == \
+                (it["p0"], it["cap"], it["nag"], blk % hkv, it["leader"], blk // hkv, it["copies"])
+            assert dsc["agents"] == it["agents"] and dsc["parts"] == it["first"]
         # lengths within the capacity are covered; one token past it is not
         plan.covers(np.minimum(sl + 5, [plan.capacity(a) for a in range(n_agents)]))
         over = np.array([plan.capacity(a) for a in range(n_agents)], np.int32)
