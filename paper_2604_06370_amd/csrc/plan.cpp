@@ -134,8 +134,11 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
         // Items of three or four agent groups stream every base page through LDS to four
         // waves and are bound by the compute unit's vector-memory issue rate, so two of them
         // on one compute unit slow each other down: they get at most one workgroup per
-        // compute unit (pages split evenly over that budget, within their page limit).  The
-        // other items take a uniform page count, chosen by a simulated greedy longest-first
+        // compute unit (pages split evenly over that budget, within their page limit), and
+        // at least 12 pages each: below that an item spends most of its time starting up
+        // (one KV head, 16 agents sharing 32K tokens: 8-page items 34.1 us per split and
+        // merge, 12 pages 28.7, 16 pages 29.7; 2K shared tokens at eight KV heads: 4-page
+        // items 45.0 us, 12 pages 36.8).  The other items take a uniform page count, chosen by a simulated greedy longest-first
         // fill of the resident slots (what the dispatcher does with the block order below).
         auto is_multi = [&](size_t i) { return sc[i].cap == fkv::kMaxPagesMulti && !rope; };
         int64_t multi_pages = 0;
@@ -144,8 +147,9 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
                 multi_pages += (int64_t)sc[i].n * (int64_t)chunk_sizes(segs[i].agents.size()).size();
             }
         const int64_t multi_budget = std::max<int64_t>(1, cus / nhb_units);
+        constexpr int64_t kMinMultiPages = 12;
         const int32_t multi_pps = multi_pages > 0
-            ? (int32_t)std::min<int64_t>(fkv::kMaxPagesMulti, std::max<int64_t>(4, (multi_pages + multi_budget - 1) / multi_budget))
+            ? (int32_t)std::min<int64_t>(fkv::kMaxPagesMulti, std::max<int64_t>(kMinMultiPages, (multi_pages + multi_budget - 1) / multi_budget))
             : fkv::kMaxPagesMulti;
         std::vector<int32_t> cand_pps(sc.size());
         auto sim = [&](auto &&pages_of) {
