@@ -216,6 +216,29 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
             };
             for (int32_t pages : {64, 128})
                 if (rope_blocks(pages) * 2 >= 5 * slots * nhb_units) rope_pages = pages;
+            // small workloads: items of 16 or 8 pages when 32 would leave fewer than 1.5
+            // workgroups per resident slot (16 agents over a 2K shared prefix: 640 -> 1280
+            // workgroups, split and merge 69.1 -> 54.9 us with the spread below)
+            if (rope_blocks(32) * 2 < 3 * slots * nhb_units)
+                rope_pages = rope_blocks(16) * 2 >= 3 * slots * nhb_units ? 16 : 8;
+        }
+        // RoPE on: items of more than one wave group carry most of the work (every page is
+        // rebuilt for each of their agents); their pages are spread so that they give every
+        // compute unit a workgroup (at least 8 pages an item, at most the size above).  One
+        // KV head, 16 agents sharing 32K tokens: 64 shared items of 32 pages -> 256 of 8,
+        // 84 -> 39 us (36 with the private items at 8 pages too, from the rule above).
+        auto is_rope_multi = [&](size_t i) {
+            for (size_t c : chunk_sizes(segs[i].agents.size()))
+                if ((int64_t)c > ag) return true;
+            return false;
+        };
+        int32_t rope_multi_pages = rope_pages;
+        if (rope) {
+            int64_t multi = 0;
+            for (size_t i = 0; i < segs.size(); ++i)
+                if (is_rope_multi(i)) multi += (int64_t)segs[i].n * (int64_t)chunk_sizes(segs[i].agents.size()).size();
+            const int64_t budget = std::max<int64_t>(1, cus / nhb_units);
+            rope_multi_pages = (int32_t)std::min<int64_t>(rope_pages, std::max<int64_t>(8, (multi + budget - 1) / budget));
         }
         for (size_t i = 0; i < segs.size(); ++i) {
             int32_t pps;
@@ -224,7 +247,7 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
                     return fkv::fail(FKV_ERR_INVALID, "fkv_decode_plan_create: pages_per_split above 128");
                 pps = std::min(prm->pages_per_split, sc[i].cap);
             } else {
-                const int32_t target = rope ? rope_pages : cand_pps[i];
+                const int32_t target = rope ? (is_rope_multi(i) ? rope_multi_pages : rope_pages) : cand_pps[i];
                 const int64_t k = (segs[i].n + target - 1) / target;
                 pps = (int32_t)((segs[i].n + k - 1) / k);
             }
