@@ -194,6 +194,25 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
         int32_t best_u = -1;
         for (int c = 8; c >= 0 && best_u < 0; --c)
             if (est[c] <= best * 1.05 && units[c] * nhb_units >= 2 * cus) best_u = cands[c];
+        if (best_u < 0 && units[0] * nhb_units * 2 < cus) {
+            // a small workload (items of 32 pages would occupy fewer than half the compute
+            // units): shorter items shorten the longest chain of pages (4 agents over a
+            // 512-token root at two KV heads: 16 workgroups of up to 32 pages -> 32 of up to 4,
+            // 12.3 -> 7.9 us; where the 32-page items already occupy most compute units, as
+            // for one KV head of 16 agents over 32K, items of 16 pages were slower, 21.3 ->
+            // 24.3 us)
+            double small_est[3];
+            const int32_t small_u[3] = {16, 8, 4};
+            for (int c = 0; c < 3; ++c) {
+                const int32_t u = small_u[c];
+                small_est[c] = sim([&](size_t i) { return is_multi(i) ? multi_pps : std::min(u, sc[i].cap); });
+                best = std::min(best, small_est[c]);
+            }
+            for (int c = 8; c >= 0 && best_u < 0; --c)
+                if (est[c] <= best * 1.01) best_u = cands[c];
+            for (int c = 0; c < 3 && best_u < 0; ++c)
+                if (small_est[c] <= best * 1.01) best_u = small_u[c];
+        }
         for (int c = 8; c >= 0 && best_u < 0; --c)
             if (est[c] <= best * 1.01) best_u = cands[c];
         if (best_u < 0) best_u = 64;
