@@ -249,7 +249,7 @@ def _parse_plan(words):
     return h, items, blocks, ptr
 
 
-# block descriptor layout (RoPE-off plans): item fields, then per-slot agents and first partials
+# block descriptor layout (every plan): item fields, then per-slot agents and first partials
 DESC_AGENT, DESC_PART = 8, 24
 DESC_WORDS = DESC_PART + 16
 
@@ -362,6 +362,58 @@ def test_decode_plan_items_cover_every_agent_page_once(hq, hkv, r, rope, pps):
         partials = h["total_rows"] * hkv * ((128 + r + 2 + 3) // 4 * 4) * 4
         assert info["workspace_bytes"] == (partials + 255) // 256 * 256
         plan.close()
+
+
+def _fanout_tables(n_agents, prefix_pages, suffix_pages, extra=16, ps=16):
+    """One shared prefix and private suffixes of the given page counts (full last pages)."""
+    mp = prefix_pages + max(suffix_pages) + extra
+    bb = np.full((n_agents, mp), -1, np.int32)
+    nxt = prefix_pages
+    for a in range(n_agents):
+        bb[a, :prefix_pages] = np.arange(prefix_pages)
+        bb[a, prefix_pages:prefix_pages + suffix_pages[a]] = np.arange(nxt, nxt + suffix_pages[a])
+        nxt += suffix_pages[a]
+    sl = np.array([(prefix_pages + s) * ps for s in suffix_pages], np.int32)
+    return bb, sl
+
+
+def test_decode_plan_sizes_items_to_the_workload():
+    """Item page counts the plan builder picks (256 compute units): the workloads it was
+    tuned on keep their plans, small workloads and a single KV head get shorter items."""
+    rng = np.random.default_rng(7)
+    suffix = [int(x) for x in rng.integers(16, 257, size=16)]
+
+    def items_of(bb, sl, hq, hkv, r, rope):
+        plan = rt.DecodePlan(bb, sl, hq, hkv, 16, num_cus=256, r=r, rope=rope)
+        h, items, blocks, _ = _parse_plan(plan.serialize())
+        plan.close()
+        return h, items, [b for b in blocks if b >= 0]
+
+    def shared(items, n):
+        return [it["end"] - it["p0"] for it in items if it["nag"] == n]
+
+    # 16 agents over 2048 shared pages, eight KV heads: RoPE on keeps items of 32 pages,
+    # RoPE off one workgroup of four agent groups per compute unit (2048 / 32 = 64 pages)
+    bb, sl = _fanout_tables(16, 2048, suffix)
+    _, items, _ = items_of(bb, sl, 32, 8, 16, True)
+    assert set(shared(items, 16)) == {32}
+    _, items, _ = items_of(bb, sl, 32, 8, 16, False)
+    assert set(shared(items, 16)) == {64}
+    # the same agents at one KV head: RoPE on spreads the shared items over every compute unit
+    # (8 pages: 256 of them) and keeps every item at 8 pages; RoPE off takes 12-page items
+    _, items, blocks = items_of(bb, sl, 4, 1, 16, True)
+    assert set(shared(items, 16)) == {8} and len(blocks) >= 512
+    assert max(it["end"] - it["p0"] for it in items) <= 8
+    _, items, _ = items_of(bb, sl, 4, 1, 16, False)
+    lens = shared(items, 16)
+    assert max(lens) == 12 and sum(lens) == 2048 and sum(x < 12 for x in lens) <= 1
+    # 4 agents over a 32-page root, 4-page tails, two KV heads: items of 4 pages (RoPE off)
+    # and 8 (RoPE on) instead of one 32-page item for the root
+    bb, sl = _fanout_tables(4, 32, [4, 4, 4, 4])
+    _, items, _ = items_of(bb, sl, 8, 2, 8, False)
+    assert max(it["end"] - it["p0"] for it in items) == 4
+    _, items, _ = items_of(bb, sl, 8, 2, 8, True)
+    assert max(it["end"] - it["p0"] for it in items) == 8
 
 
 def test_noalloc_decode_rejects_plans_beyond_its_static_workspace():
