@@ -407,6 +407,13 @@ def test_decode_plan_sizes_items_to_the_workload():
     _, items, _ = items_of(bb, sl, 4, 1, 16, False)
     lens = shared(items, 16)
     assert max(lens) == 12 and sum(lens) == 2048 and sum(x < 12 for x in lens) <= 1
+    # twelve agents (three groups of four) over a shared prefix: one item per page range
+    # without RoPE (four groups' waves, one idle), 8 + 4 agents with RoPE
+    bb, sl = _fanout_tables(12, 512, suffix[:12])
+    _, items, _ = items_of(bb, sl, 32, 8, 16, False)
+    assert {it["nag"] for it in items if it["p0"] < 512} == {12}
+    _, items, _ = items_of(bb, sl, 32, 8, 16, True)
+    assert {it["nag"] for it in items if it["p0"] < 512} == {8, 4}
     # 4 agents over a 32-page root, 4-page tails, two KV heads: items of 4 pages (RoPE off)
     # and 8 (RoPE on) instead of one 32-page item for the root
     bb, sl = _fanout_tables(4, 32, [4, 4, 4, 4])
