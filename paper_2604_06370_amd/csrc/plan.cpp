@@ -243,11 +243,15 @@ fkv_status fkv_decode_plan_create(const fkv_decode_plan_params *prm, const int32
             // workgroups, split and merge 69.1 -> 54.9 us with the spread below)
             if (rope_blocks(32) * 2 < 3 * slots * nhb_units)
                 rope_pages = rope_blocks(16) * 2 >= 3 * slots * nhb_units ? 16 : 8;
+            // and 4 when even 8-page items occupy fewer than half the compute units (4 agents
+            // over a 512-token root: 9.5 -> 7.9 us; one KV head of 16 agents over 32K, 536
+            // workgroups of 8 pages: 36.5 us, with 4 pages 46.5)
+            if (rope_pages == 8 && rope_blocks(8) * 2 < cus) rope_pages = 4;
         }
         // RoPE on: items of more than one wave group carry most of the work (every page is
         // rebuilt for each of their agents); their pages are spread so that they give every
-        // compute unit a workgroup (at least 8 pages an item, at most the size above).  One
-        // KV head, 16 agents sharing 32K tokens: 64 shared items of 32 pages -> 256 of 8,
+        // compute unit a workgroup (8 pages an item or more, capped at the size chosen above).
+        // One KV head, 16 agents sharing 32K tokens: 64 shared items of 32 pages -> 256 of 8,
         // 84 -> 39 us (36 with the private items at 8 pages too, from the rule above).
         auto is_rope_multi = [&](size_t i) {
             for (size_t c : chunk_sizes(segs[i].agents.size()))

@@ -414,13 +414,13 @@ def test_decode_plan_sizes_items_to_the_workload():
     assert {it["nag"] for it in items if it["p0"] < 512} == {12}
     _, items, _ = items_of(bb, sl, 32, 8, 16, True)
     assert {it["nag"] for it in items if it["p0"] < 512} == {8, 4}
-    # 4 agents over a 32-page root, 4-page tails, two KV heads: items of 4 pages (RoPE off)
-    # and 8 (RoPE on) instead of one 32-page item for the root
+    # 4 agents over a 32-page root, 4-page tails, two KV heads: items of 4 pages, RoPE off
+    # and on, instead of one 32-page item for the root
     bb, sl = _fanout_tables(4, 32, [4, 4, 4, 4])
     _, items, _ = items_of(bb, sl, 8, 2, 8, False)
     assert max(it["end"] - it["p0"] for it in items) == 4
     _, items, _ = items_of(bb, sl, 8, 2, 8, True)
-    assert max(it["end"] - it["p0"] for it in items) == 8
+    assert max(it["end"] - it["p0"] for it in items) == 4
 
 
 def test_noalloc_decode_rejects_plans_beyond_its_static_workspace():
